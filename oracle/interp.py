@@ -1,0 +1,111 @@
+"""Runs a function sequence with the textbook ops: one training step (test infrastructure).
+
+The result of an out-of-core step equals that of the ordinary in-core step,
+because swaps only move bytes (Section 1, Section 3); this interpreter is that
+ordinary step.  It executes the functions of ``oracle.lower`` in order, in
+the given dtype (float64 for parity), and returns every variable's final
+value, so tests can compare the loss, parameter gradients and updated
+parameters with the device.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+from . import ops
+
+
+def run(reg, x, labels, params, state=None, dtype=np.float64):
+    """One step.  ``params`` / ``state``: {name: array}.  Returns {var name: array}.
+
+    ``state`` holds momentum buffers by name (``m:<param>``); missing ones start at 0.
+    """
+    state = state or {}
+    names = [v["name"] for v in reg["vars"]]
+    env = {}
+    for v in reg["vars"]:
+        nm = v["name"]
+        if nm == "x":
+            env[nm] = np.asarray(x, dtype=dtype)
+        elif nm == "labels":
+            env[nm] = np.asarray(labels, dtype=np.int64)
+        elif v["kind"] == 1:
+            env[nm] = np.asarray(params[nm], dtype=dtype).copy()
+        elif v["kind"] == 2:
+            env[nm] = np.asarray(state.get(nm, np.zeros(v["shape"])), dtype=dtype).copy()
+    bnstat = {}
+    for f in reg["fns"]:
+        op, a = f["op"], f["attrs"]
+        vs = [names[i] for i, _ in f["vars"]]
+        g = env.get
+        if op == "linear_fwd":
+            X, Wn, b, Y = vs
+            env[Y] = ops.linear_fwd(g(X), g(Wn), g(b))
+        elif op == "conv_fwd":
+            X, Wn, Y = vs
+            env[Y] = ops.conv_fwd(g(X), g(Wn), a["stride"], a["pad"])
+        elif op == "bn_fwd":
+            X, gm, bt, Y, st = vs
+            env[Y], mean, invstd = ops.bn_fwd(g(X), g(gm), g(bt))
+            bnstat[st] = (mean, invstd)
+            env[st] = np.concatenate([mean, invstd, np.zeros(2 * a["slices"] * a["C"])])
+        elif op == "relu_fwd":
+            X, Y = vs
+            env[Y] = ops.relu_fwd(g(X))
+        elif op == "maxpool_fwd":
+            X, Y, ix = vs
+            env[Y], env[ix] = ops.maxpool_fwd(g(X), a["k"], a["stride"], a["pad"])
+        elif op == "avgpool_fwd":
+            X, Y = vs
+            env[Y] = ops.avgpool_fwd(g(X))
+        elif op == "add_fwd":
+            A, B, Y = vs
+            env[Y] = g(A) + g(B)
+        elif op == "softmax_ce":
+            lg, lb, loss, dl = vs
+            rows, mean, env[dl] = ops.softmax_ce(g(lg), g(lb))
+            env[loss] = np.concatenate([rows, [mean]])
+        elif op == "linear_bwd_w":
+            X, dY, dW, db = vs
+            env[dW], env[db] = ops.linear_bwd_w(g(X), g(dY))
+        elif op == "linear_bwd_x":
+            Wn, dY, dX = vs
+            env[dX] = ops.linear_bwd_x(g(Wn), g(dY))
+        elif op == "conv_bwd_w":
+            X, dY, dW = vs[:3]
+            shape = (a["K"], a["R"], a["S"], a["C"])
+            env[dW] = ops.conv_bwd_w(g(X), g(dY), shape, a["stride"], a["pad"])
+        elif op == "conv_bwd_x":
+            Wn, dY, dX = vs
+            shape = (a["N"], a["H"], a["W"], a["C"])
+            env[dX] = ops.conv_bwd_x(g(Wn), g(dY), shape, a["stride"], a["pad"])
+        elif op == "bn_bwd":
+            X, gm, st, dY, dX, dg, dbt = vs
+            mean, invstd = bnstat[st]
+            env[dX], env[dg], env[dbt] = ops.bn_bwd(g(X), g(gm), mean, invstd, g(dY))
+        elif op == "relu_bwd":
+            Y, dY, dX = vs
+            env[dX] = ops.relu_bwd(g(Y), g(dY))
+        elif op == "maxpool_bwd":
+            ix, dY, dX = vs
+            shape = (a["N"], a["H"], a["W"], a["C"])
+            env[dX] = ops.maxpool_bwd(g(ix), g(dY), shape, a["k"], a["stride"], a["pad"])
+        elif op == "avgpool_bwd":
+            dY, dX = vs
+            env[dX] = ops.avgpool_bwd(g(dY), (a["N"], a["H"], a["W"], a["C"]))
+        elif op == "add_grad":
+            A, B, Y = vs
+            env[Y] = g(A) + g(B)
+        elif op == "sgd":
+            lr, mu = a["lr"], a["momentum"]
+            step = 3 if mu else 2
+            for j in range(0, len(vs), step):
+                p, dp = vs[j], vs[j + 1]
+                if mu:
+                    m = vs[j + 2]
+                    env[p], env[m] = ops.sgd_momentum(g(p), g(dp), g(m), lr, mu)
+                else:
+                    env[p] = ops.sgd(g(p), g(dp), lr)
+        else:
+            raise ValueError(f"unknown function {op}")
+    return env

@@ -1,0 +1,182 @@
+"""Textbook forward, backward and SGD of every layer kind, in NumPy (test infrastructure).
+
+The paper trains ordinary networks (ResNet-50 and others, Section 5); it
+fixes none of these formulas, so each is the standard definition, computed in
+the dtype of its inputs (float64 for parity).  Layouts follow the library
+boundary: images NHWC, conv weights [K, R, S, C], dense weights [out, in].
+
+* dense:        Y = X W^T + b
+* conv:         cross-correlation with zero padding,
+                Y[n,p,q,k] = sum_{r,s,c} Xpad[n, p*st + r, q*st + s, c] W[k,r,s,c]
+* BatchNorm:    training mode, batch mean and biased variance over N, H, W,
+                eps = 1e-5, y = gamma * (x - mean) / sqrt(var + eps) + beta
+* ReLU:         y = max(x, 0); backward through the output: dx = dy * [y > 0]
+* max pool:     window max over valid taps; ties go to the first tap in
+                row-major window order; backward routes dy to that tap
+* global average pool over H, W
+* softmax cross-entropy, mean over the batch
+* SGD:          w -= lr g;  with momentum mu: v = mu v + g, w -= lr v
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+BN_EPS = 1e-5
+
+
+# ---------------------------------------------------------------- dense
+def linear_fwd(X, W, b):
+    return X @ W.T + b
+
+
+def linear_bwd_w(X, dY):
+    """dW = dY^T X, db = sum_n dY."""
+    return dY.T @ X, dY.sum(axis=0)
+
+
+def linear_bwd_x(W, dY):
+    """dX = dY W."""
+    return dY @ W
+
+
+# ---------------------------------------------------------------- conv
+def _out_size(h, k, stride, pad):
+    return (h + 2 * pad - k) // stride + 1
+
+
+def conv_fwd(X, Wt, stride, pad):
+    N, H, Wd, C = X.shape
+    K, R, S, C2 = Wt.shape
+    assert C == C2
+    P, Q = _out_size(H, R, stride, pad), _out_size(Wd, S, stride, pad)
+    Xp = np.pad(X, ((0, 0), (pad, pad), (pad, pad), (0, 0)))
+    Y = np.zeros((N, P, Q, K), dtype=X.dtype)
+    for r in range(R):
+        for s in range(S):
+            tap = Xp[:, r:r + stride * (P - 1) + 1:stride, s:s + stride * (Q - 1) + 1:stride, :]
+            Y += tap @ Wt[:, r, s, :].T
+    return Y
+
+
+def conv_bwd_x(Wt, dY, x_shape, stride, pad):
+    """dX: every output gradient is sent back through the tap that produced it."""
+    N, H, Wd, C = x_shape
+    K, R, S, _ = Wt.shape
+    _, P, Q, _ = dY.shape
+    dXp = np.zeros((N, H + 2 * pad, Wd + 2 * pad, C), dtype=dY.dtype)
+    for r in range(R):
+        for s in range(S):
+            dXp[:, r:r + stride * (P - 1) + 1:stride, s:s + stride * (Q - 1) + 1:stride, :] += \
+                dY @ Wt[:, r, s, :]
+    return dXp[:, pad:pad + H, pad:pad + Wd, :]
+
+
+def conv_bwd_w(X, dY, w_shape, stride, pad):
+    """dW[k,r,s,c] = sum_{n,p,q} dY[n,p,q,k] Xpad[n, p*st + r, q*st + s, c]."""
+    K, R, S, C = w_shape
+    _, P, Q, _ = dY.shape
+    Xp = np.pad(X, ((0, 0), (pad, pad), (pad, pad), (0, 0)))
+    dW = np.zeros(w_shape, dtype=dY.dtype)
+    for r in range(R):
+        for s in range(S):
+            tap = Xp[:, r:r + stride * (P - 1) + 1:stride, s:s + stride * (Q - 1) + 1:stride, :]
+            dW[:, r, s, :] = np.tensordot(dY, tap, axes=([0, 1, 2], [0, 1, 2]))
+    return dW
+
+
+# ---------------------------------------------------------------- BatchNorm
+def bn_fwd(X, gamma, beta):
+    """Returns (Y, mean, invstd); statistics over every axis but the channel (last) one."""
+    axes = tuple(range(X.ndim - 1))
+    mean = X.mean(axis=axes)
+    var = ((X - mean) ** 2).mean(axis=axes)
+    invstd = 1.0 / np.sqrt(var + BN_EPS)
+    xhat = (X - mean) * invstd
+    return gamma * xhat + beta, mean, invstd
+
+
+def bn_bwd(X, gamma, mean, invstd, dY):
+    """Returns (dX, dgamma, dbeta) of the training-mode normalisation."""
+    axes = tuple(range(X.ndim - 1))
+    m = X.size // X.shape[-1]
+    xhat = (X - mean) * invstd
+    dbeta = dY.sum(axis=axes)
+    dgamma = (dY * xhat).sum(axis=axes)
+    dX = gamma * invstd / m * (m * dY - dbeta - xhat * dgamma)
+    return dX, dgamma, dbeta
+
+
+# ---------------------------------------------------------------- ReLU
+def relu_fwd(X):
+    return np.maximum(X, 0)
+
+
+def relu_bwd(Y, dY):
+    return dY * (Y > 0)
+
+
+# ---------------------------------------------------------------- pooling
+def maxpool_fwd(X, k, stride, pad):
+    """Returns (Y, idx): idx = r*k + s of the first maximal valid tap (uint8)."""
+    N, H, Wd, C = X.shape
+    P, Q = _out_size(H, k, stride, pad), _out_size(Wd, k, stride, pad)
+    Y = np.full((N, P, Q, C), -np.inf, dtype=X.dtype)
+    idx = np.zeros((N, P, Q, C), dtype=np.uint8)
+    for p in range(P):
+        for q in range(Q):
+            for r in range(k):
+                for s in range(k):
+                    h, w = p * stride + r - pad, q * stride + s - pad
+                    if 0 <= h < H and 0 <= w < Wd:
+                        v = X[:, h, w, :]
+                        better = v > Y[:, p, q, :]
+                        Y[:, p, q, :] = np.where(better, v, Y[:, p, q, :])
+                        idx[:, p, q, :] = np.where(better, r * k + s, idx[:, p, q, :])
+    return Y, idx
+
+
+def maxpool_bwd(idx, dY, x_shape, k, stride, pad):
+    N, H, Wd, C = x_shape
+    _, P, Q, _ = dY.shape
+    dX = np.zeros(x_shape, dtype=dY.dtype)
+    for p in range(P):
+        for q in range(Q):
+            for r in range(k):
+                for s in range(k):
+                    h, w = p * stride + r - pad, q * stride + s - pad
+                    if 0 <= h < H and 0 <= w < Wd:
+                        dX[:, h, w, :] += np.where(idx[:, p, q, :] == r * k + s, dY[:, p, q, :], 0)
+    return dX
+
+
+def avgpool_fwd(X):
+    return X.mean(axis=(1, 2))
+
+
+def avgpool_bwd(dY, x_shape):
+    N, H, Wd, C = x_shape
+    return np.broadcast_to(dY[:, None, None, :] / (H * Wd), x_shape).copy()
+
+
+# ---------------------------------------------------------------- loss
+def softmax_ce(logits, labels):
+    """Returns (per-row losses, mean loss, dlogits) of the mean softmax cross-entropy."""
+    N = logits.shape[0]
+    z = logits - logits.max(axis=1, keepdims=True)
+    lse = np.log(np.exp(z).sum(axis=1))
+    rows = lse - z[np.arange(N), labels]
+    prob = np.exp(z - lse[:, None])
+    onehot = np.zeros_like(prob)
+    onehot[np.arange(N), labels] = 1.0
+    return rows, rows.mean(), (prob - onehot) / N
+
+
+# ---------------------------------------------------------------- update
+def sgd(w, g, lr):
+    return w - lr * g
+
+
+def sgd_momentum(w, g, v, lr, mu):
+    v_new = mu * v + g
+    return w - lr * v_new, v_new

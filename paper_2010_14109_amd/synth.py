@@ -1,0 +1,184 @@
+"""Seeded synthetic workloads: network descriptions and input/parameter bytes.
+
+This module is shared by the product path and by the CPU oracle, so it holds
+no part of the out-of-core method: no function sequence, no byte accounting,
+no scheduling, no layer arithmetic.  It only states *which* network is trained
+(layer kinds and their hyper-parameters, in topological order) and draws the
+random bytes fed to both sides:
+
+* data    -- ``numpy.random.Generator(PCG64(0))``: ``x`` as standard normal
+             float32, then the labels as ``integers(0, classes)`` (int32);
+* weights -- ``numpy.random.Generator(PCG64(1))``: He-normal fan-in for conv
+             and dense weights, zero biases, BatchNorm gamma = 1, beta = 0.
+
+Layouts are those of the library boundary: images are NHWC, conv weights are
+``[K, R, S, C]`` (output channel, filter row, filter column, input channel),
+dense weights are ``[out, in]``.
+
+The workloads stand in for the ones the paper trains (ResNet-50 on 224x224
+ImageNet batches, Section 5.1 and Table 1) plus smaller networks of the same
+layer kinds; ImageNet itself is not used.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+# --------------------------------------------------------------------------
+# network descriptions (plain data)
+# --------------------------------------------------------------------------
+
+
+def mlp(batch=256, width=1024, depth=8, classes=10, lr=0.01, momentum=0.0):
+    """``depth`` dense layers of ``width`` with ReLU between them, last one to ``classes``."""
+    layers = []
+    prev = "x"
+    for i in range(depth):
+        out = classes if i == depth - 1 else width
+        layers.append({"name": f"fc{i + 1}", "op": "linear", "in": [prev],
+                       "in_features": width, "out_features": out})
+        prev = f"fc{i + 1}"
+        if i != depth - 1:
+            layers.append({"name": f"relu{i + 1}", "op": "relu", "in": [prev]})
+            prev = f"relu{i + 1}"
+    return {"name": f"mlp{depth}_w{width}_b{batch}", "input": [batch, width],
+            "classes": classes, "layers": layers, "logits": prev,
+            "optimizer": {"lr": lr, "momentum": momentum}}
+
+
+def plain_cnn(batch=128, channels=64, depth=10, hw=32, in_ch=3, classes=10,
+              lr=0.01, momentum=0.0):
+    """``depth`` x [conv3x3 s1 p1 + BatchNorm + ReLU], global average pool, dense head."""
+    layers = []
+    prev = "x"
+    cin = in_ch
+    for i in range(depth):
+        layers.append({"name": f"conv{i + 1}", "op": "conv", "in": [prev], "cin": cin,
+                       "cout": channels, "k": 3, "stride": 1, "pad": 1})
+        layers.append({"name": f"bn{i + 1}", "op": "bn", "in": [f"conv{i + 1}"], "c": channels})
+        layers.append({"name": f"relu{i + 1}", "op": "relu", "in": [f"bn{i + 1}"]})
+        prev = f"relu{i + 1}"
+        cin = channels
+    layers.append({"name": "gap", "op": "avgpool", "in": [prev]})
+    layers.append({"name": "fc", "op": "linear", "in": ["gap"], "in_features": channels,
+                   "out_features": classes})
+    return {"name": f"cnn{depth}_c{channels}_b{batch}", "input": [batch, hw, hw, in_ch],
+            "classes": classes, "layers": layers, "logits": "fc",
+            "optimizer": {"lr": lr, "momentum": momentum}}
+
+
+def resnet(batch=256, hw=224, classes=1000, blocks=(3, 4, 6, 3), width=64,
+           lr=0.01, momentum=0.9):
+    """Bottleneck ResNet (ResNet-50 for blocks (3,4,6,3)); stride on the 3x3 conv."""
+    layers = []
+
+    def conv_bn(name, src, cin, cout, k, stride, pad, relu=True):
+        layers.append({"name": f"{name}.conv", "op": "conv", "in": [src], "cin": cin,
+                       "cout": cout, "k": k, "stride": stride, "pad": pad})
+        layers.append({"name": f"{name}.bn", "op": "bn", "in": [f"{name}.conv"], "c": cout})
+        if relu:
+            layers.append({"name": f"{name}.relu", "op": "relu", "in": [f"{name}.bn"]})
+            return f"{name}.relu"
+        return f"{name}.bn"
+
+    prev = conv_bn("stem", "x", 3, width, 7, 2, 3)
+    layers.append({"name": "stem.pool", "op": "maxpool", "in": [prev], "k": 3, "stride": 2,
+                   "pad": 1})
+    prev = "stem.pool"
+    cin = width
+    for stage, nblocks in enumerate(blocks):
+        mid = width * (2 ** stage)
+        cout = mid * 4
+        for b in range(nblocks):
+            stride = 2 if (b == 0 and stage > 0) else 1
+            base = f"s{stage + 1}b{b + 1}"
+            h = conv_bn(f"{base}.a", prev, cin, mid, 1, 1, 0)
+            h = conv_bn(f"{base}.b", h, mid, mid, 3, stride, 1)
+            h = conv_bn(f"{base}.c", h, mid, cout, 1, 1, 0, relu=False)
+            if b == 0:
+                sc = conv_bn(f"{base}.down", prev, cin, cout, 1, stride, 0, relu=False)
+            else:
+                sc = prev
+            layers.append({"name": f"{base}.add", "op": "add", "in": [h, sc]})
+            layers.append({"name": f"{base}.out", "op": "relu", "in": [f"{base}.add"]})
+            prev = f"{base}.out"
+            cin = cout
+    layers.append({"name": "gap", "op": "avgpool", "in": [prev]})
+    layers.append({"name": "fc", "op": "linear", "in": ["gap"], "in_features": cin,
+                   "out_features": classes})
+    depth = 2 + 3 * sum(blocks)
+    return {"name": f"resnet{depth}_b{batch}_{hw}", "input": [batch, hw, hw, 3],
+            "classes": classes, "layers": layers, "logits": "fc",
+            "optimizer": {"lr": lr, "momentum": momentum}}
+
+
+#: The five workloads: name -> (network description, budget as a fraction of
+#: the in-core peak).  Budget fractions follow the workload list of the build.
+WORKLOADS = {
+    "mlp": (lambda: mlp(), 0.40),
+    "cnn": (lambda: plain_cnn(), 0.50),
+    "resnet50_b256": (lambda: resnet(batch=256), 0.25),
+    "resnet50_b1440": (lambda: resnet(batch=1440), 1.0 / 7.5),
+}
+
+
+def workload(name, **overrides):
+    """Network description of a named workload, with keyword overrides (e.g. ``batch=8``)."""
+    builders = {"mlp": mlp, "cnn": plain_cnn, "resnet50_b256": resnet,
+                "resnet50_b1440": resnet}
+    defaults = {"resnet50_b256": {"batch": 256}, "resnet50_b1440": {"batch": 1440}}
+    kw = dict(defaults.get(name, {}))
+    kw.update(overrides)
+    return builders[name](**kw)
+
+
+def budget_fraction(name):
+    return WORKLOADS[name][1]
+
+
+# --------------------------------------------------------------------------
+# seeded bytes
+# --------------------------------------------------------------------------
+
+
+def param_shapes(spec):
+    """Parameter tensors of a network description, in layer order: ``[(name, shape)]``.
+
+    The shapes are read off the layer hyper-parameters only.
+    """
+    out = []
+    for L in spec["layers"]:
+        if L["op"] == "linear":
+            out.append((L["name"] + ".W", (L["out_features"], L["in_features"])))
+            out.append((L["name"] + ".b", (L["out_features"],)))
+        elif L["op"] == "conv":
+            out.append((L["name"] + ".W", (L["cout"], L["k"], L["k"], L["cin"])))
+        elif L["op"] == "bn":
+            out.append((L["name"] + ".gamma", (L["c"],)))
+            out.append((L["name"] + ".beta", (L["c"],)))
+    return out
+
+
+def make_inputs(spec, seed=0):
+    """``(x, labels)``: x float32 of the description's input shape, labels int32 [N]."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    x = g.standard_normal(size=tuple(spec["input"]), dtype=np.float32)
+    labels = g.integers(0, spec["classes"], size=spec["input"][0]).astype(np.int32)
+    return x, labels
+
+
+def make_params(spec, seed=1):
+    """Initial parameters ``{name: float32 array}`` (He-normal fan-in, zero bias, BN 1/0)."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    params = {}
+    for name, shape in param_shapes(spec):
+        kind = name.rsplit(".", 1)[1]
+        if kind == "W":
+            fan_in = int(np.prod(shape[1:]))
+            std = np.float32(np.sqrt(2.0 / fan_in))
+            params[name] = (g.standard_normal(size=shape, dtype=np.float32) * std).astype(np.float32)
+        elif kind == "gamma":
+            params[name] = np.ones(shape, np.float32)
+        else:  # bias or beta
+            params[name] = np.zeros(shape, np.float32)
+    return params

@@ -1,0 +1,312 @@
+"""Pins of the oracle scheduler against what the paper fixes (CPU only).
+
+* a hand-derived worked example of the procedure of Section 3 / Fig. 2;
+* the window definition of Section 3, recomputed by brute force;
+* an independent replayer (``oracle.check``): budget never exceeded, every
+  variable resident and current when a function runs, oldest swap-outs waited
+  first, final values written back;
+* the naive schedule of Section 1 as the zero-window limit;
+* the in-core limit (unbounded window and budget);
+* the feasibility boundary (the largest per-function footprint).
+"""
+
+import os
+import random
+from collections import Counter
+
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import check, naive, schedule as S
+from oracle.lower import lower, as_schedule_input
+from paper_2010_14109_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "window_schedule_4vars.txt")
+NAMES = {n: i for i, n in enumerate(S.OP_NAMES)}
+PH = {"PRE": S.PRE, "POST": S.POST, "END": S.END}
+
+
+def golden_case():
+    kinds = [S.INPUT, S.TEMP, S.TEMP, S.TEMP]
+    A, B, C, D = range(4)
+    fns = [[(A, S.R), (B, S.W)], [(B, S.R), (C, S.W)], [(C, S.R), (D, S.W)],
+           [(D, S.R), (C, S.R)], [(B, S.R)], [(A, S.R)]]
+    return [8] * 4, kinds, fns
+
+
+def parse_golden():
+    out = {}
+    cur = None
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if not line:
+                continue
+            t = line.split()
+            if t[0] == "windows":
+                out["windows"] = [int(x) for x in t[1:]]
+            elif t[0] == "policy":
+                cur = t[1]
+                out[cur] = {"ops": [], "held": []}
+            elif t[0] == "totals":
+                out[cur]["peak"], out[cur]["h2d"], out[cur]["d2h"] = int(t[2]), int(t[4]), int(t[6])
+            else:
+                fn, ph, op, var, held = t
+                out[cur]["ops"].append((int(fn) - 1, PH[ph], NAMES[op], "ABCD".index(var)))
+                out[cur]["held"].append(int(held))
+    return out
+
+
+@pytest.mark.parametrize("policy", ["C", "L"])
+def test_golden_worked_example(policy):
+    g = parse_golden()
+    b, k, f = golden_case()
+    out = S.build(b, k, f, budget=24, window=24, chunk=1, policy=policy)
+    assert out["windows"] == g["windows"]
+    assert out["ops"] == g[policy]["ops"]
+    assert out["held"] == g[policy]["held"]
+    assert (out["peak"], out["h2d"], out["d2h"]) == (g[policy]["peak"], g[policy]["h2d"],
+                                                      g[policy]["d2h"])
+    check.replay(b, k, f, out["ops"], 24, policy=policy, held=out["held"])
+
+
+# ---------------------------------------------------------------- registrations
+def random_registration(rng, nv=10, nf=14, maxsize=64):
+    kinds = [rng.choice([S.INPUT, S.PARAM, S.STATE, S.TEMP, S.TEMP, S.TEMP, S.OUTPUT])
+             for _ in range(nv)]
+    sizes = [rng.randint(1, maxsize) for _ in range(nv)]
+    produced = [k in (S.INPUT, S.PARAM, S.STATE) for k in kinds]
+    fns = []
+    for _ in range(nf):
+        vs = rng.sample(range(nv), rng.randint(1, min(4, nv)))
+        row = []
+        for v in vs:
+            if not produced[v]:
+                a = S.W
+            elif kinds[v] == S.INPUT:
+                a = S.R
+            else:
+                a = rng.choice([S.R, S.R, S.RW, S.W])
+            produced[v] = True
+            row.append((v, a))
+        fns.append(row)
+    return sizes, kinds, fns
+
+
+def small_networks():
+    return [
+        synth.mlp(batch=4, width=16, depth=4, classes=5),
+        synth.plain_cnn(batch=2, channels=4, depth=3, hw=8, classes=5),
+        synth.resnet(batch=2, hw=32, classes=7, blocks=(1, 2, 1, 1), width=4),
+        synth.resnet(batch=1, hw=32, classes=7, blocks=(1, 1, 1, 1), width=4, momentum=0.0),
+    ]
+
+
+def brute_window(seq, sizes, l, W):
+    best = l - 1
+    for r in range(l, len(seq)):
+        if sum(sizes[seq[p]] for p in range(l, r + 1)) <= W:
+            best = r
+    return best
+
+
+def test_windows_match_definition():
+    rng = random.Random(7)
+    for _ in range(40):
+        b, k, f = random_registration(rng)
+        W = rng.choice([0, 10, 40, 100, 400])
+        out = S.build(b, k, f, budget=10 ** 9, window=W)
+        fn = S.normalize(f)
+        seq, first, last = S.sequence(fn)
+        prev = -1
+        for i in range(len(fn)):
+            expect = max(brute_window(seq, b, first[i], W), last[i], prev)
+            assert out["windows"][i] == expect
+            prev = expect
+
+
+@pytest.mark.parametrize("policy", ["C", "L"])
+def test_random_schedules_replay(policy):
+    rng = random.Random(11 if policy == "C" else 12)
+    for _ in range(150):
+        b, k, f = random_registration(rng)
+        ws = S.working_set_max(b, f)
+        B = rng.randint(ws, ws * 3)
+        W = rng.choice([0, 16, 64, 256, S.INCORE])
+        out = S.build(b, k, f, budget=B, window=W, policy=policy)
+        res = check.replay(b, k, f, out["ops"], B, policy=policy, held=out["held"])
+        assert res["peak"] == out["peak"] <= B
+        assert (res["h2d"], res["d2h"]) == (out["h2d"], out["d2h"])
+
+
+def test_resident_set_is_window_plus_pending():
+    """Policy C: before f_i the device holds exactly the window's variables and the
+    pending swap-outs (nothing else, nothing missing)."""
+    rng = random.Random(3)
+    for _ in range(60):
+        b, k, f = random_registration(rng)
+        B = 10 ** 9  # no truncation
+        W = rng.choice([0, 16, 64, 256])
+        out = S.build(b, k, f, budget=B, window=W)
+        fn = S.normalize(f)
+        seq, first, _ = S.sequence(fn)
+        for i in range(len(fn)):
+            dev, pend = check.resident_before(f, out["ops"], i)
+            window_vars = set(seq[first[i]:out["windows"][i] + 1])
+            assert dev == window_vars
+            assert not (pend & dev)
+
+
+@pytest.mark.parametrize("spec", small_networks(), ids=lambda s: s["name"])
+@pytest.mark.parametrize("policy", ["C", "L"])
+def test_network_schedules_replay(spec, policy):
+    reg = lower(spec)
+    b, k, f = as_schedule_input(reg)
+    for chunk in (1, 256):
+        p = S.incore_peak(b, k, f, chunk)
+        ws = S.working_set_max(b, f, chunk)
+        for frac in (1.0, 0.75, 0.5, 0.4, 0.25, 1 / 7.5, 0.2, 0.0):
+            B = max(S.budget_for(frac, p, chunk), ws)
+            for W in (0, B // 8, B // 2, B, S.INCORE):
+                out = S.build(b, k, f, B, W, chunk, policy)
+                res = check.replay(b, k, f, out["ops"], B, chunk, policy, held=out["held"])
+                assert res["peak"] <= B
+
+
+def test_naive_schedule_is_zero_window_limit():
+    """Policy L with a zero window moves exactly what the naive swap-every-layer schedule
+    moves (Section 1), and it is feasible exactly from the largest footprint on."""
+    rng = random.Random(5)
+    cases = [random_registration(rng) for _ in range(60)]
+    cases += [as_schedule_input(lower(s)) for s in small_networks()]
+    for b, k, f in cases:
+        ws = naive.working_set(b, f)
+        out = S.build(b, k, f, budget=ws, window=0, policy="L")
+        got = Counter()
+        for (i, ph, kind, v) in out["ops"]:
+            if kind == S.SWAPIN:
+                got[("in", i, v)] += 1
+            elif kind == S.SWAPOUT:
+                got[("out", i, v)] += 1
+        assert got == naive.transfers(k, f)
+        with pytest.raises(S.Infeasible):
+            S.build(b, k, f, budget=ws - 1, window=0, policy="L")
+
+
+def test_zero_window_policy_c_swaps_after_every_use():
+    rng = random.Random(6)
+    for _ in range(40):
+        b, k, f = random_registration(rng)
+        out = S.build(b, k, f, budget=10 ** 9, window=0, policy="C")
+        fn = S.normalize(f)
+        seq, first, last = S.sequence(fn)
+        assert out["windows"] == last
+        outs = {(i, v) for (i, ph, kind, v) in out["ops"] if kind == S.SWAPOUT}
+        for i, vs in enumerate(fn):
+            for v, _ in vs:
+                later = any(v in [u for u, _ in fn[j]] for j in range(i + 1, len(fn)))
+                if later or k[v] in (S.PARAM, S.STATE, S.OUTPUT):
+                    assert (i, v) in outs
+
+
+def test_incore_limit():
+    """Unbounded window and budget: only the first loads and the final write-backs move,
+    and no swap-out is waited for before the end."""
+    rng = random.Random(8)
+    cases = [random_registration(rng) for _ in range(40)]
+    cases += [as_schedule_input(lower(s)) for s in small_networks()]
+    for b, k, f in cases:
+        B = sum(b)
+        out = S.build(b, k, f, budget=B, window=S.INCORE)
+        fn = S.normalize(f)
+        uses = {}
+        for i, vs in enumerate(fn):
+            for v, _ in vs:
+                uses.setdefault(v, []).append(i)
+        ins = [(i, v) for (i, ph, kind, v) in out["ops"] if kind == S.SWAPIN]
+        outs = [(i, v) for (i, ph, kind, v) in out["ops"] if kind == S.SWAPOUT]
+        assert sorted(v for _, v in ins) == sorted(v for v in uses if k[v] in S.PERSISTENT)
+        assert all(i == 0 for i, _ in ins)
+        assert sorted(outs) == sorted((uses[v][-1], v) for v in uses if k[v] in S.WRITE_BACK)
+        assert all(ph == S.END for (_, ph, kind, _) in out["ops"] if kind == S.WAIT_OUT)
+        assert not any(kind == S.CANCEL for (_, _, kind, _) in out["ops"])
+
+
+@pytest.mark.parametrize("spec", small_networks(), ids=lambda s: s["name"])
+def test_feasibility_boundary(spec):
+    b, k, f = as_schedule_input(lower(spec))
+    for chunk in (1, 64):
+        ws = S.working_set_max(b, f, chunk)
+        for W in (0, 1000, S.INCORE):
+            for policy in ("C", "L"):
+                out = S.build(b, k, f, ws, W, chunk, policy)
+                check.replay(b, k, f, out["ops"], ws, chunk, policy, held=out["held"])
+                with pytest.raises(S.Infeasible):
+                    S.build(b, k, f, ws - 1, W, chunk, policy)
+
+
+def test_invalid_registrations():
+    with pytest.raises(S.Invalid):   # TEMP read before written
+        S.build([4, 4], [S.INPUT, S.TEMP], [[(0, S.R), (1, S.R)]], 100, 100)
+    with pytest.raises(S.Invalid):   # INPUT written
+        S.build([4], [S.INPUT], [[(0, S.RW)]], 100, 100)
+    with pytest.raises(S.Invalid):   # unknown variable
+        S.build([4], [S.INPUT], [[(3, S.R)]], 100, 100)
+    with pytest.raises(S.Invalid):   # empty function
+        S.build([4], [S.INPUT], [[]], 100, 100)
+    with pytest.raises(S.Invalid):   # zero-byte variable
+        S.build([0], [S.INPUT], [[(0, S.R)]], 100, 100)
+
+
+# ---------------------------------------------------------------- the replayer catches mistakes
+def test_replayer_catches_planted_mistakes():
+    """Every plausible scheduler slip must be caught by the replayer."""
+    b, k, f = golden_case()
+    good = S.build(b, k, f, 24, 24)["ops"]
+    check.replay(b, k, f, good, 24)
+    mutants = []
+    # dropped swap-in
+    mutants.append([o for o in good if o != (0, S.PRE, S.SWAPIN, 0)])
+    # waits taken in the wrong order (newest first)
+    m = list(good)
+    m[good.index((2, S.PRE, S.WAIT_OUT, 0))] = (2, S.PRE, S.WAIT_OUT, 1)
+    mutants.append(m)
+    # a cancel replaced by a swap-in of a variable whose swap-out is still pending
+    m = list(good)
+    m[good.index((3, S.PRE, S.CANCEL, 2))] = (3, S.PRE, S.SWAPIN, 2)
+    mutants.append(m)
+    # a variable freed although used later
+    m = list(good)
+    m[good.index((1, S.POST, S.SWAPOUT, 1))] = (1, S.POST, S.FREE, 1)
+    mutants.append(m)
+    # budget too small for the same ops
+    for mt in mutants:
+        with pytest.raises(check.ScheduleError):
+            check.replay(b, k, f, mt, 24)
+    with pytest.raises(check.ScheduleError):
+        check.replay(b, k, f, good, 23)
+    # a PARAM whose update is never written back
+    kinds = [S.PARAM]
+    fns = [[(0, S.RW)]]
+    with pytest.raises(check.ScheduleError):
+        check.replay([4], kinds, fns, [(0, S.PRE, S.SWAPIN, 0), (0, S.POST, S.FREE, 0)], 8)
+
+
+# ---------------------------------------------------------------- fuzz
+@settings(max_examples=200, deadline=None)
+@given(seed=st.integers(0, 10 ** 9), nv=st.integers(1, 12), nf=st.integers(1, 20),
+       wsel=st.integers(0, 4), bsel=st.integers(0, 3), policy=st.sampled_from(["C", "L"]),
+       chunk=st.sampled_from([1, 8, 32]))
+def test_fuzz_chains_with_skips(seed, nv, nf, wsel, bsel, policy, chunk):
+    rng = random.Random(seed)
+    b, k, f = random_registration(rng, nv=nv, nf=nf)
+    ws = S.working_set_max(b, f, chunk)
+    B = [ws, ws + chunk, 2 * ws, 10 ** 9][bsel]
+    W = [0, 8, 64, 512, S.INCORE][wsel]
+    out = S.build(b, k, f, B, W, chunk, policy)
+    check.replay(b, k, f, out["ops"], B, chunk, policy, held=out["held"])
+    r = out["windows"]
+    fn = S.normalize(f)
+    _, first, last = S.sequence(fn)
+    assert all(r[i] >= last[i] for i in range(len(r)))
+    assert all(r[i] >= r[i - 1] for i in range(1, len(r)))
