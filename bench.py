@@ -1,0 +1,273 @@
+"""Benchmark of the out-of-core training step on one MI355X.
+
+Prints one JSON line: samples/s of the out-of-core step at the workload's
+budget (the value), the in-core step on the same data, host-link rates, the
+device bytes the pool owns, the roofline of the dominant kernel and the CPU
+oracle timed on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload cnn|mlp|resnet50_b256|resnet50_b1440]
+
+Inputs and parameters are seeded and synthetic (shapes of the workload).  In
+the out-of-core step the pinned host arena is the variables' home: the step
+swaps them in and out itself, and that traffic is the method's work, so it is
+inside the timed region.  The in-core step keeps everything in HBM.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+from paper_2010_14109_amd import netdef, ooc, synth
+
+PEAK_FP32_TFLOPS = 157.3       # MI355X dense fp32 (matrix and vector)
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PCIE5_X16_GBS = 63.0           # theoretical, per direction
+
+GEMM_OPS = {"linear_fwd", "linear_bwd_w", "linear_bwd_x", "conv_fwd", "conv_bwd_x", "conv_bwd_w"}
+
+
+def fn_work(op, attrs):
+    """Algorithmic work of one function: ('flop', n) for GEMM-shaped ops, ('byte', n) for
+    memory-bound ones (compulsory HBM bytes: every operand read once, every result
+    written once)."""
+    a = attrs
+    if op in ("linear_fwd", "linear_bwd_w", "linear_bwd_x"):
+        return "flop", 2 * a[0] * a[1] * a[2]
+    if op in ("conv_fwd", "conv_bwd_x", "conv_bwd_w"):
+        N, H, W, C, K, R, S, st, pd, P, Q = a[:11]
+        return "flop", 2 * N * P * Q * K * R * S * C
+    if op == "relu_fwd":
+        return "byte", 8 * a[0]
+    if op in ("relu_bwd", "add"):
+        return "byte", 12 * a[0]
+    if op == "bn_fwd":
+        return "byte", 8 * a[0] * a[1]
+    if op == "bn_bwd":
+        return "byte", 12 * a[0] * a[1]
+    if op == "maxpool_fwd":
+        N, H, W, C, k, st, pd, P, Q = a
+        return "byte", 4 * N * H * W * C + 5 * N * P * Q * C
+    if op == "maxpool_bwd":
+        N, H, W, C, k, st, pd, P, Q = a
+        return "byte", 5 * N * P * Q * C + 4 * N * H * W * C
+    if op in ("avgpool_fwd", "avgpool_bwd"):
+        N, H, W, C = a
+        return "byte", 4 * N * H * W * C + 4 * N * C
+    if op == "softmax_ce":
+        return "byte", 8 * a[0] * a[1]
+    return "byte", 0
+
+
+def sgd_bytes(net, j):
+    mom = net.fn_attrs[j][1]
+    total = 0
+    for v, acc in net.fn_vars[j]:
+        total += net.var_bytes[v] * (2 if acc == ooc.RW else 1)
+    return total if mom in (0, 1) else 0
+
+
+def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup):
+    ctx = ooc.Context(0)
+    try:
+        net.register(ctx)
+        ctx.set_chunk(chunk)
+        ctx.set_budget(budget)
+        if window is not None:
+            ctx.set_window(window)
+        ctx.build_schedule()
+        ctx.prepare()
+        net.view(ctx, "x")[...] = x
+        net.view(ctx, "labels")[...] = labels
+        for name in net.param_names():
+            net.view(ctx, name)[...] = params[name]
+        for name in net.names:
+            if name.startswith("m:"):
+                net.view(ctx, name)[...] = 0
+        ctx.upload()
+        lr, mu = spec["optimizer"]["lr"], spec["optimizer"]["momentum"]
+        for _ in range(warmup):
+            ctx.step(lr, mu)
+        # ooc_step returns after all three streams are synchronized
+        t0 = time.perf_counter()
+        loss = None
+        step_ms = []
+        for _ in range(steps):
+            s0 = time.perf_counter()
+            loss = ctx.step(lr, mu)
+            step_ms.append((time.perf_counter() - s0) * 1e3)
+        elapsed = time.perf_counter() - t0
+        return {"elapsed": elapsed, "loss": loss, "stats": ctx.stats(), "fn_ms": ctx.fn_times(),
+                "step_ms": step_ms}
+    finally:
+        ctx.close()
+
+
+def kernel_table(net, fn_ms):
+    table = {}
+    for j, (op, attrs) in enumerate(zip(net.fn_ops, net.fn_attrs)):
+        kind, work = fn_work(op, attrs)
+        if op == "sgd":
+            kind, work = "byte", sgd_bytes(net, j)
+        e = table.setdefault(op, {"ms": 0.0, "launches": 0, "unit": kind, "work": 0})
+        e["ms"] += fn_ms[j]
+        e["launches"] += 1
+        e["work"] += work
+    for op, e in table.items():
+        sec = e["ms"] / 1e3
+        if e["unit"] == "flop":
+            e["rate"] = e["work"] / sec / 1e12 if sec > 0 else 0.0
+            e["rate_unit"] = "TFLOP/s"
+        else:
+            e["rate"] = e["work"] / sec / 1e9 if sec > 0 else 0.0
+            e["rate_unit"] = "GB/s"
+    return table
+
+
+def cpu_baseline(name, budget_seconds=15.0):
+    """The float32 oracle step (``oracle.interp``) on a reduced batch of the same network."""
+    from oracle.interp import run as oracle_run
+    from oracle.lower import lower
+    small = {"mlp": 256, "cnn": 8, "resnet50_b256": 2, "resnet50_b1440": 2}[name]
+    spec = synth.workload(name, batch=small)
+    reg = lower(spec)
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001 - informational only
+        threads = len(os.sched_getaffinity(0))
+    oracle_run(reg, x, labels, params, dtype=np.float32)     # warm-up
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle_run(reg, x, labels, params, dtype=np.float32)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_seconds or n >= 50:
+            break
+    return {"value": n * small / el, "unit": "samples/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} float32 oracle steps of {spec['name']} (batch {small}) in "
+                      f"{el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="cnn", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--budget-frac", type=float, default=None)
+    ap.add_argument("--window-frac", type=float, default=0.5)
+    ap.add_argument("--chunk", type=int, default=2 << 20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-incore", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
+                                   "(multi-GPU sharding is described, not built)"}))
+        sys.exit(2)
+
+    spec = synth.workload(args.workload)
+    net = netdef.Net(spec)
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    chunk = args.chunk
+    frac = args.budget_frac if args.budget_frac is not None else synth.budget_fraction(args.workload)
+    hctx = ooc.Context(-1)
+    net.register(hctx)
+    hctx.set_chunk(chunk)
+    p_incore = hctx.incore_peak()
+    ws_max = hctx.working_set_max()
+    hctx.close()
+    budget = max(int(p_incore * frac) // chunk * chunk, ws_max)
+    window = int(budget * args.window_frac)
+    batch = spec["input"][0]
+
+    link = ooc.link_probe(0, 1 << 30, 3)
+    inc = None
+    if not args.no_incore:
+        inc = run_mode(net, spec, x, labels, params, ooc.UNLIMITED, None, chunk, args.steps,
+                       args.warmup)
+    out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps, args.warmup)
+    st = out["stats"]
+    ms = out["elapsed"] / args.steps * 1e3
+    value = batch * args.steps / out["elapsed"]
+    table = kernel_table(net, out["fn_ms"])
+    dom_op = max(table, key=lambda o: table[o]["ms"])
+    dom = table[dom_op]
+    if dom["unit"] == "flop":
+        roof = {"bound": "mfma", "achieved": round(dom["rate"], 3), "peak": PEAK_FP32_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(dom["rate"] / PEAK_FP32_TFLOPS, 4),
+                "traffic": None}
+    else:
+        roof = {"bound": "hbm", "achieved": round(dom["rate"], 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(dom["rate"] / PEAK_HBM_GBS, 4), "traffic": None}
+    roof["kernel"] = dom_op
+    roof["launches_per_step"] = dom["launches"]
+    roof["avg_launch_ms"] = round(dom["ms"] / max(1, dom["launches"]), 4)
+
+    step_s = out["elapsed"] / args.steps
+    moved = st["h2d_bytes"] + st["d2h_bytes"]
+    res = {
+        "metric": "samples/s at budget B as % of in-core; host-link GB/s; peak device bytes",
+        "value": round(value, 3),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded N(0,1) inputs, uniform labels, He-normal weights)",
+        "config": {"workload": spec["name"], "batch": batch, "budget_bytes": budget,
+                   "budget_frac_of_incore_peak": round(budget / p_incore, 4),
+                   "incore_peak_bytes": p_incore, "window_bytes": window, "chunk_bytes": chunk,
+                   "policy": "cancel"},
+        "roofline": roof,
+        "incore": None if inc is None else {
+            "samples_per_s": round(batch * args.steps / inc["elapsed"], 3),
+            "ms_per_step": round(inc["elapsed"] / args.steps * 1e3, 3),
+            "pool_bytes": inc["stats"]["pool_bytes"]},
+        "pct_of_incore": None if inc is None else round(100 * inc["elapsed"] / out["elapsed"], 2),
+        "host_link": {
+            "h2d_bytes_per_step": st["h2d_bytes"], "d2h_bytes_per_step": st["d2h_bytes"],
+            "sched_d2h_bytes_per_step": st["sched_d2h_bytes"],
+            "achieved_GBps": round(moved / step_s / 1e9, 2),
+            "h2d_busy_GBps": round(st["h2d_bytes"] / (st["h2d_busy_ms"] / 1e3) / 1e9, 2)
+            if st["h2d_busy_ms"] > 0 else None,
+            "d2h_busy_GBps": round(st["d2h_bytes"] / (st["d2h_busy_ms"] / 1e3) / 1e9, 2)
+            if st["d2h_busy_ms"] > 0 else None,
+            "h2d_busy_ms": round(st["h2d_busy_ms"], 2), "d2h_busy_ms": round(st["d2h_busy_ms"], 2),
+            "probe_GBps": {k: round(v, 2) for k, v in link.items()},
+            "pcie5_x16_theoretical_GBps_per_dir": PCIE5_X16_GBS,
+            "link_bound_ms": round(max(st["h2d_bytes"] / link["h2d"],
+                                       st["d2h_bytes"] / link["d2h"],
+                                       moved / link["both"]) / 1e6, 2),
+        },
+        "peak_device_bytes": {"pool": st["pool_bytes"], "max_chunks_in_use_bytes":
+                              st["max_chunks_used"] * chunk, "peak_accounted": st["peak_accounted"],
+                              "hipMemGetInfo_delta": st["device_bytes_delta"],
+                              "budget": budget},
+        "compute_busy_ms_per_step": round(st["compute_busy_ms"], 2),
+        "loss": out["loss"],
+        "kernels": {op: {"ms": round(e["ms"], 3), "launches": e["launches"],
+                         "rate": round(e["rate"], 3), "unit": e["rate_unit"]}
+                    for op, e in sorted(table.items(), key=lambda kv: -kv[1]["ms"])},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(args.workload)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

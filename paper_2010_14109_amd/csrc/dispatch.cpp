@@ -1,0 +1,72 @@
+// Maps a registered function to its kernel launches.  Shapes come from the
+// attributes, which ooc_add_fn has checked against every variable's size.
+#include "kernels.h"
+
+namespace ooc {
+
+hipError_t launch_fn(const Fn& fn, void* const* p, const uint64_t* bytes, float lr, float mu,
+                     hipStream_t s) {
+  const auto& a = fn.attrs;
+  auto F = [&](int j) { return static_cast<float*>(p[j]); };
+  auto conv = [&]() {
+    return ConvShape{a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7], a[8], a[9], a[10]};
+  };
+  auto pool = [&]() { return PoolShape{a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7], a[8]}; };
+  switch (fn.op) {
+    case OOC_OP_NOOP:
+      return hipSuccess;
+    case OOC_OP_LINEAR_FWD:
+      return linear_fwd(F(0), F(1), F(2), F(3), a[0], a[1], a[2], s);
+    case OOC_OP_LINEAR_BWD_W:
+      return linear_bwd_w(F(0), F(1), F(2), F(3), a[0], a[1], a[2], s);
+    case OOC_OP_LINEAR_BWD_X:
+      return linear_bwd_x(F(0), F(1), F(2), a[0], a[1], a[2], s);
+    case OOC_OP_RELU_FWD:
+      return relu_fwd(F(0), F(1), a[0], s);
+    case OOC_OP_RELU_BWD:
+      return relu_bwd(F(0), F(1), F(2), a[0], s);
+    case OOC_OP_ADD:
+      return add(F(0), F(1), F(2), a[0], s);
+    case OOC_OP_SOFTMAX_CE:
+      return softmax_ce(F(0), static_cast<const int32_t*>(p[1]), F(2), F(3), a[0], a[1], s);
+    case OOC_OP_SGD: {
+      const int per = a[1] ? 3 : 2;
+      for (int64_t k = 0; k < a[0]; ++k) {
+        const int j = (int)(k * per);
+        hipError_t e = sgd(F(j), F(j + 1), a[1] ? F(j + 2) : nullptr, (int64_t)(bytes[j] / 4), lr,
+                           mu, s);
+        if (e != hipSuccess) return e;
+      }
+      return hipSuccess;
+    }
+    case OOC_OP_MIX: {
+      const int n = (int)fn.vars.size();
+      uint64_t words[64];
+      if (n > 64) return hipErrorInvalidValue;
+      for (int j = 0; j < n; ++j) words[j] = bytes[j] / 4;
+      return mix(p, words, n, (uint32_t)a[0], s, (fn.vars[n - 1].access & OOC_R) != 0);
+    }
+    case OOC_OP_CONV_FWD:
+      return conv_fwd(F(0), F(1), F(2), conv(), s);
+    case OOC_OP_CONV_BWD_X:
+      return conv_bwd_x(F(0), F(1), F(2), conv(), s);
+    case OOC_OP_CONV_BWD_W:
+      return conv_bwd_w(F(0), F(1), F(2), a[11] > 1 ? F(3) : nullptr, a[11], conv(), s);
+    case OOC_OP_BN_FWD:
+      return bn_fwd(F(0), F(1), F(2), F(3), F(4), a[0], a[1], a[2], s);
+    case OOC_OP_BN_BWD:
+      return bn_bwd(F(0), F(1), F(2), F(3), F(4), F(5), F(6), a[0], a[1], a[2], s);
+    case OOC_OP_MAXPOOL_FWD:
+      return maxpool_fwd(F(0), F(1), static_cast<uint8_t*>(p[2]), pool(), s);
+    case OOC_OP_MAXPOOL_BWD:
+      return maxpool_bwd(static_cast<const uint8_t*>(p[0]), F(1), F(2), pool(), s);
+    case OOC_OP_AVGPOOL_FWD:
+      return avgpool_fwd(F(0), F(1), a[0], a[1] * a[2], a[3], s);
+    case OOC_OP_AVGPOOL_BWD:
+      return avgpool_bwd(F(0), F(1), a[0], a[1] * a[2], a[3], s);
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace ooc

@@ -1,0 +1,509 @@
+// Executor: builds the virtual-address pool and the pinned host arena, turns
+// the schedule into a stream program, and runs one training step.
+//
+// Pool (Section 4).  The pool owns exactly as many physical chunks of m_c
+// bytes as the plan ever has in use (never more than budget / m_c).  Every
+// residency interval -- one device copy of one variable -- gets its own
+// contiguous virtual range, onto which its chunks are mapped in plan order.
+// The schedule is fixed, so all ranges are reserved and mapped once, here;
+// a step only looks up addresses.  A chunk may therefore be mapped at several
+// virtual addresses, one per interval that uses it at some time.
+//
+// Streams.  Kernels run on the compute stream; swap-ins on the h2d stream,
+// swap-outs on the d2h stream.  Events order them:
+//  * a kernel waits for the swap-in of each variable it reads;
+//  * a swap-out waits for the function after which it was reserved;
+//  * whoever first writes an interval (its swap-in copy, or the first kernel
+//    using an allocated one) waits until every interval that used the same
+//    chunks before is released: its last kernel finished and its last
+//    swap-out copy completed (the device-side meaning of step (b), "wait for
+//    the swap-out right before f_i");
+//  * a swap-in waits for the last swap-out copy into the same host slot.
+// Two kinds of swap-out need no copy and are not issued: one that is later
+// cancelled (its host copy is never read: the variable is kept on the device
+// and any later swap-out writes a newer copy) and one of a variable whose
+// host copy is still current (not written since it was swapped in).
+#include <algorithm>
+#include <chrono>
+#include <cstring>
+#include <set>
+
+#include "ctx.h"
+#include "kernels.h"
+
+namespace ooc {
+
+static const uint64_t kSlotAlign = 4096;
+
+#define HIPCK(call)                                                               \
+  do {                                                                            \
+    hipError_t e_ = (call);                                                       \
+    if (e_ != hipSuccess) {                                                       \
+      ctx->err = std::string(#call) + " failed: " + hipGetErrorString(e_);        \
+      return OOC_E_DEVICE;                                                        \
+    }                                                                             \
+  } while (0)
+
+void release_device(ooc_ctx* ctx) {
+  if (ctx->device < 0) return;
+  hipSetDevice(ctx->device);
+  if (ctx->cs) hipStreamSynchronize(ctx->cs);
+  if (ctx->hs) hipStreamSynchronize(ctx->hs);
+  if (ctx->ds) hipStreamSynchronize(ctx->ds);
+  for (hipEvent_t e : ctx->events) hipEventDestroy(e);
+  ctx->events.clear();
+  if (ctx->cs) hipStreamDestroy(ctx->cs);
+  if (ctx->hs) hipStreamDestroy(ctx->hs);
+  if (ctx->ds) hipStreamDestroy(ctx->ds);
+  ctx->cs = ctx->hs = ctx->ds = nullptr;
+  if (ctx->va_base) {
+    hipMemUnmap(ctx->va_base, ctx->va_bytes);
+    hipMemAddressFree(ctx->va_base, ctx->va_bytes);
+    ctx->va_base = nullptr;
+  }
+  for (auto h : ctx->chunks) hipMemRelease(h);
+  ctx->chunks.clear();
+  if (ctx->arena) hipHostFree(ctx->arena);
+  ctx->arena = nullptr;
+}
+
+static int32_t new_event(ooc_ctx* ctx, int8_t stream) {
+  ctx->event_stream.push_back(stream);
+  return (int32_t)ctx->event_stream.size() - 1;
+}
+
+// Turns the schedule and the chunk plan into per-function stream programs.
+static ooc_status compile(ooc_ctx* ctx) {
+  const auto& ops = ctx->sched.ops;
+  const auto& plan = ctx->plan;
+  const int64_t N = (int64_t)ctx->fns.size();
+  const int64_t NI = (int64_t)plan.intervals.size();
+  const int64_t nv = (int64_t)ctx->vars.size();
+  ctx->prog.assign(N, FnProgram{});
+  ctx->event_stream.clear();
+  ctx->ev_begin = new_event(ctx, 0);
+  for (int64_t i = 0; i < N; ++i) {
+    ctx->prog[i].ev_pre = new_event(ctx, 0);
+    ctx->prog[i].ev_fn = new_event(ctx, 0);
+  }
+  ctx->ev_end = new_event(ctx, 0);
+
+  // swap-outs that a later CANCEL undoes
+  std::vector<uint8_t> cancelled(ops.size(), 0);
+  {
+    std::vector<int64_t> pend_op(nv, -1);
+    for (int64_t k = 0; k < (int64_t)ops.size(); ++k) {
+      if (ops[k].kind == OOC_SWAPOUT) pend_op[ops[k].var] = k;
+      if (ops[k].kind == OOC_CANCEL && pend_op[ops[k].var] >= 0) {
+        cancelled[pend_op[ops[k].var]] = 1;
+        pend_op[ops[k].var] = -1;
+      }
+      if (ops[k].kind == OOC_WAIT_OUT) pend_op[ops[k].var] = -1;
+    }
+  }
+
+  std::vector<int64_t> working(nv, -1);
+  std::vector<uint8_t> acquired(NI, 0), host_valid(nv, 0);
+  std::vector<int64_t> last_fn(NI, -1), last_d2h(NI, -1), in_ev(NI, -1), var_d2h(nv, -1);
+  std::vector<std::vector<int32_t>> release(NI), preds(NI);
+  std::vector<int64_t> owner(plan.n_chunks, -1);
+  for (int64_t v = 0; v < nv; ++v)
+    host_valid[v] = ctx->vars[v].kind == OOC_INPUT || ctx->vars[v].kind == OOC_PARAM ||
+                    ctx->vars[v].kind == OOC_STATE;
+
+  auto opened = [&](int64_t J) {
+    std::set<int64_t> ps;
+    for (int32_t c : plan.intervals[J].chunks) {
+      if (owner[c] >= 0) ps.insert(owner[c]);
+      owner[c] = J;
+    }
+    for (int64_t p : ps)
+      for (int32_t e : release[p]) preds[J].push_back(e);
+  };
+  auto closed = [&](int64_t J) {
+    release[J].clear();
+    if (last_fn[J] >= 0) release[J].push_back(ctx->prog[last_fn[J]].ev_fn);
+    if (last_d2h[J] >= 0) release[J].push_back((int32_t)last_d2h[J]);
+  };
+  auto add_waits = [&](std::vector<int32_t>* w, const std::vector<int32_t>& evs, int8_t stream) {
+    for (int32_t e : evs)
+      if (ctx->event_stream[e] != stream) w->push_back(e);
+  };
+  // in-core mode: persistent variables are resident from the start
+  ctx->resident.assign(nv, -1);
+  for (int64_t J = 0; J < NI; ++J)
+    if (plan.intervals[J].open < 0) {
+      opened(J);
+      acquired[J] = 1;
+      working[plan.intervals[J].var] = J;
+      ctx->resident[plan.intervals[J].var] = J;
+    }
+
+  ctx->prog_h2d = ctx->prog_d2h = 0;
+  int64_t k = 0;
+  const int64_t K = (int64_t)ops.size();
+  for (int64_t i = 0; i <= N; ++i) {
+    // PRE ops of f_i (END ops when i == N)
+    while (k < K && ops[k].fn == i && ops[k].phase != OOC_POST) {
+      const Op& o = ops[k];
+      const int64_t J = plan.op_interval[k];
+      switch (o.kind) {
+        case OOC_SWAPIN: {
+          opened(J);
+          working[o.var] = J;
+          Copy c{ctx->iv_ptr[J], ctx->host_slot[o.var], ctx->vars[o.var].bytes, {}, 0, 0};
+          add_waits(&c.waits, preds[J], 1);
+          if (var_d2h[o.var] >= 0) add_waits(&c.waits, {(int32_t)var_d2h[o.var]}, 1);
+          c.ev_start = new_event(ctx, 1);
+          c.ev_done = new_event(ctx, 1);
+          in_ev[J] = c.ev_done;
+          ctx->prog_h2d += c.bytes;
+          ctx->prog[i].h2d.push_back(std::move(c));
+          break;
+        }
+        case OOC_ALLOC:
+          opened(J);
+          working[o.var] = J;
+          break;
+        case OOC_CANCEL:
+          working[o.var] = J;
+          break;
+        case OOC_WAIT_OUT:
+        case OOC_FREE:
+          closed(J);
+          break;
+      }
+      ++k;
+    }
+    if (i == N) break;
+    // f_i's kernels
+    FnProgram& fp = ctx->prog[i];
+    for (const FnVar& fv : ctx->fns[i].vars) {
+      const int64_t J = working[fv.var];
+      if (J < 0) {
+        ctx->err = "schedule leaves variable " + std::to_string(fv.var) + " of function " +
+                   std::to_string(i) + " off the device";
+        return OOC_E_INVALID;
+      }
+      if (!acquired[J]) {
+        if (in_ev[J] >= 0)
+          add_waits(&fp.cwaits, {(int32_t)in_ev[J]}, 0);
+        else
+          add_waits(&fp.cwaits, preds[J], 0);
+        acquired[J] = 1;
+      }
+      fp.ptrs.push_back(ctx->iv_ptr[J]);
+      fp.sizes.push_back(ctx->vars[fv.var].bytes);
+      last_fn[J] = i;
+      if (fv.access & OOC_W) host_valid[fv.var] = 0;
+    }
+    // POST ops of f_i
+    while (k < K && ops[k].fn == i && ops[k].phase == OOC_POST) {
+      const Op& o = ops[k];
+      const int64_t J = plan.op_interval[k];
+      if (o.kind == OOC_SWAPOUT) {
+        working[o.var] = -1;
+        if (!cancelled[k] && !host_valid[o.var]) {
+          Copy c{ctx->host_slot[o.var], ctx->iv_ptr[J], ctx->vars[o.var].bytes, {}, 0, 0};
+          c.waits.push_back(fp.ev_fn);
+          c.ev_start = new_event(ctx, 2);
+          c.ev_done = new_event(ctx, 2);
+          last_d2h[J] = c.ev_done;
+          var_d2h[o.var] = c.ev_done;
+          host_valid[o.var] = 1;
+          ctx->prog_d2h += c.bytes;
+          fp.d2h.push_back(std::move(c));
+        }
+      } else if (o.kind == OOC_FREE) {
+        working[o.var] = -1;
+        closed(J);
+      }
+      ++k;
+    }
+  }
+  return OOC_OK;
+}
+
+ooc_status prepare(ooc_ctx* ctx) {
+  auto t0 = std::chrono::steady_clock::now();
+  HIPCK(hipSetDevice(ctx->device));
+  hipMemAllocationProp prop = {};
+  prop.type = hipMemAllocationTypePinned;
+  prop.location.type = hipMemLocationTypeDevice;
+  prop.location.id = ctx->device;
+  size_t gran = 0;
+  HIPCK(hipMemGetAllocationGranularity(&gran, &prop, hipMemAllocationGranularityMinimum));
+  if (gran == 0 || ctx->chunk % gran != 0) {
+    ctx->err = "chunk size " + std::to_string(ctx->chunk) +
+               " is not a multiple of the allocation granularity " + std::to_string(gran);
+    return OOC_E_INVALID;
+  }
+  size_t free0 = 0, total0 = 0, free1 = 0, total1 = 0;
+  HIPCK(hipMemGetInfo(&free0, &total0));
+
+  // physical chunks
+  const Plan& plan = ctx->plan;
+  ctx->chunks.resize(plan.n_chunks);
+  for (uint64_t c = 0; c < plan.n_chunks; ++c) {
+    hipError_t e = hipMemCreate(&ctx->chunks[c], ctx->chunk, &prop, 0);
+    if (e != hipSuccess) {
+      ctx->chunks.resize(c);
+      ctx->err = "hipMemCreate of chunk " + std::to_string(c) + " failed: " +
+                 hipGetErrorString(e);
+      return OOC_E_DEVICE;
+    }
+  }
+  // one virtual range per interval, carved out of one reservation
+  const int64_t NI = (int64_t)plan.intervals.size();
+  uint64_t total = 0;
+  std::vector<uint64_t> off(NI);
+  for (int64_t J = 0; J < NI; ++J) {
+    off[J] = total;
+    total += plan.intervals[J].chunks.size() * ctx->chunk;
+  }
+  ctx->iv_ptr.assign(NI, nullptr);
+  if (total > 0) {
+    HIPCK(hipMemAddressReserve(&ctx->va_base, total, ctx->chunk, nullptr, 0));
+    ctx->va_bytes = total;
+    uint64_t maps = 0;
+    for (int64_t J = 0; J < NI; ++J) {
+      char* base = (char*)ctx->va_base + off[J];
+      ctx->iv_ptr[J] = base;
+      const auto& cs = plan.intervals[J].chunks;
+      for (size_t j = 0; j < cs.size(); ++j) {
+        HIPCK(hipMemMap(base + j * ctx->chunk, ctx->chunk, 0, ctx->chunks[cs[j]], 0));
+        ++maps;
+      }
+    }
+    hipMemAccessDesc ad = {};
+    ad.location.type = hipMemLocationTypeDevice;
+    ad.location.id = ctx->device;
+    ad.flags = hipMemAccessFlagsProtReadWrite;
+    HIPCK(hipMemSetAccess(ctx->va_base, total, &ad, 1));
+    ctx->stats.n_mappings = maps;
+  }
+  HIPCK(hipMemGetInfo(&free1, &total1));
+
+  // pinned host arena: every persistent variable, and every TEMP that is
+  // ever swapped out (it may be copied back later)
+  const int64_t nv = (int64_t)ctx->vars.size();
+  std::vector<uint8_t> backed(nv, 0);
+  for (int64_t v = 0; v < nv; ++v) backed[v] = ctx->vars[v].kind != OOC_TEMP;
+  for (const Op& o : ctx->sched.ops)
+    if (o.kind == OOC_SWAPOUT || o.kind == OOC_SWAPIN) backed[o.var] = 1;
+  uint64_t hb = 0;
+  std::vector<uint64_t> hoff(nv, 0);
+  for (int64_t v = 0; v < nv; ++v)
+    if (backed[v]) {
+      hoff[v] = hb;
+      hb += round_up(ctx->vars[v].bytes, kSlotAlign);
+    }
+  ctx->host_slot.assign(nv, nullptr);
+  if (hb > 0) {
+    hipError_t e = hipHostMalloc((void**)&ctx->arena, hb, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      ctx->arena = nullptr;
+      ctx->err = "pinned host arena of " + std::to_string(hb) + " bytes: " + hipGetErrorString(e);
+      return OOC_E_HOST_OOM;
+    }
+    ctx->arena_bytes = hb;
+    for (int64_t v = 0; v < nv; ++v)
+      if (backed[v]) ctx->host_slot[v] = ctx->arena + hoff[v];
+  }
+
+  HIPCK(hipStreamCreateWithFlags(&ctx->cs, hipStreamNonBlocking));
+  HIPCK(hipStreamCreateWithFlags(&ctx->hs, hipStreamNonBlocking));
+  HIPCK(hipStreamCreateWithFlags(&ctx->ds, hipStreamNonBlocking));
+
+  {
+    ooc_status s = compile(ctx);
+    if (s) return s;
+  }
+  ctx->events.resize(ctx->event_stream.size(), nullptr);
+  for (size_t j = 0; j < ctx->events.size(); ++j) {
+    hipError_t e = hipEventCreate(&ctx->events[j]);
+    if (e != hipSuccess) {
+      ctx->events.resize(j);
+      ctx->err = std::string("hipEventCreate failed: ") + hipGetErrorString(e);
+      return OOC_E_DEVICE;
+    }
+  }
+  for (int64_t i = (int64_t)ctx->fns.size() - 1; i >= 0; --i)
+    if (ctx->fns[i].op == OOC_OP_SOFTMAX_CE) {
+      ctx->loss_var = ctx->fns[i].vars[2].var;
+      break;
+    }
+
+  auto t1 = std::chrono::steady_clock::now();
+  ooc_stats& st = ctx->stats;
+  st.pool_chunks = plan.n_chunks;
+  st.pool_bytes = plan.n_chunks * ctx->chunk;
+  st.max_chunks_used = plan.max_chunks_used;
+  st.device_bytes_delta = free0 > free1 ? (uint64_t)(free0 - free1) : 0;
+  st.host_bytes = hb;
+  st.n_intervals = (uint64_t)NI;
+  st.prepare_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
+  return OOC_OK;
+}
+
+static ooc_status enqueue_copy(ooc_ctx* ctx, const Copy& c, hipStream_t s, hipMemcpyKind kind) {
+  for (int32_t w : c.waits) HIPCK(hipStreamWaitEvent(s, ctx->events[w], 0));
+  HIPCK(hipEventRecord(ctx->events[c.ev_start], s));
+  HIPCK(hipMemcpyAsync(c.dst, c.src, c.bytes, kind, s));
+  HIPCK(hipEventRecord(ctx->events[c.ev_done], s));
+  return OOC_OK;
+}
+
+ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out) {
+  HIPCK(hipSetDevice(ctx->device));
+  auto t0 = std::chrono::steady_clock::now();
+  hipStream_t cs = ctx->cs;
+  HIPCK(hipEventRecord(ctx->events[ctx->ev_begin], cs));
+  const int64_t N = (int64_t)ctx->fns.size();
+  for (int64_t i = 0; i < N; ++i) {
+    const FnProgram& fp = ctx->prog[i];
+    for (const Copy& c : fp.h2d) {
+      ooc_status s = enqueue_copy(ctx, c, ctx->hs, hipMemcpyHostToDevice);
+      if (s) return s;
+    }
+    for (int32_t w : fp.cwaits) HIPCK(hipStreamWaitEvent(cs, ctx->events[w], 0));
+    HIPCK(hipEventRecord(ctx->events[fp.ev_pre], cs));
+    hipError_t e = launch_fn(ctx->fns[i], fp.ptrs.data(), fp.sizes.data(), lr, mu, cs);
+    if (e != hipSuccess) {
+      ctx->err = "kernel launch of function " + std::to_string(i) + " failed: " +
+                 hipGetErrorString(e);
+      return OOC_E_DEVICE;
+    }
+    HIPCK(hipEventRecord(ctx->events[fp.ev_fn], cs));
+    for (const Copy& c : fp.d2h) {
+      ooc_status s = enqueue_copy(ctx, c, ctx->ds, hipMemcpyDeviceToHost);
+      if (s) return s;
+    }
+  }
+  HIPCK(hipEventRecord(ctx->events[ctx->ev_end], cs));
+  HIPCK(hipStreamSynchronize(cs));
+  HIPCK(hipStreamSynchronize(ctx->hs));
+  HIPCK(hipStreamSynchronize(ctx->ds));
+  auto t1 = std::chrono::steady_clock::now();
+
+  ooc_stats& st = ctx->stats;
+  st.step_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
+  float ms = 0;
+  HIPCK(hipEventElapsedTime(&ms, ctx->events[ctx->ev_begin], ctx->events[ctx->ev_end]));
+  st.step_gpu_ms = ms;
+  double hbusy = 0, dbusy = 0, cbusy = 0;
+  ctx->fn_ms.assign(N, 0.0);
+  for (int64_t i = 0; i < N; ++i) {
+    const FnProgram& fp = ctx->prog[i];
+    for (const Copy& c : fp.h2d) {
+      HIPCK(hipEventElapsedTime(&ms, ctx->events[c.ev_start], ctx->events[c.ev_done]));
+      hbusy += ms;
+    }
+    for (const Copy& c : fp.d2h) {
+      HIPCK(hipEventElapsedTime(&ms, ctx->events[c.ev_start], ctx->events[c.ev_done]));
+      dbusy += ms;
+    }
+    HIPCK(hipEventElapsedTime(&ms, ctx->events[fp.ev_pre], ctx->events[fp.ev_fn]));
+    cbusy += ms;
+    ctx->fn_ms[i] = ms;
+  }
+  st.h2d_busy_ms = hbusy;
+  st.d2h_busy_ms = dbusy;
+  st.compute_busy_ms = cbusy;
+  st.h2d_bytes = ctx->prog_h2d;
+  st.d2h_bytes = ctx->prog_d2h;
+
+  if (loss_out) {
+    float loss = __builtin_nanf("");
+    if (ctx->loss_var >= 0) {
+      const uint64_t b = ctx->vars[ctx->loss_var].bytes;
+      if (ctx->incore) {
+        const char* d = ctx->iv_ptr[ctx->resident[ctx->loss_var]];
+        HIPCK(hipMemcpy(&loss, d + b - 4, 4, hipMemcpyDeviceToHost));
+      } else {
+        std::memcpy(&loss, ctx->host_slot[ctx->loss_var] + b - 4, 4);
+      }
+    }
+    *loss_out = loss;
+  }
+  return OOC_OK;
+}
+
+ooc_status transfer_resident(ooc_ctx* ctx, bool to_device) {
+  if (!ctx->incore) return OOC_OK;
+  HIPCK(hipSetDevice(ctx->device));
+  for (int64_t v = 0; v < (int64_t)ctx->vars.size(); ++v) {
+    const int32_t kind = ctx->vars[v].kind;
+    if (kind == OOC_TEMP || ctx->resident[v] < 0) continue;
+    char* d = ctx->iv_ptr[ctx->resident[v]];
+    if (to_device && (kind == OOC_INPUT || kind == OOC_PARAM || kind == OOC_STATE))
+      HIPCK(hipMemcpy(d, ctx->host_slot[v], ctx->vars[v].bytes, hipMemcpyHostToDevice));
+    if (!to_device && kind != OOC_INPUT)
+      HIPCK(hipMemcpy(ctx->host_slot[v], d, ctx->vars[v].bytes, hipMemcpyDeviceToHost));
+  }
+  HIPCK(hipDeviceSynchronize());
+  return OOC_OK;
+}
+
+ooc_status link_probe(int32_t device, uint64_t bytes, int32_t reps, double* h2d, double* d2h,
+                      double* both, std::string* err) {
+  ooc_ctx dummy;
+  ooc_ctx* ctx = &dummy;
+  void *hp1 = nullptr, *hp2 = nullptr, *d1 = nullptr, *d2 = nullptr;
+  hipStream_t s1 = nullptr, s2 = nullptr;
+  hipEvent_t e[4] = {};
+  ooc_status st = OOC_OK;
+  auto run = [&]() -> ooc_status {
+    HIPCK(hipSetDevice(device));
+    HIPCK(hipHostMalloc(&hp1, bytes, hipHostMallocDefault));
+    HIPCK(hipHostMalloc(&hp2, bytes, hipHostMallocDefault));
+    HIPCK(hipMalloc(&d1, bytes));
+    HIPCK(hipMalloc(&d2, bytes));
+    std::memset(hp1, 1, bytes);
+    std::memset(hp2, 2, bytes);
+    HIPCK(hipStreamCreateWithFlags(&s1, hipStreamNonBlocking));
+    HIPCK(hipStreamCreateWithFlags(&s2, hipStreamNonBlocking));
+    for (auto& x : e) HIPCK(hipEventCreate(&x));
+    double bh = 0, bd = 0, bb = 0;
+    for (int r = 0; r < reps; ++r) {
+      float ms = 0;
+      HIPCK(hipEventRecord(e[0], s1));
+      HIPCK(hipMemcpyAsync(d1, hp1, bytes, hipMemcpyHostToDevice, s1));
+      HIPCK(hipEventRecord(e[1], s1));
+      HIPCK(hipEventSynchronize(e[1]));
+      HIPCK(hipEventElapsedTime(&ms, e[0], e[1]));
+      bh = std::max(bh, bytes / (ms * 1e6));
+      HIPCK(hipEventRecord(e[0], s2));
+      HIPCK(hipMemcpyAsync(hp2, d2, bytes, hipMemcpyDeviceToHost, s2));
+      HIPCK(hipEventRecord(e[1], s2));
+      HIPCK(hipEventSynchronize(e[1]));
+      HIPCK(hipEventElapsedTime(&ms, e[0], e[1]));
+      bd = std::max(bd, bytes / (ms * 1e6));
+      HIPCK(hipDeviceSynchronize());
+      auto t0 = std::chrono::steady_clock::now();
+      HIPCK(hipMemcpyAsync(d1, hp1, bytes, hipMemcpyHostToDevice, s1));
+      HIPCK(hipMemcpyAsync(hp2, d2, bytes, hipMemcpyDeviceToHost, s2));
+      HIPCK(hipStreamSynchronize(s1));
+      HIPCK(hipStreamSynchronize(s2));
+      auto t1 = std::chrono::steady_clock::now();
+      bb = std::max(bb, 2.0 * bytes / (std::chrono::duration<double>(t1 - t0).count() * 1e9));
+    }
+    *h2d = bh;
+    *d2h = bd;
+    *both = bb;
+    return OOC_OK;
+  };
+  st = run();
+  *err = ctx->err;
+  for (auto x : e)
+    if (x) hipEventDestroy(x);
+  if (s1) hipStreamDestroy(s1);
+  if (s2) hipStreamDestroy(s2);
+  if (d1) hipFree(d1);
+  if (d2) hipFree(d2);
+  if (hp1) hipHostFree(hp1);
+  if (hp2) hipHostFree(hp2);
+  return st;
+}
+
+}  // namespace ooc

@@ -1,0 +1,630 @@
+// Dense and convolution layers as one fp32 MFMA GEMM kernel (gfx950).
+//
+// C[M][N] = sum_k A[m][k] B[k][n].  A 256-thread workgroup computes a
+// 128 x 128 tile of C; each of its four wave64s owns a 64 x 64 quarter made
+// of 2 x 2 blocks of v_mfma_f32_32x32x2f32.  K is walked in tiles of 32,
+// double-buffered through LDS: while the waves multiply tile t out of one
+// buffer, every thread has tile t+1 in flight from global memory into
+// registers and writes it to the other buffer.  Within a K tile the two
+// half-waves take the two halves of the tile (the MFMA reduces over both), so
+// each lane reads four consecutive k values of its row at once.
+//
+// Operands reach LDS through loaders, one per way the operand sits in
+// memory: plain row-major matrices (contiguous along k, or along m / n) and
+// the implicit-GEMM views of NHWC convolutions (forward: the input patches;
+// input gradient: the output gradient gathered through the filter taps;
+// filter gradient: the input patches seen along the batch-pixel axis).  A
+// loader zero-fills everything outside the matrix, so no shape needs
+// padding.  LDS layout follows the contiguous direction: "row of k" tiles
+// ([128][32 + 4]) are written and read with 16-byte accesses, "row of m"
+// tiles ([32][128 + 4]) are written with 16-byte accesses and read with
+// 4-byte ones; the +4 pads keep half-wave reads free of bank conflicts.
+//
+// Split-K: the filter gradient reduces over N P Q (millions of pixels), so
+// its grid's second dimension cuts that axis into slices whose partial
+// tiles go to separate buffers and are summed afterwards in slice order.
+// No atomics anywhere: results do not depend on scheduling or addresses.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace ooc {
+
+namespace {
+
+constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int LDK = BK + 4;    // row-of-k tile stride (floats)
+constexpr int LDM = BM + 4;    // row-of-m tile stride (floats)
+constexpr int THREADS = 256;
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+__device__ inline float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+
+// ---------------------------------------------------------------- loaders
+// Each loader: init(mn0, MN) once per workgroup (mn0 = tile origin along m or
+// n, MN = extent), fetch(k0, kend, r) loads this thread's 16 values of the
+// 32-wide K tile starting at k0 (zero at k >= kend), store(lds, r) writes them.
+//
+// Row-of-k thread map: rows (t >> 3) + 32 j, k offset (t & 7) * 4.
+// Row-of-m thread map: k rows (t >> 5) + 8 j, m offset (t & 31) * 4.
+
+struct RowK {
+  static constexpr bool kRowOfK = true;
+  __device__ static void store(float* lds, const float4 (&r)[4]) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<float4*>(&lds[((t >> 3) + 32 * j) * LDK + (t & 7) * 4]) = r[j];
+  }
+};
+struct RowM {
+  static constexpr bool kRowOfK = false;
+  __device__ static void store(float* lds, const float4 (&r)[4]) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<float4*>(&lds[((t >> 5) + 8 * j) * LDM + (t & 31) * 4]) = r[j];
+  }
+};
+
+// X[i][k] = p[i * ld + k]  (contiguous along k)
+template <bool VEC>
+struct MatK : RowK {
+  const float* p;
+  int64_t ld;
+  int64_t row0;
+  int64_t rows;
+  __device__ void init(int64_t mn0, int64_t MN) {
+    row0 = mn0;
+    rows = MN;
+  }
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
+    const int t = threadIdx.x;
+    const int64_t k = k0 + (t & 7) * 4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t i = row0 + (t >> 3) + 32 * j;
+      const float* q = p + i * ld + k;
+      if (VEC) {
+        r[j] = (i < rows && k < kend) ? *reinterpret_cast<const float4*>(q) : zero4();
+      } else {
+        const bool ok = i < rows;
+        r[j].x = (ok && k + 0 < kend) ? q[0] : 0.f;
+        r[j].y = (ok && k + 1 < kend) ? q[1] : 0.f;
+        r[j].z = (ok && k + 2 < kend) ? q[2] : 0.f;
+        r[j].w = (ok && k + 3 < kend) ? q[3] : 0.f;
+      }
+    }
+  }
+};
+
+// X[i][k] = p[k * ld + i]  (contiguous along m or n)
+template <bool VEC>
+struct MatM : RowM {
+  const float* p;
+  int64_t ld;
+  int64_t i0;
+  int64_t rows;
+  __device__ void init(int64_t mn0, int64_t MN) {
+    i0 = mn0 + (threadIdx.x & 31) * 4;
+    rows = MN;
+  }
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t k = k0 + (t >> 5) + 8 * j;
+      const float* q = p + k * ld + i0;
+      if (VEC) {
+        r[j] = (k < kend && i0 < rows) ? *reinterpret_cast<const float4*>(q) : zero4();
+      } else {
+        const bool ok = k < kend;
+        r[j].x = (ok && i0 + 0 < rows) ? q[0] : 0.f;
+        r[j].y = (ok && i0 + 1 < rows) ? q[1] : 0.f;
+        r[j].z = (ok && i0 + 2 < rows) ? q[2] : 0.f;
+        r[j].w = (ok && i0 + 3 < rows) ? q[3] : 0.f;
+      }
+    }
+  }
+};
+
+// Convolution forward, A = input patches: A[m = (n, p, q)][kk = (r, s, c)] =
+// X[n][p st - pad + r][q st - pad + s][c]   (row-of-k; VEC needs C % 4 == 0)
+template <bool VEC>
+struct ConvPatch : RowK {
+  const float* x;
+  int H, W, C, S, st, pad, P, Q;
+  int64_t M;
+  int n_[4], h_[4], w_[4];   // per row: image, top-left input coordinates; n = -1: no row
+  __device__ void init(int64_t mn0, int64_t MN) {
+    M = MN;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t m = mn0 + (threadIdx.x >> 3) + 32 * j;
+      if (m < M) {
+        const int64_t pq = (int64_t)P * Q;
+        const int n = (int)(m / pq);
+        const int rem = (int)(m - (int64_t)n * pq);
+        const int p = rem / Q, q = rem - p * Q;
+        n_[j] = n;
+        h_[j] = p * st - pad;
+        w_[j] = q * st - pad;
+      } else {
+        n_[j] = -1;
+      }
+    }
+  }
+  __device__ float at(int j, int64_t kk, int64_t kend) const {
+    if (n_[j] < 0 || kk >= kend) return 0.f;
+    const int sc = S * C;
+    const int r = (int)(kk / sc);
+    const int rem = (int)(kk - (int64_t)r * sc);
+    const int s = rem / C, c = rem - s * C;
+    const int h = h_[j] + r, w = w_[j] + s;
+    if (h < 0 || h >= H || w < 0 || w >= W) return 0.f;
+    return x[(((int64_t)n_[j] * H + h) * W + w) * C + c];
+  }
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
+    const int64_t kk = k0 + (threadIdx.x & 7) * 4;
+    if (VEC) {
+      int rr = 0, s = 0, c = 0;
+      const bool kin = kk < kend;
+      if (kin) {
+        const int sc = S * C;
+        rr = (int)(kk / sc);
+        const int rem = (int)(kk - (int64_t)rr * sc);
+        s = rem / C;
+        c = rem - s * C;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int h = h_[j] + rr, w = w_[j] + s;
+        const bool ok = kin && n_[j] >= 0 && h >= 0 && h < H && w >= 0 && w < W;
+        r[j] = ok ? *reinterpret_cast<const float4*>(
+                        &x[(((int64_t)n_[j] * H + h) * W + w) * C + c])
+                  : zero4();
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        r[j].x = at(j, kk + 0, kend);
+        r[j].y = at(j, kk + 1, kend);
+        r[j].z = at(j, kk + 2, kend);
+        r[j].w = at(j, kk + 3, kend);
+      }
+    }
+  }
+};
+
+// Convolution input gradient, A = output gradient through the taps:
+// A[m = (n, h, w)][kk = (r, s, k)] = dY[n][p][q][k] with p st = h + pad - r,
+// q st = w + pad - s (zero when not an exact, in-range output position).
+// Row-of-k; VEC needs K % 4 == 0.
+template <bool VEC>
+struct ConvGradTap : RowK {
+  const float* dy;
+  int H, W, K, S, st, pad, P, Q;
+  int64_t M;
+  int n_[4], h_[4], w_[4];   // per row: image, h + pad, w + pad
+  __device__ void init(int64_t mn0, int64_t MN) {
+    M = MN;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t m = mn0 + (threadIdx.x >> 3) + 32 * j;
+      if (m < M) {
+        const int64_t hw = (int64_t)H * W;
+        const int n = (int)(m / hw);
+        const int rem = (int)(m - (int64_t)n * hw);
+        const int h = rem / W, w = rem - h * W;
+        n_[j] = n;
+        h_[j] = h + pad;
+        w_[j] = w + pad;
+      } else {
+        n_[j] = -1;
+      }
+    }
+  }
+  __device__ float at(int j, int64_t kk, int64_t kend) const {
+    if (n_[j] < 0 || kk >= kend) return 0.f;
+    const int sk = S * K;
+    const int r = (int)(kk / sk);
+    const int rem = (int)(kk - (int64_t)r * sk);
+    const int s = rem / K, k = rem - s * K;
+    const int ph = h_[j] - r, qw = w_[j] - s;
+    if (ph < 0 || qw < 0 || ph % st || qw % st) return 0.f;
+    const int p = ph / st, q = qw / st;
+    if (p >= P || q >= Q) return 0.f;
+    return dy[(((int64_t)n_[j] * P + p) * Q + q) * K + k];
+  }
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
+    const int64_t kk = k0 + (threadIdx.x & 7) * 4;
+    if (VEC) {
+      int rr = 0, s = 0, k = 0;
+      const bool kin = kk < kend;
+      if (kin) {
+        const int sk = S * K;
+        rr = (int)(kk / sk);
+        const int rem = (int)(kk - (int64_t)rr * sk);
+        s = rem / K;
+        k = rem - s * K;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int ph = h_[j] - rr, qw = w_[j] - s;
+        bool ok = kin && n_[j] >= 0 && ph >= 0 && qw >= 0 && ph % st == 0 && qw % st == 0;
+        const int p = ok ? ph / st : 0, q = ok ? qw / st : 0;
+        ok = ok && p < P && q < Q;
+        r[j] = ok ? *reinterpret_cast<const float4*>(
+                        &dy[(((int64_t)n_[j] * P + p) * Q + q) * K + k])
+                  : zero4();
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        r[j].x = at(j, kk + 0, kend);
+        r[j].y = at(j, kk + 1, kend);
+        r[j].z = at(j, kk + 2, kend);
+        r[j].w = at(j, kk + 3, kend);
+      }
+    }
+  }
+};
+
+// Convolution input gradient, B = filter seen per tap:
+// B[kk = (r, s, k)][c] = W[k][r][s][c]   (row-of-m; needs C % 4 == 0)
+struct ConvFilterTap : RowM {
+  const float* w;
+  int C, K, R, S;
+  int64_t c0;
+  __device__ void init(int64_t mn0, int64_t) { c0 = mn0 + (threadIdx.x & 31) * 4; }
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t kk = k0 + (threadIdx.x >> 5) + 8 * j;
+      if (kk < kend && c0 < C) {
+        const int sk = S * K;
+        const int rr = (int)(kk / sk);
+        const int rem = (int)(kk - (int64_t)rr * sk);
+        const int s = rem / K, k = rem - s * K;
+        r[j] = *reinterpret_cast<const float4*>(&w[(((int64_t)k * R + rr) * S + s) * C + c0]);
+      } else {
+        r[j] = zero4();
+      }
+    }
+  }
+};
+
+// Convolution filter gradient, B = input patches along the pixel axis:
+// B[kk = (n, p, q)][col = (r, s, c)] = X[n][p st - pad + r][q st - pad + s][c]
+// (row-of-m; VEC needs C % 4 == 0)
+template <bool VEC>
+struct ConvPixelPatch : RowM {
+  const float* x;
+  int H, W, C, S, st, pad, P, Q;
+  int64_t RSC;
+  int r_[4], s_[4], c_[4];   // per column of this thread; r = -1: no column
+  __device__ void init(int64_t mn0, int64_t MN) {
+    RSC = MN;
+    const int64_t col = mn0 + (threadIdx.x & 31) * 4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t cc = col + e;
+      if (cc < RSC && (VEC ? e == 0 : true)) {
+        const int sc = S * C;
+        const int r = (int)(cc / sc);
+        const int rem = (int)(cc - (int64_t)r * sc);
+        r_[e] = r;
+        s_[e] = rem / C;
+        c_[e] = rem - s_[e] * C;
+      } else {
+        r_[e] = -1;
+      }
+    }
+  }
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t kk = k0 + (threadIdx.x >> 5) + 8 * j;
+      r[j] = zero4();
+      if (kk >= kend) continue;
+      const int64_t pq = (int64_t)P * Q;
+      const int n = (int)(kk / pq);
+      const int rem = (int)(kk - (int64_t)n * pq);
+      const int p = rem / Q, q = rem - p * Q;
+      const int hb = p * st - pad, wb = q * st - pad;
+      if (VEC) {
+        const int h = hb + r_[0], w = wb + s_[0];
+        if (r_[0] >= 0 && h >= 0 && h < H && w >= 0 && w < W)
+          r[j] = *reinterpret_cast<const float4*>(&x[(((int64_t)n * H + h) * W + w) * C + c_[0]]);
+      } else {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int h = hb + r_[e], w = wb + s_[e];
+          v[e] = (r_[e] >= 0 && h >= 0 && h < H && w >= 0 && w < W)
+                     ? x[(((int64_t)n * H + h) * W + w) * C + c_[e]]
+                     : 0.f;
+        }
+        r[j] = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    }
+  }
+};
+
+// ---------------------------------------------------------------- kernel
+template <bool ROWK>
+__device__ inline float4 read_op(const float* lds, int i, int k) {
+  if (ROWK) return *reinterpret_cast<const float4*>(&lds[i * LDK + k]);
+  return make_float4(lds[(k + 0) * LDM + i], lds[(k + 1) * LDM + i], lds[(k + 2) * LDM + i],
+                     lds[(k + 3) * LDM + i]);
+}
+
+__device__ inline float comp(const float4& v, int t) {
+  return t == 0 ? v.x : t == 1 ? v.y : t == 2 ? v.z : v.w;
+}
+
+template <class LA, class LB, bool BIAS>
+__global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __restrict__ c,
+                                                       int64_t ldc, int64_t slice_stride,
+                                                       const float* __restrict__ bias, int64_t M,
+                                                       int64_t N, int64_t K, int64_t k_slice,
+                                                       int tiles_m, int tiles_n) {
+  constexpr int ASZ = LA::kRowOfK ? BM * LDK : BK * LDM;
+  constexpr int BSZ = LB::kRowOfK ? BN * LDK : BK * LDM;
+  __shared__ __attribute__((aligned(16))) float As[2][ASZ];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BSZ];
+
+  // grouped tile order: 8 tile-rows share their B tiles in L2
+  const int t = blockIdx.x;
+  const int group = 8;
+  const int per_group = group * tiles_n;
+  const int g = t / per_group;
+  const int first_m = g * group;
+  const int gsize = min(tiles_m - first_m, group);
+  const int tm = first_m + (t % per_group) % gsize;
+  const int tn = (t % per_group) / gsize;
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  const int64_t kb = (int64_t)blockIdx.y * k_slice;
+  const int64_t ke = min(K, kb + k_slice);
+
+  la.init(m0, M);
+  lb.init(n0, N);
+  float4 ra[4], rb[4];
+  floatx16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int half = lane >> 5;
+  const int li = lane & 31;
+
+  if (kb < ke) {
+    la.fetch(kb, ke, ra);
+    lb.fetch(kb, ke, rb);
+    la.store(As[0], ra);
+    lb.store(Bs[0], rb);
+  }
+  __syncthreads();
+  int buf = 0;
+  for (int64_t k0 = kb; k0 < ke; k0 += BK) {
+    const bool more = k0 + BK < ke;
+    if (more) {
+      la.fetch(k0 + BK, ke, ra);
+      lb.fetch(k0 + BK, ke, rb);
+    }
+    const float* A = As[buf];
+    const float* B = Bs[buf];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kq = half * 16 + 4 * j;
+      float4 a[2], b[2];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) a[mb] = read_op<LA::kRowOfK>(A, wm * 64 + mb * 32 + li, kq);
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) b[nb] = read_op<LB::kRowOfK>(B, wn * 64 + nb * 32 + li, kq);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a[mb], s), comp(b[nb], s),
+                                                              acc[mb][nb], 0, 0, 0);
+    }
+    if (more) {
+      la.store(As[buf ^ 1], ra);
+      lb.store(Bs[buf ^ 1], rb);
+    }
+    __syncthreads();
+    buf ^= 1;
+  }
+
+  float* out = c + (int64_t)blockIdx.y * slice_stride;
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int64_t col = n0 + wn * 64 + nb * 32 + li;
+      if (col >= N) continue;
+      const float bv = BIAS ? bias[col] : 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * 64 + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (row < M) out[row * ldc + col] = acc[mb][nb][r] + bv;
+      }
+    }
+}
+
+template <class LA, class LB, bool BIAS>
+hipError_t run_gemm(const LA& la, const LB& lb, float* c, int64_t ldc, const float* bias,
+                    int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s) {
+  const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+  if (tiles_m * tiles_n > INT32_MAX / 2 || slices > 65535) return hipErrorInvalidValue;
+  int64_t k_slice = (K + slices - 1) / slices;
+  k_slice = (k_slice + BK - 1) / BK * BK;
+  dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices);
+  hipLaunchKernelGGL((gemm_kernel<LA, LB, BIAS>), grid, dim3(THREADS), 0, s, la, lb, c, ldc,
+                     M * ldc, bias, M, N, K, k_slice, (int)tiles_m, (int)tiles_n);
+  return hipGetLastError();
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// ---------------------------------------------------------------- small kernels
+// db[n] = sum over rows m of dY[m][n], rows summed in order
+__global__ void colsum_kernel(const float* __restrict__ dy, float* __restrict__ db, int64_t M,
+                              int64_t N) {
+  const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  float acc = 0.f;
+  for (int64_t m = 0; m < M; ++m) acc += dy[m * N + n];
+  db[n] = acc;
+}
+
+// out[j] = sum over slices s (in order) of part[s][j]
+__global__ void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
+                                 int64_t n, int64_t slices) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  float acc = 0.f;
+  for (int64_t s = 0; s < slices; ++s) acc += part[s * n + j];
+  out[j] = acc;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+hipError_t linear_fwd(const float* X, const float* W, const float* b, float* Y, int64_t M,
+                      int64_t K, int64_t N, hipStream_t s) {
+  const bool vec = K % 4 == 0 && aligned16(X) && aligned16(W);
+  if (vec) {
+    MatK<true> a{}, bb{};
+    a.p = X; a.ld = K; bb.p = W; bb.ld = K;
+    return run_gemm<MatK<true>, MatK<true>, true>(a, bb, Y, N, b, M, N, K, 1, s);
+  }
+  MatK<false> a{}, bb{};
+  a.p = X; a.ld = K; bb.p = W; bb.ld = K;
+  return run_gemm<MatK<false>, MatK<false>, true>(a, bb, Y, N, b, M, N, K, 1, s);
+}
+
+hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, int64_t K,
+                        int64_t N, hipStream_t s) {
+  // dX[M][K] = dY[M][N] W[N][K]: A = dY (row-of-k over N), B[n_out][k_in] = W, contiguous in k_in
+  if (N % 4 == 0 && K % 4 == 0 && aligned16(W) && aligned16(dY)) {
+    MatK<true> a{};
+    MatM<true> bb{};
+    a.p = dY; a.ld = N; bb.p = W; bb.ld = K;
+    return run_gemm<MatK<true>, MatM<true>, false>(a, bb, dX, K, nullptr, M, K, N, 1, s);
+  }
+  MatK<false> a{};
+  MatM<false> bb{};
+  a.p = dY; a.ld = N; bb.p = W; bb.ld = K;
+  return run_gemm<MatK<false>, MatM<false>, false>(a, bb, dX, K, nullptr, M, K, N, 1, s);
+}
+
+hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, int64_t M,
+                        int64_t K, int64_t N, hipStream_t s) {
+  // dW[N][K] = dY^T X: A[n][m] = dY[m][n] (contiguous in n), B[m][k] = X[m][k] (contiguous in k)
+  hipError_t e;
+  if (N % 4 == 0 && K % 4 == 0 && aligned16(X) && aligned16(dY)) {
+    MatM<true> a{}, bb{};
+    a.p = dY; a.ld = N; bb.p = X; bb.ld = K;
+    e = run_gemm<MatM<true>, MatM<true>, false>(a, bb, dW, K, nullptr, N, K, M, 1, s);
+  } else {
+    MatM<false> a{}, bb{};
+    a.p = dY; a.ld = N; bb.p = X; bb.ld = K;
+    e = run_gemm<MatM<false>, MatM<false>, false>(a, bb, dW, K, nullptr, N, K, M, 1, s);
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s, dY, db,
+                     M, N);
+  return hipGetLastError();
+}
+
+hipError_t conv_fwd(const float* X, const float* W, float* Y, const ConvShape& c, hipStream_t s) {
+  const int64_t M = c.N * c.P * c.Q, N = c.K, K = c.R * c.S * c.C;
+  auto fill = [&](auto& a) {
+    a.x = X; a.H = (int)c.H; a.W = (int)c.W; a.C = (int)c.C; a.S = (int)c.S;
+    a.st = (int)c.stride; a.pad = (int)c.pad; a.P = (int)c.P; a.Q = (int)c.Q;
+  };
+  if (c.C % 4 == 0) {
+    ConvPatch<true> a{};
+    fill(a);
+    MatK<true> b{};
+    b.p = W; b.ld = K;
+    return run_gemm<ConvPatch<true>, MatK<true>, false>(a, b, Y, N, nullptr, M, N, K, 1, s);
+  }
+  ConvPatch<false> a{};
+  fill(a);
+  MatK<false> b{};
+  b.p = W; b.ld = K;
+  return run_gemm<ConvPatch<false>, MatK<false>, false>(a, b, Y, N, nullptr, M, N, K, 1, s);
+}
+
+hipError_t conv_bwd_x(const float* W, const float* dY, float* dX, const ConvShape& c,
+                      hipStream_t s) {
+  if (c.C % 4 != 0) return hipErrorInvalidValue;   // every conv with an input gradient has C % 4 == 0
+  const int64_t M = c.N * c.H * c.W, N = c.C, K = c.R * c.S * c.K;
+  ConvFilterTap b{};
+  b.w = W; b.C = (int)c.C; b.K = (int)c.K; b.R = (int)c.R; b.S = (int)c.S;
+  auto fill = [&](auto& a) {
+    a.dy = dY; a.H = (int)c.H; a.W = (int)c.W; a.K = (int)c.K; a.S = (int)c.S;
+    a.st = (int)c.stride; a.pad = (int)c.pad; a.P = (int)c.P; a.Q = (int)c.Q;
+  };
+  if (c.K % 4 == 0) {
+    ConvGradTap<true> a{};
+    fill(a);
+    return run_gemm<ConvGradTap<true>, ConvFilterTap, false>(a, b, dX, N, nullptr, M, N, K, 1, s);
+  }
+  ConvGradTap<false> a{};
+  fill(a);
+  return run_gemm<ConvGradTap<false>, ConvFilterTap, false>(a, b, dX, N, nullptr, M, N, K, 1, s);
+}
+
+hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, int64_t slices,
+                      const ConvShape& c, hipStream_t s) {
+  // dW[K][RSC] = sum over pixels of dY[pixel][k] * patch[pixel][rsc]
+  const int64_t M = c.K, N = c.R * c.S * c.C, K = c.N * c.P * c.Q;
+  float* out = slices > 1 ? part : dW;
+  auto fill = [&](auto& b) {
+    b.x = X; b.H = (int)c.H; b.W = (int)c.W; b.C = (int)c.C; b.S = (int)c.S;
+    b.st = (int)c.stride; b.pad = (int)c.pad; b.P = (int)c.P; b.Q = (int)c.Q;
+  };
+  hipError_t e;
+  if (c.K % 4 == 0) {
+    MatM<true> a{};
+    a.p = dY; a.ld = c.K;
+    if (c.C % 4 == 0) {
+      ConvPixelPatch<true> b{};
+      fill(b);
+      e = run_gemm<MatM<true>, ConvPixelPatch<true>, false>(a, b, out, N, nullptr, M, N, K,
+                                                            slices, s);
+    } else {
+      ConvPixelPatch<false> b{};
+      fill(b);
+      e = run_gemm<MatM<true>, ConvPixelPatch<false>, false>(a, b, out, N, nullptr, M, N, K,
+                                                             slices, s);
+    }
+  } else {
+    MatM<false> a{};
+    a.p = dY; a.ld = c.K;
+    ConvPixelPatch<false> b{};
+    fill(b);
+    e = run_gemm<MatM<false>, ConvPixelPatch<false>, false>(a, b, out, N, nullptr, M, N, K,
+                                                            slices, s);
+  }
+  if (e != hipSuccess || slices <= 1) return e;
+  const int64_t n = M * N;
+  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part,
+                     dW, n, slices);
+  return hipGetLastError();
+}
+
+}  // namespace ooc

@@ -1,0 +1,80 @@
+// Internal structures of the out-of-core training library.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/ooc.h"
+
+namespace ooc {
+
+enum State : uint8_t { UNMAT = 0, HOST = 1, DEV = 2, PEND = 3 };
+
+struct Var {
+  uint64_t bytes;
+  int32_t kind;
+};
+
+struct FnVar {
+  int64_t var;
+  uint8_t access;
+};
+
+struct Fn {
+  int32_t op;
+  std::vector<FnVar> vars;      // merged: first position kept, accesses or-ed
+  std::vector<int64_t> attrs;
+};
+
+struct Op {
+  int32_t fn;
+  uint8_t phase;
+  uint8_t kind;
+  int64_t var;
+  uint64_t held;
+};
+
+struct Schedule {
+  std::vector<Op> ops;
+  std::vector<int64_t> windows;
+  uint64_t peak = 0, h2d = 0, d2h = 0;
+};
+
+// Residency interval: one device copy of one variable (Section 4: one
+// virtual range per allocation request).
+struct Interval {
+  int64_t var;
+  int64_t open;    // op index, -1 = resident for the whole step
+  int64_t close;   // op index, -1 = never closed
+  std::vector<int32_t> chunks;
+};
+
+struct Plan {
+  std::vector<Interval> intervals;
+  std::vector<int64_t> op_interval;   // per op: the interval it opens / closes / touches (-1)
+  uint64_t max_chunks_used = 0;
+  uint64_t n_chunks = 0;              // chunks the pool must own
+};
+
+// Scheduler (Section 3, Fig. 2).  Returns OOC_OK, OOC_E_INFEASIBLE.
+ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& fns,
+                          uint64_t budget, uint64_t window, uint64_t chunk, int policy,
+                          Schedule* out, std::string* err);
+// In-core plan: persistent variables resident for the whole step, TEMPs from
+// first to last use, no transfers.
+void build_incore(const std::vector<Var>& vars, const std::vector<Fn>& fns, uint64_t chunk,
+                  Schedule* out);
+uint64_t incore_peak(const std::vector<Var>& vars, const std::vector<Fn>& fns, uint64_t chunk);
+uint64_t working_set_max(const std::vector<Var>& vars, const std::vector<Fn>& fns,
+                         uint64_t chunk);
+// Chunk plan: replays the schedule through the pool (lowest free chunk first).
+void build_plan(const std::vector<Var>& vars, const Schedule& s, bool incore, uint64_t chunk,
+                Plan* out);
+
+// Function-sequence rules and operation signatures; returns "" when valid.
+std::string check_fn(const std::vector<Var>& vars, const Fn& fn);
+
+inline uint64_t round_up(uint64_t b, uint64_t c) { return (b + c - 1) / c * c; }
+
+}  // namespace ooc

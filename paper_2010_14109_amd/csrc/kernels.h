@@ -1,0 +1,55 @@
+// Host-side launchers of the HIP kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace ooc {
+
+// Runs function fn on stream s; ptrs[j] is the device address of fn.vars[j],
+// bytes[j] its size.
+hipError_t launch_fn(const Fn& fn, void* const* ptrs, const uint64_t* bytes, float lr, float mu,
+                     hipStream_t s);
+
+// GEMM family (gemm.hip).  Shapes as in the operation table of ooc.h.
+hipError_t linear_fwd(const float* X, const float* W, const float* b, float* Y, int64_t M,
+                      int64_t K, int64_t N, hipStream_t s);
+hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, int64_t M,
+                        int64_t K, int64_t N, hipStream_t s);
+hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, int64_t K,
+                        int64_t N, hipStream_t s);
+struct ConvShape {
+  int64_t N, H, W, C, K, R, S, stride, pad, P, Q;
+};
+hipError_t conv_fwd(const float* X, const float* W, float* Y, const ConvShape& c, hipStream_t s);
+hipError_t conv_bwd_x(const float* W, const float* dY, float* dX, const ConvShape& c,
+                      hipStream_t s);
+hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, int64_t slices,
+                      const ConvShape& c, hipStream_t s);
+
+// Elementwise, loss, update, normalisation and pooling (ops.hip).
+hipError_t relu_fwd(const float* x, float* y, int64_t n, hipStream_t s);
+hipError_t relu_bwd(const float* y, const float* dy, float* dx, int64_t n, hipStream_t s);
+hipError_t add(const float* a, const float* b, float* y, int64_t n, hipStream_t s);
+hipError_t sgd(float* w, const float* g, float* v, int64_t n, float lr, float mu, hipStream_t s);
+hipError_t softmax_ce(const float* logits, const int32_t* labels, float* loss, float* dlogits,
+                      int64_t N, int64_t classes, hipStream_t s);
+hipError_t bn_fwd(const float* x, const float* gamma, const float* beta, float* y, float* stats,
+                  int64_t rows, int64_t C, int64_t slices, hipStream_t s);
+hipError_t bn_bwd(const float* x, const float* gamma, float* stats, const float* dy, float* dx,
+                  float* dgamma, float* dbeta, int64_t rows, int64_t C, int64_t slices,
+                  hipStream_t s);
+struct PoolShape {
+  int64_t N, H, W, C, k, stride, pad, P, Q;
+};
+hipError_t maxpool_fwd(const float* x, float* y, uint8_t* idx, const PoolShape& p, hipStream_t s);
+hipError_t maxpool_bwd(const uint8_t* idx, const float* dy, float* dx, const PoolShape& p,
+                       hipStream_t s);
+hipError_t avgpool_fwd(const float* x, float* y, int64_t N, int64_t HW, int64_t C, hipStream_t s);
+hipError_t avgpool_bwd(const float* dy, float* dx, int64_t N, int64_t HW, int64_t C,
+                       hipStream_t s);
+hipError_t mix(void* const* ptrs, const uint64_t* words, int nvars, uint32_t seed, hipStream_t s,
+               bool y_read);
+
+}  // namespace ooc

@@ -1,0 +1,500 @@
+// Memory-bound layers: ReLU, addition, SGD, softmax cross-entropy, batch
+// normalisation, pooling, and the swap-integrity test op (gfx950).
+//
+// These kernels are bound by HBM bandwidth, not arithmetic: they stream
+// with 16-byte accesses in grid-stride loops sized to fill the 256 CUs, and
+// every reduction runs in a fixed order (per-slice partials written to the
+// function's own variables, then summed slice by slice), so results never
+// depend on scheduling or on where a variable lives.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "kernels.h"
+
+namespace ooc {
+
+namespace {
+
+constexpr int TPB = 256;
+
+unsigned grid_for(int64_t work, int64_t per_block = TPB) {
+  int64_t g = (work + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  if (g > 16384) g = 16384;
+  return (unsigned)g;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// ---------------------------------------------------------------- elementwise
+template <int OP>   // 0: relu fwd, 1: relu bwd, 2: add
+__global__ void ew_kernel(const float* __restrict__ a, const float* __restrict__ b,
+                          float* __restrict__ y, int64_t n, bool vec) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  auto f = [](float x, float z) {
+    if (OP == 0) return x > 0.f ? x : 0.f;
+    if (OP == 1) return x > 0.f ? z : 0.f;
+    return x + z;
+  };
+  int64_t done = 0;
+  if (vec) {
+    const int64_t n4 = n / 4;
+    for (int64_t j = i; j < n4; j += stride) {
+      const float4 x = reinterpret_cast<const float4*>(a)[j];
+      const float4 z = OP == 0 ? x : reinterpret_cast<const float4*>(b)[j];
+      reinterpret_cast<float4*>(y)[j] = make_float4(f(x.x, z.x), f(x.y, z.y), f(x.z, z.z),
+                                                    f(x.w, z.w));
+    }
+    done = n4 * 4;
+  }
+  for (int64_t j = done + i; j < n; j += stride) y[j] = f(a[j], OP == 0 ? a[j] : b[j]);
+}
+
+template <int OP>
+hipError_t ew(const float* a, const float* b, float* y, int64_t n, hipStream_t s) {
+  const bool vec = aligned16(a) && aligned16(y) && (OP == 0 || aligned16(b));
+  hipLaunchKernelGGL(ew_kernel<OP>, dim3(grid_for((n + 3) / 4)), dim3(TPB), 0, s, a, b, y, n, vec);
+  return hipGetLastError();
+}
+
+__global__ void sgd_kernel(float* __restrict__ w, const float* __restrict__ g,
+                           float* __restrict__ v, int64_t n, float lr, float mu, bool vec) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t done = 0;
+  if (vec) {
+    const int64_t n4 = n / 4;
+    for (int64_t j = i; j < n4; j += stride) {
+      float4 ww = reinterpret_cast<float4*>(w)[j];
+      float4 gg = reinterpret_cast<const float4*>(g)[j];
+      if (v) {
+        float4 vv = reinterpret_cast<float4*>(v)[j];
+        vv.x = mu * vv.x + gg.x; vv.y = mu * vv.y + gg.y;
+        vv.z = mu * vv.z + gg.z; vv.w = mu * vv.w + gg.w;
+        reinterpret_cast<float4*>(v)[j] = vv;
+        gg = vv;
+      }
+      ww.x -= lr * gg.x; ww.y -= lr * gg.y; ww.z -= lr * gg.z; ww.w -= lr * gg.w;
+      reinterpret_cast<float4*>(w)[j] = ww;
+    }
+    done = n4 * 4;
+  }
+  for (int64_t j = done + i; j < n; j += stride) {
+    float gg = g[j];
+    if (v) {
+      v[j] = mu * v[j] + gg;
+      gg = v[j];
+    }
+    w[j] -= lr * gg;
+  }
+}
+
+// ---------------------------------------------------------------- softmax cross-entropy
+__device__ inline float wave_max(float x) {
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+__device__ inline float wave_sum(float x) {
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// one wave64 per row
+__global__ void softmax_ce_rows(const float* __restrict__ z, const int32_t* __restrict__ labels,
+                                float* __restrict__ loss, float* __restrict__ dz, int64_t N,
+                                int64_t C) {
+  const int64_t row = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= N) return;
+  const float* zr = z + row * C;
+  float* dr = dz + row * C;
+  const int32_t lab = labels[row];
+  const bool ok = lab >= 0 && lab < C;
+  float mx = -INFINITY;
+  for (int64_t c = lane; c < C; c += 64) mx = fmaxf(mx, zr[c]);
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int64_t c = lane; c < C; c += 64) sum += expf(zr[c] - mx);
+  sum = wave_sum(sum);
+  const float inv_n = 1.f / (float)N;
+  const float lse = logf(sum);
+  for (int64_t c = lane; c < C; c += 64) {
+    const float p = expf(zr[c] - mx - lse);
+    dr[c] = ok ? (p - (c == lab ? 1.f : 0.f)) * inv_n : 0.f;
+  }
+  if (lane == 0) loss[row] = ok ? lse - (zr[lab] - mx) : NAN;
+}
+
+// loss[N] = mean of loss[0..N), summed in a fixed order by one workgroup
+__global__ void mean_rows(float* __restrict__ loss, int64_t N) {
+  __shared__ float part[TPB];
+  float acc = 0.f;
+  for (int64_t r = threadIdx.x; r < N; r += TPB) acc += loss[r];
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = TPB / 2; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) loss[N] = part[0] / (float)N;
+}
+
+// ---------------------------------------------------------------- batch normalisation
+// Rows split into `slices` contiguous slices; a workgroup takes one slice and
+// 64 channels: 16 channel lanes x 4 channels, 16 row lanes.
+struct SliceMap {
+  int64_t rows, slices, len;
+  __device__ int64_t begin(int64_t s) const { return s * len; }
+  __device__ int64_t end(int64_t s) const { return min(rows, (s + 1) * len); }
+};
+
+// per (slice, channel): sums of (x - shift) and (x - shift)^2, shift = x[row 0]
+// (mode 0), or of dy and dy * xhat (mode 1)
+template <int MODE>
+__global__ void bn_partials(const float* __restrict__ x, const float* __restrict__ dy,
+                            float* __restrict__ stats, SliceMap sm, int64_t C) {
+  __shared__ float sa[16][64], sb[16][64];
+  const int s = blockIdx.x;
+  const int rl = threadIdx.x >> 4, cl = threadIdx.x & 15;
+  const int64_t c0 = (int64_t)blockIdx.y * 64 + cl * 4;
+  float a[4] = {0, 0, 0, 0}, b[4] = {0, 0, 0, 0};
+  float sh[4] = {0, 0, 0, 0}, inv[4] = {0, 0, 0, 0};
+  for (int e = 0; e < 4; ++e) {
+    const int64_t c = c0 + e;
+    if (c < C) {
+      if (MODE == 0) {
+        sh[e] = x[c];
+      } else {
+        sh[e] = stats[c];
+        inv[e] = stats[C + c];
+      }
+    }
+  }
+  const bool vec = (C % 4 == 0) && c0 + 3 < C;
+  for (int64_t r = sm.begin(s) + rl; r < sm.end(s); r += 16) {
+    float xv[4], gv[4] = {0, 0, 0, 0};
+    if (vec) {
+      const float4 t = *reinterpret_cast<const float4*>(&x[r * C + c0]);
+      xv[0] = t.x; xv[1] = t.y; xv[2] = t.z; xv[3] = t.w;
+      if (MODE == 1) {
+        const float4 u = *reinterpret_cast<const float4*>(&dy[r * C + c0]);
+        gv[0] = u.x; gv[1] = u.y; gv[2] = u.z; gv[3] = u.w;
+      }
+    } else {
+      for (int e = 0; e < 4; ++e) {
+        const int64_t c = c0 + e;
+        xv[e] = c < C ? x[r * C + c] : 0.f;
+        if (MODE == 1) gv[e] = c < C ? dy[r * C + c] : 0.f;
+      }
+    }
+    for (int e = 0; e < 4; ++e) {
+      if (MODE == 0) {
+        const float d = xv[e] - sh[e];
+        a[e] += d;
+        b[e] += d * d;
+      } else {
+        const float xh = (xv[e] - sh[e]) * inv[e];
+        a[e] += gv[e];
+        b[e] += gv[e] * xh;
+      }
+    }
+  }
+  for (int e = 0; e < 4; ++e) {
+    sa[rl][cl * 4 + e] = a[e];
+    sb[rl][cl * 4 + e] = b[e];
+  }
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int64_t c = (int64_t)blockIdx.y * 64 + threadIdx.x;
+    if (c < C) {
+      float ta = 0.f, tb = 0.f;
+      for (int j = 0; j < 16; ++j) {
+        ta += sa[j][threadIdx.x];
+        tb += sb[j][threadIdx.x];
+      }
+      float* part = stats + 2 * C + (int64_t)s * 2 * C;
+      part[c] = ta;
+      part[C + c] = tb;
+    }
+  }
+}
+
+// combine slice partials in slice order (double): forward -> mean, invstd;
+// backward -> dgamma, dbeta
+template <int MODE>
+__global__ void bn_finalize(const float* __restrict__ x, float* __restrict__ stats,
+                            float* __restrict__ dgamma, float* __restrict__ dbeta, int64_t rows,
+                            int64_t C, int64_t slices) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  double a = 0, b = 0;
+  for (int64_t s = 0; s < slices; ++s) {
+    const float* part = stats + 2 * C + s * 2 * C;
+    a += part[c];
+    b += part[C + c];
+  }
+  if (MODE == 0) {
+    const double m1 = a / (double)rows;
+    double var = b / (double)rows - m1 * m1;
+    if (var < 0) var = 0;
+    stats[c] = (float)((double)x[c] + m1);
+    stats[C + c] = (float)(1.0 / sqrt(var + 1e-5));
+  } else {
+    dbeta[c] = (float)a;
+    dgamma[c] = (float)b;
+  }
+}
+
+// forward: y = (x - mean) invstd gamma + beta; backward:
+// dx = gamma invstd (dy - dbeta / rows - xhat dgamma / rows)
+template <int MODE>
+__global__ void bn_apply(const float* __restrict__ x, const float* __restrict__ dy,
+                         const float* __restrict__ stats, const float* __restrict__ gamma,
+                         const float* __restrict__ beta, const float* __restrict__ dgamma,
+                         float* __restrict__ out, int64_t rows, int64_t C, bool vec) {
+  const int64_t n = rows * C;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const float inv_rows = 1.f / (float)rows;
+  auto f = [&](float xv, float gv, int64_t c) {
+    const float mean = stats[c], invstd = stats[C + c];
+    const float xh = (xv - mean) * invstd;
+    if (MODE == 0) return xh * gamma[c] + beta[c];
+    return gamma[c] * invstd * (gv - beta[c] * inv_rows - xh * dgamma[c] * inv_rows);
+  };
+  int64_t done = 0;
+  if (vec) {
+    const int64_t n4 = n / 4;
+    for (int64_t j = i; j < n4; j += stride) {
+      const int64_t c = (j * 4) % C;
+      const float4 xv = reinterpret_cast<const float4*>(x)[j];
+      float4 gv = make_float4(0, 0, 0, 0);
+      if (MODE == 1) gv = reinterpret_cast<const float4*>(dy)[j];
+      reinterpret_cast<float4*>(out)[j] = make_float4(f(xv.x, gv.x, c), f(xv.y, gv.y, c + 1),
+                                                      f(xv.z, gv.z, c + 2), f(xv.w, gv.w, c + 3));
+    }
+    done = n4 * 4;
+  }
+  for (int64_t j = done + i; j < n; j += stride)
+    out[j] = f(x[j], MODE == 1 ? dy[j] : 0.f, j % C);
+}
+
+// ---------------------------------------------------------------- pooling
+__global__ void maxpool_fwd_kernel(const float* __restrict__ x, float* __restrict__ y,
+                                   uint8_t* __restrict__ idx, PoolShape p) {
+  const int64_t total = p.N * p.P * p.Q * p.C;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total; o += stride) {
+    const int64_t c = o % p.C;
+    int64_t t = o / p.C;
+    const int64_t q = t % p.Q;
+    t /= p.Q;
+    const int64_t pp = t % p.P;
+    const int64_t n = t / p.P;
+    float best = 0.f;
+    int bi = -1;
+    for (int r = 0; r < p.k; ++r) {
+      const int64_t h = pp * p.stride + r - p.pad;
+      if (h < 0 || h >= p.H) continue;
+      for (int s = 0; s < p.k; ++s) {
+        const int64_t w = q * p.stride + s - p.pad;
+        if (w < 0 || w >= p.W) continue;
+        const float v = x[((n * p.H + h) * p.W + w) * p.C + c];
+        if (bi < 0 || v > best) {
+          best = v;
+          bi = r * (int)p.k + s;
+        }
+      }
+    }
+    y[o] = best;
+    idx[o] = (uint8_t)(bi < 0 ? 0 : bi);
+  }
+}
+
+__global__ void maxpool_bwd_kernel(const uint8_t* __restrict__ idx, const float* __restrict__ dy,
+                                   float* __restrict__ dx, PoolShape p) {
+  const int64_t total = p.N * p.H * p.W * p.C;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total; o += stride) {
+    const int64_t c = o % p.C;
+    int64_t t = o / p.C;
+    const int64_t w = t % p.W;
+    t /= p.W;
+    const int64_t h = t % p.H;
+    const int64_t n = t / p.H;
+    // output rows whose window covers h: p st - pad <= h <= p st - pad + k - 1
+    int64_t plo = h + p.pad - p.k + 1;
+    plo = plo <= 0 ? 0 : (plo + p.stride - 1) / p.stride;
+    int64_t phi = (h + p.pad) / p.stride;
+    if (phi > p.P - 1) phi = p.P - 1;
+    int64_t qlo = w + p.pad - p.k + 1;
+    qlo = qlo <= 0 ? 0 : (qlo + p.stride - 1) / p.stride;
+    int64_t qhi = (w + p.pad) / p.stride;
+    if (qhi > p.Q - 1) qhi = p.Q - 1;
+    float acc = 0.f;
+    for (int64_t pp = plo; pp <= phi; ++pp)
+      for (int64_t q = qlo; q <= qhi; ++q) {
+        const int64_t r = h - (pp * p.stride - p.pad), s = w - (q * p.stride - p.pad);
+        const int64_t oi = ((n * p.P + pp) * p.Q + q) * p.C + c;
+        if (idx[oi] == r * p.k + s) acc += dy[oi];
+      }
+    dx[o] = acc;
+  }
+}
+
+__global__ void avgpool_fwd_kernel(const float* __restrict__ x, float* __restrict__ y, int64_t N,
+                                   int64_t HW, int64_t C) {
+  const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (o >= N * C) return;
+  const int64_t n = o / C, c = o % C;
+  float acc = 0.f;
+  for (int64_t j = 0; j < HW; ++j) acc += x[(n * HW + j) * C + c];
+  y[o] = acc / (float)HW;
+}
+
+__global__ void avgpool_bwd_kernel(const float* __restrict__ dy, float* __restrict__ dx, int64_t N,
+                                   int64_t HW, int64_t C) {
+  const int64_t total = N * HW * C;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const float inv = 1.f / (float)HW;
+  for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total; o += stride) {
+    const int64_t c = o % C, n = o / (HW * C);
+    dx[o] = dy[n * C + c] * inv;
+  }
+}
+
+// ---------------------------------------------------------------- test op
+constexpr int kMixMax = 16;
+struct MixArgs {
+  const uint32_t* src[kMixMax];
+  uint64_t len[kMixMax];
+  int nsrc;
+  uint32_t* y;
+  uint64_t ylen;
+  uint32_t seed;
+};
+
+__global__ void mix_kernel(MixArgs a) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; j < a.ylen; j += stride) {
+    uint32_t acc = 0;
+    for (int k = 0; k < a.nsrc; ++k) acc += a.src[k][j % a.len[k]];
+    a.y[j] = a.seed ^ (uint32_t)(j * 2654435761ull) ^ acc;
+  }
+}
+
+}  // namespace
+
+hipError_t relu_fwd(const float* x, float* y, int64_t n, hipStream_t s) {
+  return ew<0>(x, nullptr, y, n, s);
+}
+hipError_t relu_bwd(const float* y, const float* dy, float* dx, int64_t n, hipStream_t s) {
+  return ew<1>(y, dy, dx, n, s);
+}
+hipError_t add(const float* a, const float* b, float* y, int64_t n, hipStream_t s) {
+  return ew<2>(a, b, y, n, s);
+}
+
+hipError_t sgd(float* w, const float* g, float* v, int64_t n, float lr, float mu, hipStream_t s) {
+  const bool vec = aligned16(w) && aligned16(g) && (!v || aligned16(v));
+  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for((n + 3) / 4)), dim3(TPB), 0, s, w, g, v, n, lr, mu,
+                     vec);
+  return hipGetLastError();
+}
+
+hipError_t softmax_ce(const float* logits, const int32_t* labels, float* loss, float* dlogits,
+                      int64_t N, int64_t classes, hipStream_t s) {
+  const int64_t rows_per_block = TPB / 64;
+  hipLaunchKernelGGL(softmax_ce_rows, dim3((unsigned)((N + rows_per_block - 1) / rows_per_block)),
+                     dim3(TPB), 0, s, logits, labels, loss, dlogits, N, classes);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mean_rows, dim3(1), dim3(TPB), 0, s, loss, N);
+  return hipGetLastError();
+}
+
+hipError_t bn_fwd(const float* x, const float* gamma, const float* beta, float* y, float* stats,
+                  int64_t rows, int64_t C, int64_t slices, hipStream_t s) {
+  SliceMap sm{rows, slices, (rows + slices - 1) / slices};
+  const unsigned cg = (unsigned)((C + 63) / 64);
+  hipLaunchKernelGGL(bn_partials<0>, dim3((unsigned)slices, cg), dim3(TPB), 0, s, x, nullptr,
+                     stats, sm, C);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(bn_finalize<0>, dim3((unsigned)((C + 255) / 256)), dim3(256), 0, s, x, stats,
+                     nullptr, nullptr, rows, C, slices);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const bool vec = C % 4 == 0 && aligned16(x) && aligned16(y);
+  hipLaunchKernelGGL(bn_apply<0>, dim3(grid_for((rows * C + 3) / 4)), dim3(TPB), 0, s, x, nullptr,
+                     stats, gamma, beta, nullptr, y, rows, C, vec);
+  return hipGetLastError();
+}
+
+hipError_t bn_bwd(const float* x, const float* gamma, float* stats, const float* dy, float* dx,
+                  float* dgamma, float* dbeta, int64_t rows, int64_t C, int64_t slices,
+                  hipStream_t s) {
+  SliceMap sm{rows, slices, (rows + slices - 1) / slices};
+  const unsigned cg = (unsigned)((C + 63) / 64);
+  hipLaunchKernelGGL(bn_partials<1>, dim3((unsigned)slices, cg), dim3(TPB), 0, s, x, dy, stats, sm,
+                     C);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(bn_finalize<1>, dim3((unsigned)((C + 255) / 256)), dim3(256), 0, s, x, stats,
+                     dgamma, dbeta, rows, C, slices);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const bool vec = C % 4 == 0 && aligned16(x) && aligned16(dy) && aligned16(dx);
+  // backward uses beta's slot for dbeta: dx = gamma invstd (dy - dbeta/rows - xhat dgamma/rows)
+  hipLaunchKernelGGL(bn_apply<1>, dim3(grid_for((rows * C + 3) / 4)), dim3(TPB), 0, s, x, dy,
+                     stats, gamma, dbeta, dgamma, dx, rows, C, vec);
+  return hipGetLastError();
+}
+
+hipError_t maxpool_fwd(const float* x, float* y, uint8_t* idx, const PoolShape& p, hipStream_t s) {
+  hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(grid_for(p.N * p.P * p.Q * p.C)), dim3(TPB), 0, s, x,
+                     y, idx, p);
+  return hipGetLastError();
+}
+
+hipError_t maxpool_bwd(const uint8_t* idx, const float* dy, float* dx, const PoolShape& p,
+                       hipStream_t s) {
+  hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(grid_for(p.N * p.H * p.W * p.C)), dim3(TPB), 0, s,
+                     idx, dy, dx, p);
+  return hipGetLastError();
+}
+
+hipError_t avgpool_fwd(const float* x, float* y, int64_t N, int64_t HW, int64_t C, hipStream_t s) {
+  hipLaunchKernelGGL(avgpool_fwd_kernel, dim3((unsigned)((N * C + TPB - 1) / TPB)), dim3(TPB), 0, s,
+                     x, y, N, HW, C);
+  return hipGetLastError();
+}
+
+hipError_t avgpool_bwd(const float* dy, float* dx, int64_t N, int64_t HW, int64_t C,
+                       hipStream_t s) {
+  hipLaunchKernelGGL(avgpool_bwd_kernel, dim3(grid_for(N * HW * C)), dim3(TPB), 0, s, dy, dx, N,
+                     HW, C);
+  return hipGetLastError();
+}
+
+// MIX: the last variable is written; the others (and the last one too when
+// `y_read`) are read
+hipError_t mix(void* const* ptrs, const uint64_t* words, int nvars, uint32_t seed, hipStream_t s,
+               bool y_read) {
+  MixArgs a{};
+  int ns = 0;
+  for (int j = 0; j < nvars - 1 + (y_read ? 1 : 0); ++j) {
+    if (ns >= kMixMax) return hipErrorInvalidValue;
+    a.src[ns] = (const uint32_t*)ptrs[j];
+    a.len[ns] = words[j];
+    ++ns;
+  }
+  a.nsrc = ns;
+  a.y = (uint32_t*)ptrs[nvars - 1];
+  a.ylen = words[nvars - 1];
+  a.seed = seed;
+  hipLaunchKernelGGL(mix_kernel, dim3(grid_for((int64_t)a.ylen)), dim3(TPB), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace ooc

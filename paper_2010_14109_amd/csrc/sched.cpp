@@ -1,0 +1,295 @@
+// Adaptive-window swap scheduler (Section 3, Fig. 2), in-core plan and the
+// chunk plan of the virtual-address pool (Section 4).
+//
+// The variable-sequence v = flatten([V_1..V_N]) is kept as position arrays;
+// next[p] is the next position holding the same variable.  Per function f_i
+// (first position l, last e):
+//   window  r = largest index with sum(b_v[p], p = l..r) <= W (two pointers
+//           over prefix sums), then r = max(r, e, r_prev);
+//   (a)+(b) admit positions r_prev+1..r: a variable on the host is swapped
+//           in, one never produced is allocated, a pending swap-out is
+//           cancelled (policy CANCEL); before each admission the oldest
+//           pending swap-outs are waited for until it fits in the budget; if
+//           nothing is left to wait for, the window ends before it (an error
+//           only when the variable belongs to f_i itself);
+//   (c)+(d) after f_i: a variable never used again is freed (INPUT, TEMP) or
+//           written back (PARAM, STATE, OUTPUT); one used again inside the
+//           window is kept; any other is swapped out.
+// Budget accounting uses chunk-rounded sizes a_v = ceil(b_v / m_c) m_c
+// (eq. 1), so the chunks the pool maps never exceed the budget.
+#include <algorithm>
+#include <functional>
+#include <queue>
+
+#include "internal.h"
+
+namespace ooc {
+
+static bool persistent(int32_t kind) {
+  return kind == OOC_INPUT || kind == OOC_PARAM || kind == OOC_STATE;
+}
+
+ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& fns,
+                          uint64_t budget, uint64_t window, uint64_t chunk, int policy,
+                          Schedule* out, std::string* err) {
+  const int64_t N = (int64_t)fns.size();
+  const int64_t nv = (int64_t)vars.size();
+  std::vector<uint64_t> a(nv);
+  for (int64_t v = 0; v < nv; ++v) a[v] = round_up(vars[v].bytes, chunk);
+
+  std::vector<int64_t> seq, first(N), last(N);
+  for (int64_t i = 0; i < N; ++i) {
+    first[i] = (int64_t)seq.size();
+    for (const FnVar& fv : fns[i].vars) seq.push_back(fv.var);
+    last[i] = (int64_t)seq.size() - 1;
+  }
+  const int64_t M = (int64_t)seq.size();
+  std::vector<int64_t> next(M, -1), seen(nv, -1);
+  for (int64_t p = M - 1; p >= 0; --p) {
+    next[p] = seen[seq[p]];
+    seen[seq[p]] = p;
+  }
+  std::vector<uint64_t> pre(M + 1, 0);
+  for (int64_t p = 0; p < M; ++p) pre[p + 1] = pre[p] + vars[seq[p]].bytes;
+
+  std::vector<uint8_t> state(nv);
+  for (int64_t v = 0; v < nv; ++v) state[v] = persistent(vars[v].kind) ? HOST : UNMAT;
+
+  // pending swap-outs, oldest first; cancelled entries are skipped lazily
+  struct Entry { int64_t var; bool alive; };
+  std::vector<Entry> fifo;
+  size_t head = 0, alive = 0;
+  std::vector<int64_t> entry_of(nv, -1);   // CANCEL policy: the variable's pending entry
+  std::vector<int32_t> queued(nv, 0);      // live entries per variable
+
+  Schedule s;
+  uint64_t held = 0;
+  auto emit = [&](int32_t i, uint8_t phase, uint8_t kind, int64_t v) {
+    s.ops.push_back(Op{i, phase, kind, v, held});
+  };
+  auto pop_oldest = [&](int32_t i, uint8_t phase) {
+    while (!fifo[head].alive) ++head;
+    const int64_t w = fifo[head].var;
+    fifo[head].alive = false;
+    ++head;
+    --alive;
+    --queued[w];
+    entry_of[w] = -1;
+    held -= a[w];
+    // the state follows the newest copy: HOST only when no newer copy exists
+    if (state[w] == PEND && queued[w] == 0) state[w] = HOST;
+    emit(i, phase, OOC_WAIT_OUT, w);
+  };
+
+  int64_t r_prev = -1, r_hat = -1;
+  for (int64_t i = 0; i < N; ++i) {
+    const int64_t l = first[i], e = last[i];
+    if (r_hat < l - 1) r_hat = l - 1;
+    while (r_hat + 1 < M && pre[r_hat + 2] - pre[l] <= window) ++r_hat;
+    int64_t r = std::max(std::max(r_hat, e), r_prev);
+
+    for (int64_t p = r_prev + 1; p <= r; ++p) {
+      const int64_t u = seq[p];
+      if (state[u] == DEV) continue;
+      if (state[u] == PEND && policy == OOC_POLICY_CANCEL) {
+        fifo[entry_of[u]].alive = false;
+        entry_of[u] = -1;
+        --alive;
+        --queued[u];
+        state[u] = DEV;
+        emit((int32_t)i, OOC_PRE, OOC_CANCEL, u);
+        continue;
+      }
+      const uint64_t need = a[u];
+      while (held + need > budget && alive > 0) pop_oldest((int32_t)i, OOC_PRE);
+      if (held + need <= budget) {
+        uint8_t kind = OOC_ALLOC;
+        if (state[u] != UNMAT) {
+          kind = OOC_SWAPIN;
+          s.h2d += vars[u].bytes;
+        }
+        state[u] = DEV;
+        held += need;
+        emit((int32_t)i, OOC_PRE, kind, u);
+      } else if (p <= e) {
+        *err = "function " + std::to_string(i) + " needs more than the budget of " +
+               std::to_string(budget) + " bytes";
+        return OOC_E_INFEASIBLE;
+      } else {
+        r = p - 1;
+        break;
+      }
+    }
+    s.windows.push_back(r);
+
+    for (size_t j = 0; j < fns[i].vars.size(); ++j) {
+      const int64_t u = fns[i].vars[j].var;
+      const int64_t n = next[l + (int64_t)j];
+      const int32_t kind = vars[u].kind;
+      if (n < 0 && (kind == OOC_INPUT || kind == OOC_TEMP)) {
+        state[u] = UNMAT;
+        held -= a[u];
+        emit((int32_t)i, OOC_POST, OOC_FREE, u);
+      } else if (n >= 0 && n <= r) {
+        // already reserved inside the window: keep it on the device
+      } else {
+        state[u] = PEND;
+        entry_of[u] = (int64_t)fifo.size();
+        fifo.push_back(Entry{u, true});
+        ++alive;
+        ++queued[u];
+        s.d2h += vars[u].bytes;
+        emit((int32_t)i, OOC_POST, OOC_SWAPOUT, u);
+      }
+    }
+    r_prev = r;
+  }
+  while (alive > 0) pop_oldest((int32_t)N, OOC_END);
+  for (const Op& o : s.ops) s.peak = std::max(s.peak, o.held);
+  *out = std::move(s);
+  return OOC_OK;
+}
+
+static void first_last_use(const std::vector<Var>& vars, const std::vector<Fn>& fns,
+                           std::vector<int64_t>* fu, std::vector<int64_t>* lu) {
+  fu->assign(vars.size(), -1);
+  lu->assign(vars.size(), -1);
+  for (int64_t i = 0; i < (int64_t)fns.size(); ++i)
+    for (const FnVar& fv : fns[i].vars) {
+      if ((*fu)[fv.var] < 0) (*fu)[fv.var] = i;
+      (*lu)[fv.var] = i;
+    }
+}
+
+void build_incore(const std::vector<Var>& vars, const std::vector<Fn>& fns, uint64_t chunk,
+                  Schedule* out) {
+  std::vector<int64_t> fu, lu;
+  first_last_use(vars, fns, &fu, &lu);
+  Schedule s;
+  uint64_t held = 0;
+  for (const Var& v : vars)
+    if (v.kind != OOC_TEMP) held += round_up(v.bytes, chunk);
+  s.peak = held;
+  for (int64_t i = 0; i < (int64_t)fns.size(); ++i) {
+    for (const FnVar& fv : fns[i].vars)
+      if (vars[fv.var].kind == OOC_TEMP && fu[fv.var] == i) {
+        held += round_up(vars[fv.var].bytes, chunk);
+        s.ops.push_back(Op{(int32_t)i, OOC_PRE, OOC_ALLOC, fv.var, held});
+        s.peak = std::max(s.peak, held);
+      }
+    for (const FnVar& fv : fns[i].vars)
+      if (vars[fv.var].kind == OOC_TEMP && lu[fv.var] == i) {
+        held -= round_up(vars[fv.var].bytes, chunk);
+        s.ops.push_back(Op{(int32_t)i, OOC_POST, OOC_FREE, fv.var, held});
+      }
+  }
+  *out = std::move(s);
+}
+
+uint64_t incore_peak(const std::vector<Var>& vars, const std::vector<Fn>& fns, uint64_t chunk) {
+  Schedule s;
+  build_incore(vars, fns, chunk, &s);
+  return s.peak;
+}
+
+uint64_t working_set_max(const std::vector<Var>& vars, const std::vector<Fn>& fns,
+                         uint64_t chunk) {
+  uint64_t best = 0;
+  for (const Fn& f : fns) {
+    uint64_t sum = 0;
+    for (const FnVar& fv : f.vars) sum += round_up(vars[fv.var].bytes, chunk);
+    best = std::max(best, sum);
+  }
+  return best;
+}
+
+// Chunk cache handing out the lowest free id first.  Freed ids are always
+// below the next fresh id, so the ids in use stay below the most chunks ever
+// in use at once: the pool needs exactly that many.
+namespace {
+struct ChunkCache {
+  std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> freed;
+  int32_t fresh = 0;
+  uint64_t in_use = 0, max_in_use = 0;
+  void take(uint64_t k, std::vector<int32_t>* out) {
+    for (uint64_t j = 0; j < k; ++j) {
+      if (!freed.empty()) {
+        out->push_back(freed.top());
+        freed.pop();
+      } else {
+        out->push_back(fresh++);
+      }
+    }
+    in_use += k;
+    max_in_use = std::max(max_in_use, in_use);
+  }
+  void give(const std::vector<int32_t>& cs) {
+    for (int32_t c : cs) freed.push(c);
+    in_use -= cs.size();
+  }
+};
+}  // namespace
+
+void build_plan(const std::vector<Var>& vars, const Schedule& s, bool incore, uint64_t chunk,
+                Plan* out) {
+  Plan plan;
+  ChunkCache cache;
+  std::vector<int64_t> working(vars.size(), -1);
+  std::vector<int64_t> pending;   // interval ids with an issued swap-out, oldest first
+  size_t head = 0;
+  auto open = [&](int64_t v, int64_t op) {
+    Interval iv{v, op, -1, {}};
+    cache.take(round_up(vars[v].bytes, chunk) / chunk, &iv.chunks);
+    plan.intervals.push_back(std::move(iv));
+    working[v] = (int64_t)plan.intervals.size() - 1;
+    return working[v];
+  };
+  auto close = [&](int64_t id, int64_t op) {
+    plan.intervals[id].close = op;
+    cache.give(plan.intervals[id].chunks);
+  };
+  if (incore)
+    for (int64_t v = 0; v < (int64_t)vars.size(); ++v)
+      if (vars[v].kind != OOC_TEMP) open(v, -1);
+  plan.op_interval.assign(s.ops.size(), -1);
+  for (int64_t k = 0; k < (int64_t)s.ops.size(); ++k) {
+    const Op& o = s.ops[k];
+    int64_t id = -1;
+    switch (o.kind) {
+      case OOC_SWAPIN:
+      case OOC_ALLOC:
+        id = open(o.var, k);
+        break;
+      case OOC_SWAPOUT:
+        id = working[o.var];
+        pending.push_back(id);
+        working[o.var] = -1;
+        break;
+      case OOC_CANCEL:
+        for (size_t j = head; j < pending.size(); ++j)
+          if (pending[j] >= 0 && plan.intervals[pending[j]].var == o.var) {
+            id = pending[j];
+            pending[j] = -1;
+            break;
+          }
+        working[o.var] = id;
+        break;
+      case OOC_WAIT_OUT:
+        while (pending[head] < 0) ++head;
+        id = pending[head++];
+        close(id, k);
+        break;
+      case OOC_FREE:
+        id = working[o.var];
+        working[o.var] = -1;
+        close(id, k);
+        break;
+    }
+    plan.op_interval[k] = id;
+  }
+  plan.max_chunks_used = cache.max_in_use;
+  plan.n_chunks = cache.max_in_use;
+  *out = std::move(plan);
+}
+
+}  // namespace ooc

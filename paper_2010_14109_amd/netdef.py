@@ -1,0 +1,273 @@
+"""Lowering of a network description to the library's function sequence.
+
+The paper executes a network as the topological sequence of its functions,
+each with the set of variables it uses (Section 2; Section 3,
+variable-sequence).  ``Net`` builds that sequence for one training step and
+registers it through the C interface:
+
+* forward functions in layer order, then the fused softmax cross-entropy;
+* per layer in reverse order: its backward functions, one SGD function for
+  its parameters, then the additions that sum the gradient contributions of
+  tensors consumed more than once (in the order the contributions appear);
+  an addition's own backward is the identity and needs no function.
+
+Variables are numbered by first appearance.  Variable lists, sizes and
+kinds follow the operation table of ``include/ooc.h``; the auxiliary sizes are
+fixed per shape: a BatchNorm keeps 2 + 2 S floats per channel with S =
+min(ceil(rows / 512), 2048) row slices, and a convolution's filter gradient
+is split over S_w = min(ceil(1024 / T), ceil(L / 1024)) pixel slices (at
+least 1) with T = ceil(K / 128) ceil(R S C / 128) output tiles and L = N P Q
+pixels, using a partial-sum variable of S_w copies of dW when S_w > 1.
+"""
+
+from __future__ import annotations
+
+from math import ceil, prod
+
+from . import ooc
+
+FLOAT = 4
+
+
+def bn_row_slices(rows):
+    return min(ceil(rows / 512), 2048)
+
+
+def wgrad_pixel_slices(k_out, rsc, pixels):
+    tiles = ceil(k_out / 128) * ceil(rsc / 128)
+    return max(1, min(ceil(1024 / tiles), ceil(pixels / 1024)))
+
+
+class Net:
+    """Function sequence of one training step of ``spec``."""
+
+    def __init__(self, spec, keep_grads=False):
+        self.spec = spec
+        self.keep_grads = keep_grads
+        self.meta = {}        # name -> (shape, dtype, kind)
+        self.calls = []       # (op, [(name, access)], attrs)
+        self.shape = {}
+        self.params = {}      # layer name -> [param names]
+        self._lower()
+        self._number()
+
+    # ------------------------------------------------------------ helpers
+    def _decl(self, name, shape, dtype="f32", kind=ooc.TEMP):
+        self.meta[name] = (tuple(int(s) for s in shape), dtype, kind)
+        return name
+
+    def _call(self, op, pairs, attrs):
+        self.calls.append((op, pairs, [int(a) for a in attrs]))
+
+    # ------------------------------------------------------------ forward
+    def _fwd_linear(self, L, X):
+        n, fin = self.shape[X]
+        fout = L["out_features"]
+        W = self._decl(L["name"] + ".W", (fout, fin), kind=ooc.PARAM)
+        b = self._decl(L["name"] + ".b", (fout,), kind=ooc.PARAM)
+        self.params[L["name"]] = [W, b]
+        Y = self._decl(L["name"], (n, fout))
+        self._call("linear_fwd", [(X, ooc.R), (W, ooc.R), (b, ooc.R), (Y, ooc.W)], [n, fin, fout])
+        return (n, fout)
+
+    def _conv_attrs(self, L, xs):
+        n, h, w, c = xs
+        k, st, pd = L["k"], L["stride"], L["pad"]
+        p_, q_ = (h + 2 * pd - k) // st + 1, (w + 2 * pd - k) // st + 1
+        return [n, h, w, c, L["cout"], k, k, st, pd, p_, q_]
+
+    def _fwd_conv(self, L, X):
+        a = self._conv_attrs(L, self.shape[X])
+        n, _, _, c, K, R, S, _, _, P, Q = a
+        W = self._decl(L["name"] + ".W", (K, R, S, c), kind=ooc.PARAM)
+        self.params[L["name"]] = [W]
+        Y = self._decl(L["name"], (n, P, Q, K))
+        self._call("conv_fwd", [(X, ooc.R), (W, ooc.R), (Y, ooc.W)], a)
+        return (n, P, Q, K)
+
+    def _fwd_bn(self, L, X):
+        xs = self.shape[X]
+        c, rows = xs[-1], prod(xs[:-1])
+        S = bn_row_slices(rows)
+        g = self._decl(L["name"] + ".gamma", (c,), kind=ooc.PARAM)
+        bt = self._decl(L["name"] + ".beta", (c,), kind=ooc.PARAM)
+        self.params[L["name"]] = [g, bt]
+        Y = self._decl(L["name"], xs)
+        st = self._decl(L["name"] + ".stats", ((2 + 2 * S) * c,))
+        self._call("bn_fwd", [(X, ooc.R), (g, ooc.R), (bt, ooc.R), (Y, ooc.W), (st, ooc.W)],
+                   [rows, c, S])
+        return xs
+
+    def _fwd_relu(self, L, X):
+        xs = self.shape[X]
+        Y = self._decl(L["name"], xs)
+        self._call("relu_fwd", [(X, ooc.R), (Y, ooc.W)], [prod(xs)])
+        return xs
+
+    def _pool_attrs(self, L, xs):
+        n, h, w, c = xs
+        k, st, pd = L["k"], L["stride"], L["pad"]
+        return [n, h, w, c, k, st, pd, (h + 2 * pd - k) // st + 1, (w + 2 * pd - k) // st + 1]
+
+    def _fwd_maxpool(self, L, X):
+        a = self._pool_attrs(L, self.shape[X])
+        ys = (a[0], a[7], a[8], a[3])
+        Y = self._decl(L["name"], ys)
+        ix = self._decl(L["name"] + ".idx", ys, dtype="u8")
+        self._call("maxpool_fwd", [(X, ooc.R), (Y, ooc.W), (ix, ooc.W)], a)
+        return ys
+
+    def _fwd_avgpool(self, L, X):
+        n, h, w, c = self.shape[X]
+        Y = self._decl(L["name"], (n, c))
+        self._call("avgpool_fwd", [(X, ooc.R), (Y, ooc.W)], [n, h, w, c])
+        return (n, c)
+
+    def _fwd_add(self, L, X):
+        B = L["in"][1]
+        xs = self.shape[X]
+        if self.shape[B] != xs:
+            raise ValueError(f"add {L['name']}: shapes differ")
+        Y = self._decl(L["name"], xs)
+        self._call("add", [(X, ooc.R), (B, ooc.R), (Y, ooc.W)], [prod(xs)])
+        return xs
+
+    # ------------------------------------------------------------ backward
+    def _grad_of_param(self, p):
+        return self._decl("d:" + p, self.meta[p][0],
+                          kind=ooc.OUTPUT if self.keep_grads else ooc.TEMP)
+
+    def _sgd(self, layer):
+        mom = self.spec["optimizer"]["momentum"]
+        pairs = []
+        for p in self.params[layer]:
+            pairs += [(p, ooc.RW), ("d:" + p, ooc.R)]
+            if mom:
+                pairs.append((self._decl("m:" + p, self.meta[p][0], kind=ooc.STATE), ooc.RW))
+        self._call("sgd", pairs, [len(self.params[layer]), 1 if mom else 0])
+
+    def _bwd(self, L, dY, out):
+        """Emits L's backward functions; appends (tensor, gradient) contributions to out."""
+        name, X = L["name"], L["in"][0]
+        xs = self.shape[X]
+        op = L["op"]
+        if op == "linear":
+            W, b = self.params[name]
+            n, fin = xs
+            attrs = [n, fin, L["out_features"]]
+            self._call("linear_bwd_w", [(X, ooc.R), (dY, ooc.R), (self._grad_of_param(W), ooc.W),
+                                        (self._grad_of_param(b), ooc.W)], attrs)
+            if X != "x":
+                dX = self._decl(f"d:{X}@{name}", xs)
+                self._call("linear_bwd_x", [(W, ooc.R), (dY, ooc.R), (dX, ooc.W)], attrs)
+                out.append((X, dX))
+            self._sgd(name)
+        elif op == "conv":
+            (W,) = self.params[name]
+            a = self._conv_attrs(L, xs)
+            n, _, _, c, K, R, S, _, _, P, Q = a
+            sw = wgrad_pixel_slices(K, R * S * c, n * P * Q)
+            pairs = [(X, ooc.R), (dY, ooc.R), (self._grad_of_param(W), ooc.W)]
+            if sw > 1:
+                pairs.append((self._decl(name + ".part", (sw * K * R * S * c,)), ooc.W))
+            self._call("conv_bwd_w", pairs, a + [sw])
+            if X != "x":
+                dX = self._decl(f"d:{X}@{name}", xs)
+                self._call("conv_bwd_x", [(W, ooc.R), (dY, ooc.R), (dX, ooc.W)], a)
+                out.append((X, dX))
+            self._sgd(name)
+        elif op == "bn":
+            g, bt = self.params[name]
+            rows, c = prod(xs[:-1]), xs[-1]
+            dX = self._decl(f"d:{X}@{name}", xs)
+            self._call("bn_bwd", [(X, ooc.R), (g, ooc.R), (name + ".stats", ooc.RW), (dY, ooc.R),
+                                  (dX, ooc.W), (self._grad_of_param(g), ooc.W),
+                                  (self._grad_of_param(bt), ooc.W)],
+                       [rows, c, bn_row_slices(rows)])
+            out.append((X, dX))
+            self._sgd(name)
+        elif op == "relu":
+            dX = self._decl(f"d:{X}@{name}", xs)
+            self._call("relu_bwd", [(name, ooc.R), (dY, ooc.R), (dX, ooc.W)], [prod(xs)])
+            out.append((X, dX))
+        elif op == "maxpool":
+            dX = self._decl(f"d:{X}@{name}", xs)
+            self._call("maxpool_bwd", [(name + ".idx", ooc.R), (dY, ooc.R), (dX, ooc.W)],
+                       self._pool_attrs(L, xs))
+            out.append((X, dX))
+        elif op == "avgpool":
+            dX = self._decl(f"d:{X}@{name}", xs)
+            self._call("avgpool_bwd", [(dY, ooc.R), (dX, ooc.W)], list(xs))
+            out.append((X, dX))
+        elif op == "add":
+            for src in L["in"]:
+                out.append((src, dY))
+
+    # ------------------------------------------------------------ whole step
+    def _lower(self):
+        spec = self.spec
+        self.shape["x"] = tuple(spec["input"])
+        self._decl("x", spec["input"], kind=ooc.INPUT)
+        fwd = {"linear": self._fwd_linear, "conv": self._fwd_conv, "bn": self._fwd_bn,
+               "relu": self._fwd_relu, "maxpool": self._fwd_maxpool,
+               "avgpool": self._fwd_avgpool, "add": self._fwd_add}
+        for L in spec["layers"]:
+            self.shape[L["name"]] = fwd[L["op"]](L, L["in"][0])
+        logits = spec["logits"]
+        n, classes = self.shape[logits]
+        self._decl("labels", (n,), dtype="i32", kind=ooc.INPUT)
+        self._decl("loss", (n + 1,), kind=ooc.OUTPUT)
+        dlogits = self._decl("d:" + logits, (n, classes))
+        self._call("softmax_ce", [(logits, ooc.R), ("labels", ooc.R), ("loss", ooc.W),
+                                  (dlogits, ooc.W)], [n, classes])
+        grads = {logits: dlogits}
+        sums = {}
+        for L in reversed(spec["layers"]):
+            if L["name"] not in grads:
+                continue
+            contributions = []
+            self._bwd(L, grads[L["name"]], contributions)
+            for tensor, g in contributions:
+                if tensor == "x":
+                    continue
+                if tensor in grads:
+                    sums[tensor] = sums.get(tensor, 1) + 1
+                    acc = self._decl(f"d:{tensor}#{sums[tensor]}", self.shape[tensor])
+                    self._call("add", [(grads[tensor], ooc.R), (g, ooc.R), (acc, ooc.W)],
+                               [prod(self.shape[tensor])])
+                    grads[tensor] = acc
+                else:
+                    grads[tensor] = g
+
+    def _number(self):
+        self.ids = {}
+        for _, pairs, _ in self.calls:
+            for nm, _ in pairs:
+                self.ids.setdefault(nm, len(self.ids))
+        self.names = sorted(self.ids, key=self.ids.get)
+        itemsize = {"f32": 4, "i32": 4, "u8": 1}
+        self.var_bytes = [prod(self.meta[n][0]) * itemsize[self.meta[n][1]] for n in self.names]
+        self.var_kinds = [self.meta[n][2] for n in self.names]
+        self.fn_vars = [[(self.ids[nm], a) for nm, a in pairs] for _, pairs, _ in self.calls]
+        self.fn_ops = [op for op, _, _ in self.calls]
+        self.fn_attrs = [attrs for _, _, attrs in self.calls]
+
+    # ------------------------------------------------------------ C interface
+    def register(self, ctx):
+        """Adds every variable and function to ``ctx`` (an ``ooc.Context``)."""
+        for nb, kd in zip(self.var_bytes, self.var_kinds):
+            ctx.add_var(nb, kd)
+        for op, vs, attrs in zip(self.fn_ops, self.fn_vars, self.fn_attrs):
+            ctx.add_fn(op, [v for v, _ in vs], [a for _, a in vs], attrs)
+        return self
+
+    def var(self, name):
+        return self.ids[name]
+
+    def view(self, ctx, name):
+        """Host slot of a persistent variable as an array of its shape."""
+        shape, dtype, _ = self.meta[name]
+        return ctx.host_view(self.ids[name], dtype, shape)
+
+    def param_names(self):
+        return [n for n in self.names if self.meta[n][2] == ooc.PARAM]

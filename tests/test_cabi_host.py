@@ -1,0 +1,238 @@
+"""The C library on the host (no GPU): exports, call order, validation, and
+bit-exact parity of its function sequence, schedule and chunk plan with the
+oracle's independent ones."""
+
+import os
+import random
+import re
+
+import pytest
+
+from oracle import pool as opool
+from oracle import schedule as S
+from oracle.lower import lower, as_schedule_input
+from paper_2010_14109_amd import netdef, ooc, synth
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "ooc.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(ooc_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol(lib):
+    names = declared_symbols()
+    assert names == sorted(ooc.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def specs_small():
+    return [
+        synth.mlp(batch=4, width=16, depth=4, classes=5),
+        synth.mlp(batch=3, width=8, depth=2, classes=3, momentum=0.9),
+        synth.plain_cnn(batch=2, channels=4, depth=3, hw=8, classes=5),
+        synth.resnet(batch=2, hw=32, classes=7, blocks=(1, 2, 1, 1), width=4),
+    ]
+
+
+def specs_full():
+    return [synth.workload(n) for n in ("mlp", "cnn", "resnet50_b256", "resnet50_b1440")]
+
+
+@pytest.mark.parametrize("spec", specs_small() + specs_full(), ids=lambda s: s["name"])
+@pytest.mark.parametrize("keep", [False, True])
+def test_function_sequence_matches_oracle_lowering(spec, keep):
+    mine = netdef.Net(spec, keep_grads=keep)
+    ref = lower(spec, keep_grads=keep)
+    assert mine.var_bytes == [v["bytes"] for v in ref["vars"]]
+    assert mine.var_kinds == [v["kind"] for v in ref["vars"]]
+    assert mine.names == [v["name"] for v in ref["vars"]]
+    opname = {"add_fwd": "add", "add_grad": "add"}
+    assert mine.fn_ops == [opname.get(f["op"], f["op"]) for f in ref["fns"]]
+    assert mine.fn_vars == [f["vars"] for f in ref["fns"]]
+
+
+def host_ctx(net, budget, window, chunk, policy):
+    ctx = ooc.Context(-1)
+    net.register(ctx)
+    ctx.set_chunk(chunk)
+    ctx.set_budget(budget)
+    if window is not None:
+        ctx.set_window(window)
+    ctx.set_policy(policy)
+    ctx.build_schedule()
+    return ctx
+
+
+@pytest.mark.parametrize("spec", specs_small() + specs_full(), ids=lambda s: s["name"])
+def test_schedule_and_plan_match_oracle(spec):
+    net = netdef.Net(spec)
+    b, k, f = as_schedule_input(lower(spec))
+    full = spec["input"][0] >= 128
+    chunks = (2 << 20,) if full else (64, 4096)
+    fracs = (1.0, 0.5, 0.25, 1 / 7.5, 0.0) if full else (1.0, 0.75, 0.5, 0.4, 0.25, 1 / 7.5, 0.2, 0.0)
+    for chunk in chunks:
+        ctx0 = host_ctx(net, ooc.UNLIMITED, None, chunk, "C")
+        p = S.incore_peak(b, k, f, chunk)
+        ws = S.working_set_max(b, f, chunk)
+        assert ctx0.incore_peak() == p
+        assert ctx0.working_set_max() == ws
+        inc = S.incore_plan(b, k, f, chunk)
+        ops0, held0 = ctx0.schedule()
+        assert ops0 == inc["ops"] and held0 == inc["held"]
+        ctx0.close()
+        for frac in fracs:
+            B = max(S.budget_for(frac, p, chunk), ws)
+            wins = (0, B // 4, B // 2, B, S.INCORE) if not full else (0, B // 2, B)
+            for W in wins:
+                for policy in ("C", "L"):
+                    ref = S.build(b, k, f, B, W, chunk, policy)
+                    ctx = host_ctx(net, B, W, chunk, policy)
+                    ops, held = ctx.schedule()
+                    assert ops == ref["ops"], (frac, W, policy)
+                    assert held == ref["held"]
+                    assert ctx.windows() == ref["windows"]
+                    st = ctx.stats()
+                    assert (st["peak_accounted"], st["sched_h2d_bytes"], st["sched_d2h_bytes"]) == \
+                        (ref["peak"], ref["h2d"], ref["d2h"])
+                    ivs, max_used = opool.assign(ref["ops"], b, B // chunk, chunk)
+                    got = ctx.plan()
+                    assert [(g["var"], g["open"], g["close"], g["chunks"]) for g in got] == \
+                        [(i["var"], i["open"], i["close"], i["chunks"]) for i in ivs]
+                    assert st["max_chunks_used"] == max_used
+                    ctx.close()
+
+
+def random_registration(rng, nv=10, nf=14, maxsize=64):
+    kinds = [rng.choice([S.INPUT, S.PARAM, S.STATE, S.TEMP, S.TEMP, S.TEMP, S.OUTPUT])
+             for _ in range(nv)]
+    sizes = [rng.randint(1, maxsize) for _ in range(nv)]
+    produced = [kd in (S.INPUT, S.PARAM, S.STATE) for kd in kinds]
+    fns = []
+    for _ in range(nf):
+        row = []
+        for v in rng.sample(range(nv), rng.randint(1, min(4, nv))):
+            if not produced[v]:
+                a = S.W
+            elif kinds[v] == S.INPUT:
+                a = S.R
+            else:
+                a = rng.choice([S.R, S.RW, S.W])
+            produced[v] = True
+            row.append((v, a))
+        fns.append(row)
+    return sizes, kinds, fns
+
+
+def test_random_sequences_match_oracle(lib):
+    rng = random.Random(2024)
+    for trial in range(300):
+        b, k, f = random_registration(rng, nv=rng.randint(1, 12), nf=rng.randint(1, 20))
+        chunk = rng.choice([1, 8, 32])
+        ws = S.working_set_max(b, f, chunk)
+        B = rng.choice([ws, ws + chunk, 2 * ws, 10 ** 6])
+        W = rng.choice([0, 8, 64, 512, S.INCORE])
+        policy = rng.choice("CL")
+        ref = S.build(b, k, f, B, W, chunk, policy)
+        ctx = ooc.Context(-1)
+        for nb, kd in zip(b, k):
+            ctx.add_var(nb, kd)
+        for vs in f:
+            ctx.add_fn("noop", [v for v, _ in vs], [a for _, a in vs])
+        ctx.set_chunk(chunk)
+        ctx.set_budget(B)
+        ctx.set_window(W)
+        ctx.set_policy(policy)
+        ctx.build_schedule()
+        ops, held = ctx.schedule()
+        assert ops == ref["ops"], trial
+        assert held == ref["held"], trial
+        assert ctx.windows() == ref["windows"], trial
+        ivs, _ = opool.assign(ref["ops"], b, B // chunk, chunk)
+        assert [(g["var"], g["open"], g["close"], g["chunks"]) for g in ctx.plan()] == \
+            [(i["var"], i["open"], i["close"], i["chunks"]) for i in ivs]
+        with pytest.raises(ooc.OocError) as e:
+            ctx.prepare()          # host-only context
+        assert e.value.status == ooc.E_UNSUPPORTED
+        ctx.close()
+
+
+def test_infeasible_budget_reports_error(lib):
+    spec = specs_small()[0]
+    net = netdef.Net(spec)
+    b, k, f = as_schedule_input(lower(spec))
+    ws = S.working_set_max(b, f, 1)
+    ctx = ooc.Context(-1)
+    net.register(ctx)
+    ctx.set_chunk(1)
+    ctx.set_budget(ws - 1)
+    with pytest.raises(ooc.OocError) as e:
+        ctx.build_schedule()
+    assert e.value.status == ooc.E_INFEASIBLE
+    ctx.close()
+
+
+def test_call_order_and_validation(lib):
+    ctx = ooc.Context(-1)
+    with pytest.raises(ooc.OocError) as e:
+        ctx.build_schedule()                       # nothing registered
+    assert e.value.status == ooc.E_INVALID
+    x = ctx.add_var(64, ooc.INPUT)
+    t = ctx.add_var(64, ooc.TEMP)
+    with pytest.raises(ooc.OocError) as e:         # TEMP read before written
+        ctx.add_fn("relu_fwd", [t, x], [ooc.R, ooc.W], [16])
+    assert e.value.status == ooc.E_INVALID
+    with pytest.raises(ooc.OocError) as e:         # INPUT written
+        ctx.add_fn("noop", [x], [ooc.RW])
+    assert e.value.status == ooc.E_INVALID
+    with pytest.raises(ooc.OocError) as e:         # sizes contradict the attributes
+        ctx.add_fn("relu_fwd", [x, t], [ooc.R, ooc.W], [17])
+    assert e.value.status == ooc.E_INVALID
+    with pytest.raises(ooc.OocError) as e:         # wrong access pattern
+        ctx.add_fn("relu_fwd", [x, t], [ooc.R, ooc.RW], [16])
+    with pytest.raises(ooc.OocError) as e:         # unknown op
+        ctx.add_fn(99, [x], [ooc.R])
+    with pytest.raises(ooc.OocError) as e:         # unknown variable
+        ctx.add_fn("noop", [7], [ooc.R])
+    ctx.add_fn("relu_fwd", [x, t], [ooc.R, ooc.W], [16])
+    with pytest.raises(ooc.OocError) as e:         # out of order
+        ctx.prepare()
+    assert e.value.status == ooc.E_STATE
+    ctx.set_budget(8 << 20)
+    ctx.build_schedule()
+    with pytest.raises(ooc.OocError) as e:
+        ctx.set_budget(5)
+    assert e.value.status == ooc.E_STATE
+    with pytest.raises(ooc.OocError) as e:
+        ctx.add_var(4, ooc.TEMP)
+    assert e.value.status == ooc.E_STATE
+    with pytest.raises(ooc.OocError) as e:
+        ctx.step(0.1)
+    assert e.value.status == ooc.E_STATE
+    ctx.close()
+    with pytest.raises(ooc.OocError):
+        ooc.Context(-2)
+
+
+def test_conv_and_bn_signatures_are_checked(lib):
+    ctx = ooc.Context(-1)
+    x = ctx.add_var(2 * 8 * 8 * 4 * 4, ooc.INPUT)
+    w = ctx.add_var(6 * 3 * 3 * 4 * 4, ooc.PARAM)
+    y = ctx.add_var(2 * 8 * 8 * 6 * 4, ooc.TEMP)
+    good = [2, 8, 8, 4, 6, 3, 3, 1, 1, 8, 8]
+    bad_out = [2, 8, 8, 4, 6, 3, 3, 1, 1, 7, 8]     # P does not follow from H
+    with pytest.raises(ooc.OocError):
+        ctx.add_fn("conv_fwd", [x, w, y], [ooc.R, ooc.R, ooc.W], bad_out)
+    with pytest.raises(ooc.OocError):
+        ctx.add_fn("conv_fwd", [x, w, y], [ooc.R, ooc.R, ooc.W], good[:-1])
+    ctx.add_fn("conv_fwd", [x, w, y], [ooc.R, ooc.R, ooc.W], good)
+    g = ctx.add_var(6 * 4, ooc.PARAM)
+    bt = ctx.add_var(6 * 4, ooc.PARAM)
+    yb = ctx.add_var(2 * 8 * 8 * 6 * 4, ooc.TEMP)
+    st = ctx.add_var((2 + 2 * 3) * 6 * 4, ooc.TEMP)
+    with pytest.raises(ooc.OocError):                 # stats too small for 4 slices
+        ctx.add_fn("bn_fwd", [y, g, bt, yb, st], [ooc.R] * 3 + [ooc.W] * 2, [128, 6, 4])
+    ctx.add_fn("bn_fwd", [y, g, bt, yb, st], [ooc.R] * 3 + [ooc.W] * 2, [128, 6, 3])
+    ctx.close()

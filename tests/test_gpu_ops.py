@@ -1,0 +1,245 @@
+"""Every kernel against the float64 oracle, one function at a time (GPU).
+
+Each case registers one function whose inputs are INPUT/PARAM variables and
+whose results are OUTPUT variables, runs it in-core through the C interface
+and compares with ``oracle.ops``.  Shapes are ragged on purpose: they span
+several 128 x 128 tiles and end in partial tiles, use channel counts that are
+and are not multiples of 4, and include empty split-K slices.
+
+Tolerance: relative L2 error <= 2e-5.  An fp32 sum of n terms carries a
+relative rounding error of order sqrt(n) * 6e-8; the longest reductions here
+(n <= 4608) stay below 5e-6, so 2e-5 leaves margin without hiding a wrong
+term (a dropped tap or a transposed operand is an O(1) error).
+"""
+
+import numpy as np
+import pytest
+
+from oracle import mixop, ops
+from paper_2010_14109_amd import netdef, ooc
+from tests.gpu_util import rel_l2
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-5
+rng = np.random.default_rng(77)
+
+NPT = {"f32": np.float32, "i32": np.int32, "u8": np.uint8, "u32": np.uint32}
+
+
+def run_fn(op, args, attrs):
+    """args: list of (array or (shape, dtype), access); arrays are inputs, tuples outputs.
+    Returns the final value of every variable, in order."""
+    ctx = ooc.Context(0)
+    try:
+        ids, dts = [], []
+        for a, acc in args:
+            if isinstance(a, np.ndarray):
+                kind = ooc.INPUT if acc == ooc.R else ooc.PARAM
+                ids.append(ctx.add_var(a.nbytes, kind))
+                dts.append((a.shape, a.dtype))
+            else:
+                shape, dt = a
+                nb = int(np.prod(shape)) * np.dtype(NPT[dt]).itemsize
+                ids.append(ctx.add_var(nb, ooc.OUTPUT))
+                dts.append((shape, np.dtype(NPT[dt])))
+        ctx.add_fn(op, ids, [acc for _, acc in args], attrs)
+        ctx.set_chunk(4096)
+        ctx.build_schedule()
+        ctx.prepare()
+        for (a, _), v, (shape, dt) in zip(args, ids, dts):
+            if isinstance(a, np.ndarray):
+                ctx.host_view(v, dt)[...] = a.reshape(-1)
+        ctx.upload()
+        ctx.step(0.0, 0.0)
+        ctx.download()
+        out = []
+        for (a, acc), v, (shape, dt) in zip(args, ids, dts):
+            if acc == ooc.R:
+                out.append(None)
+            else:
+                out.append(np.array(ctx.host_view(v, dt)).reshape(shape))
+        return out
+    finally:
+        ctx.close()
+
+
+def f32(*shape, scale=1.0):
+    return (rng.standard_normal(shape) * scale).astype(np.float32)
+
+
+def d(a):
+    return np.asarray(a, dtype=np.float64)
+
+
+# ---------------------------------------------------------------- dense
+@pytest.mark.parametrize("M,K,N", [(300, 200, 130), (5, 147, 10), (256, 1024, 1024), (1, 3, 1)])
+def test_linear(M, K, N):
+    X, Wt, b, G = f32(M, K), f32(N, K), f32(N), f32(M, N)
+    print(f"linear M={M} K={K} N={N}", flush=True)
+    (_, _, _, Y) = run_fn("linear_fwd", [(X, ooc.R), (Wt, ooc.R), (b, ooc.R),
+                                          (((M, N), "f32"), ooc.W)], [M, K, N])
+    assert rel_l2(Y, ops.linear_fwd(d(X), d(Wt), d(b))) < TOL
+    (_, _, dW, db) = run_fn("linear_bwd_w", [(X, ooc.R), (G, ooc.R), (((N, K), "f32"), ooc.W),
+                                              (((N,), "f32"), ooc.W)], [M, K, N])
+    rdW, rdb = ops.linear_bwd_w(d(X), d(G))
+    assert rel_l2(dW, rdW) < TOL and rel_l2(db, rdb) < TOL
+    (_, _, dX) = run_fn("linear_bwd_x", [(Wt, ooc.R), (G, ooc.R), (((M, K), "f32"), ooc.W)],
+                        [M, K, N])
+    assert rel_l2(dX, ops.linear_bwd_x(d(Wt), d(G))) < TOL
+
+
+# ---------------------------------------------------------------- conv
+CONVS = [  # N, H, W, C, K, k, stride, pad
+    (2, 9, 9, 4, 8, 3, 1, 1),
+    (2, 9, 9, 4, 8, 3, 2, 1),
+    (2, 15, 13, 3, 8, 7, 2, 3),
+    (2, 9, 9, 8, 12, 1, 1, 0),
+    (2, 9, 10, 8, 12, 1, 2, 0),
+    (3, 8, 8, 64, 64, 3, 1, 1),
+    (1, 5, 5, 132, 136, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", CONVS, ids=lambda s: "x".join(map(str, s)))
+def test_conv(shape):
+    N, H, Wd, C, K, k, st, pd = shape
+    print(f"conv {shape}", flush=True)
+    P, Q = (H + 2 * pd - k) // st + 1, (Wd + 2 * pd - k) // st + 1
+    a = [N, H, Wd, C, K, k, k, st, pd, P, Q]
+    X, Wt, G = f32(N, H, Wd, C), f32(K, k, k, C), f32(N, P, Q, K)
+    (_, _, Y) = run_fn("conv_fwd", [(X, ooc.R), (Wt, ooc.R), (((N, P, Q, K), "f32"), ooc.W)], a)
+    assert rel_l2(Y, ops.conv_fwd(d(X), d(Wt), st, pd)) < TOL
+    ref_dW = ops.conv_bwd_w(d(X), d(G), Wt.shape, st, pd)
+    for slices in sorted({1, netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q), 3, 7}):
+        slices = min(slices, N * P * Q)
+        args = [(X, ooc.R), (G, ooc.R), (((K, k, k, C), "f32"), ooc.W)]
+        if slices > 1:
+            args.append((((slices * K * k * k * C,), "f32"), ooc.W))
+        out = run_fn("conv_bwd_w", args, a + [slices])
+        assert rel_l2(out[2], ref_dW) < TOL, slices
+    if C % 4 == 0:
+        (_, _, dX) = run_fn("conv_bwd_x", [(Wt, ooc.R), (G, ooc.R),
+                                            (((N, H, Wd, C), "f32"), ooc.W)], a)
+        assert rel_l2(dX, ops.conv_bwd_x(d(Wt), d(G), X.shape, st, pd)) < TOL
+
+
+# ---------------------------------------------------------------- BatchNorm
+@pytest.mark.parametrize("rows,C,slices", [(162, 12, 1), (162, 12, 5), (162, 6, 4), (4096, 64, 8),
+                                           (3, 128, 3)])
+def test_batchnorm(rows, C, slices):
+    X = f32(rows, C, scale=2.0) + 0.5
+    g, b, G = f32(C), f32(C), f32(rows, C)
+    sb = (2 + 2 * slices) * C
+    print(f"bn rows={rows} C={C} slices={slices}", flush=True)
+    (_, _, _, Y, st) = run_fn("bn_fwd", [(X, ooc.R), (g, ooc.R), (b, ooc.R),
+                                          (((rows, C), "f32"), ooc.W), (((sb,), "f32"), ooc.W)],
+                              [rows, C, slices])
+    rY, mean, invstd = ops.bn_fwd(d(X), d(g), d(b))
+    assert rel_l2(Y, rY) < TOL
+    assert rel_l2(st[:C], mean) < TOL and rel_l2(st[C:2 * C], invstd) < TOL
+    out = run_fn("bn_bwd", [(X, ooc.R), (g, ooc.R), (st.astype(np.float32), ooc.RW), (G, ooc.R),
+                            (((rows, C), "f32"), ooc.W), (((C,), "f32"), ooc.W),
+                            (((C,), "f32"), ooc.W)], [rows, C, slices])
+    rdX, rdg, rdb = ops.bn_bwd(d(X), d(g), d(st[:C]), d(st[C:2 * C]), d(G))
+    assert rel_l2(out[4], rdX) < TOL and rel_l2(out[5], rdg) < TOL and rel_l2(out[6], rdb) < TOL
+
+
+# ---------------------------------------------------------------- elementwise
+@pytest.mark.parametrize("n", [1003, 4096, 1])
+def test_relu_add(n):
+    x, y, g = f32(n), f32(n), f32(n)
+    (_, r) = run_fn("relu_fwd", [(x, ooc.R), (((n,), "f32"), ooc.W)], [n])
+    assert np.array_equal(r, ops.relu_fwd(x))
+    (_, _, dx) = run_fn("relu_bwd", [(r, ooc.R), (g, ooc.R), (((n,), "f32"), ooc.W)], [n])
+    assert np.array_equal(dx, ops.relu_bwd(r, g))
+    (_, _, s) = run_fn("add", [(x, ooc.R), (y, ooc.R), (((n,), "f32"), ooc.W)], [n])
+    assert np.array_equal(s, x + y)
+
+
+def test_sgd_plain_and_momentum():
+    n = 1001
+    ctx_args = []
+    w, g, v = f32(n), f32(n), f32(n)
+    ctx = ooc.Context(0)
+    try:
+        iw, ig, iv = ctx.add_var(n * 4, ooc.PARAM), ctx.add_var(n * 4, ooc.INPUT), \
+            ctx.add_var(n * 4, ooc.STATE)
+        iw2 = ctx.add_var(n * 4, ooc.PARAM)
+        ctx.add_fn("sgd", [iw, ig, iv], [ooc.RW, ooc.R, ooc.RW], [1, 1])
+        ctx.add_fn("sgd", [iw2, ig], [ooc.RW, ooc.R], [1, 0])
+        ctx.set_chunk(4096)
+        ctx.build_schedule()
+        ctx.prepare()
+        for i, a in ((iw, w), (ig, g), (iv, v), (iw2, w)):
+            ctx.host_view(i)[...] = a
+        ctx.upload()
+        ctx.step(0.1, 0.9)
+        ctx.download()
+        rw, rv = ops.sgd_momentum(d(w), d(g), d(v), 0.1, 0.9)
+        assert rel_l2(ctx.host_view(iw), rw) < 1e-6 and rel_l2(ctx.host_view(iv), rv) < 1e-6
+        assert rel_l2(ctx.host_view(iw2), ops.sgd(d(w), d(g), 0.1)) < 1e-6
+    finally:
+        ctx.close()
+    del ctx_args
+
+
+# ---------------------------------------------------------------- pooling
+def test_maxpool_with_ties():
+    N, H, Wd, C, k, st, pd = 2, 9, 8, 8, 3, 2, 1
+    P, Q = (H + 2 * pd - k) // st + 1, (Wd + 2 * pd - k) // st + 1
+    X = f32(N, H, Wd, C)
+    X[0, 0, 0, :] = X[0, 0, 1, :] = 7.0
+    X[1, 4, 4, 3] = X[1, 4, 5, 3] = X[1, 5, 4, 3] = 9.0
+    a = [N, H, Wd, C, k, st, pd, P, Q]
+    (_, Y, idx) = run_fn("maxpool_fwd", [(X, ooc.R), (((N, P, Q, C), "f32"), ooc.W),
+                                         (((N, P, Q, C), "u8"), ooc.W)], a)
+    rY, ridx = ops.maxpool_fwd(d(X), k, st, pd)
+    assert np.array_equal(Y, rY.astype(np.float32)) and np.array_equal(idx, ridx)
+    G = f32(N, P, Q, C)
+    (_, _, dX) = run_fn("maxpool_bwd", [(ridx, ooc.R), (G, ooc.R),
+                                        (((N, H, Wd, C), "f32"), ooc.W)], a)
+    assert rel_l2(dX, ops.maxpool_bwd(ridx, d(G), X.shape, k, st, pd)) < 1e-6
+
+
+def test_avgpool():
+    N, H, Wd, C = 3, 7, 5, 12
+    X, G = f32(N, H, Wd, C), f32(N, C)
+    (_, Y) = run_fn("avgpool_fwd", [(X, ooc.R), (((N, C), "f32"), ooc.W)], [N, H, Wd, C])
+    assert rel_l2(Y, ops.avgpool_fwd(d(X))) < TOL
+    (_, dX) = run_fn("avgpool_bwd", [(G, ooc.R), (((N, H, Wd, C), "f32"), ooc.W)], [N, H, Wd, C])
+    assert rel_l2(dX, ops.avgpool_bwd(d(G), X.shape)) < TOL
+
+
+# ---------------------------------------------------------------- loss
+@pytest.mark.parametrize("N,C", [(37, 10), (5, 1000), (1, 1)])
+def test_softmax_ce(N, C):
+    Z = f32(N, C, scale=3.0)
+    y = rng.integers(0, C, N).astype(np.int32)
+    (_, _, loss, dZ) = run_fn("softmax_ce", [(Z, ooc.R), (y, ooc.R), (((N + 1,), "f32"), ooc.W),
+                                             (((N, C), "f32"), ooc.W)], [N, C])
+    rows, mean, rdZ = ops.softmax_ce(d(Z), y)
+    assert rel_l2(loss[:N], rows) < TOL and abs(loss[N] - mean) <= TOL * abs(mean) + 1e-7
+    assert rel_l2(dZ, rdZ) < TOL or np.abs(dZ - rdZ).max() < 1e-7
+
+
+def test_softmax_ce_out_of_range_label():
+    N, C = 4, 6
+    Z = f32(N, C)
+    y = np.array([0, 6, -1, 5], dtype=np.int32)
+    (_, _, loss, dZ) = run_fn("softmax_ce", [(Z, ooc.R), (y, ooc.R), (((N + 1,), "f32"), ooc.W),
+                                             (((N, C), "f32"), ooc.W)], [N, C])
+    assert np.isnan(loss[1]) and np.isnan(loss[2]) and np.isnan(loss[N])
+    assert np.all(dZ[1] == 0) and np.all(dZ[2] == 0)
+    rows, _, rdZ = ops.softmax_ce(d(Z[[0, 3]]), y[[0, 3]])
+    assert rel_l2(loss[[0, 3]], rows) < TOL
+
+
+# ---------------------------------------------------------------- integrity op
+def test_mix_op():
+    a = rng.integers(0, 2 ** 32, 17, dtype=np.uint64).astype(np.uint32)
+    b = rng.integers(0, 2 ** 32, 5, dtype=np.uint64).astype(np.uint32)
+    y0 = rng.integers(0, 2 ** 32, 9, dtype=np.uint64).astype(np.uint32)
+    (_, _, y) = run_fn("mix", [(a, ooc.R), (b, ooc.R), (y0, ooc.RW)], [12345])
+    assert np.array_equal(y, mixop.mix([a, b, y0], 9, 12345))
+    (_, y) = run_fn("mix", [(a, ooc.R), (((33,), "u32"), ooc.W)], [7])
+    assert np.array_equal(y, mixop.mix([a], 33, 7))
