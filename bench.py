@@ -72,6 +72,47 @@ def sgd_bytes(net, j):
     return total if mom in (0, 1) else 0
 
 
+MAP_ENTRY_LIMIT = 40000   # chunks + mappings per plan; the process table holds ~65530
+
+
+def plan_for(net, frac, window_frac, chunk):
+    """Budget, window and (chunks, mappings) of the out-of-core and in-core plans."""
+    ctx = ooc.Context(-1)
+    try:
+        net.register(ctx)
+        ctx.set_chunk(chunk)
+        p_incore, ws_max = ctx.incore_peak(), ctx.working_set_max()
+    finally:
+        ctx.close()
+    budget = max(int(p_incore * frac) // chunk * chunk, ws_max)
+    window = int(budget * window_frac)
+    counts = []
+    for b, w in ((budget, window), (ooc.UNLIMITED, None)):
+        ctx = ooc.Context(-1)
+        try:
+            net.register(ctx)
+            ctx.set_chunk(chunk)
+            ctx.set_budget(b)
+            if w is not None:
+                ctx.set_window(w)
+            ctx.build_schedule()
+            counts.append(sum(ctx.plan_counts()))
+        finally:
+            ctx.close()
+    return {"p_incore": p_incore, "ws_max": ws_max, "budget": budget, "window": window,
+            "map_entries": max(counts)}
+
+
+def choose_chunk(net, frac, window_frac):
+    """Smallest chunk (2 MiB .. 256 MiB) whose plans fit the memory-map table: the
+    trade-off of Section 4 between mapping overhead and internal fragmentation."""
+    for mib in (2, 4, 8, 16, 32, 64, 128, 256):
+        plan = plan_for(net, frac, window_frac, mib << 20)
+        if plan["map_entries"] <= MAP_ENTRY_LIMIT:
+            return mib << 20, plan
+    return 256 << 20, plan
+
+
 def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup):
     ctx = ooc.Context(0)
     try:
@@ -163,9 +204,10 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="cnn", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's batch")
     ap.add_argument("--budget-frac", type=float, default=None)
     ap.add_argument("--window-frac", type=float, default=0.5)
-    ap.add_argument("--chunk", type=int, default=2 << 20)
+    ap.add_argument("--chunk", type=int, default=0, help="bytes; 0 = smallest that fits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-incore", action="store_true")
     args = ap.parse_args()
@@ -174,20 +216,16 @@ def main():
                                    "(multi-GPU sharding is described, not built)"}))
         sys.exit(2)
 
-    spec = synth.workload(args.workload)
+    spec = synth.workload(args.workload, **({"batch": args.batch} if args.batch else {}))
     net = netdef.Net(spec)
+    frac = args.budget_frac if args.budget_frac is not None else synth.budget_fraction(args.workload)
+    if args.chunk:
+        chunk, plan = args.chunk, plan_for(net, frac, args.window_frac, args.chunk)
+    else:
+        chunk, plan = choose_chunk(net, frac, args.window_frac)
+    p_incore, budget, window = plan["p_incore"], plan["budget"], plan["window"]
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
-    chunk = args.chunk
-    frac = args.budget_frac if args.budget_frac is not None else synth.budget_fraction(args.workload)
-    hctx = ooc.Context(-1)
-    net.register(hctx)
-    hctx.set_chunk(chunk)
-    p_incore = hctx.incore_peak()
-    ws_max = hctx.working_set_max()
-    hctx.close()
-    budget = max(int(p_incore * frac) // chunk * chunk, ws_max)
-    window = int(budget * args.window_frac)
     batch = spec["input"][0]
 
     link = ooc.link_probe(0, 1 << 30, 3)
@@ -231,6 +269,7 @@ def main():
         "config": {"workload": spec["name"], "batch": batch, "budget_bytes": budget,
                    "budget_frac_of_incore_peak": round(budget / p_incore, 4),
                    "incore_peak_bytes": p_incore, "window_bytes": window, "chunk_bytes": chunk,
+                   "map_entries": plan["map_entries"],
                    "policy": "cancel"},
         "roofline": roof,
         "incore": None if inc is None else {

@@ -264,7 +264,10 @@ ooc_status ooc_plan_intervals(const ooc_ctx *ctx, ooc_interval *buf, uint64_t ca
 ooc_status ooc_plan_chunks(const ooc_ctx *ctx, int32_t *buf, uint64_t cap, uint64_t *n);
 
 /* Creates the physical chunks, maps every interval's chunks into its own
- * virtual range, allocates the pinned host arena, streams and events. */
+ * virtual range, allocates the pinned host arena, streams and events.
+ * Each chunk and each mapping of a chunk takes one entry of the process's
+ * memory-map table (vm.max_map_count, typically 65530): a plan needing more
+ * than the entries left returns OOC_E_UNSUPPORTED (choose a larger chunk). */
 ooc_status ooc_prepare(ooc_ctx *ctx);
 
 /* Pinned host slot of a host-backed variable (INPUT, PARAM, STATE, OUTPUT;

@@ -11,8 +11,11 @@
 
 namespace ooc {
 
-// One host<->device copy of the step program.
+// One host<->device copy of the step program (addresses resolved once the
+// host arena exists).
 struct Copy {
+  int64_t var;
+  int64_t iv;                   // device interval copied to or from
   void* dst;
   const void* src;
   uint64_t bytes;

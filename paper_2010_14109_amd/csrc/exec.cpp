@@ -25,6 +25,7 @@
 // host copy is still current (not written since it was swapped in).
 #include <algorithm>
 #include <chrono>
+#include <cstdio>
 #include <cstring>
 #include <set>
 
@@ -65,6 +66,23 @@ void release_device(ooc_ctx* ctx) {
   ctx->chunks.clear();
   if (ctx->arena) hipHostFree(ctx->arena);
   ctx->arena = nullptr;
+}
+
+// Entries of the process memory-map table still free (-1 if unknown).
+static int64_t map_entries_left() {
+  FILE* f = std::fopen("/proc/sys/vm/max_map_count", "r");
+  if (!f) return -1;
+  long long limit = -1;
+  if (std::fscanf(f, "%lld", &limit) != 1) limit = -1;
+  std::fclose(f);
+  if (limit < 0) return -1;
+  f = std::fopen("/proc/self/maps", "r");
+  if (!f) return -1;
+  int64_t used = 0;
+  for (int c; (c = std::fgetc(f)) != EOF;)
+    if (c == '\n') ++used;
+  std::fclose(f);
+  return limit - used;
 }
 
 static int32_t new_event(ooc_ctx* ctx, int8_t stream) {
@@ -151,7 +169,7 @@ static ooc_status compile(ooc_ctx* ctx) {
         case OOC_SWAPIN: {
           opened(J);
           working[o.var] = J;
-          Copy c{ctx->iv_ptr[J], ctx->host_slot[o.var], ctx->vars[o.var].bytes, {}, 0, 0};
+          Copy c{o.var, J, nullptr, nullptr, ctx->vars[o.var].bytes, {}, 0, 0};
           add_waits(&c.waits, preds[J], 1);
           if (var_d2h[o.var] >= 0) add_waits(&c.waits, {(int32_t)var_d2h[o.var]}, 1);
           c.ev_start = new_event(ctx, 1);
@@ -204,7 +222,7 @@ static ooc_status compile(ooc_ctx* ctx) {
       if (o.kind == OOC_SWAPOUT) {
         working[o.var] = -1;
         if (!cancelled[k] && !host_valid[o.var]) {
-          Copy c{ctx->host_slot[o.var], ctx->iv_ptr[J], ctx->vars[o.var].bytes, {}, 0, 0};
+          Copy c{o.var, J, nullptr, nullptr, ctx->vars[o.var].bytes, {}, 0, 0};
           c.waits.push_back(fp.ev_fn);
           c.ev_start = new_event(ctx, 2);
           c.ev_done = new_event(ctx, 2);
@@ -241,6 +259,21 @@ ooc_status prepare(ooc_ctx* ctx) {
   size_t free0 = 0, total0 = 0, free1 = 0, total1 = 0;
   HIPCK(hipMemGetInfo(&free0, &total0));
 
+  // Every physical chunk and every mapping of a chunk takes one entry of the
+  // process's memory-map table (vm.max_map_count); beyond it the driver
+  // rejects further access grants.  Refuse plans that cannot fit.
+  {
+    uint64_t maps = ctx->plan.n_chunks;
+    for (const Interval& iv : ctx->plan.intervals) maps += iv.chunks.size();
+    const int64_t room = map_entries_left();
+    if (room >= 0 && maps + 2048 > (uint64_t)room) {
+      ctx->err = "the plan needs " + std::to_string(maps) +
+                 " memory-map entries (chunks + mappings) but the process has " +
+                 std::to_string(room) + " left; use a larger chunk size";
+      return OOC_E_UNSUPPORTED;
+    }
+  }
+
   // physical chunks
   const Plan& plan = ctx->plan;
   ctx->chunks.resize(plan.n_chunks);
@@ -275,22 +308,44 @@ ooc_status prepare(ooc_ctx* ctx) {
         ++maps;
       }
     }
+    // read/write access, set per interval in pieces of at most 1 GiB (one call
+    // over a reservation of ~100 GiB is rejected as an invalid argument)
     hipMemAccessDesc ad = {};
     ad.location.type = hipMemLocationTypeDevice;
     ad.location.id = ctx->device;
     ad.flags = hipMemAccessFlagsProtReadWrite;
-    HIPCK(hipMemSetAccess(ctx->va_base, total, &ad, 1));
+    const uint64_t piece = std::max<uint64_t>(ctx->chunk, (1ull << 30) / ctx->chunk * ctx->chunk);
+    for (int64_t J = 0; J < NI; ++J) {
+      const uint64_t len = plan.intervals[J].chunks.size() * ctx->chunk;
+      for (uint64_t o = 0; o < len; o += piece)
+        HIPCK(hipMemSetAccess(ctx->iv_ptr[J] + o, std::min(piece, len - o), &ad, 1));
+    }
     ctx->stats.n_mappings = maps;
   }
   HIPCK(hipMemGetInfo(&free1, &total1));
 
-  // pinned host arena: every persistent variable, and every TEMP that is
-  // ever swapped out (it may be copied back later)
+  HIPCK(hipStreamCreateWithFlags(&ctx->cs, hipStreamNonBlocking));
+  HIPCK(hipStreamCreateWithFlags(&ctx->hs, hipStreamNonBlocking));
+  HIPCK(hipStreamCreateWithFlags(&ctx->ds, hipStreamNonBlocking));
+
+  {
+    ooc_status s = compile(ctx);
+    if (s) return s;
+  }
+
+  // pinned host arena: every persistent variable, and every TEMP the step
+  // program actually copies out (cancelled and clean swap-outs need no slot)
   const int64_t nv = (int64_t)ctx->vars.size();
   std::vector<uint8_t> backed(nv, 0);
   for (int64_t v = 0; v < nv; ++v) backed[v] = ctx->vars[v].kind != OOC_TEMP;
-  for (const Op& o : ctx->sched.ops)
-    if (o.kind == OOC_SWAPOUT || o.kind == OOC_SWAPIN) backed[o.var] = 1;
+  for (const FnProgram& fp : ctx->prog)
+    for (const Copy& c : fp.d2h) backed[c.var] = 1;
+  for (const FnProgram& fp : ctx->prog)
+    for (const Copy& c : fp.h2d)
+      if (!backed[c.var]) {
+        ctx->err = "swap-in of variable " + std::to_string(c.var) + " with no host copy";
+        return OOC_E_INVALID;
+      }
   uint64_t hb = 0;
   std::vector<uint64_t> hoff(nv, 0);
   for (int64_t v = 0; v < nv; ++v)
@@ -310,15 +365,17 @@ ooc_status prepare(ooc_ctx* ctx) {
     for (int64_t v = 0; v < nv; ++v)
       if (backed[v]) ctx->host_slot[v] = ctx->arena + hoff[v];
   }
-
-  HIPCK(hipStreamCreateWithFlags(&ctx->cs, hipStreamNonBlocking));
-  HIPCK(hipStreamCreateWithFlags(&ctx->hs, hipStreamNonBlocking));
-  HIPCK(hipStreamCreateWithFlags(&ctx->ds, hipStreamNonBlocking));
-
-  {
-    ooc_status s = compile(ctx);
-    if (s) return s;
+  for (FnProgram& fp : ctx->prog) {
+    for (Copy& c : fp.h2d) {
+      c.dst = ctx->iv_ptr[c.iv];
+      c.src = ctx->host_slot[c.var];
+    }
+    for (Copy& c : fp.d2h) {
+      c.dst = ctx->host_slot[c.var];
+      c.src = ctx->iv_ptr[c.iv];
+    }
   }
+
   ctx->events.resize(ctx->event_stream.size(), nullptr);
   for (size_t j = 0; j < ctx->events.size(); ++j) {
     hipError_t e = hipEventCreate(&ctx->events[j]);

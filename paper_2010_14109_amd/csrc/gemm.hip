@@ -1,8 +1,9 @@
 // Dense and convolution layers as one fp32 MFMA GEMM kernel (gfx950).
 //
 // C[M][N] = sum_k A[m][k] B[k][n].  A 256-thread workgroup computes a
-// 128 x 128 tile of C; each of its four wave64s owns a 64 x 64 quarter made
-// of 2 x 2 blocks of v_mfma_f32_32x32x2f32.  K is walked in tiles of 32,
+// 128 x 128 tile of C (or 128 x 64 / 64 x 128 when one side is at most 64
+// wide); each of its four wave64s owns a quarter of the tile made of
+// v_mfma_f32_32x32x2f32 blocks (2 x 2 of them for 128 x 128).  K is walked in tiles of 32,
 // double-buffered through LDS: while the waves multiply tile t out of one
 // buffer, every thread has tile t+1 in flight from global memory into
 // registers and writes it to the other buffer.  Within a K tile the two
@@ -16,8 +17,8 @@
 // filter gradient: the input patches seen along the batch-pixel axis).  A
 // loader zero-fills everything outside the matrix, so no shape needs
 // padding.  LDS layout follows the contiguous direction: "row of k" tiles
-// ([128][32 + 4]) are written and read with 16-byte accesses, "row of m"
-// tiles ([32][128 + 4]) are written with 16-byte accesses and read with
+// ([rows][32 + 4]) are written and read with 16-byte accesses, "row of m"
+// tiles ([32][rows + 4]) are written with 16-byte accesses and read with
 // 4-byte ones; the +4 pads keep half-wave reads free of bank conflicts.
 //
 // Split-K: the filter gradient reduces over N P Q (millions of pixels), so
@@ -32,9 +33,8 @@ namespace ooc {
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int BK = 32;
 constexpr int LDK = BK + 4;    // row-of-k tile stride (floats)
-constexpr int LDM = BM + 4;    // row-of-m tile stride (floats)
 constexpr int THREADS = 256;
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
@@ -42,35 +42,46 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 __device__ inline float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 
 // ---------------------------------------------------------------- loaders
-// Each loader: init(mn0, MN) once per workgroup (mn0 = tile origin along m or
-// n, MN = extent), fetch(k0, kend, r) loads this thread's 16 values of the
-// 32-wide K tile starting at k0 (zero at k >= kend), store(lds, r) writes them.
+// A loader feeds one operand tile of extent E (tile rows along m or n) by 32
+// along k.  init(mn0, MN) runs once per workgroup (mn0 = tile origin, MN =
+// extent of the matrix), fetch(k0, kend, r) loads this thread's E / 8 values
+// of the K tile starting at k0 as E / 32 float4 (zero at k >= kend),
+// store(lds, r) writes them.
 //
-// Row-of-k thread map: rows (t >> 3) + 32 j, k offset (t & 7) * 4.
-// Row-of-m thread map: k rows (t >> 5) + 8 j, m offset (t & 31) * 4.
+// Row-of-k layout [E][32 + 4]: thread t loads rows (t >> 3) + 32 j, k offset
+// (t & 7) * 4.  Row-of-m layout [32][E + 4]: E / 4 threads per k row; thread
+// t loads k rows t / (E / 4) + (1024 / E) j, m offset (t % (E / 4)) * 4.
 
+template <int E>
 struct RowK {
   static constexpr bool kRowOfK = true;
-  __device__ static void store(float* lds, const float4 (&r)[4]) {
-    const int t = threadIdx.x;
+  static constexpr int kN = E / 32;
+  static constexpr int kLds = E * LDK;
+  __device__ static int row(int j) { return (threadIdx.x >> 3) + 32 * j; }
+  __device__ static int koff() { return (threadIdx.x & 7) * 4; }
+  __device__ static void store(float* lds, const float4 (&r)[kN]) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<float4*>(&lds[((t >> 3) + 32 * j) * LDK + (t & 7) * 4]) = r[j];
+    for (int j = 0; j < kN; ++j) *reinterpret_cast<float4*>(&lds[row(j) * LDK + koff()]) = r[j];
   }
 };
+template <int E>
 struct RowM {
   static constexpr bool kRowOfK = false;
-  __device__ static void store(float* lds, const float4 (&r)[4]) {
-    const int t = threadIdx.x;
+  static constexpr int kN = E / 32;
+  static constexpr int kLd = E + 4;
+  static constexpr int kLds = BK * kLd;
+  __device__ static int krow(int j) { return (int)threadIdx.x / (E / 4) + (1024 / E) * j; }
+  __device__ static int moff() { return ((int)threadIdx.x % (E / 4)) * 4; }
+  __device__ static void store(float* lds, const float4 (&r)[kN]) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<float4*>(&lds[((t >> 5) + 8 * j) * LDM + (t & 31) * 4]) = r[j];
+    for (int j = 0; j < kN; ++j) *reinterpret_cast<float4*>(&lds[krow(j) * kLd + moff()]) = r[j];
   }
 };
 
 // X[i][k] = p[i * ld + k]  (contiguous along k)
-template <bool VEC>
-struct MatK : RowK {
+template <int E, bool VEC>
+struct MatK : RowK<E> {
+  using Base = RowK<E>;
   const float* p;
   int64_t ld;
   int64_t row0;
@@ -79,12 +90,11 @@ struct MatK : RowK {
     row0 = mn0;
     rows = MN;
   }
-  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
-    const int t = threadIdx.x;
-    const int64_t k = k0 + (t & 7) * 4;
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
+    const int64_t k = k0 + Base::koff();
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t i = row0 + (t >> 3) + 32 * j;
+    for (int j = 0; j < Base::kN; ++j) {
+      const int64_t i = row0 + Base::row(j);
       const float* q = p + i * ld + k;
       if (VEC) {
         r[j] = (i < rows && k < kend) ? *reinterpret_cast<const float4*>(q) : zero4();
@@ -100,21 +110,21 @@ struct MatK : RowK {
 };
 
 // X[i][k] = p[k * ld + i]  (contiguous along m or n)
-template <bool VEC>
-struct MatM : RowM {
+template <int E, bool VEC>
+struct MatM : RowM<E> {
+  using Base = RowM<E>;
   const float* p;
   int64_t ld;
   int64_t i0;
   int64_t rows;
   __device__ void init(int64_t mn0, int64_t MN) {
-    i0 = mn0 + (threadIdx.x & 31) * 4;
+    i0 = mn0 + Base::moff();
     rows = MN;
   }
-  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
-    const int t = threadIdx.x;
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t k = k0 + (t >> 5) + 8 * j;
+    for (int j = 0; j < Base::kN; ++j) {
+      const int64_t k = k0 + Base::krow(j);
       const float* q = p + k * ld + i0;
       if (VEC) {
         r[j] = (k < kend && i0 < rows) ? *reinterpret_cast<const float4*>(q) : zero4();
@@ -131,17 +141,18 @@ struct MatM : RowM {
 
 // Convolution forward, A = input patches: A[m = (n, p, q)][kk = (r, s, c)] =
 // X[n][p st - pad + r][q st - pad + s][c]   (row-of-k; VEC needs C % 4 == 0)
-template <bool VEC>
-struct ConvPatch : RowK {
+template <int E, bool VEC>
+struct ConvPatch : RowK<E> {
+  using Base = RowK<E>;
   const float* x;
   int H, W, C, S, st, pad, P, Q;
   int64_t M;
-  int n_[4], h_[4], w_[4];   // per row: image, top-left input coordinates; n = -1: no row
+  int n_[Base::kN], h_[Base::kN], w_[Base::kN];   // per row: image, top-left input coordinates
   __device__ void init(int64_t mn0, int64_t MN) {
     M = MN;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t m = mn0 + (threadIdx.x >> 3) + 32 * j;
+    for (int j = 0; j < Base::kN; ++j) {
+      const int64_t m = mn0 + Base::row(j);
       if (m < M) {
         const int64_t pq = (int64_t)P * Q;
         const int n = (int)(m / pq);
@@ -165,8 +176,8 @@ struct ConvPatch : RowK {
     if (h < 0 || h >= H || w < 0 || w >= W) return 0.f;
     return x[(((int64_t)n_[j] * H + h) * W + w) * C + c];
   }
-  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
-    const int64_t kk = k0 + (threadIdx.x & 7) * 4;
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
+    const int64_t kk = k0 + Base::koff();
     if (VEC) {
       int rr = 0, s = 0, c = 0;
       const bool kin = kk < kend;
@@ -178,7 +189,7 @@ struct ConvPatch : RowK {
         c = rem - s * C;
       }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < Base::kN; ++j) {
         const int h = h_[j] + rr, w = w_[j] + s;
         const bool ok = kin && n_[j] >= 0 && h >= 0 && h < H && w >= 0 && w < W;
         r[j] = ok ? *reinterpret_cast<const float4*>(
@@ -187,7 +198,7 @@ struct ConvPatch : RowK {
       }
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < Base::kN; ++j) {
         r[j].x = at(j, kk + 0, kend);
         r[j].y = at(j, kk + 1, kend);
         r[j].z = at(j, kk + 2, kend);
@@ -201,17 +212,18 @@ struct ConvPatch : RowK {
 // A[m = (n, h, w)][kk = (r, s, k)] = dY[n][p][q][k] with p st = h + pad - r,
 // q st = w + pad - s (zero when not an exact, in-range output position).
 // Row-of-k; VEC needs K % 4 == 0.
-template <bool VEC>
-struct ConvGradTap : RowK {
+template <int E, bool VEC>
+struct ConvGradTap : RowK<E> {
+  using Base = RowK<E>;
   const float* dy;
   int H, W, K, S, st, pad, P, Q;
   int64_t M;
-  int n_[4], h_[4], w_[4];   // per row: image, h + pad, w + pad
+  int n_[Base::kN], h_[Base::kN], w_[Base::kN];   // per row: image, h + pad, w + pad
   __device__ void init(int64_t mn0, int64_t MN) {
     M = MN;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t m = mn0 + (threadIdx.x >> 3) + 32 * j;
+    for (int j = 0; j < Base::kN; ++j) {
+      const int64_t m = mn0 + Base::row(j);
       if (m < M) {
         const int64_t hw = (int64_t)H * W;
         const int n = (int)(m / hw);
@@ -237,8 +249,8 @@ struct ConvGradTap : RowK {
     if (p >= P || q >= Q) return 0.f;
     return dy[(((int64_t)n_[j] * P + p) * Q + q) * K + k];
   }
-  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
-    const int64_t kk = k0 + (threadIdx.x & 7) * 4;
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
+    const int64_t kk = k0 + Base::koff();
     if (VEC) {
       int rr = 0, s = 0, k = 0;
       const bool kin = kk < kend;
@@ -250,7 +262,7 @@ struct ConvGradTap : RowK {
         k = rem - s * K;
       }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < Base::kN; ++j) {
         const int ph = h_[j] - rr, qw = w_[j] - s;
         bool ok = kin && n_[j] >= 0 && ph >= 0 && qw >= 0 && ph % st == 0 && qw % st == 0;
         const int p = ok ? ph / st : 0, q = ok ? qw / st : 0;
@@ -261,7 +273,7 @@ struct ConvGradTap : RowK {
       }
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < Base::kN; ++j) {
         r[j].x = at(j, kk + 0, kend);
         r[j].y = at(j, kk + 1, kend);
         r[j].z = at(j, kk + 2, kend);
@@ -273,15 +285,17 @@ struct ConvGradTap : RowK {
 
 // Convolution input gradient, B = filter seen per tap:
 // B[kk = (r, s, k)][c] = W[k][r][s][c]   (row-of-m; needs C % 4 == 0)
-struct ConvFilterTap : RowM {
+template <int E>
+struct ConvFilterTap : RowM<E> {
+  using Base = RowM<E>;
   const float* w;
   int C, K, R, S;
   int64_t c0;
-  __device__ void init(int64_t mn0, int64_t) { c0 = mn0 + (threadIdx.x & 31) * 4; }
-  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
+  __device__ void init(int64_t mn0, int64_t) { c0 = mn0 + Base::moff(); }
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t kk = k0 + (threadIdx.x >> 5) + 8 * j;
+    for (int j = 0; j < Base::kN; ++j) {
+      const int64_t kk = k0 + Base::krow(j);
       if (kk < kend && c0 < C) {
         const int sk = S * K;
         const int rr = (int)(kk / sk);
@@ -298,15 +312,16 @@ struct ConvFilterTap : RowM {
 // Convolution filter gradient, B = input patches along the pixel axis:
 // B[kk = (n, p, q)][col = (r, s, c)] = X[n][p st - pad + r][q st - pad + s][c]
 // (row-of-m; VEC needs C % 4 == 0)
-template <bool VEC>
-struct ConvPixelPatch : RowM {
+template <int E, bool VEC>
+struct ConvPixelPatch : RowM<E> {
+  using Base = RowM<E>;
   const float* x;
   int H, W, C, S, st, pad, P, Q;
   int64_t RSC;
   int r_[4], s_[4], c_[4];   // per column of this thread; r = -1: no column
   __device__ void init(int64_t mn0, int64_t MN) {
     RSC = MN;
-    const int64_t col = mn0 + (threadIdx.x & 31) * 4;
+    const int64_t col = mn0 + Base::moff();
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int64_t cc = col + e;
@@ -322,10 +337,10 @@ struct ConvPixelPatch : RowM {
       }
     }
   }
-  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[4]) const {
+  __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t kk = k0 + (threadIdx.x >> 5) + 8 * j;
+    for (int j = 0; j < Base::kN; ++j) {
+      const int64_t kk = k0 + Base::krow(j);
       r[j] = zero4();
       if (kk >= kend) continue;
       const int64_t pq = (int64_t)P * Q;
@@ -353,27 +368,29 @@ struct ConvPixelPatch : RowM {
 };
 
 // ---------------------------------------------------------------- kernel
-template <bool ROWK>
+template <class L>
 __device__ inline float4 read_op(const float* lds, int i, int k) {
-  if (ROWK) return *reinterpret_cast<const float4*>(&lds[i * LDK + k]);
-  return make_float4(lds[(k + 0) * LDM + i], lds[(k + 1) * LDM + i], lds[(k + 2) * LDM + i],
-                     lds[(k + 3) * LDM + i]);
+  if (L::kRowOfK) return *reinterpret_cast<const float4*>(&lds[i * LDK + k]);
+  constexpr int ld = L::kRowOfK ? LDK : (L::kLds / BK);
+  return make_float4(lds[(k + 0) * ld + i], lds[(k + 1) * ld + i], lds[(k + 2) * ld + i],
+                     lds[(k + 3) * ld + i]);
 }
 
 __device__ inline float comp(const float4& v, int t) {
   return t == 0 ? v.x : t == 1 ? v.y : t == 2 ? v.z : v.w;
 }
 
-template <class LA, class LB, bool BIAS>
+// BM x BN tile; the four waves form a 2 x 2 grid of (BM/2) x (BN/2) sub-tiles,
+// each made of (BM/64) x (BN/64) MFMA 32 x 32 blocks.
+template <int BM, int BN, class LA, class LB, bool BIAS>
 __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __restrict__ c,
                                                        int64_t ldc, int64_t slice_stride,
                                                        const float* __restrict__ bias, int64_t M,
                                                        int64_t N, int64_t K, int64_t k_slice,
                                                        int tiles_m, int tiles_n) {
-  constexpr int ASZ = LA::kRowOfK ? BM * LDK : BK * LDM;
-  constexpr int BSZ = LB::kRowOfK ? BN * LDK : BK * LDM;
-  __shared__ __attribute__((aligned(16))) float As[2][ASZ];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BSZ];
+  constexpr int MB = BM / 64, NB = BN / 64;
+  __shared__ __attribute__((aligned(16))) float As[2][LA::kLds];
+  __shared__ __attribute__((aligned(16))) float Bs[2][LB::kLds];
 
   // grouped tile order: 8 tile-rows share their B tiles in L2
   const int t = blockIdx.x;
@@ -390,12 +407,12 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
 
   la.init(m0, M);
   lb.init(n0, N);
-  float4 ra[4], rb[4];
-  floatx16 acc[2][2];
+  float4 ra[LA::kN], rb[LB::kN];
+  floatx16 acc[MB][NB];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MB; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
@@ -408,8 +425,8 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
   if (kb < ke) {
     la.fetch(kb, ke, ra);
     lb.fetch(kb, ke, rb);
-    la.store(As[0], ra);
-    lb.store(Bs[0], rb);
+    LA::store(As[0], ra);
+    LB::store(Bs[0], rb);
   }
   __syncthreads();
   int buf = 0;
@@ -424,23 +441,23 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int kq = half * 16 + 4 * j;
-      float4 a[2], b[2];
+      float4 a[MB], b[NB];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) a[mb] = read_op<LA::kRowOfK>(A, wm * 64 + mb * 32 + li, kq);
+      for (int mb = 0; mb < MB; ++mb) a[mb] = read_op<LA>(A, wm * (BM / 2) + mb * 32 + li, kq);
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) b[nb] = read_op<LB::kRowOfK>(B, wn * 64 + nb * 32 + li, kq);
+      for (int nb = 0; nb < NB; ++nb) b[nb] = read_op<LB>(B, wn * (BN / 2) + nb * 32 + li, kq);
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
+          for (int nb = 0; nb < NB; ++nb)
             acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a[mb], s), comp(b[nb], s),
                                                               acc[mb][nb], 0, 0, 0);
     }
     if (more) {
-      la.store(As[buf ^ 1], ra);
-      lb.store(Bs[buf ^ 1], rb);
+      LA::store(As[buf ^ 1], ra);
+      LB::store(Bs[buf ^ 1], rb);
     }
     __syncthreads();
     buf ^= 1;
@@ -448,21 +465,21 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
 
   float* out = c + (int64_t)blockIdx.y * slice_stride;
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int64_t col = n0 + wn * 64 + nb * 32 + li;
+    for (int nb = 0; nb < NB; ++nb) {
+      const int64_t col = n0 + wn * (BN / 2) + nb * 32 + li;
       if (col >= N) continue;
       const float bv = BIAS ? bias[col] : 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * 64 + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const int64_t row = m0 + wm * (BM / 2) + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
         if (row < M) out[row * ldc + col] = acc[mb][nb][r] + bv;
       }
     }
 }
 
-template <class LA, class LB, bool BIAS>
+template <int BM, int BN, class LA, class LB, bool BIAS>
 hipError_t run_gemm(const LA& la, const LB& lb, float* c, int64_t ldc, const float* bias,
                     int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s) {
   const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
@@ -470,12 +487,62 @@ hipError_t run_gemm(const LA& la, const LB& lb, float* c, int64_t ldc, const flo
   int64_t k_slice = (K + slices - 1) / slices;
   k_slice = (k_slice + BK - 1) / BK * BK;
   dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices);
-  hipLaunchKernelGGL((gemm_kernel<LA, LB, BIAS>), grid, dim3(THREADS), 0, s, la, lb, c, ldc,
-                     M * ldc, bias, M, N, K, k_slice, (int)tiles_m, (int)tiles_n);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, BIAS>), grid, dim3(THREADS), 0, s, la, lb, c,
+                     ldc, M * ldc, bias, M, N, K, k_slice, (int)tiles_m, (int)tiles_n);
   return hipGetLastError();
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// Tile shape: 128 x 128, or 64 along a dimension that is at most 64 wide
+// (half of a 128-wide tile would compute zeros).
+enum Shape { S128x128, S128x64, S64x128 };
+Shape pick_shape(int64_t M, int64_t N) {
+  if (N <= 64 && M > 64) return S128x64;
+  if (M <= 64) return S64x128;
+  return S128x128;
+}
+
+// Runs the GEMM with loader templates A<E>, B<E> instantiated for the chosen
+// tile shape; `make_a(tag)` / `make_b(tag)` build them.
+template <template <int> class LAT, template <int> class LBT, bool BIAS, class FA, class FB>
+hipError_t dispatch(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int64_t M, int64_t N,
+                    int64_t K, int64_t slices, hipStream_t s) {
+  switch (pick_shape(M, N)) {
+    case S128x64: {
+      LAT<128> a{};
+      LBT<64> b{};
+      fa(a);
+      fb(b);
+      return run_gemm<128, 64, LAT<128>, LBT<64>, BIAS>(a, b, c, ldc, bias, M, N, K, slices, s);
+    }
+    case S64x128: {
+      LAT<64> a{};
+      LBT<128> b{};
+      fa(a);
+      fb(b);
+      return run_gemm<64, 128, LAT<64>, LBT<128>, BIAS>(a, b, c, ldc, bias, M, N, K, slices, s);
+    }
+    default: {
+      LAT<128> a{};
+      LBT<128> b{};
+      fa(a);
+      fb(b);
+      return run_gemm<128, 128, LAT<128>, LBT<128>, BIAS>(a, b, c, ldc, bias, M, N, K, slices, s);
+    }
+  }
+}
+
+template <int E> using MatKv = MatK<E, true>;
+template <int E> using MatKs = MatK<E, false>;
+template <int E> using MatMv = MatM<E, true>;
+template <int E> using MatMs = MatM<E, false>;
+template <int E> using ConvPatchV = ConvPatch<E, true>;
+template <int E> using ConvPatchS = ConvPatch<E, false>;
+template <int E> using ConvGradTapV = ConvGradTap<E, true>;
+template <int E> using ConvGradTapS = ConvGradTap<E, false>;
+template <int E> using ConvPixelPatchV = ConvPixelPatch<E, true>;
+template <int E> using ConvPixelPatchS = ConvPixelPatch<E, false>;
 
 // ---------------------------------------------------------------- small kernels
 // db[n] = sum over rows m of dY[m][n], rows summed in order
@@ -488,14 +555,20 @@ __global__ void colsum_kernel(const float* __restrict__ dy, float* __restrict__ 
   db[n] = acc;
 }
 
-// out[j] = sum over slices s (in order) of part[s][j]
+// out[j] = sum over slices of part[s][j]: four interleaved accumulators
+// (slices s = u mod 4), added in a fixed order
 __global__ void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
                                  int64_t n, int64_t slices) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n) return;
-  float acc = 0.f;
-  for (int64_t s = 0; s < slices; ++s) acc += part[s * n + j];
-  out[j] = acc;
+  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  int64_t s = 0;
+  for (; s + 4 <= slices; s += 4) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) a[u] += part[(s + u) * n + j];
+  }
+  for (; s < slices; ++s) a[0] += part[s * n + j];
+  out[j] = (a[0] + a[1]) + (a[2] + a[3]);
 }
 
 }  // namespace
@@ -503,45 +576,33 @@ __global__ void slice_sum_kernel(const float* __restrict__ part, float* __restri
 // ---------------------------------------------------------------- launchers
 hipError_t linear_fwd(const float* X, const float* W, const float* b, float* Y, int64_t M,
                       int64_t K, int64_t N, hipStream_t s) {
-  const bool vec = K % 4 == 0 && aligned16(X) && aligned16(W);
-  if (vec) {
-    MatK<true> a{}, bb{};
-    a.p = X; a.ld = K; bb.p = W; bb.ld = K;
-    return run_gemm<MatK<true>, MatK<true>, true>(a, bb, Y, N, b, M, N, K, 1, s);
-  }
-  MatK<false> a{}, bb{};
-  a.p = X; a.ld = K; bb.p = W; bb.ld = K;
-  return run_gemm<MatK<false>, MatK<false>, true>(a, bb, Y, N, b, M, N, K, 1, s);
+  auto fa = [&](auto& a) { a.p = X; a.ld = K; };
+  auto fb = [&](auto& bb) { bb.p = W; bb.ld = K; };
+  if (K % 4 == 0 && aligned16(X) && aligned16(W))
+    return dispatch<MatKv, MatKv, true>(fa, fb, Y, N, b, M, N, K, 1, s);
+  return dispatch<MatKs, MatKs, true>(fa, fb, Y, N, b, M, N, K, 1, s);
 }
 
 hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, int64_t K,
                         int64_t N, hipStream_t s) {
-  // dX[M][K] = dY[M][N] W[N][K]: A = dY (row-of-k over N), B[n_out][k_in] = W, contiguous in k_in
-  if (N % 4 == 0 && K % 4 == 0 && aligned16(W) && aligned16(dY)) {
-    MatK<true> a{};
-    MatM<true> bb{};
-    a.p = dY; a.ld = N; bb.p = W; bb.ld = K;
-    return run_gemm<MatK<true>, MatM<true>, false>(a, bb, dX, K, nullptr, M, K, N, 1, s);
-  }
-  MatK<false> a{};
-  MatM<false> bb{};
-  a.p = dY; a.ld = N; bb.p = W; bb.ld = K;
-  return run_gemm<MatK<false>, MatM<false>, false>(a, bb, dX, K, nullptr, M, K, N, 1, s);
+  // dX[M][K] = dY[M][N] W[N][K]: A = dY (contiguous along the reduction), B[n_out][k_in] = W
+  auto fa = [&](auto& a) { a.p = dY; a.ld = N; };
+  auto fb = [&](auto& bb) { bb.p = W; bb.ld = K; };
+  if (N % 4 == 0 && K % 4 == 0 && aligned16(W) && aligned16(dY))
+    return dispatch<MatKv, MatMv, false>(fa, fb, dX, K, nullptr, M, K, N, 1, s);
+  return dispatch<MatKs, MatMs, false>(fa, fb, dX, K, nullptr, M, K, N, 1, s);
 }
 
 hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, int64_t M,
                         int64_t K, int64_t N, hipStream_t s) {
   // dW[N][K] = dY^T X: A[n][m] = dY[m][n] (contiguous in n), B[m][k] = X[m][k] (contiguous in k)
+  auto fa = [&](auto& a) { a.p = dY; a.ld = N; };
+  auto fb = [&](auto& bb) { bb.p = X; bb.ld = K; };
   hipError_t e;
-  if (N % 4 == 0 && K % 4 == 0 && aligned16(X) && aligned16(dY)) {
-    MatM<true> a{}, bb{};
-    a.p = dY; a.ld = N; bb.p = X; bb.ld = K;
-    e = run_gemm<MatM<true>, MatM<true>, false>(a, bb, dW, K, nullptr, N, K, M, 1, s);
-  } else {
-    MatM<false> a{}, bb{};
-    a.p = dY; a.ld = N; bb.p = X; bb.ld = K;
-    e = run_gemm<MatM<false>, MatM<false>, false>(a, bb, dW, K, nullptr, N, K, M, 1, s);
-  }
+  if (N % 4 == 0 && K % 4 == 0 && aligned16(X) && aligned16(dY))
+    e = dispatch<MatMv, MatMv, false>(fa, fb, dW, K, nullptr, N, K, M, 1, s);
+  else
+    e = dispatch<MatMs, MatMs, false>(fa, fb, dW, K, nullptr, N, K, M, 1, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s, dY, db,
                      M, N);
@@ -550,42 +611,29 @@ hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, i
 
 hipError_t conv_fwd(const float* X, const float* W, float* Y, const ConvShape& c, hipStream_t s) {
   const int64_t M = c.N * c.P * c.Q, N = c.K, K = c.R * c.S * c.C;
-  auto fill = [&](auto& a) {
+  auto fa = [&](auto& a) {
     a.x = X; a.H = (int)c.H; a.W = (int)c.W; a.C = (int)c.C; a.S = (int)c.S;
     a.st = (int)c.stride; a.pad = (int)c.pad; a.P = (int)c.P; a.Q = (int)c.Q;
   };
-  if (c.C % 4 == 0) {
-    ConvPatch<true> a{};
-    fill(a);
-    MatK<true> b{};
-    b.p = W; b.ld = K;
-    return run_gemm<ConvPatch<true>, MatK<true>, false>(a, b, Y, N, nullptr, M, N, K, 1, s);
-  }
-  ConvPatch<false> a{};
-  fill(a);
-  MatK<false> b{};
-  b.p = W; b.ld = K;
-  return run_gemm<ConvPatch<false>, MatK<false>, false>(a, b, Y, N, nullptr, M, N, K, 1, s);
+  auto fb = [&](auto& b) { b.p = W; b.ld = K; };
+  if (c.C % 4 == 0) return dispatch<ConvPatchV, MatKv, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
+  return dispatch<ConvPatchS, MatKs, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
 }
 
 hipError_t conv_bwd_x(const float* W, const float* dY, float* dX, const ConvShape& c,
                       hipStream_t s) {
   if (c.C % 4 != 0) return hipErrorInvalidValue;   // every conv with an input gradient has C % 4 == 0
   const int64_t M = c.N * c.H * c.W, N = c.C, K = c.R * c.S * c.K;
-  ConvFilterTap b{};
-  b.w = W; b.C = (int)c.C; b.K = (int)c.K; b.R = (int)c.R; b.S = (int)c.S;
-  auto fill = [&](auto& a) {
+  auto fa = [&](auto& a) {
     a.dy = dY; a.H = (int)c.H; a.W = (int)c.W; a.K = (int)c.K; a.S = (int)c.S;
     a.st = (int)c.stride; a.pad = (int)c.pad; a.P = (int)c.P; a.Q = (int)c.Q;
   };
-  if (c.K % 4 == 0) {
-    ConvGradTap<true> a{};
-    fill(a);
-    return run_gemm<ConvGradTap<true>, ConvFilterTap, false>(a, b, dX, N, nullptr, M, N, K, 1, s);
-  }
-  ConvGradTap<false> a{};
-  fill(a);
-  return run_gemm<ConvGradTap<false>, ConvFilterTap, false>(a, b, dX, N, nullptr, M, N, K, 1, s);
+  auto fb = [&](auto& b) {
+    b.w = W; b.C = (int)c.C; b.K = (int)c.K; b.R = (int)c.R; b.S = (int)c.S;
+  };
+  if (c.K % 4 == 0)
+    return dispatch<ConvGradTapV, ConvFilterTap, false>(fa, fb, dX, N, nullptr, M, N, K, 1, s);
+  return dispatch<ConvGradTapS, ConvFilterTap, false>(fa, fb, dX, N, nullptr, M, N, K, 1, s);
 }
 
 hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, int64_t slices,
@@ -593,32 +641,19 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
   // dW[K][RSC] = sum over pixels of dY[pixel][k] * patch[pixel][rsc]
   const int64_t M = c.K, N = c.R * c.S * c.C, K = c.N * c.P * c.Q;
   float* out = slices > 1 ? part : dW;
-  auto fill = [&](auto& b) {
+  auto fa = [&](auto& a) { a.p = dY; a.ld = c.K; };
+  auto fb = [&](auto& b) {
     b.x = X; b.H = (int)c.H; b.W = (int)c.W; b.C = (int)c.C; b.S = (int)c.S;
     b.st = (int)c.stride; b.pad = (int)c.pad; b.P = (int)c.P; b.Q = (int)c.Q;
   };
   hipError_t e;
   if (c.K % 4 == 0) {
-    MatM<true> a{};
-    a.p = dY; a.ld = c.K;
-    if (c.C % 4 == 0) {
-      ConvPixelPatch<true> b{};
-      fill(b);
-      e = run_gemm<MatM<true>, ConvPixelPatch<true>, false>(a, b, out, N, nullptr, M, N, K,
-                                                            slices, s);
-    } else {
-      ConvPixelPatch<false> b{};
-      fill(b);
-      e = run_gemm<MatM<true>, ConvPixelPatch<false>, false>(a, b, out, N, nullptr, M, N, K,
-                                                             slices, s);
-    }
+    if (c.C % 4 == 0)
+      e = dispatch<MatMv, ConvPixelPatchV, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
+    else
+      e = dispatch<MatMv, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
   } else {
-    MatM<false> a{};
-    a.p = dY; a.ld = c.K;
-    ConvPixelPatch<false> b{};
-    fill(b);
-    e = run_gemm<MatM<false>, ConvPixelPatch<false>, false>(a, b, out, N, nullptr, M, N, K,
-                                                            slices, s);
+    e = dispatch<MatMs, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
   }
   if (e != hipSuccess || slices <= 1) return e;
   const int64_t n = M * N;

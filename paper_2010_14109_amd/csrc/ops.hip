@@ -221,29 +221,51 @@ __global__ void bn_partials(const float* __restrict__ x, const float* __restrict
   }
 }
 
-// combine slice partials in slice order (double): forward -> mean, invstd;
-// backward -> dgamma, dbeta
+// combine slice partials (double) in a fixed order: wave w of the workgroup
+// sums slices w, w + 4, ... with four interleaved accumulators, then the four
+// waves are added in order.  Forward -> mean, invstd; backward -> dgamma, dbeta.
 template <int MODE>
-__global__ void bn_finalize(const float* __restrict__ x, float* __restrict__ stats,
-                            float* __restrict__ dgamma, float* __restrict__ dbeta, int64_t rows,
-                            int64_t C, int64_t slices) {
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  double a = 0, b = 0;
-  for (int64_t s = 0; s < slices; ++s) {
-    const float* part = stats + 2 * C + s * 2 * C;
-    a += part[c];
-    b += part[C + c];
+__global__ __launch_bounds__(TPB) void bn_finalize(const float* __restrict__ x,
+                                                   const float* __restrict__ part,
+                                                   float* __restrict__ head,
+                                                   float* __restrict__ dgamma,
+                                                   float* __restrict__ dbeta, int64_t rows,
+                                                   int64_t C, int64_t slices) {
+  __shared__ double sa[4][64], sb[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+  double a[4] = {0, 0, 0, 0}, b[4] = {0, 0, 0, 0};
+  if (c < C) {
+    int64_t s = w;
+    for (; s + 12 < slices; s += 16) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float* p = part + (s + 4 * u) * 2 * C;
+        a[u] += p[c];
+        b[u] += p[C + c];
+      }
+    }
+    for (; s < slices; s += 4) {
+      const float* p = part + s * 2 * C;
+      a[0] += p[c];
+      b[0] += p[C + c];
+    }
   }
+  sa[w][lane] = (a[0] + a[1]) + (a[2] + a[3]);
+  sb[w][lane] = (b[0] + b[1]) + (b[2] + b[3]);
+  __syncthreads();
+  if (w != 0 || c >= C) return;
+  const double ta = ((sa[0][lane] + sa[1][lane]) + sa[2][lane]) + sa[3][lane];
+  const double tb = ((sb[0][lane] + sb[1][lane]) + sb[2][lane]) + sb[3][lane];
   if (MODE == 0) {
-    const double m1 = a / (double)rows;
-    double var = b / (double)rows - m1 * m1;
+    const double m1 = ta / (double)rows;
+    double var = tb / (double)rows - m1 * m1;
     if (var < 0) var = 0;
-    stats[c] = (float)((double)x[c] + m1);
-    stats[C + c] = (float)(1.0 / sqrt(var + 1e-5));
+    head[c] = (float)((double)x[c] + m1);
+    head[C + c] = (float)(1.0 / sqrt(var + 1e-5));
   } else {
-    dbeta[c] = (float)a;
-    dgamma[c] = (float)b;
+    dbeta[c] = (float)ta;
+    dgamma[c] = (float)tb;
   }
 }
 
@@ -344,14 +366,29 @@ __global__ void maxpool_bwd_kernel(const uint8_t* __restrict__ idx, const float*
   }
 }
 
-__global__ void avgpool_fwd_kernel(const float* __restrict__ x, float* __restrict__ y, int64_t N,
-                                   int64_t HW, int64_t C) {
-  const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (o >= N * C) return;
-  const int64_t n = o / C, c = o % C;
-  float acc = 0.f;
-  for (int64_t j = 0; j < HW; ++j) acc += x[(n * HW + j) * C + c];
-  y[o] = acc / (float)HW;
+// workgroup per (image, 64 channels): lane = channel, wave w sums pixels
+// w, w + 4, ...; the four wave sums are added in order
+__global__ __launch_bounds__(TPB) void avgpool_fwd_kernel(const float* __restrict__ x,
+                                                          float* __restrict__ y, int64_t HW,
+                                                          int64_t C) {
+  __shared__ float part[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t n = blockIdx.y;
+  const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+  float acc[2] = {0.f, 0.f};
+  if (c < C) {
+    const float* xn = x + n * HW * C + c;
+    int64_t j = w;
+    for (; j + 4 < HW; j += 8) {
+      acc[0] += xn[j * C];
+      acc[1] += xn[(j + 4) * C];
+    }
+    for (; j < HW; j += 4) acc[0] += xn[j * C];
+  }
+  part[w][lane] = acc[0] + acc[1];
+  __syncthreads();
+  if (w == 0 && c < C)
+    y[n * C + c] = (((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane]) / (float)HW;
 }
 
 __global__ void avgpool_bwd_kernel(const float* __restrict__ dy, float* __restrict__ dx, int64_t N,
@@ -423,8 +460,8 @@ hipError_t bn_fwd(const float* x, const float* gamma, const float* beta, float* 
                      stats, sm, C);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(bn_finalize<0>, dim3((unsigned)((C + 255) / 256)), dim3(256), 0, s, x, stats,
-                     nullptr, nullptr, rows, C, slices);
+  hipLaunchKernelGGL(bn_finalize<0>, dim3(cg), dim3(TPB), 0, s, x, stats + 2 * C, stats, nullptr,
+                     nullptr, rows, C, slices);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const bool vec = C % 4 == 0 && aligned16(x) && aligned16(y);
   hipLaunchKernelGGL(bn_apply<0>, dim3(grid_for((rows * C + 3) / 4)), dim3(TPB), 0, s, x, nullptr,
@@ -441,8 +478,8 @@ hipError_t bn_bwd(const float* x, const float* gamma, float* stats, const float*
                      C);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(bn_finalize<1>, dim3((unsigned)((C + 255) / 256)), dim3(256), 0, s, x, stats,
-                     dgamma, dbeta, rows, C, slices);
+  hipLaunchKernelGGL(bn_finalize<1>, dim3(cg), dim3(TPB), 0, s, x, stats + 2 * C, stats, dgamma,
+                     dbeta, rows, C, slices);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const bool vec = C % 4 == 0 && aligned16(x) && aligned16(dy) && aligned16(dx);
   // backward uses beta's slot for dbeta: dx = gamma invstd (dy - dbeta/rows - xhat dgamma/rows)
@@ -465,8 +502,8 @@ hipError_t maxpool_bwd(const uint8_t* idx, const float* dy, float* dx, const Poo
 }
 
 hipError_t avgpool_fwd(const float* x, float* y, int64_t N, int64_t HW, int64_t C, hipStream_t s) {
-  hipLaunchKernelGGL(avgpool_fwd_kernel, dim3((unsigned)((N * C + TPB - 1) / TPB)), dim3(TPB), 0, s,
-                     x, y, N, HW, C);
+  hipLaunchKernelGGL(avgpool_fwd_kernel, dim3((unsigned)((C + 63) / 64), (unsigned)N), dim3(TPB), 0,
+                     s, x, y, HW, C);
   return hipGetLastError();
 }
 

@@ -241,6 +241,12 @@ class Context:
                         "chunks": list(cs[iv.first_chunk:iv.first_chunk + iv.n_chunks])})
         return out
 
+    def plan_counts(self):
+        """(physical chunks the pool needs, chunk mappings over all intervals)."""
+        m = ctypes.c_uint64()
+        _check(self.lib.ooc_plan_chunks(self.h, None, 0, ctypes.byref(m)), self.h)
+        return self.stats()["max_chunks_used"], m.value
+
     def prepare(self):
         _check(self.lib.ooc_prepare(self.h), self.h)
 
