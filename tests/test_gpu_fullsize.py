@@ -1,0 +1,97 @@
+"""Full-size steps in the configuration ``bench.py`` times (GPU).
+
+Deep networks are ill-conditioned in fp32: near-zero ReLU inputs and
+BatchNorm over few rows make any fp32 evaluation differ from the float64
+step.  Even the oracle run in float32 differs from float64 by 3e-3 (plain CNN,
+batch 128) to 4e-2 (ResNet-50) on some gradients.  For these networks the
+bar is therefore derived from the arithmetic: for every parameter gradient,
+updated parameter and momentum buffer, the device's relative L2 error against
+float64 must be at most 4 times the float32 oracle's own error (and never
+has to be smaller than 1e-4).  The loss, a well-conditioned forward
+quantity, must match float64 within 1e-5.
+
+The out-of-core step must equal the in-core step bit for bit in the exact
+bench configuration (budget, window, chunk size).
+"""
+
+import numpy as np
+import pytest
+
+import bench
+from oracle.interp import run as oracle_run
+from oracle.lower import lower
+from paper_2010_14109_amd import netdef, synth
+from tests.gpu_util import rel_l2, run_net
+
+pytestmark = pytest.mark.gpu
+
+
+def derived_check(spec, loss, outs):
+    reg = lower(spec, keep_grads=True)
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    e64 = oracle_run(reg, x, labels, {k: v.astype(np.float64) for k, v in params.items()})
+    e32 = oracle_run(reg, x, labels, {k: v.astype(np.float32) for k, v in params.items()},
+                     dtype=np.float32)
+    assert abs(loss - e64["loss"][-1]) <= 1e-5 * abs(e64["loss"][-1])
+    worst = 0.0
+    for name, val in outs.items():
+        if name == "loss":
+            continue
+        ref = e64[name]
+        err = rel_l2(val.reshape(ref.shape), ref)
+        base = rel_l2(e32[name], ref)
+        assert err <= max(1e-4, 4 * base), (name, err, base)
+        worst = max(worst, err / max(1e-4, base))
+    print(f"{spec['name']}: worst error / max(1e-4, fp32 oracle error) = {worst:.2f}", flush=True)
+
+
+def bench_config(name, **over):
+    spec = synth.workload(name, **over)
+    net = netdef.Net(spec)
+    chunk, plan = bench.choose_chunk(net, synth.budget_fraction(name), 0.5)
+    return spec, chunk, plan
+
+
+def test_plain_cnn_batch128_bench_config():
+    spec, chunk, plan = bench_config("cnn")
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    print(f"cnn b128: budget {plan['budget']} chunk {chunk}", flush=True)
+    loss, outs, st = run_net(spec, x, labels, params, budget=plan["budget"],
+                             window=plan["window"], chunk=chunk)
+    assert st["pool_bytes"] <= plan["budget"]
+    loss0, outs0, _ = run_net(spec, x, labels, params, chunk=chunk)
+    assert np.float32(loss).tobytes() == np.float32(loss0).tobytes()
+    for n in outs0:
+        assert outs[n].tobytes() == outs0[n].tobytes(), n
+    print("cnn b128: bit-identical to in-core; checking against the oracle", flush=True)
+    derived_check(spec, loss, outs)
+
+
+@pytest.mark.parametrize("batch,hw", [(16, 64), (4, 224)])
+def test_resnet50_against_oracle(batch, hw):
+    spec = synth.resnet(batch=batch, hw=hw)
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    net = netdef.Net(spec, keep_grads=True)
+    chunk, plan = bench.choose_chunk(net, 1 / 7.5, 0.5)
+    print(f"resnet50 b{batch} {hw}x{hw}: budget {plan['budget']} chunk {chunk}", flush=True)
+    loss, outs, st = run_net(spec, x, labels, params, budget=plan["budget"],
+                             window=plan["window"], chunk=chunk)
+    assert st["pool_bytes"] <= plan["budget"]
+    derived_check(spec, loss, outs)
+
+
+def test_resnet50_batch256_bench_config_matches_incore():
+    spec, chunk, plan = bench_config("resnet50_b256")
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    print(f"resnet50 b256: budget {plan['budget']} chunk {chunk}", flush=True)
+    loss, outs, st = run_net(spec, x, labels, params, budget=plan["budget"],
+                             window=plan["window"], chunk=chunk, keep_grads=False)
+    assert st["pool_bytes"] <= plan["budget"] and st["device_bytes_delta"] <= plan["budget"]
+    loss0, outs0, _ = run_net(spec, x, labels, params, chunk=chunk, keep_grads=False)
+    assert np.isfinite(loss) and np.float32(loss).tobytes() == np.float32(loss0).tobytes()
+    for n in outs0:
+        assert outs[n].tobytes() == outs0[n].tobytes(), n
