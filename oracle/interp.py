@@ -26,7 +26,7 @@ def run(reg, x, labels, params, state=None, dtype=np.float64):
     for v in reg["vars"]:
         nm = v["name"]
         if nm == "x":
-            env[nm] = np.asarray(x, dtype=dtype)
+            env[nm] = np.asarray(x, dtype=np.int64 if v["dtype"] == "i32" else dtype)
         elif nm == "labels":
             env[nm] = np.asarray(labels, dtype=np.int64)
         elif v["kind"] == 1:
@@ -106,6 +106,34 @@ def run(reg, x, labels, params, state=None, dtype=np.float64):
                     env[p], env[m] = ops.sgd_momentum(g(p), g(dp), g(m), lr, mu)
                 else:
                     env[p] = ops.sgd(g(p), g(dp), lr)
+        elif op == "embed_fwd":
+            ids, E, pos, Y = vs
+            env[Y] = ops.embed_fwd(g(ids), g(E), g(pos))
+        elif op == "embed_bwd":
+            ids, dY, dE, dpos = vs
+            env[dE], env[dpos] = ops.embed_bwd(g(ids), g(dY), a["V"])
+        elif op == "layernorm_fwd":
+            X, gm, bt, Y, st = vs
+            env[Y], mean, rstd = ops.layernorm_fwd(g(X), g(gm), g(bt))
+            bnstat[st] = (mean, rstd)
+            env[st] = np.concatenate([mean, rstd, np.zeros(2 * a["slices"] * a["d"])])
+        elif op == "layernorm_bwd":
+            X, gm, st, dY, dX, dg, dbt = vs
+            mean, rstd = bnstat[st]
+            env[dX], env[dg], env[dbt] = ops.layernorm_bwd(g(X), g(gm), mean, rstd, g(dY))
+        elif op == "gelu_fwd":
+            X, Y = vs
+            env[Y] = ops.gelu_fwd(g(X))
+        elif op == "gelu_bwd":
+            X, dY, dX = vs
+            env[dX] = ops.gelu_bwd(g(X), g(dY))
+        elif op == "attention_fwd":
+            X, Pv, Y = vs
+            env[Pv], env[Y] = ops.attention_fwd(g(X), a["B"], a["T"], a["H"], bool(a["causal"]))
+        elif op == "attention_bwd":
+            X, Pv, dY, dX, dS = vs
+            env[dX] = ops.attention_bwd(g(X), g(Pv), g(dY), a["B"], a["T"], a["H"])
+            env[dS] = np.zeros_like(g(Pv))
         else:
             raise ValueError(f"unknown function {op}")
     return env

@@ -33,6 +33,14 @@ maxpool_bwd    idx R, dY R, dX W
 avgpool_bwd    dY R, dX W
 add_grad       g R, c R, g' W             (g' = g + c)
 sgd            per parameter p in layer order: p RW, dp R [, m_p RW with momentum]
+embed_fwd      ids R, E R, pos R, Y W
+embed_bwd      ids R, dY R, dE W, dpos W
+layernorm_fwd  X R, gamma R, beta R, Y W, stats W
+layernorm_bwd  X R, gamma R, stats RW, dY R, dX W, dgamma W, dbeta W
+gelu_fwd       X R, Y W
+gelu_bwd       X R, dY R, dX W            (X = the GELU input)
+attention_fwd  qkv R, P W, Y W            (P = the attention probabilities [B, H, T, T])
+attention_bwd  qkv R, P R, dY R, dqkv W, dS W   (dS = scratch of P's size)
 =============  ======================================================================
 
 The backward of an addition is the identity, so both inputs receive the
@@ -42,11 +50,14 @@ Sizes: float32 tensors except ``labels`` (int32) and ``idx`` (uint8);
 ``loss`` holds the per-row losses followed by their mean ([N + 1]);
 ``stats`` holds mean and 1/std per channel followed by two partial sums per
 channel for each of S row slices, S = min(ceil(rows / 512), 2048) with rows =
-N H W; ``part`` holds S_w slices of dW, S_w = min(ceil(1024 / T), ceil(L /
+N H W; a LayerNorm's ``stats`` holds mean and 1/std per row followed by two
+partial sums per feature for each of S row slices (same S); ``part`` holds S_w slices of dW, S_w = min(ceil(1024 / T), ceil(L /
 1024)) with T = ceil(K / 128) ceil(R S C / 128) output tiles and L = N P Q.
 
 Kinds: x and labels INPUT, parameters PARAM, momentum buffers STATE, loss
 OUTPUT (parameter gradients too when ``keep_grads``), everything else TEMP.
+Token inputs (``x`` of a transformer) are int32 [B, T]; there is one label per
+row of the logits.
 """
 
 from __future__ import annotations
@@ -83,8 +94,7 @@ def lower(spec, keep_grads=False):
         decl[name] = (tuple(shape), dtype, kind)
         return name
 
-    N = spec["input"][0]
-    var("x", spec["input"], kind=INPUT)
+    var("x", spec["input"], dtype="i32" if spec.get("tokens") else "f32", kind=INPUT)
     params_of = {}
 
     # ---------------- forward
@@ -149,12 +159,46 @@ def lower(spec, keep_grads=False):
             shapes[name] = xs
             var(name, xs)
             fns.append(("add_fwd", [(X, R), (B, R), (name, W)], {"n": math.prod(xs)}))
+        elif op == "embed":
+            Bt, T = xs
+            d = L["d"]
+            E = var(name + ".E", (L["vocab"], d), kind=PARAM)
+            pos = var(name + ".pos", (T, d), kind=PARAM)
+            shapes[name] = (Bt * T, d)
+            var(name, shapes[name])
+            params_of[name] = [E, pos]
+            fns.append(("embed_fwd", [(X, R), (E, R), (pos, R), (name, W)],
+                        {"B": Bt, "T": T, "V": L["vocab"], "d": d}))
+        elif op == "layernorm":
+            rows, d = xs
+            S = bn_slices(rows)
+            g = var(name + ".gamma", (d,), kind=PARAM)
+            bt = var(name + ".beta", (d,), kind=PARAM)
+            st_ = var(name + ".stats", (2 * rows + 2 * S * d,))
+            shapes[name] = xs
+            var(name, xs)
+            params_of[name] = [g, bt]
+            fns.append(("layernorm_fwd", [(X, R), (g, R), (bt, R), (name, W), (st_, W)],
+                        {"rows": rows, "d": d, "slices": S}))
+        elif op == "gelu":
+            shapes[name] = xs
+            var(name, xs)
+            fns.append(("gelu_fwd", [(X, R), (name, W)], {"n": math.prod(xs)}))
+        elif op == "attention":
+            rows, d3 = xs
+            d, H = d3 // 3, L["heads"]
+            Bt, T = spec["input"]
+            Pv = var(name + ".P", (Bt, H, T, T))
+            shapes[name] = (rows, d)
+            var(name, shapes[name])
+            fns.append(("attention_fwd", [(X, R), (Pv, W), (name, W)],
+                        {"B": Bt, "T": T, "H": H, "dh": d // H, "causal": int(L["causal"])}))
         else:
             raise ValueError(f"unknown layer kind {op}")
 
     # ---------------- loss
     logits = spec["logits"]
-    ncls = shapes[logits][1]
+    N, ncls = shapes[logits]
     var("labels", (N,), dtype="i32", kind=INPUT)
     var("loss", (N + 1,), kind=OUTPUT)
     dlog = var("d:" + logits, shapes[logits])
@@ -260,6 +304,38 @@ def lower(spec, keep_grads=False):
         elif op == "add":
             for src in L["in"]:
                 contribute(src, dY, pending)
+        elif op == "embed":
+            E, pos = params_of[name]
+            dE = var("d:" + E, decl[E][0], kind=grad_kind)
+            dpos = var("d:" + pos, decl[pos][0], kind=grad_kind)
+            fns.append(("embed_bwd", [(X, R), (dY, R), (dE, W), (dpos, W)],
+                        {"B": xs[0], "T": xs[1], "V": L["vocab"], "d": L["d"]}))
+            update(name)
+        elif op == "layernorm":
+            g, bt = params_of[name]
+            rows, d = xs
+            dX = var(f"d:{X}@{name}", xs)
+            dg = var("d:" + g, decl[g][0], kind=grad_kind)
+            dbt = var("d:" + bt, decl[bt][0], kind=grad_kind)
+            fns.append(("layernorm_bwd", [(X, R), (g, R), (name + ".stats", RW), (dY, R),
+                                          (dX, W), (dg, W), (dbt, W)],
+                        {"rows": rows, "d": d, "slices": bn_slices(rows)}))
+            contribute(X, dX, pending)
+            update(name)
+        elif op == "gelu":
+            dX = var(f"d:{X}@{name}", xs)
+            fns.append(("gelu_bwd", [(X, R), (dY, R), (dX, W)], {"n": math.prod(xs)}))
+            contribute(X, dX, pending)
+        elif op == "attention":
+            rows, d3 = xs
+            Bt, T = spec["input"]
+            H = L["heads"]
+            dX = var(f"d:{X}@{name}", xs)
+            dS = var(name + ".dS", (Bt, H, T, T))
+            fns.append(("attention_bwd", [(X, R), (name + ".P", R), (dY, R), (dX, W), (dS, W)],
+                        {"B": Bt, "T": T, "H": H, "dh": d3 // 3 // H,
+                         "causal": int(L["causal"])}))
+            contribute(X, dX, pending)
         settle(pending)
 
     # ---------------- number variables by first appearance

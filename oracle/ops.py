@@ -16,13 +16,22 @@ boundary: images NHWC, conv weights [K, R, S, C], dense weights [out, in].
 * global average pool over H, W
 * softmax cross-entropy, mean over the batch
 * SGD:          w -= lr g;  with momentum mu: v = mu v + g, w -= lr v
+* LayerNorm:    per row over the features, biased variance, eps = 1e-5
+* GELU:         exact, x Phi(x) with the normal CDF Phi
+* attention:    per batch and head, P = softmax(q k^T / sqrt(dh)) with future
+                positions masked (causal), context = P v; q, k, v are the
+                column thirds of one [rows, 3 d] projection, head h owning
+                columns h dh .. (h + 1) dh of each third
+* embedding:    x[b, t] = E[id[b, t]] + pos[t]
 """
 
 from __future__ import annotations
 
 import numpy as np
+from scipy.special import erf
 
 BN_EPS = 1e-5
+LN_EPS = 1e-5
 
 
 # ---------------------------------------------------------------- dense
@@ -180,3 +189,84 @@ def sgd(w, g, lr):
 def sgd_momentum(w, g, v, lr, mu):
     v_new = mu * v + g
     return w - lr * v_new, v_new
+
+
+# ---------------------------------------------------------------- LayerNorm
+def layernorm_fwd(X, gamma, beta):
+    """Returns (Y, mean, rstd) over the last axis."""
+    mean = X.mean(axis=-1, keepdims=True)
+    var = ((X - mean) ** 2).mean(axis=-1, keepdims=True)
+    rstd = 1.0 / np.sqrt(var + LN_EPS)
+    return (X - mean) * rstd * gamma + beta, mean[..., 0], rstd[..., 0]
+
+
+def layernorm_bwd(X, gamma, mean, rstd, dY):
+    """Returns (dX, dgamma, dbeta)."""
+    xhat = (X - mean[..., None]) * rstd[..., None]
+    g = dY * gamma
+    dX = rstd[..., None] * (g - g.mean(axis=-1, keepdims=True)
+                            - xhat * (g * xhat).mean(axis=-1, keepdims=True))
+    return dX, (dY * xhat).sum(axis=0), dY.sum(axis=0)
+
+
+# ---------------------------------------------------------------- GELU
+def gelu_fwd(X):
+    return 0.5 * X * (1.0 + erf(X / np.sqrt(2.0)))
+
+
+def gelu_bwd(X, dY):
+    cdf = 0.5 * (1.0 + erf(X / np.sqrt(2.0)))
+    pdf = np.exp(-0.5 * X * X) / np.sqrt(2.0 * np.pi)
+    return dY * (cdf + X * pdf)
+
+
+# ---------------------------------------------------------------- attention
+def _heads(qkv, B, T, H):
+    """Split [B T, 3 d] into q, k, v of shape [B, H, T, dh]."""
+    d = qkv.shape[1] // 3
+    dh = d // H
+    t = qkv.reshape(B, T, 3, H, dh)
+    return t[:, :, 0].transpose(0, 2, 1, 3), t[:, :, 1].transpose(0, 2, 1, 3), \
+        t[:, :, 2].transpose(0, 2, 1, 3)
+
+
+def attention_fwd(qkv, B, T, H, causal=True):
+    """Returns (P [B, H, T, T], context [B T, d])."""
+    q, k, v = _heads(qkv, B, T, H)
+    dh = q.shape[-1]
+    S = q @ k.transpose(0, 1, 3, 2) / np.sqrt(dh)
+    if causal:
+        S = np.where(np.tril(np.ones((T, T), dtype=bool)), S, -np.inf)
+    S = S - S.max(axis=-1, keepdims=True)
+    P = np.exp(S)
+    P /= P.sum(axis=-1, keepdims=True)
+    ctx = P @ v                                    # [B, H, T, dh]
+    return P, ctx.transpose(0, 2, 1, 3).reshape(B * T, H * dh)
+
+
+def attention_bwd(qkv, P, dctx, B, T, H):
+    """Returns dqkv [B T, 3 d] for context = softmax(q k^T / sqrt(dh)) v."""
+    q, k, v = _heads(qkv, B, T, H)
+    dh = q.shape[-1]
+    dO = dctx.reshape(B, T, H, dh).transpose(0, 2, 1, 3)
+    dv = P.transpose(0, 1, 3, 2) @ dO
+    dP = dO @ v.transpose(0, 1, 3, 2)
+    dS = P * (dP - (dP * P).sum(axis=-1, keepdims=True)) / np.sqrt(dh)
+    dq = dS @ k
+    dk = dS.transpose(0, 1, 3, 2) @ q
+    out = np.stack([dq, dk, dv], axis=2)           # [B, H, 3, T, dh]
+    return out.transpose(0, 3, 2, 1, 4).reshape(B * T, 3 * H * dh)
+
+
+# ---------------------------------------------------------------- embedding
+def embed_fwd(ids, E, pos):
+    B, T = ids.shape
+    return (E[ids] + pos[None, :T]).reshape(B * T, E.shape[1])
+
+
+def embed_bwd(ids, dX, vocab):
+    B, T = ids.shape
+    d = dX.shape[1]
+    dE = np.zeros((vocab, d), dtype=dX.dtype)
+    np.add.at(dE, ids.reshape(-1), dX)
+    return dE, dX.reshape(B, T, d).sum(axis=0)

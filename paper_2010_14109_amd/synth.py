@@ -13,7 +13,9 @@ random bytes fed to both sides:
 
 Layouts are those of the library boundary: images are NHWC, conv weights are
 ``[K, R, S, C]`` (output channel, filter row, filter column, input channel),
-dense weights are ``[out, in]``.
+dense weights are ``[out, in]``; token batches are ``[B, T]`` int32 and the
+transformer's activations are ``[B T, features]``.  Transformer weights are
+drawn N(0, 0.02).
 
 The workloads stand in for the ones the paper trains (ResNet-50 on 224x224
 ImageNet batches, Section 5.1 and Table 1) plus smaller networks of the same
@@ -112,6 +114,39 @@ def resnet(batch=256, hw=224, classes=1000, blocks=(3, 4, 6, 3), width=64,
             "optimizer": {"lr": lr, "momentum": momentum}}
 
 
+def transformer(batch=64, seq=512, d=1024, heads=16, ffn=4096, layers=48, vocab=32000,
+                lr=0.01, momentum=0.0):
+    """Pre-LN causal transformer encoder with learned positions and an untied LM head,
+    trained on next-token cross-entropy."""
+    L = [{"name": "embed", "op": "embed", "in": ["x"], "vocab": vocab, "d": d}]
+    prev = "embed"
+    for i in range(layers):
+        b = f"l{i + 1}"
+        L += [
+            {"name": f"{b}.ln1", "op": "layernorm", "in": [prev]},
+            {"name": f"{b}.qkv", "op": "linear", "in": [f"{b}.ln1"], "in_features": d,
+             "out_features": 3 * d},
+            {"name": f"{b}.attn", "op": "attention", "in": [f"{b}.qkv"], "heads": heads,
+             "causal": True},
+            {"name": f"{b}.proj", "op": "linear", "in": [f"{b}.attn"], "in_features": d,
+             "out_features": d},
+            {"name": f"{b}.res1", "op": "add", "in": [f"{b}.proj", prev]},
+            {"name": f"{b}.ln2", "op": "layernorm", "in": [f"{b}.res1"]},
+            {"name": f"{b}.fc1", "op": "linear", "in": [f"{b}.ln2"], "in_features": d,
+             "out_features": ffn},
+            {"name": f"{b}.gelu", "op": "gelu", "in": [f"{b}.fc1"]},
+            {"name": f"{b}.fc2", "op": "linear", "in": [f"{b}.gelu"], "in_features": ffn,
+             "out_features": d},
+            {"name": f"{b}.res2", "op": "add", "in": [f"{b}.fc2", f"{b}.res1"]},
+        ]
+        prev = f"{b}.res2"
+    L += [{"name": "lnf", "op": "layernorm", "in": [prev]},
+          {"name": "head", "op": "linear", "in": ["lnf"], "in_features": d, "out_features": vocab}]
+    return {"name": f"transformer{layers}_d{d}_b{batch}_t{seq}", "input": [batch, seq],
+            "tokens": True, "classes": vocab, "layers": L, "logits": "head", "init": "normal",
+            "optimizer": {"lr": lr, "momentum": momentum}}
+
+
 #: The five workloads: name -> (network description, budget as a fraction of
 #: the in-core peak).  Budget fractions follow the workload list of the build.
 WORKLOADS = {
@@ -119,13 +154,14 @@ WORKLOADS = {
     "cnn": (lambda: plain_cnn(), 0.50),
     "resnet50_b256": (lambda: resnet(batch=256), 0.25),
     "resnet50_b1440": (lambda: resnet(batch=1440), 1.0 / 7.5),
+    "transformer": (lambda: transformer(), 0.20),
 }
 
 
 def workload(name, **overrides):
     """Network description of a named workload, with keyword overrides (e.g. ``batch=8``)."""
     builders = {"mlp": mlp, "cnn": plain_cnn, "resnet50_b256": resnet,
-                "resnet50_b1440": resnet}
+                "resnet50_b1440": resnet, "transformer": transformer}
     defaults = {"resnet50_b256": {"batch": 256}, "resnet50_b1440": {"batch": 1440}}
     kw = dict(defaults.get(name, {}))
     kw.update(overrides)
@@ -148,7 +184,13 @@ def param_shapes(spec):
     """
     out = []
     for L in spec["layers"]:
-        if L["op"] == "linear":
+        if L["op"] == "embed":
+            out.append((L["name"] + ".E", (L["vocab"], L["d"])))
+            out.append((L["name"] + ".pos", (spec["input"][1], L["d"])))
+        elif L["op"] == "layernorm":
+            out.append((L["name"] + ".gamma", (_width(spec, L),)))
+            out.append((L["name"] + ".beta", (_width(spec, L),)))
+        elif L["op"] == "linear":
             out.append((L["name"] + ".W", (L["out_features"], L["in_features"])))
             out.append((L["name"] + ".b", (L["out_features"],)))
         elif L["op"] == "conv":
@@ -159,9 +201,20 @@ def param_shapes(spec):
     return out
 
 
+def _width(spec, layer):
+    """Feature width of a transformer LayerNorm: the model width of the embedding."""
+    return next(L["d"] for L in spec["layers"] if L["op"] == "embed")
+
+
 def make_inputs(spec, seed=0):
-    """``(x, labels)``: x float32 of the description's input shape, labels int32 [N]."""
+    """``(x, labels)``.  Images: x float32 of the input shape, labels int32 [N] uniform over
+    the classes.  Tokens: ids [B, T + 1] uniform over the vocabulary; x = ids[:, :T] (int32)
+    and the labels are the next tokens ids[:, 1:] flattened to [B T]."""
     g = np.random.Generator(np.random.PCG64(seed))
+    if spec.get("tokens"):
+        B, T = spec["input"]
+        ids = g.integers(0, spec["classes"], size=(B, T + 1)).astype(np.int32)
+        return np.ascontiguousarray(ids[:, :T]), np.ascontiguousarray(ids[:, 1:]).reshape(-1)
     x = g.standard_normal(size=tuple(spec["input"]), dtype=np.float32)
     labels = g.integers(0, spec["classes"], size=spec["input"][0]).astype(np.int32)
     return x, labels
@@ -171,9 +224,13 @@ def make_params(spec, seed=1):
     """Initial parameters ``{name: float32 array}`` (He-normal fan-in, zero bias, BN 1/0)."""
     g = np.random.Generator(np.random.PCG64(seed))
     params = {}
+    normal = spec.get("init") == "normal"
     for name, shape in param_shapes(spec):
         kind = name.rsplit(".", 1)[1]
-        if kind == "W":
+        if normal and kind in ("W", "E", "pos"):
+            params[name] = (g.standard_normal(size=shape, dtype=np.float32)
+                            * np.float32(0.02)).astype(np.float32)
+        elif kind == "W":
             fan_in = int(np.prod(shape[1:]))
             std = np.float32(np.sqrt(2.0 / fan_in))
             params[name] = (g.standard_normal(size=shape, dtype=np.float32) * std).astype(np.float32)

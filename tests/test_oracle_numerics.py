@@ -256,3 +256,91 @@ def test_momentum_step_changes_state():
     for name in params:
         assert np.allclose(env["m:" + name], env["d:" + name])        # v1 = g (v0 = 0)
         assert np.allclose(env[name], params[name] - spec["optimizer"]["lr"] * env["d:" + name])
+
+
+# ---------------------------------------------------------------- transformer ops
+def test_layernorm_identities_and_fd():
+    X = rng.standard_normal((5, 12)) * 3 + 1
+    gamma, beta = rng.standard_normal(12), rng.standard_normal(12)
+    Y, mean, rstd = ops.layernorm_fwd(X, gamma, beta)
+    xhat = (Y - beta) / gamma
+    assert np.allclose(xhat.mean(axis=1), 0, atol=1e-12)
+    assert np.allclose(mean, X.mean(axis=1)) and np.allclose(1 / rstd ** 2 - ops.LN_EPS, X.var(axis=1))
+    G = rng.standard_normal(X.shape)
+    dX, dg, db = ops.layernorm_bwd(X, gamma, mean, rstd, G)
+    assert np.allclose(dX.sum(axis=1), 0, atol=1e-12)        # orthogonal to 1 per row
+    loss = lambda: float((ops.layernorm_fwd(X, gamma, beta)[0] * G).sum())
+    for arr, got in ((X, dX), (gamma, dg), (beta, db)):
+        idx, g = fd_grad(loss, arr)
+        assert_close(got.reshape(-1)[idx], g)
+
+
+def test_gelu_closed_form_and_fd():
+    from scipy.stats import norm
+    X = rng.standard_normal(50) * 3
+    assert_close(ops.gelu_fwd(X), X * norm.cdf(X), 1e-13)
+    assert ops.gelu_fwd(np.array([0.0]))[0] == 0.0
+    G = rng.standard_normal(50)
+    idx, g = fd_grad(lambda: float((ops.gelu_fwd(X) * G).sum()), X)
+    assert_close(ops.gelu_bwd(X, G)[idx], g)
+
+
+def test_attention_brute_force_and_fd():
+    import math
+    B, T, H, dh = 2, 5, 3, 4
+    d = H * dh
+    qkv = rng.standard_normal((B * T, 3 * d))
+    P, ctx = ops.attention_fwd(qkv, B, T, H, causal=True)
+    for b in range(B):
+        for h in range(H):
+            for i in range(T):
+                q = qkv[b * T + i, h * dh:(h + 1) * dh]
+                sc = []
+                for j in range(i + 1):                          # causal: keys up to i
+                    k = qkv[b * T + j, d + h * dh:d + (h + 1) * dh]
+                    sc.append(sum(q[u] * k[u] for u in range(dh)) / math.sqrt(dh))
+                m = max(sc)
+                e = [math.exp(s - m) for s in sc]
+                p = [x / sum(e) for x in e]
+                assert np.allclose(P[b, h, i, :i + 1], p) and np.all(P[b, h, i, i + 1:] == 0)
+                out = sum(p[j] * qkv[b * T + j, 2 * d + h * dh:2 * d + (h + 1) * dh]
+                          for j in range(i + 1))
+                assert np.allclose(ctx[b * T + i, h * dh:(h + 1) * dh], out)
+    G = rng.standard_normal(ctx.shape)
+    dqkv = ops.attention_bwd(qkv, P, G, B, T, H)
+    idx, g = fd_grad(lambda: float((ops.attention_fwd(qkv, B, T, H)[1] * G).sum()), qkv, n=80)
+    assert_close(dqkv.reshape(-1)[idx], g)
+
+
+def test_embedding_fd():
+    B, T, V, d = 3, 4, 7, 5
+    ids = rng.integers(0, V, (B, T))
+    ids[0, 0] = ids[1, 2] = 3                                   # a repeated token
+    E, pos = rng.standard_normal((V, d)), rng.standard_normal((T, d))
+    X = ops.embed_fwd(ids, E, pos)
+    assert np.allclose(X[1 * T + 2], E[3] + pos[2])
+    G = rng.standard_normal(X.shape)
+    dE, dpos = ops.embed_bwd(ids, G, V)
+    loss = lambda: float((ops.embed_fwd(ids, E, pos) * G).sum())
+    for arr, got in ((E, dE), (pos, dpos)):
+        idx, g = fd_grad(loss, arr)
+        assert_close(got.reshape(-1)[idx], g)
+
+
+def test_tiny_transformer_gradients_by_finite_differences():
+    spec = synth.transformer(batch=2, seq=6, d=16, heads=2, ffn=24, layers=2, vocab=11)
+    reg = lower(spec, keep_grads=True)
+    x, labels = synth.make_inputs(spec, 3)
+    params = {k: v.astype(np.float64) for k, v in synth.make_params(spec, 4).items()}
+    noise = np.random.default_rng(5)
+    for k in params:
+        params[k] += 0.05 * noise.standard_normal(params[k].shape)
+    env = run(reg, x, labels, params)
+
+    def loss():
+        return float(run(reg, x, labels, params)["loss"][-1])
+
+    for name, arr in params.items():
+        idx, g = fd_grad(loss, arr, n=4, seed=len(name))
+        got = env["d:" + name].reshape(-1)[idx]
+        assert np.allclose(got, g, rtol=1e-5, atol=1e-9), name
