@@ -119,6 +119,25 @@ enum { OOC_PRE = 0, OOC_POST = 1, OOC_END = 2 };
  *  MAXPOOL_BWD                        idx[R] dY[R] dX[W]           N H W C k stride pad P Q
  *  AVGPOOL_FWD   global average over H W   X[R] Y[W]               N H W C
  *  AVGPOOL_BWD                        dY[R] dX[W]                  N H W C
+ *  EMBED_FWD     Y[r] = E[ids[r]] + pos[r mod T] for the B T token rows;
+ *                ids int32 (an id outside [0, V) gives a NaN row)
+ *                                     ids[R] E[R] pos[R] Y[W]          B T V d
+ *  EMBED_BWD     dE[v] = sum of dY rows of tokens with id v (token order),
+ *                dpos[t] = sum over b of dY[b T + t]
+ *                                     ids[R] dY[R] dE[W] dpos[W]       B T V d
+ *  LAYERNORM_FWD per row over d features, biased variance, eps 1e-5;
+ *                stats = mean[rows] rstd[rows] then 2 d floats per row slice
+ *                                     X[R] gamma[R] beta[R] Y[W] stats[W]   rows d slices
+ *  LAYERNORM_BWD                      X[R] gamma[R] stats[RW] dY[R] dX[W] dgamma[W] dbeta[W]
+ *                                                                      rows d slices
+ *  GELU_FWD      Y = X Phi(X) (exact, normal CDF)    X[R] Y[W]          n
+ *  GELU_BWD      dX = dY (Phi(X) + X phi(X))         X[R] dY[R] dX[W]   n
+ *  ATTENTION_FWD qkv [B T][3 H dh] holds q, k, v as column thirds, head h in
+ *                columns h dh .. (h+1) dh of each; P[b][h] = softmax(q k^T /
+ *                sqrt(dh)) with keys after the query masked when causal;
+ *                Y [B T][H dh] = P v                qkv[R] P[W] Y[W]    B T H dh causal
+ *  ATTENTION_BWD dqkv of the above; dS is scratch of P's size
+ *                                     qkv[R] P[R] dY[R] dqkv[W] dS[W]  B T H dh causal
  *  MIX           swap-integrity test op on uint32 words (sizes multiple of
  *                4): the last variable y is the only one written (W or RW),
  *                the others are read; y[j] = seed ^ (j * 2654435761) ^ sum
@@ -146,7 +165,15 @@ enum {
   OOC_OP_AVGPOOL_FWD = 16,
   OOC_OP_AVGPOOL_BWD = 17,
   OOC_OP_MIX = 18,
-  OOC_OP_COUNT = 19
+  OOC_OP_EMBED_FWD = 19,
+  OOC_OP_EMBED_BWD = 20,
+  OOC_OP_LAYERNORM_FWD = 21,
+  OOC_OP_LAYERNORM_BWD = 22,
+  OOC_OP_GELU_FWD = 23,
+  OOC_OP_GELU_BWD = 24,
+  OOC_OP_ATTENTION_FWD = 25,
+  OOC_OP_ATTENTION_BWD = 26,
+  OOC_OP_COUNT = 27
 };
 
 /* One schedule op.  fn = N for END ops; held = budget bytes held after it

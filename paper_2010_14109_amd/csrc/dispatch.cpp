@@ -64,6 +64,24 @@ hipError_t launch_fn(const Fn& fn, void* const* p, const uint64_t* bytes, float 
       return avgpool_fwd(F(0), F(1), a[0], a[1] * a[2], a[3], s);
     case OOC_OP_AVGPOOL_BWD:
       return avgpool_bwd(F(0), F(1), a[0], a[1] * a[2], a[3], s);
+    case OOC_OP_EMBED_FWD:
+      return embed_fwd(static_cast<const int32_t*>(p[0]), F(1), F(2), F(3), a[0], a[1], a[2],
+                       a[3], s);
+    case OOC_OP_EMBED_BWD:
+      return embed_bwd(static_cast<const int32_t*>(p[0]), F(1), F(2), F(3), a[0], a[1], a[2],
+                       a[3], s);
+    case OOC_OP_LAYERNORM_FWD:
+      return layernorm_fwd(F(0), F(1), F(2), F(3), F(4), a[0], a[1], a[2], s);
+    case OOC_OP_LAYERNORM_BWD:
+      return layernorm_bwd(F(0), F(1), F(2), F(3), F(4), F(5), F(6), a[0], a[1], a[2], s);
+    case OOC_OP_GELU_FWD:
+      return gelu_fwd(F(0), F(1), a[0], s);
+    case OOC_OP_GELU_BWD:
+      return gelu_bwd(F(0), F(1), F(2), a[0], s);
+    case OOC_OP_ATTENTION_FWD:
+      return attention_fwd(F(0), F(1), F(2), a[0], a[1], a[2], a[3], a[4] != 0, s);
+    case OOC_OP_ATTENTION_BWD:
+      return attention_bwd(F(0), F(1), F(2), F(3), F(4), a[0], a[1], a[2], a[3], a[4] != 0, s);
     default:
       return hipErrorInvalidValue;
   }

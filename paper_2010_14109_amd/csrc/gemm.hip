@@ -382,13 +382,31 @@ __device__ inline float comp(const float4& v, int t) {
 
 // BM x BN tile; the four waves form a 2 x 2 grid of (BM/2) x (BN/2) sub-tiles,
 // each made of (BM/64) x (BN/64) MFMA 32 x 32 blocks.
-template <int BM, int BN, class LA, class LB, bool BIAS>
+// Batched problems (grid z): batch z = (zo, zi) with zi = z mod inner; operand
+// and result pointers move by zo * outer stride + zi * inner stride.
+struct Batch {
+  int64_t inner;
+  int64_t a_o, a_i, b_o, b_i, c_o, c_i;
+};
+
+template <class L>
+__device__ inline void shift(L& l, int64_t d) {
+  l.p += d;
+}
+
+template <int BM, int BN, class LA, class LB, bool BIAS, bool BATCHED>
 __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __restrict__ c,
                                                        int64_t ldc, int64_t slice_stride,
                                                        const float* __restrict__ bias, int64_t M,
                                                        int64_t N, int64_t K, int64_t k_slice,
-                                                       int tiles_m, int tiles_n) {
+                                                       int tiles_m, int tiles_n, Batch bt) {
   constexpr int MB = BM / 64, NB = BN / 64;
+  if constexpr (BATCHED) {
+    const int64_t z = blockIdx.z, zo = z / bt.inner, zi = z % bt.inner;
+    shift(la, zo * bt.a_o + zi * bt.a_i);
+    shift(lb, zo * bt.b_o + zi * bt.b_i);
+    c += zo * bt.c_o + zi * bt.c_i;
+  }
   __shared__ __attribute__((aligned(16))) float As[2][LA::kLds];
   __shared__ __attribute__((aligned(16))) float Bs[2][LB::kLds];
 
@@ -479,16 +497,18 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
     }
 }
 
-template <int BM, int BN, class LA, class LB, bool BIAS>
+template <int BM, int BN, class LA, class LB, bool BIAS, bool BATCHED = false>
 hipError_t run_gemm(const LA& la, const LB& lb, float* c, int64_t ldc, const float* bias,
-                    int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s) {
+                    int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s,
+                    int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0}) {
   const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  if (tiles_m * tiles_n > INT32_MAX / 2 || slices > 65535) return hipErrorInvalidValue;
+  if (tiles_m * tiles_n > INT32_MAX / 2 || slices > 65535 || batches > 65535 || batches < 1)
+    return hipErrorInvalidValue;
   int64_t k_slice = (K + slices - 1) / slices;
   k_slice = (k_slice + BK - 1) / BK * BK;
-  dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, BIAS>), grid, dim3(THREADS), 0, s, la, lb, c,
-                     ldc, M * ldc, bias, M, N, K, k_slice, (int)tiles_m, (int)tiles_n);
+  dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices, (unsigned)batches);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, BIAS, BATCHED>), grid, dim3(THREADS), 0, s, la,
+                     lb, c, ldc, M * ldc, bias, M, N, K, k_slice, (int)tiles_m, (int)tiles_n, bt);
   return hipGetLastError();
 }
 
@@ -505,30 +525,35 @@ Shape pick_shape(int64_t M, int64_t N) {
 
 // Runs the GEMM with loader templates A<E>, B<E> instantiated for the chosen
 // tile shape; `make_a(tag)` / `make_b(tag)` build them.
-template <template <int> class LAT, template <int> class LBT, bool BIAS, class FA, class FB>
+template <template <int> class LAT, template <int> class LBT, bool BIAS, bool BATCHED = false,
+          class FA, class FB>
 hipError_t dispatch(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int64_t M, int64_t N,
-                    int64_t K, int64_t slices, hipStream_t s) {
+                    int64_t K, int64_t slices, hipStream_t s, int64_t batches = 1,
+                    Batch bt = Batch{1, 0, 0, 0, 0, 0, 0}) {
   switch (pick_shape(M, N)) {
     case S128x64: {
       LAT<128> a{};
       LBT<64> b{};
       fa(a);
       fb(b);
-      return run_gemm<128, 64, LAT<128>, LBT<64>, BIAS>(a, b, c, ldc, bias, M, N, K, slices, s);
+      return run_gemm<128, 64, LAT<128>, LBT<64>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
+                                                                 slices, s, batches, bt);
     }
     case S64x128: {
       LAT<64> a{};
       LBT<128> b{};
       fa(a);
       fb(b);
-      return run_gemm<64, 128, LAT<64>, LBT<128>, BIAS>(a, b, c, ldc, bias, M, N, K, slices, s);
+      return run_gemm<64, 128, LAT<64>, LBT<128>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
+                                                                 slices, s, batches, bt);
     }
     default: {
       LAT<128> a{};
       LBT<128> b{};
       fa(a);
       fb(b);
-      return run_gemm<128, 128, LAT<128>, LBT<128>, BIAS>(a, b, c, ldc, bias, M, N, K, slices, s);
+      return run_gemm<128, 128, LAT<128>, LBT<128>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
+                                                                   slices, s, batches, bt);
     }
   }
 }
@@ -607,6 +632,32 @@ hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, i
   hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s, dY, db,
                      M, N);
   return hipGetLastError();
+}
+
+hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, const float* B,
+                        int64_t ldb, float* C, int64_t ldc, int64_t M, int64_t N, int64_t K,
+                        int64_t batches, const BatchStrides& st, hipStream_t s) {
+  const Batch bt{st.inner, st.a_outer, st.a_inner, st.b_outer, st.b_inner, st.c_outer,
+                 st.c_inner};
+  auto fa = [&](auto& a) { a.p = A; a.ld = lda; };
+  auto fb = [&](auto& b) { b.p = B; b.ld = ldb; };
+  const bool vec = lda % 4 == 0 && ldb % 4 == 0 && aligned16(A) && aligned16(B) &&
+                   (a_rowk ? K % 4 == 0 : M % 4 == 0) && (b_rowk ? K % 4 == 0 : N % 4 == 0) &&
+                   st.a_outer % 4 == 0 && st.a_inner % 4 == 0 && st.b_outer % 4 == 0 &&
+                   st.b_inner % 4 == 0;
+#define GEMM_BATCHED_CASE(LA, LB) \
+  return dispatch<LA, LB, false, true>(fa, fb, C, ldc, nullptr, M, N, K, 1, s, batches, bt)
+  if (vec) {
+    if (a_rowk && b_rowk) GEMM_BATCHED_CASE(MatKv, MatKv);
+    if (a_rowk) GEMM_BATCHED_CASE(MatKv, MatMv);
+    if (b_rowk) GEMM_BATCHED_CASE(MatMv, MatKv);
+    GEMM_BATCHED_CASE(MatMv, MatMv);
+  }
+  if (a_rowk && b_rowk) GEMM_BATCHED_CASE(MatKs, MatKs);
+  if (a_rowk) GEMM_BATCHED_CASE(MatKs, MatMs);
+  if (b_rowk) GEMM_BATCHED_CASE(MatMs, MatKs);
+  GEMM_BATCHED_CASE(MatMs, MatMs);
+#undef GEMM_BATCHED_CASE
 }
 
 hipError_t conv_fwd(const float* X, const float* W, float* Y, const ConvShape& c, hipStream_t s) {

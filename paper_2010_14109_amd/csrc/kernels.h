@@ -19,6 +19,18 @@ hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, i
                         int64_t K, int64_t N, hipStream_t s);
 hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, int64_t K,
                         int64_t N, hipStream_t s);
+// Batched GEMM: C_z[M][N] = sum_k A_z[m][k] B_z[k][n] for z < batches.  A is
+// "row of k" (A[m][k] = A[m lda + k]) or not (A[m][k] = A[k lda + m]); B is
+// "row of k" (B[k][n] = B[n ldb + k]) or not (B[k][n] = B[k ldb + n]).
+// Batch z = zo inner + zi moves A, B, C by zo * outer + zi * inner strides.
+struct BatchStrides {
+  int64_t inner;
+  int64_t a_outer, a_inner, b_outer, b_inner, c_outer, c_inner;
+};
+hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, const float* B,
+                        int64_t ldb, float* C, int64_t ldc, int64_t M, int64_t N, int64_t K,
+                        int64_t batches, const BatchStrides& st, hipStream_t s);
+
 struct ConvShape {
   int64_t N, H, W, C, K, R, S, stride, pad, P, Q;
 };
@@ -49,6 +61,23 @@ hipError_t maxpool_bwd(const uint8_t* idx, const float* dy, float* dx, const Poo
 hipError_t avgpool_fwd(const float* x, float* y, int64_t N, int64_t HW, int64_t C, hipStream_t s);
 hipError_t avgpool_bwd(const float* dy, float* dx, int64_t N, int64_t HW, int64_t C,
                        hipStream_t s);
+// Transformer layers (transformer.hip).
+hipError_t embed_fwd(const int32_t* ids, const float* E, const float* pos, float* y, int64_t B,
+                     int64_t T, int64_t V, int64_t d, hipStream_t s);
+hipError_t embed_bwd(const int32_t* ids, const float* dy, float* dE, float* dpos, int64_t B,
+                     int64_t T, int64_t V, int64_t d, hipStream_t s);
+hipError_t layernorm_fwd(const float* x, const float* gamma, const float* beta, float* y,
+                         float* stats, int64_t rows, int64_t d, int64_t slices, hipStream_t s);
+hipError_t layernorm_bwd(const float* x, const float* gamma, float* stats, const float* dy,
+                         float* dx, float* dgamma, float* dbeta, int64_t rows, int64_t d,
+                         int64_t slices, hipStream_t s);
+hipError_t gelu_fwd(const float* x, float* y, int64_t n, hipStream_t s);
+hipError_t gelu_bwd(const float* x, const float* dy, float* dx, int64_t n, hipStream_t s);
+hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_t T, int64_t H,
+                         int64_t dh, bool causal, hipStream_t s);
+hipError_t attention_bwd(const float* qkv, const float* P, const float* dy, float* dqkv, float* dS,
+                         int64_t B, int64_t T, int64_t H, int64_t dh, bool causal, hipStream_t s);
+
 hipError_t mix(void* const* ptrs, const uint64_t* words, int nvars, uint32_t seed, hipStream_t s,
                bool y_read);
 

@@ -1,0 +1,395 @@
+// Transformer layers: embedding, LayerNorm, exact GELU and causal attention
+// (gfx950).
+//
+// Row-wise work (LayerNorm, softmax rows) runs one wave64 per row with the
+// row held in registers, lane l owning columns l, l + 64, ...; reductions
+// use cross-lane shuffles, so a row's statistics are exact sums in a fixed
+// order.  Column sums over rows (LayerNorm's dgamma / dbeta, the position
+// embedding's gradient) go through per-slice partials summed in slice order,
+// and the token embedding's gradient gathers, per vocabulary row, the
+// gradient rows of the tokens carrying that id in token order.  No atomics:
+// results do not depend on scheduling.
+//
+// Attention materialises the probabilities P = softmax(q k^T / sqrt(dh))
+// per batch and head (the variable the scheduler swaps like any other):
+// batched MFMA GEMMs compute q k^T into P and P v into the context, a row
+// kernel applies the scale, the causal mask and the softmax in place.  The
+// backward pass runs the four batched GEMMs of dv, dP, dq, dk around the row
+// kernel dS = scale P (dP - rowsum(dP P)).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "kernels.h"
+
+namespace ooc {
+
+namespace {
+
+constexpr int TPB = 256;
+
+unsigned grid_for(int64_t work) {
+  int64_t g = (work + TPB - 1) / TPB;
+  if (g < 1) g = 1;
+  if (g > 16384) g = 16384;
+  return (unsigned)g;
+}
+
+__device__ inline float wave_sum(float x) {
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+__device__ inline float wave_max(float x) {
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+// ---------------------------------------------------------------- embedding
+__global__ void embed_fwd_kernel(const int32_t* __restrict__ ids, const float* __restrict__ E,
+                                 const float* __restrict__ pos, float* __restrict__ y,
+                                 int64_t rows, int64_t T, int64_t V, int64_t d) {
+  const int64_t n = rows * d;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int64_t r = i / d, c = i - r * d;
+    const int32_t id = ids[r];
+    y[i] = (id >= 0 && id < V) ? E[(int64_t)id * d + c] + pos[(r % T) * d + c] : NAN;
+  }
+}
+
+// dpos[t][c] = sum over b (in order) of dy[b T + t][c]
+__global__ void embed_pos_grad(const float* __restrict__ dy, float* __restrict__ dpos, int64_t B,
+                               int64_t T, int64_t d) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= T * d) return;
+  float acc = 0.f;
+  for (int64_t b = 0; b < B; ++b) acc += dy[b * T * d + i];
+  dpos[i] = acc;
+}
+
+// dE[v][c] = sum over tokens r with ids[r] == v, in token order, of dy[r][c];
+// one wave per vocabulary row, 512 columns per pass
+__global__ void embed_tok_grad(const int32_t* __restrict__ ids, const float* __restrict__ dy,
+                               float* __restrict__ dE, int64_t N, int64_t V, int64_t d) {
+  const int64_t v = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (v >= V) return;
+  for (int64_t c0 = 0; c0 < d; c0 += 512) {
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int64_t base = 0; base < N; base += 64) {
+      const int64_t r = base + lane;
+      const bool m = r < N && ids[r] == v;
+      unsigned long long mask = __ballot(m);
+      while (mask) {
+        const int j = __ffsll((long long)mask) - 1;
+        mask &= mask - 1;
+        const float* row = dy + (base + j) * d;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int64_t c = c0 + lane + 64 * u;
+          if (c < d) acc[u] += row[c];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t c = c0 + lane + 64 * u;
+      if (c < d) dE[v * d + c] = acc[u];
+    }
+  }
+}
+
+// ---------------------------------------------------------------- LayerNorm
+template <int J>
+__global__ __launch_bounds__(TPB) void ln_fwd_kernel(const float* __restrict__ x,
+                                                     const float* __restrict__ gamma,
+                                                     const float* __restrict__ beta,
+                                                     float* __restrict__ y,
+                                                     float* __restrict__ stats, int64_t rows,
+                                                     int64_t d) {
+  const int64_t r = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const float* xr = x + r * d;
+  float v[J];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int64_t c = lane + 64 * j;
+    v[j] = c < d ? xr[c] : 0.f;
+    s += v[j];
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int64_t c = lane + 64 * j;
+    const float t = c < d ? v[j] - mean : 0.f;
+    q += t * t;
+  }
+  const float rstd = 1.f / sqrtf(wave_sum(q) / (float)d + 1e-5f);
+  float* yr = y + r * d;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int64_t c = lane + 64 * j;
+    if (c < d) yr[c] = (v[j] - mean) * rstd * gamma[c] + beta[c];
+  }
+  if (lane == 0) {
+    stats[r] = mean;
+    stats[rows + r] = rstd;
+  }
+}
+
+// dx per row; per-slice partial sums of dy xhat and dy per feature, the four
+// waves of the workgroup added in wave order
+template <int J>
+__global__ __launch_bounds__(TPB) void ln_bwd_kernel(const float* __restrict__ x,
+                                                     const float* __restrict__ gamma,
+                                                     const float* __restrict__ st,
+                                                     const float* __restrict__ dy,
+                                                     float* __restrict__ dx,
+                                                     float* __restrict__ part, int64_t rows,
+                                                     int64_t d, int64_t len) {
+  extern __shared__ float lds[];   // [2][d]
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t s = blockIdx.x;
+  const int64_t r0 = s * len, r1 = min(rows, r0 + len);
+  float ag[J], ab[J], gm[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int64_t c = lane + 64 * j;
+    ag[j] = ab[j] = 0.f;
+    gm[j] = c < d ? gamma[c] : 0.f;
+  }
+  for (int64_t r = r0 + w; r < r1; r += TPB / 64) {
+    const float mean = st[r], rstd = st[rows + r];
+    float xh[J], g[J];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int64_t c = lane + 64 * j;
+      const float dv = c < d ? dy[r * d + c] : 0.f;
+      xh[j] = c < d ? (x[r * d + c] - mean) * rstd : 0.f;
+      g[j] = dv * gm[j];
+      s1 += g[j];
+      s2 += g[j] * xh[j];
+      ag[j] += dv * xh[j];
+      ab[j] += dv;
+    }
+    const float m1 = wave_sum(s1) / (float)d, m2 = wave_sum(s2) / (float)d;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int64_t c = lane + 64 * j;
+      if (c < d) dx[r * d + c] = rstd * (g[j] - m1 - xh[j] * m2);
+    }
+  }
+  for (int k = 0; k < TPB / 64; ++k) {
+    if (w == k) {
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int64_t c = lane + 64 * j;
+        if (c < d) {
+          lds[c] = (k == 0 ? 0.f : lds[c]) + ag[j];
+          lds[d + c] = (k == 0 ? 0.f : lds[d + c]) + ab[j];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  for (int64_t c = threadIdx.x; c < 2 * d; c += TPB) part[s * 2 * d + c] = lds[c];
+}
+
+// dgamma[c] / dbeta[c] = sum over slices of the partials, four interleaved
+// accumulators added in a fixed order
+__global__ void ln_finalize(const float* __restrict__ part, float* __restrict__ dgamma,
+                            float* __restrict__ dbeta, int64_t d, int64_t slices) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= d) return;
+  float a[4] = {0, 0, 0, 0}, b[4] = {0, 0, 0, 0};
+  int64_t s = 0;
+  for (; s + 4 <= slices; s += 4)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      a[u] += part[(s + u) * 2 * d + c];
+      b[u] += part[(s + u) * 2 * d + d + c];
+    }
+  for (; s < slices; ++s) {
+    a[0] += part[s * 2 * d + c];
+    b[0] += part[s * 2 * d + d + c];
+  }
+  dgamma[c] = (a[0] + a[1]) + (a[2] + a[3]);
+  dbeta[c] = (b[0] + b[1]) + (b[2] + b[3]);
+}
+
+// ---------------------------------------------------------------- GELU
+__global__ void gelu_kernel(const float* __restrict__ x, const float* __restrict__ dy,
+                            float* __restrict__ out, int64_t n, bool backward) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const float v = x[i];
+    const float cdf = 0.5f * (1.f + erff(v * 0.70710678118654752f));
+    if (!backward) {
+      out[i] = v * cdf;
+    } else {
+      const float pdf = expf(-0.5f * v * v) * 0.39894228040143268f;
+      out[i] = dy[i] * (cdf + v * pdf);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- attention rows
+// P row (b, h, i) in place: scale, causal mask (keys j > i get 0), softmax
+__global__ void attn_softmax(float* __restrict__ P, int64_t nrows, int64_t T, float scale,
+                             bool causal) {
+  const int64_t row = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= nrows) return;
+  const int64_t i = row % T;
+  const int64_t n = causal ? i + 1 : T;
+  float* p = P + row * T;
+  float mx = -INFINITY;
+  for (int64_t j = lane; j < n; j += 64) mx = fmaxf(mx, p[j] * scale);
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int64_t j = lane; j < n; j += 64) sum += expf(p[j] * scale - mx);
+  sum = wave_sum(sum);
+  const float inv = 1.f / sum;
+  for (int64_t j = lane; j < T; j += 64) p[j] = j < n ? expf(p[j] * scale - mx) * inv : 0.f;
+}
+
+// dS row in place: dS = scale P (dP - sum_j dP P)
+__global__ void attn_softmax_bwd(const float* __restrict__ P, float* __restrict__ dS,
+                                 int64_t nrows, int64_t T, float scale) {
+  const int64_t row = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= nrows) return;
+  const float* p = P + row * T;
+  float* g = dS + row * T;
+  float dot = 0.f;
+  for (int64_t j = lane; j < T; j += 64) dot += g[j] * p[j];
+  dot = wave_sum(dot);
+  for (int64_t j = lane; j < T; j += 64) g[j] = scale * p[j] * (g[j] - dot);
+}
+
+template <int J>
+hipError_t ln_fwd_j(const float* x, const float* g, const float* b, float* y, float* st,
+                    int64_t rows, int64_t d, hipStream_t s) {
+  hipLaunchKernelGGL(ln_fwd_kernel<J>, dim3((unsigned)((rows + 3) / 4)), dim3(TPB), 0, s, x, g, b,
+                     y, st, rows, d);
+  return hipGetLastError();
+}
+
+template <int J>
+hipError_t ln_bwd_j(const float* x, const float* g, float* st, const float* dy, float* dx,
+                    int64_t rows, int64_t d, int64_t slices, hipStream_t s) {
+  const int64_t len = (rows + slices - 1) / slices;
+  hipLaunchKernelGGL(ln_bwd_kernel<J>, dim3((unsigned)slices), dim3(TPB),
+                     (unsigned)(2 * d * sizeof(float)), s, x, g, st, dy, dx, st + 2 * rows, rows,
+                     d, len);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t embed_fwd(const int32_t* ids, const float* E, const float* pos, float* y, int64_t B,
+                     int64_t T, int64_t V, int64_t d, hipStream_t s) {
+  hipLaunchKernelGGL(embed_fwd_kernel, dim3(grid_for(B * T * d)), dim3(TPB), 0, s, ids, E, pos, y,
+                     B * T, T, V, d);
+  return hipGetLastError();
+}
+
+hipError_t embed_bwd(const int32_t* ids, const float* dy, float* dE, float* dpos, int64_t B,
+                     int64_t T, int64_t V, int64_t d, hipStream_t s) {
+  hipLaunchKernelGGL(embed_pos_grad, dim3((unsigned)((T * d + TPB - 1) / TPB)), dim3(TPB), 0, s,
+                     dy, dpos, B, T, d);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(embed_tok_grad, dim3((unsigned)((V + 3) / 4)), dim3(TPB), 0, s, ids, dy, dE,
+                     B * T, V, d);
+  return hipGetLastError();
+}
+
+#define LN_DISPATCH(CALL)                 \
+  if (d <= 64) return CALL(1);            \
+  if (d <= 128) return CALL(2);           \
+  if (d <= 256) return CALL(4);           \
+  if (d <= 512) return CALL(8);           \
+  if (d <= 1024) return CALL(16);         \
+  if (d <= 2048) return CALL(32);         \
+  if (d <= 4096) return CALL(64);         \
+  return hipErrorInvalidValue
+
+hipError_t layernorm_fwd(const float* x, const float* gamma, const float* beta, float* y,
+                         float* stats, int64_t rows, int64_t d, int64_t slices, hipStream_t s) {
+  (void)slices;
+#define LN_F(J) ln_fwd_j<J>(x, gamma, beta, y, stats, rows, d, s)
+  LN_DISPATCH(LN_F);
+#undef LN_F
+}
+
+hipError_t layernorm_bwd(const float* x, const float* gamma, float* stats, const float* dy,
+                         float* dx, float* dgamma, float* dbeta, int64_t rows, int64_t d,
+                         int64_t slices, hipStream_t s) {
+  hipError_t e;
+#define LN_B(J) ln_bwd_j<J>(x, gamma, stats, dy, dx, rows, d, slices, s)
+  e = [&]() -> hipError_t { LN_DISPATCH(LN_B); }();
+#undef LN_B
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(ln_finalize, dim3((unsigned)((d + TPB - 1) / TPB)), dim3(TPB), 0, s,
+                     stats + 2 * rows, dgamma, dbeta, d, slices);
+  return hipGetLastError();
+}
+
+hipError_t gelu_fwd(const float* x, float* y, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(gelu_kernel, dim3(grid_for(n)), dim3(TPB), 0, s, x, nullptr, y, n, false);
+  return hipGetLastError();
+}
+
+hipError_t gelu_bwd(const float* x, const float* dy, float* dx, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(gelu_kernel, dim3(grid_for(n)), dim3(TPB), 0, s, x, dy, dx, n, true);
+  return hipGetLastError();
+}
+
+hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_t T, int64_t H,
+                         int64_t dh, bool causal, hipStream_t s) {
+  const int64_t d = H * dh, d3 = 3 * d, TT = T * T;
+  // S = q k^T into P
+  BatchStrides st{H, T * d3, dh, T * d3, dh, H * TT, TT};
+  hipError_t e = gemm_batched(true, qkv, d3, true, qkv + d, d3, P, T, T, T, dh, B * H, st, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_softmax, dim3((unsigned)((B * H * T + 3) / 4)), dim3(TPB), 0, s, P,
+                     B * H * T, T, 1.f / sqrtf((float)dh), causal);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // context = P v
+  BatchStrides sv{H, H * TT, TT, T * d3, dh, T * d, dh};
+  return gemm_batched(true, P, T, false, qkv + 2 * d, d3, y, d, T, dh, T, B * H, sv, s);
+}
+
+hipError_t attention_bwd(const float* qkv, const float* P, const float* dy, float* dqkv, float* dS,
+                         int64_t B, int64_t T, int64_t H, int64_t dh, bool causal, hipStream_t s) {
+  (void)causal;   // P is zero above the diagonal, so dS is too
+  const int64_t d = H * dh, d3 = 3 * d, TT = T * T;
+  hipError_t e;
+  // dv = P^T dO
+  BatchStrides s1{H, H * TT, TT, T * d, dh, T * d3, dh};
+  if ((e = gemm_batched(false, P, T, false, dy, d, dqkv + 2 * d, d3, T, dh, T, B * H, s1, s)) !=
+      hipSuccess)
+    return e;
+  // dP = dO v^T into dS
+  BatchStrides s2{H, T * d, dh, T * d3, dh, H * TT, TT};
+  if ((e = gemm_batched(true, dy, d, true, qkv + 2 * d, d3, dS, T, T, T, dh, B * H, s2, s)) !=
+      hipSuccess)
+    return e;
+  hipLaunchKernelGGL(attn_softmax_bwd, dim3((unsigned)((B * H * T + 3) / 4)), dim3(TPB), 0, s, P,
+                     dS, B * H * T, T, 1.f / sqrtf((float)dh));
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // dq = dS k
+  BatchStrides s3{H, H * TT, TT, T * d3, dh, T * d3, dh};
+  if ((e = gemm_batched(true, dS, T, false, qkv + d, d3, dqkv, d3, T, dh, T, B * H, s3, s)) !=
+      hipSuccess)
+    return e;
+  // dk = dS^T q
+  return gemm_batched(false, dS, T, false, qkv, d3, dqkv + d, d3, T, dh, T, B * H, s3, s);
+}
+
+}  // namespace ooc

@@ -37,6 +37,14 @@ const Sig kSig[OOC_OP_COUNT] = {
     {"AVGPOOL_FWD", 2, 4, {OOC_R, OOC_W}},
     {"AVGPOOL_BWD", 2, 4, {OOC_R, OOC_W}},
     {"MIX", -1, 1, {}},
+    {"EMBED_FWD", 4, 4, {OOC_R, OOC_R, OOC_R, OOC_W}},
+    {"EMBED_BWD", 4, 4, {OOC_R, OOC_R, OOC_W, OOC_W}},
+    {"LAYERNORM_FWD", 5, 3, {OOC_R, OOC_R, OOC_R, OOC_W, OOC_W}},
+    {"LAYERNORM_BWD", 7, 3, {OOC_R, OOC_R, OOC_RW, OOC_R, OOC_W, OOC_W, OOC_W}},
+    {"GELU_FWD", 2, 1, {OOC_R, OOC_W}},
+    {"GELU_BWD", 3, 1, {OOC_R, OOC_R, OOC_W}},
+    {"ATTENTION_FWD", 3, 5, {OOC_R, OOC_W, OOC_W}},
+    {"ATTENTION_BWD", 5, 5, {OOC_R, OOC_R, OOC_R, OOC_W, OOC_W}},
 };
 
 const int64_t kMaxElems = int64_t(1) << 40;
@@ -213,6 +221,67 @@ std::string check_fn(const std::vector<Var>& vars, const Fn& fn) {
       } else {
         NEED(0, N * C * 4, "dY");
         NEED(1, N * H * W * C * 4, "dX");
+      }
+      return "";
+    }
+    case OOC_OP_EMBED_FWD:
+    case OOC_OP_EMBED_BWD: {
+      int64_t B = a[0], T = a[1], V = a[2], d = a[3];
+      if (B <= 0 || T <= 0 || V <= 0 || d <= 0 || V > INT32_MAX) return nm + ": bad attributes";
+      NEED(0, B * T * 4, "ids");
+      if (fn.op == OOC_OP_EMBED_FWD) {
+        NEED(1, V * d * 4, "E");
+        NEED(2, T * d * 4, "pos");
+        NEED(3, B * T * d * 4, "Y");
+      } else {
+        NEED(1, B * T * d * 4, "dY");
+        NEED(2, V * d * 4, "dE");
+        NEED(3, T * d * 4, "dpos");
+      }
+      return "";
+    }
+    case OOC_OP_LAYERNORM_FWD:
+    case OOC_OP_LAYERNORM_BWD: {
+      int64_t rows = a[0], d = a[1], S = a[2];
+      if (rows <= 0 || d <= 0 || d > 4096 || S < 1 || S > rows) return nm + ": bad attributes";
+      const int64_t xb = rows * d * 4, cb = d * 4, sb = (2 * rows + 2 * S * d) * 4;
+      if (fn.op == OOC_OP_LAYERNORM_FWD) {
+        NEED(0, xb, "X");
+        NEED(1, cb, "gamma");
+        NEED(2, cb, "beta");
+        NEED(3, xb, "Y");
+        NEED(4, sb, "stats");
+      } else {
+        NEED(0, xb, "X");
+        NEED(1, cb, "gamma");
+        NEED(2, sb, "stats");
+        NEED(3, xb, "dY");
+        NEED(4, xb, "dX");
+        NEED(5, cb, "dgamma");
+        NEED(6, cb, "dbeta");
+      }
+      return "";
+    }
+    case OOC_OP_GELU_FWD:
+    case OOC_OP_GELU_BWD:
+      for (int j = 0; j < nv; ++j) NEED(j, a[0] * 4, "tensor");
+      return "";
+    case OOC_OP_ATTENTION_FWD:
+    case OOC_OP_ATTENTION_BWD: {
+      int64_t B = a[0], T = a[1], H = a[2], dh = a[3], causal = a[4];
+      if (B <= 0 || T <= 0 || H <= 0 || dh <= 0 || (causal != 0 && causal != 1) ||
+          B * H > 65535)
+        return nm + ": bad attributes";
+      const int64_t qb = B * T * 3 * H * dh * 4, pb = B * H * T * T * 4, yb = B * T * H * dh * 4;
+      NEED(0, qb, "qkv");
+      if (fn.op == OOC_OP_ATTENTION_FWD) {
+        NEED(1, pb, "P");
+        NEED(2, yb, "Y");
+      } else {
+        NEED(1, pb, "P");
+        NEED(2, yb, "dY");
+        NEED(3, qb, "dqkv");
+        NEED(4, pb, "dS");
       }
       return "";
     }

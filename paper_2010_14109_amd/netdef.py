@@ -5,7 +5,8 @@ each with the set of variables it uses (Section 2; Section 3,
 variable-sequence).  ``Net`` builds that sequence for one training step and
 registers it through the C interface:
 
-* forward functions in layer order, then the fused softmax cross-entropy;
+* forward functions in layer order, then the fused softmax cross-entropy
+  (one label per row of the logits);
 * per layer in reverse order: its backward functions, one SGD function for
   its parameters, then the additions that sum the gradient contributions of
   tensors consumed more than once (in the order the contributions appear);
@@ -17,7 +18,10 @@ fixed per shape: a BatchNorm keeps 2 + 2 S floats per channel with S =
 min(ceil(rows / 512), 2048) row slices, and a convolution's filter gradient
 is split over S_w = min(ceil(1024 / T), ceil(L / 1024)) pixel slices (at
 least 1) with T = ceil(K / 128) ceil(R S C / 128) output tiles and L = N P Q
-pixels, using a partial-sum variable of S_w copies of dW when S_w > 1.
+pixels, using a partial-sum variable of S_w copies of dW when S_w > 1.  A
+LayerNorm keeps mean and 1/std per row and 2 S floats per feature (same S
+formula over its rows); attention keeps its probabilities [B, H, T, T] and its
+backward a scratch of the same size.
 """
 
 from __future__ import annotations
@@ -132,6 +136,49 @@ class Net:
         self._call("add", [(X, ooc.R), (B, ooc.R), (Y, ooc.W)], [prod(xs)])
         return xs
 
+    def _fwd_embed(self, L, X):
+        B, T = self.shape[X]
+        d = L["d"]
+        E = self._decl(L["name"] + ".E", (L["vocab"], d), kind=ooc.PARAM)
+        pos = self._decl(L["name"] + ".pos", (T, d), kind=ooc.PARAM)
+        self.params[L["name"]] = [E, pos]
+        Y = self._decl(L["name"], (B * T, d))
+        self._call("embed_fwd", [(X, ooc.R), (E, ooc.R), (pos, ooc.R), (Y, ooc.W)],
+                   [B, T, L["vocab"], d])
+        return (B * T, d)
+
+    def _fwd_layernorm(self, L, X):
+        rows, d = self.shape[X]
+        S = bn_row_slices(rows)
+        g = self._decl(L["name"] + ".gamma", (d,), kind=ooc.PARAM)
+        bt = self._decl(L["name"] + ".beta", (d,), kind=ooc.PARAM)
+        self.params[L["name"]] = [g, bt]
+        Y = self._decl(L["name"], (rows, d))
+        st = self._decl(L["name"] + ".stats", (2 * rows + 2 * S * d,))
+        self._call("layernorm_fwd", [(X, ooc.R), (g, ooc.R), (bt, ooc.R), (Y, ooc.W),
+                                     (st, ooc.W)], [rows, d, S])
+        return (rows, d)
+
+    def _fwd_gelu(self, L, X):
+        xs = self.shape[X]
+        Y = self._decl(L["name"], xs)
+        self._call("gelu_fwd", [(X, ooc.R), (Y, ooc.W)], [prod(xs)])
+        return xs
+
+    def _attn_attrs(self, L, X):
+        rows, d3 = self.shape[X]
+        B, T = self.spec["input"]
+        H = L["heads"]
+        return [B, T, H, d3 // 3 // H, 1 if L["causal"] else 0]
+
+    def _fwd_attention(self, L, X):
+        a = self._attn_attrs(L, X)
+        B, T, H, dh, _ = a
+        Pr = self._decl(L["name"] + ".P", (B, H, T, T))
+        Y = self._decl(L["name"], (B * T, H * dh))
+        self._call("attention_fwd", [(X, ooc.R), (Pr, ooc.W), (Y, ooc.W)], a)
+        return (B * T, H * dh)
+
     # ------------------------------------------------------------ backward
     def _grad_of_param(self, p):
         return self._decl("d:" + p, self.meta[p][0],
@@ -202,15 +249,48 @@ class Net:
         elif op == "add":
             for src in L["in"]:
                 out.append((src, dY))
+        elif op == "embed":
+            E, pos = self.params[name]
+            B, T = xs
+            self._call("embed_bwd", [(X, ooc.R), (dY, ooc.R), (self._grad_of_param(E), ooc.W),
+                                     (self._grad_of_param(pos), ooc.W)],
+                       [B, T, L["vocab"], L["d"]])
+            self._sgd(name)
+        elif op == "layernorm":
+            g, bt = self.params[name]
+            rows, d = xs
+            dX = self._decl(f"d:{X}@{name}", xs)
+            self._call("layernorm_bwd", [(X, ooc.R), (g, ooc.R), (name + ".stats", ooc.RW),
+                                         (dY, ooc.R), (dX, ooc.W),
+                                         (self._grad_of_param(g), ooc.W),
+                                         (self._grad_of_param(bt), ooc.W)],
+                       [rows, d, bn_row_slices(rows)])
+            out.append((X, dX))
+            self._sgd(name)
+        elif op == "gelu":
+            dX = self._decl(f"d:{X}@{name}", xs)
+            self._call("gelu_bwd", [(X, ooc.R), (dY, ooc.R), (dX, ooc.W)], [prod(xs)])
+            out.append((X, dX))
+        elif op == "attention":
+            a = self._attn_attrs(L, X)
+            B, T, H, dh, _ = a
+            dX = self._decl(f"d:{X}@{name}", xs)
+            dS = self._decl(name + ".dS", (B, H, T, T))
+            self._call("attention_bwd", [(X, ooc.R), (name + ".P", ooc.R), (dY, ooc.R),
+                                         (dX, ooc.W), (dS, ooc.W)], a)
+            out.append((X, dX))
 
     # ------------------------------------------------------------ whole step
     def _lower(self):
         spec = self.spec
         self.shape["x"] = tuple(spec["input"])
-        self._decl("x", spec["input"], kind=ooc.INPUT)
+        self._decl("x", spec["input"], dtype="i32" if spec.get("tokens") else "f32",
+                   kind=ooc.INPUT)
         fwd = {"linear": self._fwd_linear, "conv": self._fwd_conv, "bn": self._fwd_bn,
                "relu": self._fwd_relu, "maxpool": self._fwd_maxpool,
-               "avgpool": self._fwd_avgpool, "add": self._fwd_add}
+               "avgpool": self._fwd_avgpool, "add": self._fwd_add, "embed": self._fwd_embed,
+               "layernorm": self._fwd_layernorm, "gelu": self._fwd_gelu,
+               "attention": self._fwd_attention}
         for L in spec["layers"]:
             self.shape[L["name"]] = fwd[L["op"]](L, L["in"][0])
         logits = spec["logits"]

@@ -28,7 +28,9 @@ OPS = {
     "noop": 0, "linear_fwd": 1, "linear_bwd_w": 2, "linear_bwd_x": 3, "relu_fwd": 4,
     "relu_bwd": 5, "add": 6, "softmax_ce": 7, "sgd": 8, "conv_fwd": 9, "conv_bwd_w": 10,
     "conv_bwd_x": 11, "bn_fwd": 12, "bn_bwd": 13, "maxpool_fwd": 14, "maxpool_bwd": 15,
-    "avgpool_fwd": 16, "avgpool_bwd": 17, "mix": 18,
+    "avgpool_fwd": 16, "avgpool_bwd": 17, "mix": 18, "embed_fwd": 19, "embed_bwd": 20,
+    "layernorm_fwd": 21, "layernorm_bwd": 22, "gelu_fwd": 23, "gelu_bwd": 24,
+    "attention_fwd": 25, "attention_bwd": 26,
 }
 
 #: every symbol ``include/ooc.h`` declares

@@ -30,6 +30,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 def specs_small():
     return [
+        synth.transformer(batch=2, seq=8, d=64, heads=4, ffn=96, layers=2, vocab=50),
         synth.mlp(batch=4, width=16, depth=4, classes=5),
         synth.mlp(batch=3, width=8, depth=2, classes=3, momentum=0.9),
         synth.plain_cnn(batch=2, channels=4, depth=3, hw=8, classes=5),
@@ -38,7 +39,8 @@ def specs_small():
 
 
 def specs_full():
-    return [synth.workload(n) for n in ("mlp", "cnn", "resnet50_b256", "resnet50_b1440")]
+    return [synth.workload(n) for n in ("mlp", "cnn", "resnet50_b256", "resnet50_b1440",
+                                        "transformer")]
 
 
 @pytest.mark.parametrize("spec", specs_small() + specs_full(), ids=lambda s: s["name"])
@@ -66,11 +68,12 @@ def host_ctx(net, budget, window, chunk, policy):
     return ctx
 
 
-@pytest.mark.parametrize("spec", specs_small() + specs_full(), ids=lambda s: s["name"])
-def test_schedule_and_plan_match_oracle(spec):
+@pytest.mark.parametrize("spec,full", [(s, False) for s in specs_small()] +
+                         [(s, True) for s in specs_full()], ids=lambda s: s["name"]
+                         if isinstance(s, dict) else ("full" if s else "small"))
+def test_schedule_and_plan_match_oracle(spec, full):
     net = netdef.Net(spec)
     b, k, f = as_schedule_input(lower(spec))
-    full = spec["input"][0] >= 128
     chunks = (2 << 20,) if full else (64, 4096)
     fracs = (1.0, 0.5, 0.25, 1 / 7.5, 0.0) if full else (1.0, 0.75, 0.5, 0.4, 0.25, 1 / 7.5, 0.2, 0.0)
     for chunk in chunks:

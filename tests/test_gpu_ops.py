@@ -243,3 +243,75 @@ def test_mix_op():
     assert np.array_equal(y, mixop.mix([a, b, y0], 9, 12345))
     (_, y) = run_fn("mix", [(a, ooc.R), (((33,), "u32"), ooc.W)], [7])
     assert np.array_equal(y, mixop.mix([a], 33, 7))
+
+
+# ---------------------------------------------------------------- transformer layers
+@pytest.mark.parametrize("rows,d,slices", [(37, 64, 1), (37, 100, 3), (130, 1024, 4), (5, 4096, 2)])
+def test_layernorm(rows, d, slices):
+    X = f32(rows, d, scale=2.0) + 0.3
+    g, b, G = f32(d), f32(d), f32(rows, d)
+    sb = 2 * rows + 2 * slices * d
+    print(f"layernorm rows={rows} d={d} slices={slices}", flush=True)
+    (_, _, _, Y, st) = run_fn("layernorm_fwd", [(X, ooc.R), (g, ooc.R), (b, ooc.R),
+                                                 (((rows, d), "f32"), ooc.W),
+                                                 (((sb,), "f32"), ooc.W)], [rows, d, slices])
+    rY, mean, rstd = ops.layernorm_fwd(X.astype(np.float64), g.astype(np.float64),
+                                       b.astype(np.float64))
+    assert rel_l2(Y, rY) < TOL
+    assert rel_l2(st[:rows], mean) < TOL and rel_l2(st[rows:2 * rows], rstd) < TOL
+    out = run_fn("layernorm_bwd", [(X, ooc.R), (g, ooc.R), (st.astype(np.float32), ooc.RW),
+                                   (G, ooc.R), (((rows, d), "f32"), ooc.W),
+                                   (((d,), "f32"), ooc.W), (((d,), "f32"), ooc.W)],
+                 [rows, d, slices])
+    rdX, rdg, rdb = ops.layernorm_bwd(X.astype(np.float64), g.astype(np.float64), mean, rstd,
+                                      G.astype(np.float64))
+    assert rel_l2(out[4], rdX) < TOL and rel_l2(out[5], rdg) < TOL and rel_l2(out[6], rdb) < TOL
+
+
+@pytest.mark.parametrize("n", [1003, 1])
+def test_gelu(n):
+    x, g = f32(n, scale=3.0), f32(n)
+    (_, y) = run_fn("gelu_fwd", [(x, ooc.R), (((n,), "f32"), ooc.W)], [n])
+    assert rel_l2(y, ops.gelu_fwd(x.astype(np.float64))) < TOL
+    (_, _, dx) = run_fn("gelu_bwd", [(x, ooc.R), (g, ooc.R), (((n,), "f32"), ooc.W)], [n])
+    assert rel_l2(dx, ops.gelu_bwd(x.astype(np.float64), g.astype(np.float64))) < TOL
+
+
+@pytest.mark.parametrize("B,T,V,dm", [(3, 5, 17, 64), (2, 7, 40, 48), (4, 64, 1000, 1024)])
+def test_embedding(B, T, V, dm):
+    ids = rng.integers(0, V, (B, T)).astype(np.int32)
+    ids[0, 0] = ids[-1, -1] = 3                        # a repeated token
+    E, pos, G = f32(V, dm), f32(T, dm), f32(B * T, dm)
+    (_, _, _, Y) = run_fn("embed_fwd", [(ids, ooc.R), (E, ooc.R), (pos, ooc.R),
+                                        (((B * T, dm), "f32"), ooc.W)], [B, T, V, dm])
+    assert np.array_equal(Y, ops.embed_fwd(ids, E, pos))
+    (_, _, dE, dpos) = run_fn("embed_bwd", [(ids, ooc.R), (G, ooc.R), (((V, dm), "f32"), ooc.W),
+                                            (((T, dm), "f32"), ooc.W)], [B, T, V, dm])
+    rdE, rdpos = ops.embed_bwd(ids, G.astype(np.float64), V)
+    assert rel_l2(dE, rdE) < TOL and rel_l2(dpos, rdpos) < TOL
+
+
+def test_embedding_out_of_range_id():
+    B, T, V, dm = 1, 3, 5, 64
+    ids = np.array([[0, 7, -2]], dtype=np.int32)
+    E, pos = f32(V, dm), f32(T, dm)
+    (_, _, _, Y) = run_fn("embed_fwd", [(ids, ooc.R), (E, ooc.R), (pos, ooc.R),
+                                        (((B * T, dm), "f32"), ooc.W)], [B, T, V, dm])
+    assert np.array_equal(Y[0], E[0] + pos[0]) and np.isnan(Y[1]).all() and np.isnan(Y[2]).all()
+
+
+@pytest.mark.parametrize("B,T,H,dh,causal", [(2, 6, 2, 8, 1), (2, 64, 4, 16, 1), (1, 130, 2, 64, 1),
+                                            (2, 33, 3, 8, 0), (1, 512, 2, 64, 1)])
+def test_attention(B, T, H, dh, causal):
+    dmod = H * dh
+    qkv, G = f32(B * T, 3 * dmod), f32(B * T, dmod)
+    print(f"attention B={B} T={T} H={H} dh={dh} causal={causal}", flush=True)
+    (_, P, Y) = run_fn("attention_fwd", [(qkv, ooc.R), (((B, H, T, T), "f32"), ooc.W),
+                                         (((B * T, dmod), "f32"), ooc.W)], [B, T, H, dh, causal])
+    rP, rY = ops.attention_fwd(qkv.astype(np.float64), B, T, H, bool(causal))
+    assert rel_l2(P, rP) < TOL and rel_l2(Y, rY) < TOL
+    out = run_fn("attention_bwd", [(qkv, ooc.R), (P, ooc.R), (G, ooc.R),
+                                   (((B * T, 3 * dmod), "f32"), ooc.W),
+                                   (((B, H, T, T), "f32"), ooc.W)], [B, T, H, dh, causal])
+    rd = ops.attention_bwd(qkv.astype(np.float64), rP, G.astype(np.float64), B, T, H)
+    assert rel_l2(out[3], rd) < TOL

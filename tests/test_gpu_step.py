@@ -32,6 +32,7 @@ def tiny_specs():
         # 64 x 64 inputs keep the last stage at 2 x 2: BatchNorm over 16 rows.  At 32 x 32
         # the last BatchNorm sees 2 rows and even the oracle run in float32 is 4e-2 off float64.
         synth.resnet(batch=4, hw=64, classes=11, blocks=(1, 1, 1, 1), width=8, momentum=0.9),
+        synth.transformer(batch=2, seq=16, d=64, heads=4, ffn=128, layers=2, vocab=97),
     ]
 
 
