@@ -66,7 +66,7 @@ def run(reg, x, labels, params, state=None, dtype=np.float64):
             rows, mean, env[dl] = ops.softmax_ce(g(lg), g(lb))
             env[loss] = np.concatenate([rows, [mean]])
         elif op == "linear_bwd_w":
-            X, dY, dW, db = vs
+            X, dY, dW, db = vs[:4]
             env[dW], env[db] = ops.linear_bwd_w(g(X), g(dY))
         elif op == "linear_bwd_x":
             Wn, dY, dX = vs

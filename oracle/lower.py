@@ -23,7 +23,7 @@ maxpool_fwd    X R, Y W, idx W
 avgpool_fwd    X R, Y W
 add_fwd        A R, B R, Y W
 softmax_ce     logits R, labels R, loss W, dlogits W
-linear_bwd_w   X R, dY R, dW W, db W
+linear_bwd_w   X R, dY R, dW W, db W [, part W] (part only when split into > 1 slice)
 linear_bwd_x   W R, dY R, dX W            (absent when X is the network input)
 conv_bwd_w     X R, dY R, dW W [, part W] (part only when split into > 1 slice)
 conv_bwd_x     W R, dY R, dX W            (absent when X is the network input)
@@ -51,8 +51,12 @@ Sizes: float32 tensors except ``labels`` (int32) and ``idx`` (uint8);
 ``stats`` holds mean and 1/std per channel followed by two partial sums per
 channel for each of S row slices, S = min(ceil(rows / 512), 2048) with rows =
 N H W; a LayerNorm's ``stats`` holds mean and 1/std per row followed by two
-partial sums per feature for each of S row slices (same S); ``part`` holds S_w slices of dW, S_w = min(ceil(1024 / T), ceil(L /
-1024)) with T = ceil(K / 128) ceil(R S C / 128) output tiles and L = N P Q.
+partial sums per feature for each of S row slices, S = min(ceil(rows / 32),
+2048); a convolution's
+``part`` holds S_w slices of dW, S_w = min(ceil(1024 / T), ceil(L / 1024))
+with T = ceil(K / 128) ceil(R S C / 128) output tiles and L = N P Q; a dense
+layer's ``part`` holds S_w slices of dW then S_w slices of db, with the same
+S_w formula over K = out, R S C = in and L = rows.
 
 Kinds: x and labels INPUT, parameters PARAM, momentum buffers STATE, loss
 OUTPUT (parameter gradients too when ``keep_grads``), everything else TEMP.
@@ -71,6 +75,10 @@ ITEMSIZE = {"f32": 4, "i32": 4, "u8": 1}
 
 def bn_slices(rows):
     return min(math.ceil(rows / 512), 2048)
+
+
+def ln_slices(rows):
+    return min(math.ceil(rows / 32), 2048)
 
 
 def conv_wgrad_slices(K, RSC, L):
@@ -171,7 +179,7 @@ def lower(spec, keep_grads=False):
                         {"B": Bt, "T": T, "V": L["vocab"], "d": d}))
         elif op == "layernorm":
             rows, d = xs
-            S = bn_slices(rows)
+            S = ln_slices(rows)
             g = var(name + ".gamma", (d,), kind=PARAM)
             bt = var(name + ".beta", (d,), kind=PARAM)
             st_ = var(name + ".stats", (2 * rows + 2 * S * d,))
@@ -249,7 +257,11 @@ def lower(spec, keep_grads=False):
             dW = var("d:" + Wn, decl[Wn][0], kind=grad_kind)
             db = var("d:" + bn_, decl[bn_][0], kind=grad_kind)
             attrs = {"M": xs[0], "K": xs[1], "N": L["out_features"]}
-            fns.append(("linear_bwd_w", [(X, R), (dY, R), (dW, W), (db, W)], attrs))
+            Sw = conv_wgrad_slices(attrs["N"], attrs["K"], attrs["M"])
+            vs = [(X, R), (dY, R), (dW, W), (db, W)]
+            if Sw > 1:
+                vs.append((var(name + ".part", (Sw * (attrs["N"] * attrs["K"] + attrs["N"]),)), W))
+            fns.append(("linear_bwd_w", vs, dict(attrs, slices=Sw)))
             if X != "x":
                 dX = var(f"d:{X}@{name}", xs)
                 fns.append(("linear_bwd_x", [(Wn, R), (dY, R), (dX, W)], attrs))
@@ -319,7 +331,7 @@ def lower(spec, keep_grads=False):
             dbt = var("d:" + bt, decl[bt][0], kind=grad_kind)
             fns.append(("layernorm_bwd", [(X, R), (g, R), (name + ".stats", RW), (dY, R),
                                           (dX, W), (dg, W), (dbt, W)],
-                        {"rows": rows, "d": d, "slices": bn_slices(rows)}))
+                        {"rows": rows, "d": d, "slices": ln_slices(rows)}))
             contribute(X, dX, pending)
             update(name)
         elif op == "gelu":

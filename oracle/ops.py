@@ -28,7 +28,7 @@ boundary: images NHWC, conv weights [K, R, S, C], dense weights [out, in].
 from __future__ import annotations
 
 import numpy as np
-from scipy.special import erf
+from scipy.special import erfc
 
 BN_EPS = 1e-5
 LN_EPS = 1e-5
@@ -210,12 +210,18 @@ def layernorm_bwd(X, gamma, mean, rstd, dY):
 
 
 # ---------------------------------------------------------------- GELU
+def _normal_cdf(X):
+    """Phi(x) = erfc(-x / sqrt 2) / 2; the erfc form keeps full relative precision in the
+    lower tail, where 1 + erf(x / sqrt 2) cancels."""
+    return 0.5 * erfc(-X / np.sqrt(2.0))
+
+
 def gelu_fwd(X):
-    return 0.5 * X * (1.0 + erf(X / np.sqrt(2.0)))
+    return X * _normal_cdf(X)
 
 
 def gelu_bwd(X, dY):
-    cdf = 0.5 * (1.0 + erf(X / np.sqrt(2.0)))
+    cdf = _normal_cdf(X)
     pdf = np.exp(-0.5 * X * X) / np.sqrt(2.0 * np.pi)
     return dY * (cdf + X * pdf)
 

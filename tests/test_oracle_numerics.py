@@ -280,6 +280,10 @@ def test_gelu_closed_form_and_fd():
     X = rng.standard_normal(50) * 3
     assert_close(ops.gelu_fwd(X), X * norm.cdf(X), 1e-13)
     assert ops.gelu_fwd(np.array([0.0]))[0] == 0.0
+    # lower tail: GELU(x) = x Phi(x) is tiny but not zero; elementwise relative error
+    T = np.array([-6.0, -9.0, -15.0, -30.0])
+    assert np.all(np.abs(ops.gelu_fwd(T) / (T * norm.cdf(T)) - 1) < 1e-12)
+    assert np.all(np.abs(ops.gelu_bwd(T, np.ones(4)) / (norm.cdf(T) + T * norm.pdf(T)) - 1) < 1e-9)
     G = rng.standard_normal(50)
     idx, g = fd_grad(lambda: float((ops.gelu_fwd(X) * G).sum()), X)
     assert_close(ops.gelu_bwd(X, G)[idx], g)
