@@ -29,8 +29,6 @@ PEAK_FP32_TFLOPS = 157.3       # MI355X dense fp32 (matrix and vector)
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PCIE5_X16_GBS = 63.0           # theoretical, per direction
 
-GEMM_OPS = {"linear_fwd", "linear_bwd_w", "linear_bwd_x", "conv_fwd", "conv_bwd_x", "conv_bwd_w"}
-
 
 def fn_work(op, attrs):
     """Algorithmic work of one function: ('flop', n) for GEMM-shaped ops, ('byte', n) for
@@ -61,6 +59,25 @@ def fn_work(op, attrs):
         return "byte", 4 * N * H * W * C + 4 * N * C
     if op == "softmax_ce":
         return "byte", 8 * a[0] * a[1]
+    if op == "embed_fwd":
+        B, T, V, d = a
+        return "byte", 8 * B * T * d + 4 * B * T + 4 * T * d
+    if op == "embed_bwd":
+        B, T, V, d = a
+        return "byte", 4 * B * T * d + 4 * B * T + 4 * V * d + 4 * T * d
+    if op == "layernorm_fwd":
+        return "byte", 8 * a[0] * a[1] + 8 * a[0]
+    if op == "layernorm_bwd":
+        return "byte", 12 * a[0] * a[1] + 8 * a[0]
+    if op == "gelu_fwd":
+        return "byte", 8 * a[0]
+    if op == "gelu_bwd":
+        return "byte", 12 * a[0]
+    if op in ("attention_fwd", "attention_bwd"):
+        # q k^T and P v forward, four products of the same size backward (dense,
+        # as computed: the causal mask zeroes P but the products are full)
+        B, T, H, dh = a[:4]
+        return "flop", (4 if op == "attention_fwd" else 8) * B * H * T * T * dh
     return "byte", 0
 
 
@@ -113,10 +130,12 @@ def choose_chunk(net, frac, window_frac):
     return 256 << 20, plan
 
 
-def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup):
+def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup, depth=None):
     ctx = ooc.Context(0)
     try:
         net.register(ctx)
+        if depth is not None:
+            ctx.set_swapout_depth(depth)
         ctx.set_chunk(chunk)
         ctx.set_budget(budget)
         if window is not None:
@@ -144,7 +163,7 @@ def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup)
             step_ms.append((time.perf_counter() - s0) * 1e3)
         elapsed = time.perf_counter() - t0
         return {"elapsed": elapsed, "loss": loss, "stats": ctx.stats(), "fn_ms": ctx.fn_times(),
-                "step_ms": step_ms}
+                "step_ms": step_ms, "timeline": ctx.timeline()}
     finally:
         ctx.close()
 
@@ -174,7 +193,8 @@ def cpu_baseline(name, budget_seconds=15.0):
     """The float32 oracle step (``oracle.interp``) on a reduced batch of the same network."""
     from oracle.interp import run as oracle_run
     from oracle.lower import lower
-    small = {"mlp": 256, "cnn": 8, "resnet50_b256": 2, "resnet50_b1440": 2}[name]
+    small = {"mlp": 256, "cnn": 8, "resnet50_b256": 2, "resnet50_b1440": 2,
+             "transformer": 1}[name]
     spec = synth.workload(name, batch=small)
     reg = lower(spec)
     x, labels = synth.make_inputs(spec, 0)
@@ -210,6 +230,10 @@ def main():
     ap.add_argument("--chunk", type=int, default=0, help="bytes; 0 = smallest that fits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-incore", action="store_true")
+    ap.add_argument("--swapout-depth", type=int, default=None,
+                    help="swap-outs in flight (library default when omitted; 0 = unbounded)")
+    ap.add_argument("--timeline", default="",
+                    help="write the last out-of-core step's kernel and copy spans (JSON) here")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
@@ -233,7 +257,12 @@ def main():
     if not args.no_incore:
         inc = run_mode(net, spec, x, labels, params, ooc.UNLIMITED, None, chunk, args.steps,
                        args.warmup)
-    out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps, args.warmup)
+    out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps, args.warmup,
+                   args.swapout_depth)
+    if args.timeline:
+        with open(args.timeline, "w") as fh:
+            json.dump({"fns": net.fn_ops, "vars": net.names,
+                       "spans": [list(t) for t in out["timeline"]]}, fh)
     st = out["stats"]
     ms = out["elapsed"] / args.steps * 1e3
     value = batch * args.steps / out["elapsed"]
@@ -270,7 +299,9 @@ def main():
                    "budget_frac_of_incore_peak": round(budget / p_incore, 4),
                    "incore_peak_bytes": p_incore, "window_bytes": window, "chunk_bytes": chunk,
                    "map_entries": plan["map_entries"],
-                   "policy": "cancel"},
+                   "policy": "cancel",
+                   "swapout_depth": "library default" if args.swapout_depth is None
+                   else args.swapout_depth},
         "roofline": roof,
         "incore": None if inc is None else {
             "samples_per_s": round(batch * args.steps / inc["elapsed"], 3),

@@ -90,7 +90,10 @@ enum { OOC_PRE = 0, OOC_POST = 1, OOC_END = 2 };
  *  NOOP          no kernel (pure scheduling studies).             attrs: -
  *  LINEAR_FWD    Y = X W^T + b        X[R] W[R] b[R] Y[W]          M K N
  *  LINEAR_BWD_W  dW = dY^T X, db = sum_rows dY
- *                                     X[R] dY[R] dW[W] db[W]       M K N
+ *                                     X[R] dY[R] dW[W] db[W] [part[W]]
+ *                                                                  M K N slices
+ *                (rows cut into slices; part = slices partial dW copies then
+ *                slices partial db copies, present iff slices > 1)
  *  LINEAR_BWD_X  dX = dY W            W[R] dY[R] dX[W]             M K N
  *  RELU_FWD      Y = max(X, 0)        X[R] Y[W]                    n
  *  RELU_BWD      dX = dY [Y > 0]      Y[R] dY[R] dX[W]             n
@@ -266,6 +269,14 @@ ooc_status ooc_set_chunk(ooc_ctx *ctx, uint64_t bytes);
 /* OOC_POLICY_CANCEL (default) or OOC_POLICY_LITERAL. */
 ooc_status ooc_set_policy(ooc_ctx *ctx, int32_t policy);
 
+/* Most swap-outs in flight on the device-to-host stream during a step: before
+ * issuing another one, the host waits for the oldest.  0 = no bound; default
+ * 4.  With dozens of device-to-host copies queued behind their event waits,
+ * the HIP runtime on MI355X moves them at 7-14 GB/s instead of the link's
+ * 57 GB/s; a short queue keeps the full rate.  Any stage; takes effect at the
+ * next step. */
+ooc_status ooc_set_swapout_depth(ooc_ctx *ctx, int64_t depth);
+
 /* Runs the scheduler of Section 3 (host only).  OOC_E_INFEASIBLE if one
  * function's variables do not fit in the budget. */
 ooc_status ooc_build_schedule(ooc_ctx *ctx);
@@ -333,6 +344,26 @@ ooc_status ooc_link_probe(int32_t hip_device, uint64_t bytes, int32_t reps, doub
  * launches (waits for swap-ins excluded).  buf caller-owned (cap entries);
  * *n receives the function count.  OOC_E_STATE before the first step. */
 ooc_status ooc_fn_times(const ooc_ctx *ctx, double *buf, uint64_t cap, uint64_t *n);
+
+/* One entry of the last step's timeline: a function's kernels (kind 0, var
+ * -1, bytes 0), a swap-in (kind 1) or a swap-out (kind 2) of variable var
+ * issued for function fn.  start_ms is measured from the step's first event
+ * on the compute stream, ms is the duration, both from the events recorded
+ * around the launches and copies (a swap's wait for its predecessors is not
+ * part of it). */
+typedef struct {
+  int32_t kind;
+  int32_t fn;
+  int64_t var;
+  uint64_t bytes;
+  double start_ms;
+  double ms;
+} ooc_span;
+
+/* Timeline of the last step: every function, then every copy, in issue
+ * order.  buf caller-owned (cap entries); *n receives the entry count.
+ * OOC_E_STATE before the first step. */
+ooc_status ooc_timeline(ooc_ctx *ctx, ooc_span *buf, uint64_t cap, uint64_t *n);
 
 #ifdef __cplusplus
 }

@@ -9,6 +9,7 @@
 namespace ooc {
 ooc_status prepare(ooc_ctx* ctx);
 ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out);
+ooc_status timeline(ooc_ctx* ctx, std::vector<ooc_span>* out);
 ooc_status transfer_resident(ooc_ctx* ctx, bool to_device);
 void release_device(ooc_ctx* ctx);
 ooc_status link_probe(int32_t device, uint64_t bytes, int32_t reps, double* h2d, double* d2h,
@@ -146,6 +147,13 @@ ooc_status ooc_set_policy(ooc_ctx* ctx, int32_t policy) {
   if (policy != OOC_POLICY_CANCEL && policy != OOC_POLICY_LITERAL)
     return fail(ctx, OOC_E_INVALID, "unknown policy");
   ctx->policy = policy;
+  return OOC_OK;
+}
+
+ooc_status ooc_set_swapout_depth(ooc_ctx* ctx, int64_t depth) {
+  REQUIRE_CTX(ctx);
+  if (depth < 0) return fail(ctx, OOC_E_INVALID, "negative swap-out depth");
+  ctx->swapout_depth = depth;
   return OOC_OK;
 }
 
@@ -325,6 +333,18 @@ ooc_status ooc_fn_times(const ooc_ctx* ctx, double* buf, uint64_t cap, uint64_t*
   *n = ctx->fn_ms.size();
   if (cap > 0 && !buf) return OOC_E_INVALID;
   for (uint64_t k = 0; k < cap && k < *n; ++k) buf[k] = ctx->fn_ms[k];
+  return OOC_OK;
+}
+
+ooc_status ooc_timeline(ooc_ctx* ctx, ooc_span* buf, uint64_t cap, uint64_t* n) {
+  REQUIRE_CTX(ctx);
+  if (!n) return fail(ctx, OOC_E_INVALID, "ooc_timeline: n is NULL");
+  if (cap > 0 && !buf) return fail(ctx, OOC_E_INVALID, "ooc_timeline: buf is NULL");
+  std::vector<ooc_span> t;
+  ooc_status st = timeline(ctx, &t);
+  if (st) return st;
+  *n = t.size();
+  for (uint64_t k = 0; k < cap && k < *n; ++k) buf[k] = t[k];
   return OOC_OK;
 }
 

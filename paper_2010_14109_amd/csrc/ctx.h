@@ -51,6 +51,7 @@ struct ooc_ctx {
   bool window_set = false;
   uint64_t chunk = 2ull << 20;
   int32_t policy = OOC_POLICY_CANCEL;
+  int64_t swapout_depth = 4;               // see ooc_set_swapout_depth
   bool incore = true;
 
   ooc::Schedule sched;

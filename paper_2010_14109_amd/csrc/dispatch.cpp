@@ -18,7 +18,8 @@ hipError_t launch_fn(const Fn& fn, void* const* p, const uint64_t* bytes, float 
     case OOC_OP_LINEAR_FWD:
       return linear_fwd(F(0), F(1), F(2), F(3), a[0], a[1], a[2], s);
     case OOC_OP_LINEAR_BWD_W:
-      return linear_bwd_w(F(0), F(1), F(2), F(3), a[0], a[1], a[2], s);
+      return linear_bwd_w(F(0), F(1), F(2), F(3), a[3] > 1 ? F(4) : nullptr, a[3], a[0], a[1], a[2],
+                          s);
     case OOC_OP_LINEAR_BWD_X:
       return linear_bwd_x(F(0), F(1), F(2), a[0], a[1], a[2], s);
     case OOC_OP_RELU_FWD:

@@ -411,12 +411,47 @@ static ooc_status enqueue_copy(ooc_ctx* ctx, const Copy& c, hipStream_t s, hipMe
   return OOC_OK;
 }
 
+ooc_status timeline(ooc_ctx* ctx, std::vector<ooc_span>* out) {
+  out->clear();
+  if (ctx->fn_ms.empty()) {
+    ctx->err = "no step has run";
+    return OOC_E_STATE;
+  }
+  const hipEvent_t t0 = ctx->events[ctx->ev_begin];
+  auto span = [&](int32_t kind, int32_t fn, int64_t var, uint64_t bytes, int32_t a,
+                  int32_t b) -> ooc_status {
+    float s = 0, d = 0;
+    HIPCK(hipEventElapsedTime(&s, t0, ctx->events[a]));
+    HIPCK(hipEventElapsedTime(&d, ctx->events[a], ctx->events[b]));
+    out->push_back(ooc_span{kind, fn, var, bytes, s, d});
+    return OOC_OK;
+  };
+  const int32_t N = (int32_t)ctx->fns.size();
+  for (int32_t i = 0; i < N; ++i) {
+    ooc_status r = span(0, i, -1, 0, ctx->prog[i].ev_pre, ctx->prog[i].ev_fn);
+    if (r) return r;
+  }
+  for (int32_t i = 0; i < N; ++i) {
+    for (const Copy& c : ctx->prog[i].h2d) {
+      ooc_status r = span(1, i, c.var, c.bytes, c.ev_start, c.ev_done);
+      if (r) return r;
+    }
+    for (const Copy& c : ctx->prog[i].d2h) {
+      ooc_status r = span(2, i, c.var, c.bytes, c.ev_start, c.ev_done);
+      if (r) return r;
+    }
+  }
+  return OOC_OK;
+}
+
 ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out) {
   HIPCK(hipSetDevice(ctx->device));
   auto t0 = std::chrono::steady_clock::now();
   hipStream_t cs = ctx->cs;
   HIPCK(hipEventRecord(ctx->events[ctx->ev_begin], cs));
   const int64_t N = (int64_t)ctx->fns.size();
+  const int64_t depth = ctx->swapout_depth;
+  std::vector<int32_t> issued;   // done events of the swap-outs issued so far
   for (int64_t i = 0; i < N; ++i) {
     const FnProgram& fp = ctx->prog[i];
     for (const Copy& c : fp.h2d) {
@@ -433,8 +468,13 @@ ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out) {
     }
     HIPCK(hipEventRecord(ctx->events[fp.ev_fn], cs));
     for (const Copy& c : fp.d2h) {
+      // bounded queue of swap-outs (see ooc_set_swapout_depth); the compute
+      // stream already holds the work up to f_i, so it keeps running meanwhile
+      if (depth > 0 && (int64_t)issued.size() >= depth)
+        HIPCK(hipEventSynchronize(ctx->events[issued[issued.size() - depth]]));
       ooc_status s = enqueue_copy(ctx, c, ctx->ds, hipMemcpyDeviceToHost);
       if (s) return s;
+      issued.push_back(c.ev_done);
     }
   }
   HIPCK(hipEventRecord(ctx->events[ctx->ev_end], cs));

@@ -21,10 +21,13 @@
 // tiles ([32][rows + 4]) are written with 16-byte accesses and read with
 // 4-byte ones; the +4 pads keep half-wave reads free of bank conflicts.
 //
-// Split-K: the filter gradient reduces over N P Q (millions of pixels), so
-// its grid's second dimension cuts that axis into slices whose partial
-// tiles go to separate buffers and are summed afterwards in slice order.
-// No atomics anywhere: results do not depend on scheduling or addresses.
+// Split-K: the filter gradients reduce over N P Q pixels or over the rows of
+// a dense layer (up to millions), so the grid's second dimension cuts that
+// axis into slices whose partial tiles go to separate buffers and are summed
+// afterwards in slice order.  A dense layer's bias gradient (the column sums
+// of dY) is taken from the A tiles already in LDS by the workgroups of the
+// first tile column, slice by slice like dW.  No atomics anywhere: results
+// do not depend on scheduling or addresses.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -394,12 +397,14 @@ __device__ inline void shift(L& l, int64_t d) {
   l.p += d;
 }
 
+// rowsum (optional): rowsum[slice][m] = sum over this slice's k of A[m][k]
 template <int BM, int BN, class LA, class LB, bool BIAS, bool BATCHED>
 __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __restrict__ c,
                                                        int64_t ldc, int64_t slice_stride,
                                                        const float* __restrict__ bias, int64_t M,
                                                        int64_t N, int64_t K, int64_t k_slice,
-                                                       int tiles_m, int tiles_n, Batch bt) {
+                                                       int tiles_m, int tiles_n, Batch bt,
+                                                       float* __restrict__ rowsum) {
   constexpr int MB = BM / 64, NB = BN / 64;
   if constexpr (BATCHED) {
     const int64_t z = blockIdx.z, zo = z / bt.inner, zi = z % bt.inner;
@@ -434,6 +439,9 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
+  const bool sums = rowsum != nullptr && tn == 0 && (int)threadIdx.x < BM;
+  float rs = 0.f;
+
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wm = wave & 1, wn = wave >> 1;
@@ -456,6 +464,13 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
     }
     const float* A = As[buf];
     const float* B = Bs[buf];
+    if (sums) {
+#pragma unroll
+      for (int k = 0; k < BK; ++k) {
+        if constexpr (LA::kRowOfK) rs += A[threadIdx.x * LDK + k];
+        else rs += A[k * (LA::kLds / BK) + threadIdx.x];
+      }
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int kq = half * 16 + 4 * j;
@@ -481,6 +496,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
     buf ^= 1;
   }
 
+  if (sums && m0 + threadIdx.x < M) rowsum[(int64_t)blockIdx.y * M + m0 + threadIdx.x] = rs;
   float* out = c + (int64_t)blockIdx.y * slice_stride;
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -500,7 +516,8 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
 template <int BM, int BN, class LA, class LB, bool BIAS, bool BATCHED = false>
 hipError_t run_gemm(const LA& la, const LB& lb, float* c, int64_t ldc, const float* bias,
                     int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s,
-                    int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0}) {
+                    int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
+                    float* rowsum = nullptr) {
   const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   if (tiles_m * tiles_n > INT32_MAX / 2 || slices > 65535 || batches > 65535 || batches < 1)
     return hipErrorInvalidValue;
@@ -508,7 +525,8 @@ hipError_t run_gemm(const LA& la, const LB& lb, float* c, int64_t ldc, const flo
   k_slice = (k_slice + BK - 1) / BK * BK;
   dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices, (unsigned)batches);
   hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, BIAS, BATCHED>), grid, dim3(THREADS), 0, s, la,
-                     lb, c, ldc, M * ldc, bias, M, N, K, k_slice, (int)tiles_m, (int)tiles_n, bt);
+                     lb, c, ldc, M * ldc, bias, M, N, K, k_slice, (int)tiles_m, (int)tiles_n, bt,
+                     rowsum);
   return hipGetLastError();
 }
 
@@ -529,7 +547,7 @@ template <template <int> class LAT, template <int> class LBT, bool BIAS, bool BA
           class FA, class FB>
 hipError_t dispatch(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int64_t M, int64_t N,
                     int64_t K, int64_t slices, hipStream_t s, int64_t batches = 1,
-                    Batch bt = Batch{1, 0, 0, 0, 0, 0, 0}) {
+                    Batch bt = Batch{1, 0, 0, 0, 0, 0, 0}, float* rowsum = nullptr) {
   switch (pick_shape(M, N)) {
     case S128x64: {
       LAT<128> a{};
@@ -537,7 +555,7 @@ hipError_t dispatch(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int6
       fa(a);
       fb(b);
       return run_gemm<128, 64, LAT<128>, LBT<64>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
-                                                                 slices, s, batches, bt);
+                                                                 slices, s, batches, bt, rowsum);
     }
     case S64x128: {
       LAT<64> a{};
@@ -545,7 +563,7 @@ hipError_t dispatch(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int6
       fa(a);
       fb(b);
       return run_gemm<64, 128, LAT<64>, LBT<128>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
-                                                                 slices, s, batches, bt);
+                                                                 slices, s, batches, bt, rowsum);
     }
     default: {
       LAT<128> a{};
@@ -553,7 +571,7 @@ hipError_t dispatch(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int6
       fa(a);
       fb(b);
       return run_gemm<128, 128, LAT<128>, LBT<128>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
-                                                                   slices, s, batches, bt);
+                                                                   slices, s, batches, bt, rowsum);
     }
   }
 }
@@ -570,16 +588,6 @@ template <int E> using ConvPixelPatchV = ConvPixelPatch<E, true>;
 template <int E> using ConvPixelPatchS = ConvPixelPatch<E, false>;
 
 // ---------------------------------------------------------------- small kernels
-// db[n] = sum over rows m of dY[m][n], rows summed in order
-__global__ void colsum_kernel(const float* __restrict__ dy, float* __restrict__ db, int64_t M,
-                              int64_t N) {
-  const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= N) return;
-  float acc = 0.f;
-  for (int64_t m = 0; m < M; ++m) acc += dy[m * N + n];
-  db[n] = acc;
-}
-
 // out[j] = sum over slices of part[s][j]: four interleaved accumulators
 // (slices s = u mod 4), added in a fixed order
 __global__ void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
@@ -618,19 +626,26 @@ hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, i
   return dispatch<MatKs, MatMs, false>(fa, fb, dX, K, nullptr, M, K, N, 1, s);
 }
 
-hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, int64_t M,
-                        int64_t K, int64_t N, hipStream_t s) {
-  // dW[N][K] = dY^T X: A[n][m] = dY[m][n] (contiguous in n), B[m][k] = X[m][k] (contiguous in k)
+hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, float* part,
+                        int64_t slices, int64_t M, int64_t K, int64_t N, hipStream_t s) {
+  // dW[N][K] = dY^T X: A[n][m] = dY[m][n] (contiguous in n), B[m][k] = X[m][k] (contiguous in k);
+  // db = the row sums of A.  With slices > 1, part holds slices copies of dW, then slices of db.
+  if (slices > 1 && part == nullptr) return hipErrorInvalidValue;
+  float* out = slices > 1 ? part : dW;
+  float* sums = slices > 1 ? part + slices * N * K : db;
   auto fa = [&](auto& a) { a.p = dY; a.ld = N; };
   auto fb = [&](auto& bb) { bb.p = X; bb.ld = K; };
+  const Batch one{1, 0, 0, 0, 0, 0, 0};
   hipError_t e;
   if (N % 4 == 0 && K % 4 == 0 && aligned16(X) && aligned16(dY))
-    e = dispatch<MatMv, MatMv, false>(fa, fb, dW, K, nullptr, N, K, M, 1, s);
+    e = dispatch<MatMv, MatMv, false>(fa, fb, out, K, nullptr, N, K, M, slices, s, 1, one, sums);
   else
-    e = dispatch<MatMs, MatMs, false>(fa, fb, dW, K, nullptr, N, K, M, 1, s);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s, dY, db,
-                     M, N);
+    e = dispatch<MatMs, MatMs, false>(fa, fb, out, K, nullptr, N, K, M, slices, s, 1, one, sums);
+  if (e != hipSuccess || slices <= 1) return e;
+  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((N * K + 255) / 256)), dim3(256), 0, s,
+                     part, dW, N * K, slices);
+  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s, sums, db,
+                     N, slices);
   return hipGetLastError();
 }
 

@@ -15,8 +15,8 @@ hipError_t launch_fn(const Fn& fn, void* const* ptrs, const uint64_t* bytes, flo
 // GEMM family (gemm.hip).  Shapes as in the operation table of ooc.h.
 hipError_t linear_fwd(const float* X, const float* W, const float* b, float* Y, int64_t M,
                       int64_t K, int64_t N, hipStream_t s);
-hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, int64_t M,
-                        int64_t K, int64_t N, hipStream_t s);
+hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, float* part,
+                        int64_t slices, int64_t M, int64_t K, int64_t N, hipStream_t s);
 hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, int64_t K,
                         int64_t N, hipStream_t s);
 // Batched GEMM: C_z[M][N] = sum_k A_z[m][k] B_z[k][n] for z < batches.  A is

@@ -199,26 +199,36 @@ __global__ __launch_bounds__(TPB) void ln_bwd_kernel(const float* __restrict__ x
   for (int64_t c = threadIdx.x; c < 2 * d; c += TPB) part[s * 2 * d + c] = lds[c];
 }
 
-// dgamma[c] / dbeta[c] = sum over slices of the partials, four interleaved
-// accumulators added in a fixed order
-__global__ void ln_finalize(const float* __restrict__ part, float* __restrict__ dgamma,
-                            float* __restrict__ dbeta, int64_t d, int64_t slices) {
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= d) return;
-  float a[4] = {0, 0, 0, 0}, b[4] = {0, 0, 0, 0};
-  int64_t s = 0;
-  for (; s + 4 <= slices; s += 4)
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      a[u] += part[(s + u) * 2 * d + c];
-      b[u] += part[(s + u) * 2 * d + d + c];
+// dgamma[c] / dbeta[c] = sum over slices of the partials.  A workgroup owns
+// 64 features; its 16 waves take the slices s = w mod 16 in increasing order,
+// and wave 0 adds the 16 results in wave order.
+constexpr int FIN_WAVES = 16;
+__global__ __launch_bounds__(64 * FIN_WAVES) void ln_finalize(const float* __restrict__ part,
+                                                              float* __restrict__ dgamma,
+                                                              float* __restrict__ dbeta, int64_t d,
+                                                              int64_t slices) {
+  __shared__ float sa[FIN_WAVES][64], sb[FIN_WAVES][64];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+  float a = 0.f, b = 0.f;
+  if (c < d)
+    for (int64_t s = w; s < slices; s += FIN_WAVES) {
+      a += part[s * 2 * d + c];
+      b += part[s * 2 * d + d + c];
     }
-  for (; s < slices; ++s) {
-    a[0] += part[s * 2 * d + c];
-    b[0] += part[s * 2 * d + d + c];
+  sa[w][lane] = a;
+  sb[w][lane] = b;
+  __syncthreads();
+  if (w == 0 && c < d) {
+    float ta = 0.f, tb = 0.f;
+#pragma unroll
+    for (int k = 0; k < FIN_WAVES; ++k) {
+      ta += sa[k][lane];
+      tb += sb[k][lane];
+    }
+    dgamma[c] = ta;
+    dbeta[c] = tb;
   }
-  dgamma[c] = (a[0] + a[1]) + (a[2] + a[3]);
-  dbeta[c] = (b[0] + b[1]) + (b[2] + b[3]);
 }
 
 // ---------------------------------------------------------------- GELU
@@ -227,7 +237,8 @@ __global__ void gelu_kernel(const float* __restrict__ x, const float* __restrict
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
     const float v = x[i];
-    const float cdf = 0.5f * (1.f + erff(v * 0.70710678118654752f));
+    // Phi(v) through erfc: 1 + erf(v / sqrt 2) cancels to 0 in the lower tail
+    const float cdf = 0.5f * erfcf(-v * 0.70710678118654752f);
     if (!backward) {
       out[i] = v * cdf;
     } else {
@@ -335,7 +346,7 @@ hipError_t layernorm_bwd(const float* x, const float* gamma, float* stats, const
   e = [&]() -> hipError_t { LN_DISPATCH(LN_B); }();
 #undef LN_B
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(ln_finalize, dim3((unsigned)((d + TPB - 1) / TPB)), dim3(TPB), 0, s,
+  hipLaunchKernelGGL(ln_finalize, dim3((unsigned)((d + 63) / 64)), dim3(64 * FIN_WAVES), 0, s,
                      stats + 2 * rows, dgamma, dbeta, d, slices);
   return hipGetLastError();
 }

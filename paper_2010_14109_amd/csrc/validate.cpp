@@ -20,7 +20,7 @@ struct Sig {
 const Sig kSig[OOC_OP_COUNT] = {
     {"NOOP", -1, -1, {}},
     {"LINEAR_FWD", 4, 3, {OOC_R, OOC_R, OOC_R, OOC_W}},
-    {"LINEAR_BWD_W", 4, 3, {OOC_R, OOC_R, OOC_W, OOC_W}},
+    {"LINEAR_BWD_W", -1, 4, {OOC_R, OOC_R, OOC_W, OOC_W}},
     {"LINEAR_BWD_X", 3, 3, {OOC_R, OOC_R, OOC_W}},
     {"RELU_FWD", 2, 1, {OOC_R, OOC_W}},
     {"RELU_BWD", 3, 1, {OOC_R, OOC_R, OOC_W}},
@@ -93,11 +93,16 @@ std::string check_fn(const std::vector<Var>& vars, const Fn& fn) {
       return "";
     }
     case OOC_OP_LINEAR_BWD_W: {
-      int64_t M = a[0], K = a[1], N = a[2];
+      int64_t M = a[0], K = a[1], N = a[2], slices = a[3];
+      if (slices < 1 || slices > M || slices > 65535) return nm + ": bad slice count";
+      if (nv != (slices > 1 ? 5 : 4)) return nm + ": partial-sum variable iff slices > 1";
+      for (int j = 0; j < nv; ++j)
+        if (v[j].access != (j < 2 ? OOC_R : OOC_W)) return nm + ": wrong access";
       NEED(0, M * K * 4, "X");
       NEED(1, M * N * 4, "dY");
       NEED(2, N * K * 4, "dW");
       NEED(3, N * 4, "db");
+      if (nv == 5) NEED(4, slices * (N * K + N) * 4, "partial sums");
       return "";
     }
     case OOC_OP_LINEAR_BWD_X: {
@@ -157,7 +162,7 @@ std::string check_fn(const std::vector<Var>& vars, const Fn& fn) {
         NEED(2, xb, "dX");
       } else {
         const int64_t slices = a[11];
-        if (slices < 1 || slices > N * P * Q) return nm + ": bad slice count";
+        if (slices < 1 || slices > N * P * Q || slices > 65535) return nm + ": bad slice count";
         if (nv != (slices > 1 ? 4 : 3)) return nm + ": partial-sum variable iff slices > 1";
         if (v[0].access != OOC_R || v[1].access != OOC_R || v[2].access != OOC_W ||
             (nv == 4 && v[3].access != OOC_W))

@@ -18,9 +18,12 @@ fixed per shape: a BatchNorm keeps 2 + 2 S floats per channel with S =
 min(ceil(rows / 512), 2048) row slices, and a convolution's filter gradient
 is split over S_w = min(ceil(1024 / T), ceil(L / 1024)) pixel slices (at
 least 1) with T = ceil(K / 128) ceil(R S C / 128) output tiles and L = N P Q
-pixels, using a partial-sum variable of S_w copies of dW when S_w > 1.  A
-LayerNorm keeps mean and 1/std per row and 2 S floats per feature (same S
-formula over its rows); attention keeps its probabilities [B, H, T, T] and its
+pixels, using a partial-sum variable of S_w copies of dW when S_w > 1; a
+dense layer's weight gradient is split the same way over its rows (K = out,
+R S C = in, L = rows), its partial-sum variable holding S_w copies of dW then
+S_w copies of db.  A
+LayerNorm keeps mean and 1/std per row and 2 S floats per feature with S =
+min(ceil(rows / 32), 2048) (its rows are d floats wide); attention keeps its probabilities [B, H, T, T] and its
 backward a scratch of the same size.
 """
 
@@ -35,6 +38,10 @@ FLOAT = 4
 
 def bn_row_slices(rows):
     return min(ceil(rows / 512), 2048)
+
+
+def ln_row_slices(rows):
+    return min(ceil(rows / 32), 2048)
 
 
 def wgrad_pixel_slices(k_out, rsc, pixels):
@@ -149,7 +156,7 @@ class Net:
 
     def _fwd_layernorm(self, L, X):
         rows, d = self.shape[X]
-        S = bn_row_slices(rows)
+        S = ln_row_slices(rows)
         g = self._decl(L["name"] + ".gamma", (d,), kind=ooc.PARAM)
         bt = self._decl(L["name"] + ".beta", (d,), kind=ooc.PARAM)
         self.params[L["name"]] = [g, bt]
@@ -201,9 +208,14 @@ class Net:
         if op == "linear":
             W, b = self.params[name]
             n, fin = xs
-            attrs = [n, fin, L["out_features"]]
-            self._call("linear_bwd_w", [(X, ooc.R), (dY, ooc.R), (self._grad_of_param(W), ooc.W),
-                                        (self._grad_of_param(b), ooc.W)], attrs)
+            fout = L["out_features"]
+            attrs = [n, fin, fout]
+            sw = wgrad_pixel_slices(fout, fin, n)
+            pairs = [(X, ooc.R), (dY, ooc.R), (self._grad_of_param(W), ooc.W),
+                     (self._grad_of_param(b), ooc.W)]
+            if sw > 1:
+                pairs.append((self._decl(name + ".part", (sw * (fout * fin + fout),)), ooc.W))
+            self._call("linear_bwd_w", pairs, attrs + [sw])
             if X != "x":
                 dX = self._decl(f"d:{X}@{name}", xs)
                 self._call("linear_bwd_x", [(W, ooc.R), (dY, ooc.R), (dX, ooc.W)], attrs)
@@ -264,7 +276,7 @@ class Net:
                                          (dY, ooc.R), (dX, ooc.W),
                                          (self._grad_of_param(g), ooc.W),
                                          (self._grad_of_param(bt), ooc.W)],
-                       [rows, d, bn_row_slices(rows)])
+                       [rows, d, ln_row_slices(rows)])
             out.append((X, dX))
             self._sgd(name)
         elif op == "gelu":

@@ -40,6 +40,7 @@ EXPORTS = [
     "ooc_schedule_get", "ooc_schedule_windows", "ooc_incore_peak", "ooc_working_set_max",
     "ooc_plan_intervals", "ooc_plan_chunks", "ooc_prepare", "ooc_host_ptr", "ooc_upload",
     "ooc_download", "ooc_step", "ooc_get_stats", "ooc_fn_times", "ooc_link_probe",
+    "ooc_timeline", "ooc_set_swapout_depth",
 ]
 
 
@@ -51,6 +52,11 @@ class ooc_op(ctypes.Structure):
 class ooc_interval(ctypes.Structure):
     _fields_ = [("var", ctypes.c_int64), ("open", ctypes.c_int64), ("close", ctypes.c_int64),
                 ("first_chunk", ctypes.c_int64), ("n_chunks", ctypes.c_int64)]
+
+
+class ooc_span(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("fn", ctypes.c_int32), ("var", ctypes.c_int64),
+                ("bytes", ctypes.c_uint64), ("start_ms", ctypes.c_double), ("ms", ctypes.c_double)]
 
 
 class ooc_stats(ctypes.Structure):
@@ -97,6 +103,7 @@ def load(path=LIB_PATH):
         "ooc_set_window": ([P, c.c_uint64], c.c_int32),
         "ooc_set_chunk": ([P, c.c_uint64], c.c_int32),
         "ooc_set_policy": ([P, c.c_int32], c.c_int32),
+        "ooc_set_swapout_depth": ([P, c.c_int64], c.c_int32),
         "ooc_build_schedule": ([P], c.c_int32),
         "ooc_schedule_get": ([P, c.POINTER(ooc_op), c.c_uint64, c.POINTER(c.c_uint64)], c.c_int32),
         "ooc_schedule_windows": ([P, c.POINTER(c.c_int64), c.c_uint64, c.POINTER(c.c_uint64)],
@@ -117,6 +124,7 @@ def load(path=LIB_PATH):
                          c.c_int32),
         "ooc_link_probe": ([c.c_int32, c.c_uint64, c.c_int32, c.POINTER(c.c_double),
                             c.POINTER(c.c_double), c.POINTER(c.c_double)], c.c_int32),
+        "ooc_timeline": ([P, c.POINTER(ooc_span), c.c_uint64, c.POINTER(c.c_uint64)], c.c_int32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -197,6 +205,9 @@ class Context:
 
     def set_policy(self, p):
         _check(self.lib.ooc_set_policy(self.h, {"C": 0, "L": 1}.get(p, p)), self.h)
+
+    def set_swapout_depth(self, depth):
+        _check(self.lib.ooc_set_swapout_depth(self.h, depth), self.h)
 
     def build_schedule(self):
         _check(self.lib.ooc_build_schedule(self.h), self.h)
@@ -283,6 +294,15 @@ class Context:
         buf = (ctypes.c_double * max(1, n.value))()
         _check(self.lib.ooc_fn_times(self.h, buf, n.value, ctypes.byref(n)), self.h)
         return list(buf[:n.value])
+
+    def timeline(self):
+        """The last step's spans: (kind, fn, var, bytes, start_ms, ms), kind 0 kernels,
+        1 swap-in, 2 swap-out."""
+        n = ctypes.c_uint64()
+        _check(self.lib.ooc_timeline(self.h, None, 0, ctypes.byref(n)), self.h)
+        buf = (ooc_span * max(1, n.value))()
+        _check(self.lib.ooc_timeline(self.h, buf, n.value, ctypes.byref(n)), self.h)
+        return [(b.kind, b.fn, b.var, b.bytes, b.start_ms, b.ms) for b in buf[:n.value]]
 
     def stats(self):
         st = ooc_stats()

@@ -6,9 +6,10 @@ from paper_2010_14109_amd import netdef, ooc
 
 
 def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk=2 << 20,
-            policy="C", keep_grads=True, momentum_state=None, steps=1):
+            policy="C", keep_grads=True, momentum_state=None, steps=1, inspect=None):
     """One (or more) training steps on device 0.  Returns (loss, outputs, stats) with
-    outputs = {name: array} for every PARAM, STATE and OUTPUT variable."""
+    outputs = {name: array} for every PARAM, STATE and OUTPUT variable.  ``inspect(ctx,
+    net)``, when given, runs after the steps."""
     net = netdef.Net(spec, keep_grads=keep_grads)
     ctx = ooc.Context(0)
     try:
@@ -31,6 +32,8 @@ def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk
         ctx.upload()
         mu = spec["optimizer"]["momentum"]
         losses = [ctx.step(spec["optimizer"]["lr"], mu) for _ in range(steps)]
+        if inspect is not None:
+            inspect(ctx, net)
         ctx.download()
         outs = {}
         for name in net.names:

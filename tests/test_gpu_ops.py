@@ -72,15 +72,21 @@ def d(a):
 
 
 # ---------------------------------------------------------------- dense
-@pytest.mark.parametrize("M,K,N", [(300, 200, 130), (5, 147, 10), (256, 1024, 1024), (1, 3, 1)])
-def test_linear(M, K, N):
+@pytest.mark.parametrize("M,K,N,S", [(300, 200, 130, 1), (5, 147, 10, 1), (256, 1024, 1024, 1),
+                                     (1, 3, 1, 1), (3000, 200, 132, 3), (2500, 64, 1000, 2),
+                                     (4100, 36, 7, 5), (100, 40, 20, 3)])
+def test_linear(M, K, N, S):
+    """S > 1 cuts the rows of the weight gradient into slices (the last one of
+    (100, 40, 20, 3) is empty)."""
     X, Wt, b, G = f32(M, K), f32(N, K), f32(N), f32(M, N)
-    print(f"linear M={M} K={K} N={N}", flush=True)
+    print(f"linear M={M} K={K} N={N} slices={S}", flush=True)
     (_, _, _, Y) = run_fn("linear_fwd", [(X, ooc.R), (Wt, ooc.R), (b, ooc.R),
                                           (((M, N), "f32"), ooc.W)], [M, K, N])
     assert rel_l2(Y, ops.linear_fwd(d(X), d(Wt), d(b))) < TOL
-    (_, _, dW, db) = run_fn("linear_bwd_w", [(X, ooc.R), (G, ooc.R), (((N, K), "f32"), ooc.W),
-                                              (((N,), "f32"), ooc.W)], [M, K, N])
+    wargs = [(X, ooc.R), (G, ooc.R), (((N, K), "f32"), ooc.W), (((N,), "f32"), ooc.W)]
+    if S > 1:
+        wargs.append((((S * (N * K + N),), "f32"), ooc.W))
+    dW, db = run_fn("linear_bwd_w", wargs, [M, K, N, S])[2:4]
     rdW, rdb = ops.linear_bwd_w(d(X), d(G))
     assert rel_l2(dW, rdW) < TOL and rel_l2(db, rdb) < TOL
     (_, _, dX) = run_fn("linear_bwd_x", [(Wt, ooc.R), (G, ooc.R), (((M, K), "f32"), ooc.W)],
@@ -246,7 +252,8 @@ def test_mix_op():
 
 
 # ---------------------------------------------------------------- transformer layers
-@pytest.mark.parametrize("rows,d,slices", [(37, 64, 1), (37, 100, 3), (130, 1024, 4), (5, 4096, 2)])
+@pytest.mark.parametrize("rows,d,slices", [(37, 64, 1), (37, 100, 3), (130, 1024, 4), (5, 4096, 2),
+                                          (2000, 1024, 63), (999, 100, 37)])
 def test_layernorm(rows, d, slices):
     X = f32(rows, d, scale=2.0) + 0.3
     g, b, G = f32(d), f32(d), f32(rows, d)
@@ -268,9 +275,12 @@ def test_layernorm(rows, d, slices):
     assert rel_l2(out[4], rdX) < TOL and rel_l2(out[5], rdg) < TOL and rel_l2(out[6], rdb) < TOL
 
 
-@pytest.mark.parametrize("n", [1003, 1])
+@pytest.mark.parametrize("n", [1003, 1, 64])
 def test_gelu(n):
+    """n = 64 spans the lower tail (x down to -12), where GELU is tiny but not 0."""
     x, g = f32(n, scale=3.0), f32(n)
+    if n == 64:
+        x = np.linspace(-12.0, 4.0, n).astype(np.float32)
     (_, y) = run_fn("gelu_fwd", [(x, ooc.R), (((n,), "f32"), ooc.W)], [n])
     assert rel_l2(y, ops.gelu_fwd(x.astype(np.float64))) < TOL
     (_, _, dx) = run_fn("gelu_bwd", [(x, ooc.R), (g, ooc.R), (((n,), "f32"), ooc.W)], [n])

@@ -119,6 +119,34 @@ def test_two_steps_keep_state_on_the_host():
         assert outs2[n].tobytes() == outs_b[n].tobytes(), n
 
 
+def test_timeline_accounts_for_every_function_and_copy():
+    """ooc_timeline lists each function once and each issued copy once; the copy bytes add
+    up to the step's transfer counters and no copy ends after the step."""
+    spec = tiny_specs()[1]
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    b, k, f = as_schedule_input(lower(spec, keep_grads=False))
+    p = S.incore_peak(b, k, f, 4096)
+    B = max(S.budget_for(0.4, p, 4096), S.working_set_max(b, f, 4096))
+    got = {}
+
+    def inspect(ctx, net):
+        got["tl"] = ctx.timeline()
+        got["st"] = ctx.stats()
+        got["n"] = len(net.calls)
+
+    run_net(spec, x, labels, params, budget=B, chunk=4096, keep_grads=False, inspect=inspect)
+    tl, st = got["tl"], got["st"]
+    kern = [t for t in tl if t[0] == 0]
+    assert [t[1] for t in kern] == list(range(got["n"]))
+    assert sum(t[3] for t in tl if t[0] == 1) == st["h2d_bytes"] > 0
+    assert sum(t[3] for t in tl if t[0] == 2) == st["d2h_bytes"] > 0
+    step = st["step_gpu_ms"]
+    for kind, fn, var, nbytes, start, ms in tl:
+        assert start >= 0 and ms >= 0 and (var >= 0) == (kind != 0)
+    assert max(t[4] + t[5] for t in kern) <= step * 1.001 + 1e-3
+
+
 def random_mix_sequence(rng, nv, nf):
     kinds = [rng.choice([ooc.INPUT, ooc.PARAM, ooc.STATE, ooc.TEMP, ooc.TEMP, ooc.OUTPUT])
              for _ in range(nv)]
