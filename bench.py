@@ -89,6 +89,38 @@ def sgd_bytes(net, j):
     return total if mom in (0, 1) else 0
 
 
+def measured_traffic(net, op):
+    """Mean HBM bytes per launch of ``op`` in this network, from the rocprofv3 FETCH_SIZE /
+    WRITE_SIZE measurements recorded under profiles/ (lines ``traffic: op=... key=<attrs>
+    bytes=... source=<file> sha256=...``).  None unless every launch's attribute list has a
+    measurement whose kernel source is unchanged since it was taken."""
+    import glob
+    import hashlib
+    here = os.path.dirname(os.path.abspath(__file__))
+    table = {}
+    for f in glob.glob(os.path.join(here, "profiles", "traffic_*.md")):
+        with open(f) as fh:
+            for line in fh:
+                if not line.startswith("traffic: "):
+                    continue
+                kv = dict(t.split("=", 1) for t in line.split()[1:])
+                src = os.path.join(here, kv["source"])
+                if not os.path.exists(src):
+                    continue
+                with open(src, "rb") as sf:
+                    if hashlib.sha256(sf.read()).hexdigest() != kv["sha256"]:
+                        continue
+                table[(kv["op"], kv["key"])] = int(kv["bytes"])
+    got = []
+    for o, attrs in zip(net.fn_ops, net.fn_attrs):
+        if o == op:
+            b = table.get((op, ",".join(str(a) for a in attrs)))
+            if b is None:
+                return None
+            got.append(b)
+    return round(sum(got) / len(got)) if got else None
+
+
 MAP_ENTRY_LIMIT = 40000   # chunks + mappings per plan; the process table holds ~65530
 
 
@@ -276,12 +308,26 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": round(dom["rate"], 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(dom["rate"] / PEAK_HBM_GBS, 4), "traffic": None}
+    roof["traffic"] = measured_traffic(net, dom_op)
+    roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)"
     roof["kernel"] = dom_op
     roof["launches_per_step"] = dom["launches"]
     roof["avg_launch_ms"] = round(dom["ms"] / max(1, dom["launches"]), 4)
 
     step_s = out["elapsed"] / args.steps
     moved = st["h2d_bytes"] + st["d2h_bytes"]
+    # link ceiling: forward compute overlapped with the swap-outs, backward compute with the
+    # swap-ins, each direction at its probed rate (the forward only swaps out, the backward
+    # mostly swaps in, so the two directions do not overlap each other)
+    ceiling = None
+    if inc is not None:
+        split = max(j for j, op in enumerate(net.fn_ops) if op == "softmax_ce") + 1
+        t_fwd, t_bwd = sum(inc["fn_ms"][:split]), sum(inc["fn_ms"][split:])
+        t_inc = inc["elapsed"] / args.steps * 1e3
+        bound = (max(t_fwd, st["d2h_bytes"] / link["d2h"] / 1e6)
+                 + max(t_bwd, st["h2d_bytes"] / link["h2d"] / 1e6))
+        ceiling = {"bound_ms": round(bound, 2), "pct_of_incore": round(100 * t_inc / bound, 2),
+                   "measured_pct_of_ceiling": round(100 * bound / ms, 2)}
     res = {
         "metric": "samples/s at budget B as % of in-core; host-link GB/s; peak device bytes",
         "value": round(value, 3),
@@ -319,9 +365,10 @@ def main():
             "h2d_busy_ms": round(st["h2d_busy_ms"], 2), "d2h_busy_ms": round(st["d2h_busy_ms"], 2),
             "probe_GBps": {k: round(v, 2) for k, v in link.items()},
             "pcie5_x16_theoretical_GBps_per_dir": PCIE5_X16_GBS,
-            "link_bound_ms": round(max(st["h2d_bytes"] / link["h2d"],
-                                       st["d2h_bytes"] / link["d2h"],
-                                       moved / link["both"]) / 1e6, 2),
+            "full_duplex_bound_ms": round(max(st["h2d_bytes"] / link["h2d"],
+                                              st["d2h_bytes"] / link["d2h"],
+                                              moved / link["both"]) / 1e6, 2),
+            "ceiling": ceiling,
         },
         "peak_device_bytes": {"pool": st["pool_bytes"], "max_chunks_in_use_bytes":
                               st["max_chunks_used"] * chunk, "peak_accounted": st["peak_accounted"],

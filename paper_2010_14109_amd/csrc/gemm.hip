@@ -16,7 +16,13 @@
 // input gradient: the output gradient gathered through the filter taps;
 // filter gradient: the input patches seen along the batch-pixel axis).  A
 // loader zero-fills everything outside the matrix, so no shape needs
-// padding.  LDS layout follows the contiguous direction: "row of k" tiles
+// padding.  Loaders keep per-row offsets from their set-up, so a K tile costs
+// one add per row; a convolution whose channel count is a multiple of 32 has
+// every K tile inside one filter tap (uniform over the workgroup), and the
+// remaining index splits use multiply-high division by invariant integers.
+// The input gradient of a strided convolution is computed per stride class
+// of input pixels (h mod st, w mod st), each class a GEMM over only the taps
+// that reach it.  LDS layout follows the contiguous direction: "row of k" tiles
 // ([rows][32 + 4]) are written and read with 16-byte accesses, "row of m"
 // tiles ([32][rows + 4]) are written with 16-byte accesses and read with
 // 4-byte ones; the +4 pads keep half-wave reads free of bank conflicts.
@@ -30,6 +36,8 @@
 // do not depend on scheduling or addresses.
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
+
 #include "kernels.h"
 
 namespace ooc {
@@ -39,6 +47,7 @@ namespace {
 constexpr int BK = 32;
 constexpr int LDK = BK + 4;    // row-of-k tile stride (floats)
 constexpr int THREADS = 256;
+constexpr uint32_t kXcds = 8;   // accelerator complex dies of an MI355X, one L2 each
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
@@ -81,28 +90,55 @@ struct RowM {
   }
 };
 
+// x / d for 0 <= x < 2^31 and an invariant d >= 1 with one multiply-high
+// (Granlund and Montgomery, division by invariant integers using
+// multiplication, 1994): with l = ceil(log2 d) and m = floor(2^(31+l) / d) + 1,
+// 2^(31+l) < m d <= 2^(31+l) + 2^l, hence floor(x m / 2^(31+l)) = floor(x / d)
+// for every x < 2^31, and m < 2^32.
+struct FastDiv {
+  uint32_t d = 1, m = 0, s = 0;
+  static FastDiv make(int64_t dv) {
+    FastDiv f;
+    f.d = (uint32_t)dv;
+    if (dv <= 1) return f;
+    uint32_t l = 0;
+    while ((1ull << l) < (uint64_t)dv) ++l;
+    f.m = (uint32_t)((1ull << (31 + l)) / (uint64_t)dv + 1);
+    f.s = l - 1;
+    return f;
+  }
+  __device__ int div(int x) const {
+    return d == 1 ? x : (int)(__umulhi((uint32_t)x, m) >> s);
+  }
+};
+
+constexpr int kFar = -(1 << 29);   // coordinate of a row past the matrix: fails every bounds check
+
+__device__ inline bool inside(int v, int n) { return (unsigned)v < (unsigned)n; }
+
 // X[i][k] = p[i * ld + k]  (contiguous along k)
 template <int E, bool VEC>
 struct MatK : RowK<E> {
   using Base = RowK<E>;
   const float* p;
   int64_t ld;
-  int64_t row0;
-  int64_t rows;
+  int64_t off_[Base::kN];   // i * ld + this lane's k offset; -1 past the last row
   __device__ void init(int64_t mn0, int64_t MN) {
-    row0 = mn0;
-    rows = MN;
+#pragma unroll
+    for (int j = 0; j < Base::kN; ++j) {
+      const int64_t i = mn0 + Base::row(j);
+      off_[j] = i < MN ? i * ld + Base::koff() : -1;
+    }
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
     const int64_t k = k0 + Base::koff();
 #pragma unroll
     for (int j = 0; j < Base::kN; ++j) {
-      const int64_t i = row0 + Base::row(j);
-      const float* q = p + i * ld + k;
+      const float* q = p + off_[j] + k0;
+      const bool ok = off_[j] >= 0;
       if (VEC) {
-        r[j] = (i < rows && k < kend) ? *reinterpret_cast<const float4*>(q) : zero4();
+        r[j] = (ok && k < kend) ? *reinterpret_cast<const float4*>(q) : zero4();
       } else {
-        const bool ok = i < rows;
         r[j].x = (ok && k + 0 < kend) ? q[0] : 0.f;
         r[j].y = (ok && k + 1 < kend) ? q[1] : 0.f;
         r[j].z = (ok && k + 2 < kend) ? q[2] : 0.f;
@@ -120,15 +156,19 @@ struct MatM : RowM<E> {
   int64_t ld;
   int64_t i0;
   int64_t rows;
+  int64_t off_[Base::kN];   // this lane's k row * ld + i0
   __device__ void init(int64_t mn0, int64_t MN) {
     i0 = mn0 + Base::moff();
     rows = MN;
+#pragma unroll
+    for (int j = 0; j < Base::kN; ++j) off_[j] = Base::krow(j) * ld + i0;
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
+    const float* pk = p + k0 * ld;
 #pragma unroll
     for (int j = 0; j < Base::kN; ++j) {
       const int64_t k = k0 + Base::krow(j);
-      const float* q = p + k * ld + i0;
+      const float* q = pk + off_[j];
       if (VEC) {
         r[j] = (k < kend && i0 < rows) ? *reinterpret_cast<const float4*>(q) : zero4();
       } else {
@@ -142,171 +182,189 @@ struct MatM : RowM<E> {
   }
 };
 
+// Loader modes of the convolution views: TAP when the reduced channel count
+// is a multiple of 32 (a K tile lies inside one filter tap, uniform over the
+// workgroup), VEC when it is a multiple of 4 (each lane splits its own k
+// index, four consecutive channels per load), SCALAR otherwise.
+enum { SCALAR = 0, VEC4 = 1, TAP = 2 };
+
 // Convolution forward, A = input patches: A[m = (n, p, q)][kk = (r, s, c)] =
-// X[n][p st - pad + r][q st - pad + s][c]   (row-of-k; VEC needs C % 4 == 0)
-template <int E, bool VEC>
+// X[n][p st - pad + r][q st - pad + s][c]   (row-of-k)
+template <int E, int MODE>
 struct ConvPatch : RowK<E> {
   using Base = RowK<E>;
   const float* x;
-  int H, W, C, S, st, pad, P, Q;
-  int64_t M;
-  int n_[Base::kN], h_[Base::kN], w_[Base::kN];   // per row: image, top-left input coordinates
-  __device__ void init(int64_t mn0, int64_t MN) {
-    M = MN;
+  int H, W, C, S, st, pad;
+  FastDiv dQ, dPQ, dC, dS, dSC;   // by Q, P Q, C, S, S C
+  int64_t base_[Base::kN];        // offset of X[n][h0][w0][0]
+  int h_[Base::kN], w_[Base::kN]; // h0 = p st - pad, w0 = q st - pad
+  __device__ void init(int64_t mn0, int64_t M) {
 #pragma unroll
     for (int j = 0; j < Base::kN; ++j) {
       const int64_t m = mn0 + Base::row(j);
       if (m < M) {
-        const int64_t pq = (int64_t)P * Q;
-        const int n = (int)(m / pq);
-        const int rem = (int)(m - (int64_t)n * pq);
-        const int p = rem / Q, q = rem - p * Q;
-        n_[j] = n;
+        const int n = dPQ.div((int)m);
+        const int rem = (int)m - n * (int)dPQ.d;
+        const int p = dQ.div(rem), q = rem - p * (int)dQ.d;
         h_[j] = p * st - pad;
         w_[j] = q * st - pad;
+        base_[j] = (((int64_t)n * H + h_[j]) * W + w_[j]) * C;
       } else {
-        n_[j] = -1;
+        h_[j] = kFar;
+        w_[j] = 0;
+        base_[j] = 0;
       }
     }
   }
-  __device__ float at(int j, int64_t kk, int64_t kend) const {
-    if (n_[j] < 0 || kk >= kend) return 0.f;
-    const int sc = S * C;
-    const int r = (int)(kk / sc);
-    const int rem = (int)(kk - (int64_t)r * sc);
-    const int s = rem / C, c = rem - s * C;
-    const int h = h_[j] + r, w = w_[j] + s;
-    if (h < 0 || h >= H || w < 0 || w >= W) return 0.f;
-    return x[(((int64_t)n_[j] * H + h) * W + w) * C + c];
+  // value at (row j, column kk < kend) or 0
+  __device__ float at(int j, int kk, int64_t kend) const {
+    if (kk >= kend) return 0.f;
+    const int r = dSC.div(kk);
+    const int rem = kk - r * (int)dSC.d;
+    const int s = dC.div(rem), c = rem - s * C;
+    if (!inside(h_[j] + r, H) || !inside(w_[j] + s, W)) return 0.f;
+    return x[base_[j] + ((int64_t)r * W + s) * C + c];
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
-    const int64_t kk = k0 + Base::koff();
-    if (VEC) {
-      int rr = 0, s = 0, c = 0;
-      const bool kin = kk < kend;
-      if (kin) {
-        const int sc = S * C;
-        rr = (int)(kk / sc);
-        const int rem = (int)(kk - (int64_t)rr * sc);
-        s = rem / C;
+    const int kk = (int)k0 + Base::koff();
+    if constexpr (MODE == SCALAR) {
+#pragma unroll
+      for (int j = 0; j < Base::kN; ++j)
+        r[j] = make_float4(at(j, kk, kend), at(j, kk + 1, kend), at(j, kk + 2, kend),
+                           at(j, kk + 3, kend));
+    } else {
+      int rr, s, c;
+      if constexpr (MODE == TAP) {   // uniform tap
+        const int tap = dC.div((int)k0);
+        rr = dS.div(tap);
+        s = tap - rr * S;
+        c = (int)k0 - tap * C + Base::koff();
+      } else {
+        rr = dSC.div(kk);
+        const int rem = kk - rr * (int)dSC.d;
+        s = dC.div(rem);
         c = rem - s * C;
       }
+      const int64_t toff = ((int64_t)rr * W + s) * C + c;
+      const bool kin = kk < kend;
 #pragma unroll
       for (int j = 0; j < Base::kN; ++j) {
-        const int h = h_[j] + rr, w = w_[j] + s;
-        const bool ok = kin && n_[j] >= 0 && h >= 0 && h < H && w >= 0 && w < W;
-        r[j] = ok ? *reinterpret_cast<const float4*>(
-                        &x[(((int64_t)n_[j] * H + h) * W + w) * C + c])
-                  : zero4();
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < Base::kN; ++j) {
-        r[j].x = at(j, kk + 0, kend);
-        r[j].y = at(j, kk + 1, kend);
-        r[j].z = at(j, kk + 2, kend);
-        r[j].w = at(j, kk + 3, kend);
+        const bool ok = kin && inside(h_[j] + rr, H) && inside(w_[j] + s, W);
+        r[j] = ok ? *reinterpret_cast<const float4*>(&x[base_[j] + toff]) : zero4();
       }
     }
   }
 };
 
-// Convolution input gradient, A = output gradient through the taps:
-// A[m = (n, h, w)][kk = (r, s, k)] = dY[n][p][q][k] with p st = h + pad - r,
-// q st = w + pad - s (zero when not an exact, in-range output position).
-// Row-of-k; VEC needs K % 4 == 0.
-template <int E, bool VEC>
+// Convolution input gradient for the input pixels of one stride class,
+// h = st hh + ph and w = st ww + pw (hh < Hc, ww < Wc).  Only the taps
+// r = r0 + st i (i < nR) and s = s0 + st j (j < nS) reach them, from the
+// output position p = hh + a - i, q = ww + b - j (a = (ph + pad - r0) / st,
+// b = (pw + pad - s0) / st); A is the output gradient gathered that way:
+// A[m = (n, hh, ww)][kk = (i, j, k)] = dY[n][hh + a - i][ww + b - j][k], zero
+// outside the output.  Stride 1 is the single class r0 = s0 = 0, a = b = pad.
+// Row-of-k; the mode refers to the output channels K.
+template <int E, int MODE>
 struct ConvGradTap : RowK<E> {
   using Base = RowK<E>;
   const float* dy;
-  int H, W, K, S, st, pad, P, Q;
-  int64_t M;
-  int n_[Base::kN], h_[Base::kN], w_[Base::kN];   // per row: image, h + pad, w + pad
-  __device__ void init(int64_t mn0, int64_t MN) {
-    M = MN;
+  int P, Q, K, nS, a, b;
+  FastDiv dWc, dHWc, dK, dnS, dSK;   // by Wc, Hc Wc, K, nS, nS K
+  int64_t base_[Base::kN];           // offset of dY[n][hh + a][ww + b][0]
+  int p_[Base::kN], q_[Base::kN];    // hh + a, ww + b
+  __device__ void init(int64_t mn0, int64_t M) {
 #pragma unroll
     for (int j = 0; j < Base::kN; ++j) {
       const int64_t m = mn0 + Base::row(j);
       if (m < M) {
-        const int64_t hw = (int64_t)H * W;
-        const int n = (int)(m / hw);
-        const int rem = (int)(m - (int64_t)n * hw);
-        const int h = rem / W, w = rem - h * W;
-        n_[j] = n;
-        h_[j] = h + pad;
-        w_[j] = w + pad;
+        const int n = dHWc.div((int)m);
+        const int rem = (int)m - n * (int)dHWc.d;
+        const int hh = dWc.div(rem), ww = rem - hh * (int)dWc.d;
+        p_[j] = hh + a;
+        q_[j] = ww + b;
+        base_[j] = (((int64_t)n * P + p_[j]) * Q + q_[j]) * K;
       } else {
-        n_[j] = -1;
+        p_[j] = kFar;
+        q_[j] = 0;
+        base_[j] = 0;
       }
     }
   }
-  __device__ float at(int j, int64_t kk, int64_t kend) const {
-    if (n_[j] < 0 || kk >= kend) return 0.f;
-    const int sk = S * K;
-    const int r = (int)(kk / sk);
-    const int rem = (int)(kk - (int64_t)r * sk);
-    const int s = rem / K, k = rem - s * K;
-    const int ph = h_[j] - r, qw = w_[j] - s;
-    if (ph < 0 || qw < 0 || ph % st || qw % st) return 0.f;
-    const int p = ph / st, q = qw / st;
-    if (p >= P || q >= Q) return 0.f;
-    return dy[(((int64_t)n_[j] * P + p) * Q + q) * K + k];
+  __device__ float at(int j, int kk, int64_t kend) const {
+    if (kk >= kend) return 0.f;
+    const int i = dSK.div(kk);
+    const int rem = kk - i * (int)dSK.d;
+    const int jj = dK.div(rem), k = rem - jj * K;
+    if (!inside(p_[j] - i, P) || !inside(q_[j] - jj, Q)) return 0.f;
+    return dy[base_[j] - ((int64_t)i * Q + jj) * K + k];
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
-    const int64_t kk = k0 + Base::koff();
-    if (VEC) {
-      int rr = 0, s = 0, k = 0;
-      const bool kin = kk < kend;
-      if (kin) {
-        const int sk = S * K;
-        rr = (int)(kk / sk);
-        const int rem = (int)(kk - (int64_t)rr * sk);
-        s = rem / K;
-        k = rem - s * K;
-      }
+    const int kk = (int)k0 + Base::koff();
+    if constexpr (MODE == SCALAR) {
 #pragma unroll
-      for (int j = 0; j < Base::kN; ++j) {
-        const int ph = h_[j] - rr, qw = w_[j] - s;
-        bool ok = kin && n_[j] >= 0 && ph >= 0 && qw >= 0 && ph % st == 0 && qw % st == 0;
-        const int p = ok ? ph / st : 0, q = ok ? qw / st : 0;
-        ok = ok && p < P && q < Q;
-        r[j] = ok ? *reinterpret_cast<const float4*>(
-                        &dy[(((int64_t)n_[j] * P + p) * Q + q) * K + k])
-                  : zero4();
-      }
+      for (int j = 0; j < Base::kN; ++j)
+        r[j] = make_float4(at(j, kk, kend), at(j, kk + 1, kend), at(j, kk + 2, kend),
+                           at(j, kk + 3, kend));
     } else {
+      int i, jj, k;
+      if constexpr (MODE == TAP) {   // uniform tap
+        const int tap = dK.div((int)k0);
+        i = dnS.div(tap);
+        jj = tap - i * nS;
+        k = (int)k0 - tap * K + Base::koff();
+      } else {
+        i = dSK.div(kk);
+        const int rem = kk - i * (int)dSK.d;
+        jj = dK.div(rem);
+        k = rem - jj * K;
+      }
+      const int64_t toff = k - ((int64_t)i * Q + jj) * K;
+      const bool kin = kk < kend;
 #pragma unroll
       for (int j = 0; j < Base::kN; ++j) {
-        r[j].x = at(j, kk + 0, kend);
-        r[j].y = at(j, kk + 1, kend);
-        r[j].z = at(j, kk + 2, kend);
-        r[j].w = at(j, kk + 3, kend);
+        const bool ok = kin && inside(p_[j] - i, P) && inside(q_[j] - jj, Q);
+        r[j] = ok ? *reinterpret_cast<const float4*>(&dy[base_[j] + toff]) : zero4();
       }
     }
   }
 };
 
-// Convolution input gradient, B = filter seen per tap:
-// B[kk = (r, s, k)][c] = W[k][r][s][c]   (row-of-m; needs C % 4 == 0)
-template <int E>
+// Convolution input gradient, B = filter at the class's taps:
+// B[kk = (i, j, k)][c] = W[k][r0 + st i][s0 + st j][c]   (row-of-m; C % 4 == 0)
+template <int E, int MODE>
 struct ConvFilterTap : RowM<E> {
   using Base = RowM<E>;
   const float* w;
-  int C, K, R, S;
-  int64_t c0;
-  __device__ void init(int64_t mn0, int64_t) { c0 = mn0 + Base::moff(); }
+  int C, K, S, st, r0, s0, nS;
+  int64_t RSC;
+  FastDiv dK, dnS, dSK;
+  int c0;
+  __device__ void init(int64_t mn0, int64_t) { c0 = (int)mn0 + Base::moff(); }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
+    if constexpr (MODE == TAP) {   // uniform tap
+      const int tap = dK.div((int)k0);
+      const int i = dnS.div(tap), jj = tap - i * nS;
+      const int kb = (int)k0 - tap * K;
+      const int64_t toff = ((int64_t)(r0 + st * i) * S + s0 + st * jj) * C + c0;
 #pragma unroll
-    for (int j = 0; j < Base::kN; ++j) {
-      const int64_t kk = k0 + Base::krow(j);
-      if (kk < kend && c0 < C) {
-        const int sk = S * K;
-        const int rr = (int)(kk / sk);
-        const int rem = (int)(kk - (int64_t)rr * sk);
-        const int s = rem / K, k = rem - s * K;
-        r[j] = *reinterpret_cast<const float4*>(&w[(((int64_t)k * R + rr) * S + s) * C + c0]);
-      } else {
-        r[j] = zero4();
+      for (int j = 0; j < Base::kN; ++j) {
+        const bool ok = k0 + Base::krow(j) < kend && c0 < C;
+        r[j] = ok ? *reinterpret_cast<const float4*>(&w[(int64_t)(kb + Base::krow(j)) * RSC + toff])
+                  : zero4();
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < Base::kN; ++j) {
+        const int kk = (int)k0 + Base::krow(j);
+        if (kk < kend && c0 < C) {
+          const int i = dSK.div(kk);
+          const int rem = kk - i * (int)dSK.d;
+          const int jj = dK.div(rem), k = rem - jj * K;
+          r[j] = *reinterpret_cast<const float4*>(
+              &w[(int64_t)k * RSC + ((int64_t)(r0 + st * i) * S + s0 + st * jj) * C + c0]);
+        } else {
+          r[j] = zero4();
+        }
       }
     }
   }
@@ -319,54 +377,67 @@ template <int E, bool VEC>
 struct ConvPixelPatch : RowM<E> {
   using Base = RowM<E>;
   const float* x;
-  int H, W, C, S, st, pad, P, Q;
-  int64_t RSC;
-  int r_[4], s_[4], c_[4];   // per column of this thread; r = -1: no column
-  __device__ void init(int64_t mn0, int64_t MN) {
-    RSC = MN;
-    const int64_t col = mn0 + Base::moff();
+  int H, W, C, st, pad;
+  FastDiv dQ, dPQ, dC, dSC;
+  int64_t toff_[4];   // per column of this lane: (r W + s) C + c
+  int r_[4], s_[4];   // kFar: no column
+  __device__ void init(int64_t mn0, int64_t RSC) {
+    const int col = (int)mn0 + Base::moff();
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int64_t cc = col + e;
+      const int cc = col + e;
       if (cc < RSC && (VEC ? e == 0 : true)) {
-        const int sc = S * C;
-        const int r = (int)(cc / sc);
-        const int rem = (int)(cc - (int64_t)r * sc);
+        const int r = dSC.div(cc);
+        const int rem = cc - r * (int)dSC.d;
+        const int s = dC.div(rem), c = rem - s * C;
         r_[e] = r;
-        s_[e] = rem / C;
-        c_[e] = rem - s_[e] * C;
+        s_[e] = s;
+        toff_[e] = ((int64_t)r * W + s) * C + c;
       } else {
-        r_[e] = -1;
+        r_[e] = kFar;
+        s_[e] = 0;
+        toff_[e] = 0;
       }
     }
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
 #pragma unroll
     for (int j = 0; j < Base::kN; ++j) {
-      const int64_t kk = k0 + Base::krow(j);
+      const int kk = (int)k0 + Base::krow(j);
       r[j] = zero4();
       if (kk >= kend) continue;
-      const int64_t pq = (int64_t)P * Q;
-      const int n = (int)(kk / pq);
-      const int rem = (int)(kk - (int64_t)n * pq);
-      const int p = rem / Q, q = rem - p * Q;
+      const int n = dPQ.div(kk);
+      const int rem = kk - n * (int)dPQ.d;
+      const int p = dQ.div(rem), q = rem - p * (int)dQ.d;
       const int hb = p * st - pad, wb = q * st - pad;
+      const int64_t base = (((int64_t)n * H + hb) * W + wb) * C;
       if (VEC) {
-        const int h = hb + r_[0], w = wb + s_[0];
-        if (r_[0] >= 0 && h >= 0 && h < H && w >= 0 && w < W)
-          r[j] = *reinterpret_cast<const float4*>(&x[(((int64_t)n * H + h) * W + w) * C + c_[0]]);
+        if (inside(hb + r_[0], H) && inside(wb + s_[0], W))
+          r[j] = *reinterpret_cast<const float4*>(&x[base + toff_[0]]);
       } else {
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int h = hb + r_[e], w = wb + s_[e];
-          v[e] = (r_[e] >= 0 && h >= 0 && h < H && w >= 0 && w < W)
-                     ? x[(((int64_t)n * H + h) * W + w) * C + c_[e]]
-                     : 0.f;
-        }
+        for (int e = 0; e < 4; ++e)
+          v[e] = (inside(hb + r_[e], H) && inside(wb + s_[e], W)) ? x[base + toff_[e]] : 0.f;
         r[j] = make_float4(v[0], v[1], v[2], v[3]);
       }
     }
+  }
+};
+
+// Where row m of C goes: m * ldc, or the NHWC input pixel of a stride class
+struct DenseOut {
+  int64_t ldc;
+  __device__ int64_t row(int64_t m) const { return m * ldc; }
+};
+struct ClassOut {
+  int H, W, C, st, ph, pw;
+  FastDiv dWc, dHWc;
+  __device__ int64_t row(int64_t m) const {
+    const int n = dHWc.div((int)m);
+    const int rem = (int)m - n * (int)dHWc.d;
+    const int hh = dWc.div(rem), ww = rem - hh * (int)dWc.d;
+    return (((int64_t)n * H + st * hh + ph) * W + st * ww + pw) * C;
   }
 };
 
@@ -398,16 +469,27 @@ __device__ inline void shift(L& l, int64_t d) {
 }
 
 // rowsum (optional): rowsum[slice][m] = sum over this slice's k of A[m][k]
-template <int BM, int BN, class LA, class LB, bool BIAS, bool BATCHED>
-__global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __restrict__ c,
-                                                       int64_t ldc, int64_t slice_stride,
+template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED>
+__global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __restrict__ c, OM om,
+                                                       int64_t slice_stride,
                                                        const float* __restrict__ bias, int64_t M,
                                                        int64_t N, int64_t K, int64_t k_slice,
                                                        int tiles_m, int tiles_n, Batch bt,
                                                        float* __restrict__ rowsum) {
   constexpr int MB = BM / 64, NB = BN / 64;
+  // Workgroup (tile, slice, batch) from an XCD-aware order: the hardware hands
+  // linear workgroup h to XCD h mod 8, so logical ids are laid out so that each
+  // XCD (with its own L2) gets one contiguous run of them, and neighbouring
+  // tiles, which share operand rows, share an L2.
+  const uint32_t gx = gridDim.x, gy = gridDim.y;
+  const uint32_t G = gx * gy * gridDim.z;
+  const uint32_t h = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const uint32_t q = G / kXcds, rem = G % kXcds, xcd = h % kXcds, local = h / kXcds;
+  const uint32_t L = xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
+  const int t = (int)(L % gx);
+  const int64_t slice = (L / gx) % gy;
   if constexpr (BATCHED) {
-    const int64_t z = blockIdx.z, zo = z / bt.inner, zi = z % bt.inner;
+    const int64_t z = L / (gx * gy), zo = z / bt.inner, zi = z % bt.inner;
     shift(la, zo * bt.a_o + zi * bt.a_i);
     shift(lb, zo * bt.b_o + zi * bt.b_i);
     c += zo * bt.c_o + zi * bt.c_i;
@@ -416,7 +498,6 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
   __shared__ __attribute__((aligned(16))) float Bs[2][LB::kLds];
 
   // grouped tile order: 8 tile-rows share their B tiles in L2
-  const int t = blockIdx.x;
   const int group = 8;
   const int per_group = group * tiles_n;
   const int g = t / per_group;
@@ -425,7 +506,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
   const int tm = first_m + (t % per_group) % gsize;
   const int tn = (t % per_group) / gsize;
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
-  const int64_t kb = (int64_t)blockIdx.y * k_slice;
+  const int64_t kb = slice * k_slice;
   const int64_t ke = min(K, kb + k_slice);
 
   la.init(m0, M);
@@ -496,8 +577,8 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
     buf ^= 1;
   }
 
-  if (sums && m0 + threadIdx.x < M) rowsum[(int64_t)blockIdx.y * M + m0 + threadIdx.x] = rs;
-  float* out = c + (int64_t)blockIdx.y * slice_stride;
+  if (sums && m0 + threadIdx.x < M) rowsum[slice * M + m0 + threadIdx.x] = rs;
+  float* out = c + slice * slice_stride;
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -508,25 +589,26 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = m0 + wm * (BM / 2) + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (row < M) out[row * ldc + col] = acc[mb][nb][r] + bv;
+        if (row < M) out[om.row(row) + col] = acc[mb][nb][r] + bv;
       }
     }
 }
 
-template <int BM, int BN, class LA, class LB, bool BIAS, bool BATCHED = false>
-hipError_t run_gemm(const LA& la, const LB& lb, float* c, int64_t ldc, const float* bias,
-                    int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s,
-                    int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
+template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED = false>
+hipError_t run_gemm(const LA& la, const LB& lb, float* c, OM om, int64_t slice_stride,
+                    const float* bias, int64_t M, int64_t N, int64_t K, int64_t slices,
+                    hipStream_t s, int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
                     float* rowsum = nullptr) {
   const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  if (tiles_m * tiles_n > INT32_MAX / 2 || slices > 65535 || batches > 65535 || batches < 1)
+  if (tiles_m * tiles_n > INT32_MAX / 2 || slices > 65535 || batches > 65535 || batches < 1 ||
+      tiles_m * tiles_n * slices * batches > INT32_MAX)
     return hipErrorInvalidValue;
   int64_t k_slice = (K + slices - 1) / slices;
   k_slice = (k_slice + BK - 1) / BK * BK;
   dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices, (unsigned)batches);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, BIAS, BATCHED>), grid, dim3(THREADS), 0, s, la,
-                     lb, c, ldc, M * ldc, bias, M, N, K, k_slice, (int)tiles_m, (int)tiles_n, bt,
-                     rowsum);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, OM, BIAS, BATCHED>), grid, dim3(THREADS), 0, s,
+                     la, lb, c, om, slice_stride, bias, M, N, K, k_slice, (int)tiles_m,
+                     (int)tiles_n, bt, rowsum);
   return hipGetLastError();
 }
 
@@ -542,50 +624,70 @@ Shape pick_shape(int64_t M, int64_t N) {
 }
 
 // Runs the GEMM with loader templates A<E>, B<E> instantiated for the chosen
-// tile shape; `make_a(tag)` / `make_b(tag)` build them.
+// tile shape; `fa(a)` / `fb(b)` fill them in.  Row m of C starts at om.row(m);
+// split-K slices of C are slice_stride floats apart.
 template <template <int> class LAT, template <int> class LBT, bool BIAS, bool BATCHED = false,
-          class FA, class FB>
-hipError_t dispatch(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int64_t M, int64_t N,
-                    int64_t K, int64_t slices, hipStream_t s, int64_t batches = 1,
-                    Batch bt = Batch{1, 0, 0, 0, 0, 0, 0}, float* rowsum = nullptr) {
+          class FA, class FB, class OM>
+hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const float* bias,
+                    int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s,
+                    int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
+                    float* rowsum = nullptr) {
   switch (pick_shape(M, N)) {
     case S128x64: {
       LAT<128> a{};
       LBT<64> b{};
       fa(a);
       fb(b);
-      return run_gemm<128, 64, LAT<128>, LBT<64>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
-                                                                 slices, s, batches, bt, rowsum);
+      return run_gemm<128, 64, LAT<128>, LBT<64>, OM, BIAS, BATCHED>(
+          a, b, c, om, slice_stride, bias, M, N, K, slices, s, batches, bt, rowsum);
     }
     case S64x128: {
       LAT<64> a{};
       LBT<128> b{};
       fa(a);
       fb(b);
-      return run_gemm<64, 128, LAT<64>, LBT<128>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
-                                                                 slices, s, batches, bt, rowsum);
+      return run_gemm<64, 128, LAT<64>, LBT<128>, OM, BIAS, BATCHED>(
+          a, b, c, om, slice_stride, bias, M, N, K, slices, s, batches, bt, rowsum);
     }
     default: {
       LAT<128> a{};
       LBT<128> b{};
       fa(a);
       fb(b);
-      return run_gemm<128, 128, LAT<128>, LBT<128>, BIAS, BATCHED>(a, b, c, ldc, bias, M, N, K,
-                                                                   slices, s, batches, bt, rowsum);
+      return run_gemm<128, 128, LAT<128>, LBT<128>, OM, BIAS, BATCHED>(
+          a, b, c, om, slice_stride, bias, M, N, K, slices, s, batches, bt, rowsum);
     }
   }
+}
+
+// row-major C with leading dimension ldc
+template <template <int> class LAT, template <int> class LBT, bool BIAS, bool BATCHED = false,
+          class FA, class FB>
+hipError_t dispatch_dense(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int64_t M,
+                          int64_t N, int64_t K, int64_t slices, hipStream_t s,
+                          int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
+                          float* rowsum = nullptr) {
+  return dispatch<LAT, LBT, BIAS, BATCHED>(fa, fb, c, DenseOut{ldc}, M * ldc, bias, M, N, K, slices,
+                                           s, batches, bt, rowsum);
 }
 
 template <int E> using MatKv = MatK<E, true>;
 template <int E> using MatKs = MatK<E, false>;
 template <int E> using MatMv = MatM<E, true>;
 template <int E> using MatMs = MatM<E, false>;
-template <int E> using ConvPatchV = ConvPatch<E, true>;
-template <int E> using ConvPatchS = ConvPatch<E, false>;
-template <int E> using ConvGradTapV = ConvGradTap<E, true>;
-template <int E> using ConvGradTapS = ConvGradTap<E, false>;
+template <int E> using ConvPatchT = ConvPatch<E, TAP>;
+template <int E> using ConvPatchV = ConvPatch<E, VEC4>;
+template <int E> using ConvPatchS = ConvPatch<E, SCALAR>;
+template <int E> using ConvGradTapT = ConvGradTap<E, TAP>;
+template <int E> using ConvGradTapV = ConvGradTap<E, VEC4>;
+template <int E> using ConvGradTapS = ConvGradTap<E, SCALAR>;
+template <int E> using ConvFilterTapT = ConvFilterTap<E, TAP>;
+template <int E> using ConvFilterTapG = ConvFilterTap<E, VEC4>;
 template <int E> using ConvPixelPatchV = ConvPixelPatch<E, true>;
 template <int E> using ConvPixelPatchS = ConvPixelPatch<E, false>;
+
+// the GEMM sizes of the convolution views index with 32-bit arithmetic
+bool fits31(int64_t v) { return v >= 0 && v < (int64_t(1) << 31) - 64; }
 
 // ---------------------------------------------------------------- small kernels
 // out[j] = sum over slices of part[s][j]: four interleaved accumulators
@@ -612,8 +714,8 @@ hipError_t linear_fwd(const float* X, const float* W, const float* b, float* Y, 
   auto fa = [&](auto& a) { a.p = X; a.ld = K; };
   auto fb = [&](auto& bb) { bb.p = W; bb.ld = K; };
   if (K % 4 == 0 && aligned16(X) && aligned16(W))
-    return dispatch<MatKv, MatKv, true>(fa, fb, Y, N, b, M, N, K, 1, s);
-  return dispatch<MatKs, MatKs, true>(fa, fb, Y, N, b, M, N, K, 1, s);
+    return dispatch_dense<MatKv, MatKv, true>(fa, fb, Y, N, b, M, N, K, 1, s);
+  return dispatch_dense<MatKs, MatKs, true>(fa, fb, Y, N, b, M, N, K, 1, s);
 }
 
 hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, int64_t K,
@@ -622,8 +724,8 @@ hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, i
   auto fa = [&](auto& a) { a.p = dY; a.ld = N; };
   auto fb = [&](auto& bb) { bb.p = W; bb.ld = K; };
   if (N % 4 == 0 && K % 4 == 0 && aligned16(W) && aligned16(dY))
-    return dispatch<MatKv, MatMv, false>(fa, fb, dX, K, nullptr, M, K, N, 1, s);
-  return dispatch<MatKs, MatMs, false>(fa, fb, dX, K, nullptr, M, K, N, 1, s);
+    return dispatch_dense<MatKv, MatMv, false>(fa, fb, dX, K, nullptr, M, K, N, 1, s);
+  return dispatch_dense<MatKs, MatMs, false>(fa, fb, dX, K, nullptr, M, K, N, 1, s);
 }
 
 hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, float* part,
@@ -638,9 +740,9 @@ hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, f
   const Batch one{1, 0, 0, 0, 0, 0, 0};
   hipError_t e;
   if (N % 4 == 0 && K % 4 == 0 && aligned16(X) && aligned16(dY))
-    e = dispatch<MatMv, MatMv, false>(fa, fb, out, K, nullptr, N, K, M, slices, s, 1, one, sums);
+    e = dispatch_dense<MatMv, MatMv, false>(fa, fb, out, K, nullptr, N, K, M, slices, s, 1, one, sums);
   else
-    e = dispatch<MatMs, MatMs, false>(fa, fb, out, K, nullptr, N, K, M, slices, s, 1, one, sums);
+    e = dispatch_dense<MatMs, MatMs, false>(fa, fb, out, K, nullptr, N, K, M, slices, s, 1, one, sums);
   if (e != hipSuccess || slices <= 1) return e;
   hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((N * K + 255) / 256)), dim3(256), 0, s,
                      part, dW, N * K, slices);
@@ -661,7 +763,7 @@ hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, c
                    st.a_outer % 4 == 0 && st.a_inner % 4 == 0 && st.b_outer % 4 == 0 &&
                    st.b_inner % 4 == 0;
 #define GEMM_BATCHED_CASE(LA, LB) \
-  return dispatch<LA, LB, false, true>(fa, fb, C, ldc, nullptr, M, N, K, 1, s, batches, bt)
+  return dispatch_dense<LA, LB, false, true>(fa, fb, C, ldc, nullptr, M, N, K, 1, s, batches, bt)
   if (vec) {
     if (a_rowk && b_rowk) GEMM_BATCHED_CASE(MatKv, MatKv);
     if (a_rowk) GEMM_BATCHED_CASE(MatKv, MatMv);
@@ -677,49 +779,87 @@ hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, c
 
 hipError_t conv_fwd(const float* X, const float* W, float* Y, const ConvShape& c, hipStream_t s) {
   const int64_t M = c.N * c.P * c.Q, N = c.K, K = c.R * c.S * c.C;
+  if (!fits31(M) || !fits31(K)) return hipErrorInvalidValue;
   auto fa = [&](auto& a) {
     a.x = X; a.H = (int)c.H; a.W = (int)c.W; a.C = (int)c.C; a.S = (int)c.S;
-    a.st = (int)c.stride; a.pad = (int)c.pad; a.P = (int)c.P; a.Q = (int)c.Q;
+    a.st = (int)c.stride; a.pad = (int)c.pad;
+    a.dQ = FastDiv::make(c.Q); a.dPQ = FastDiv::make(c.P * c.Q); a.dC = FastDiv::make(c.C);
+    a.dS = FastDiv::make(c.S); a.dSC = FastDiv::make(c.S * c.C);
   };
   auto fb = [&](auto& b) { b.p = W; b.ld = K; };
-  if (c.C % 4 == 0) return dispatch<ConvPatchV, MatKv, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
-  return dispatch<ConvPatchS, MatKs, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
+  if (c.C % 32 == 0)
+    return dispatch_dense<ConvPatchT, MatKv, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
+  if (c.C % 4 == 0)
+    return dispatch_dense<ConvPatchV, MatKv, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
+  return dispatch_dense<ConvPatchS, MatKs, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
 }
 
 hipError_t conv_bwd_x(const float* W, const float* dY, float* dX, const ConvShape& c,
                       hipStream_t s) {
   if (c.C % 4 != 0) return hipErrorInvalidValue;   // every conv with an input gradient has C % 4 == 0
-  const int64_t M = c.N * c.H * c.W, N = c.C, K = c.R * c.S * c.K;
-  auto fa = [&](auto& a) {
-    a.dy = dY; a.H = (int)c.H; a.W = (int)c.W; a.K = (int)c.K; a.S = (int)c.S;
-    a.st = (int)c.stride; a.pad = (int)c.pad; a.P = (int)c.P; a.Q = (int)c.Q;
-  };
-  auto fb = [&](auto& b) {
-    b.w = W; b.C = (int)c.C; b.K = (int)c.K; b.R = (int)c.R; b.S = (int)c.S;
-  };
-  if (c.K % 4 == 0)
-    return dispatch<ConvGradTapV, ConvFilterTap, false>(fa, fb, dX, N, nullptr, M, N, K, 1, s);
-  return dispatch<ConvGradTapS, ConvFilterTap, false>(fa, fb, dX, N, nullptr, M, N, K, 1, s);
+  if (!fits31(c.N * c.H * c.W) || !fits31(c.R * c.S * c.K)) return hipErrorInvalidValue;
+  const int64_t st = c.stride;
+  // one GEMM per stride class (ph, pw) of input pixels; a class no tap reaches gets zeros
+  for (int64_t ph = 0; ph < st; ++ph)
+    for (int64_t pw = 0; pw < st; ++pw) {
+      const int64_t Hc = (c.H - ph + st - 1) / st, Wc = (c.W - pw + st - 1) / st;
+      const int64_t r0 = (ph + c.pad) % st, s0 = (pw + c.pad) % st;
+      const int64_t nR = r0 < c.R ? (c.R - r0 + st - 1) / st : 0;
+      const int64_t nS = s0 < c.S ? (c.S - s0 + st - 1) / st : 0;
+      const int64_t M = c.N * Hc * Wc, N = c.C, K = nR * nS * c.K;
+      if (M == 0) continue;
+      auto fa = [&](auto& a) {
+        a.dy = dY; a.P = (int)c.P; a.Q = (int)c.Q; a.K = (int)c.K; a.nS = (int)nS;
+        a.a = (int)((ph + c.pad - r0) / st); a.b = (int)((pw + c.pad - s0) / st);
+        a.dWc = FastDiv::make(Wc); a.dHWc = FastDiv::make(Hc * Wc); a.dK = FastDiv::make(c.K);
+        a.dnS = FastDiv::make(nS > 0 ? nS : 1); a.dSK = FastDiv::make(nS > 0 ? nS * c.K : 1);
+      };
+      auto fb = [&](auto& b) {
+        b.w = W; b.C = (int)c.C; b.K = (int)c.K; b.S = (int)c.S; b.st = (int)st; b.r0 = (int)r0;
+        b.s0 = (int)s0; b.nS = (int)nS; b.RSC = c.R * c.S * c.C;
+        b.dK = FastDiv::make(c.K); b.dnS = FastDiv::make(nS > 0 ? nS : 1);
+        b.dSK = FastDiv::make(nS > 0 ? nS * c.K : 1);
+      };
+      const ClassOut om{(int)c.H, (int)c.W, (int)c.C, (int)st, (int)ph, (int)pw,
+                        FastDiv::make(Wc), FastDiv::make(Hc * Wc)};
+      hipError_t e;
+      if (c.K % 32 == 0)
+        e = dispatch<ConvGradTapT, ConvFilterTapT, false>(fa, fb, dX, om, 0, nullptr, M, N, K, 1,
+                                                          s);
+      else if (c.K % 4 == 0)
+        e = dispatch<ConvGradTapV, ConvFilterTapG, false>(fa, fb, dX, om, 0, nullptr, M, N, K, 1,
+                                                          s);
+      else
+        e = dispatch<ConvGradTapS, ConvFilterTapG, false>(fa, fb, dX, om, 0, nullptr, M, N, K, 1,
+                                                          s);
+      if (e != hipSuccess) return e;
+    }
+  return hipSuccess;
 }
 
 hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, int64_t slices,
                       const ConvShape& c, hipStream_t s) {
   // dW[K][RSC] = sum over pixels of dY[pixel][k] * patch[pixel][rsc]
   const int64_t M = c.K, N = c.R * c.S * c.C, K = c.N * c.P * c.Q;
+  if (!fits31(K) || !fits31(N)) return hipErrorInvalidValue;
+  if (slices > 1 && part == nullptr) return hipErrorInvalidValue;
   float* out = slices > 1 ? part : dW;
   auto fa = [&](auto& a) { a.p = dY; a.ld = c.K; };
   auto fb = [&](auto& b) {
-    b.x = X; b.H = (int)c.H; b.W = (int)c.W; b.C = (int)c.C; b.S = (int)c.S;
-    b.st = (int)c.stride; b.pad = (int)c.pad; b.P = (int)c.P; b.Q = (int)c.Q;
+    b.x = X; b.H = (int)c.H; b.W = (int)c.W; b.C = (int)c.C; b.st = (int)c.stride;
+    b.pad = (int)c.pad; b.dQ = FastDiv::make(c.Q); b.dPQ = FastDiv::make(c.P * c.Q);
+    b.dC = FastDiv::make(c.C); b.dSC = FastDiv::make(c.S * c.C);
   };
   hipError_t e;
   if (c.K % 4 == 0) {
     if (c.C % 4 == 0)
-      e = dispatch<MatMv, ConvPixelPatchV, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
+      e = dispatch_dense<MatMv, ConvPixelPatchV, false>(fa, fb, out, N, nullptr, M, N, K, slices,
+                                                        s);
     else
-      e = dispatch<MatMv, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
+      e = dispatch_dense<MatMv, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices,
+                                                        s);
   } else {
-    e = dispatch<MatMs, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
+    e = dispatch_dense<MatMs, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
   }
   if (e != hipSuccess || slices <= 1) return e;
   const int64_t n = M * N;

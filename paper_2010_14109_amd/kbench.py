@@ -1,0 +1,138 @@
+"""Single-function harness for kernel profiling.
+
+``python -m paper_2010_14109_amd.kbench CASE [REPS]`` registers one function
+with seeded inputs, runs it in-core REPS times through the library and prints
+its event-timed duration; under ``rocprofv3`` it gives clean per-kernel
+statistics and counters.  CASE is ``op:n1,n2,...``:
+
+* ``conv_fwd | conv_bwd_x | conv_bwd_w : N,H,W,C,K,k,stride,pad``
+* ``linear_fwd | linear_bwd_x | linear_bwd_w : M,K,N``
+* ``relu_fwd : n``  (reads 4 n bytes, writes 4 n bytes: the calibration kernel)
+
+``python -m paper_2010_14109_amd.kbench --traffic FETCH_DIR WRITE_DIR CAL_DIR``
+turns ``rocprofv3 --pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` output of a case
+(FETCH_DIR, WRITE_DIR) into HBM bytes per call, scaling each counter by what
+it reads for ``relu_fwd:268435456`` (CAL_DIR holds both counters of that run).
+"""
+
+from __future__ import annotations
+
+import csv
+import glob
+import os
+import sys
+import time
+from collections import defaultdict
+
+import numpy as np
+
+from . import netdef, ooc
+
+CAL_N = 268435456   # floats of the calibration ReLU: 1 GiB read, 1 GiB written
+
+
+def _conv_attrs(N, H, W, C, K, k, st, pd):
+    P = (H + 2 * pd - k) // st + 1
+    Q = (W + 2 * pd - k) // st + 1
+    return [N, H, W, C, K, k, k, st, pd, P, Q], P, Q
+
+
+def case(spec):
+    """(op, [(bytes, kind, access)], attrs) of a case string."""
+    op, nums = spec.split(":")
+    v = [int(x) for x in nums.split(",")]
+    I, O, R, Wr = ooc.INPUT, ooc.OUTPUT, ooc.R, ooc.W
+    if op == "relu_fwd":
+        return op, [(v[0] * 4, I, R), (v[0] * 4, O, Wr)], [v[0]]
+    if op.startswith("conv"):
+        N, H, W, C, K, k, st, pd = v
+        a, P, Q = _conv_attrs(N, H, W, C, K, k, st, pd)
+        xb, wb, yb = N * H * W * C * 4, K * k * k * C * 4, N * P * Q * K * 4
+        if op == "conv_fwd":
+            return op, [(xb, I, R), (wb, I, R), (yb, O, Wr)], a
+        if op == "conv_bwd_x":
+            return op, [(wb, I, R), (yb, I, R), (xb, O, Wr)], a
+        s = netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q)
+        vs = [(xb, I, R), (yb, I, R), (wb, O, Wr)] + ([(s * wb, O, Wr)] if s > 1 else [])
+        return op, vs, a + [s]
+    M, K, N = v
+    if op == "linear_fwd":
+        return op, [(M * K * 4, I, R), (N * K * 4, I, R), (N * 4, I, R), (M * N * 4, O, Wr)], v
+    if op == "linear_bwd_x":
+        return op, [(N * K * 4, I, R), (M * N * 4, I, R), (M * K * 4, O, Wr)], v
+    s = netdef.wgrad_pixel_slices(N, K, M)
+    vs = [(M * K * 4, I, R), (M * N * 4, I, R), (N * K * 4, O, Wr), (N * 4, O, Wr)]
+    if s > 1:
+        vs.append((s * (N * K + N) * 4, O, Wr))
+    return op, vs, v + [s]
+
+
+def run(spec, reps=20):
+    op, vs, attrs = case(spec)
+    ctx = ooc.Context(0)
+    try:
+        ids = [ctx.add_var(b, k) for b, k, _ in vs]
+        ctx.add_fn(op, ids, [a for _, _, a in vs], attrs)
+        ctx.set_chunk(2 << 20)
+        ctx.build_schedule()
+        ctx.prepare()
+        rng = np.random.default_rng(0)
+        for (b, k, _), v in zip(vs, ids):
+            if k == ooc.INPUT:
+                ctx.host_view(v, np.float32)[...] = rng.standard_normal(b // 4).astype(np.float32)
+        ctx.upload()
+        ctx.step(0.0, 0.0)
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            ctx.step(0.0, 0.0)
+        wall = (time.perf_counter() - t0) / reps * 1e3
+        return ctx.fn_times()[0], wall
+    finally:
+        ctx.close()
+
+
+def _counters(d):
+    """{kernel: {counter: mean per dispatch}} of the rocprofv3 csv files under d."""
+    acc = defaultdict(lambda: defaultdict(list))
+    for f in glob.glob(os.path.join(d, "**", "*_counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                name = r["Kernel_Name"].replace("ooc::(anonymous namespace)::", "")
+                name = name.replace("void ", "").split("(")[0]
+                acc[name][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    return {k: {c: sum(x) / len(x) for c, x in v.items()} for k, v in acc.items()}
+
+
+def traffic(fetch_dir, write_dir, cal_dir):
+    """Calibrated HBM bytes per call: {kernel: (fetch_bytes, write_bytes)} and the scales."""
+    cal = _counters(cal_dir)
+    ew = [v for k, v in cal.items() if k.startswith("ew_kernel")]
+    if len(ew) != 1:
+        raise SystemExit(f"calibration run {cal_dir} must hold exactly one ReLU kernel")
+    ref = CAL_N * 4
+    fs, ws = ref / (ew[0]["FETCH_SIZE"] * 1024), ref / (ew[0]["WRITE_SIZE"] * 1024)
+    f, w = _counters(fetch_dir), _counters(write_dir)
+    out = {k: (f[k]["FETCH_SIZE"] * 1024 * fs, w.get(k, {}).get("WRITE_SIZE", 0.0) * 1024 * ws)
+           for k in f}
+    return out, fs, ws
+
+
+def main(argv):
+    if argv and argv[0] == "--traffic":
+        res, fs, ws = traffic(*argv[1:4])
+        print(f"scales: FETCH_SIZE x {fs:.4f}, WRITE_SIZE x {ws:.4f}")
+        total = 0.0
+        for k, (fb, wb) in res.items():
+            print(f"{k}: fetch {fb / 1e6:.2f} MB, write {wb / 1e6:.2f} MB")
+            total += fb + wb
+        print(f"total bytes per call: {int(total)}")
+        return 0
+    spec = argv[0]
+    reps = int(argv[1]) if len(argv) > 1 else 20
+    ev, wall = run(spec, reps)
+    print(f"{spec}: {ev:.4f} ms per call (events), {wall:.3f} ms wall", flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main(sys.argv[1:]))

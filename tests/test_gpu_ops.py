@@ -103,6 +103,14 @@ CONVS = [  # N, H, W, C, K, k, stride, pad
     (2, 9, 10, 8, 12, 1, 2, 0),
     (3, 8, 8, 64, 64, 3, 1, 1),
     (1, 5, 5, 132, 136, 3, 1, 1),
+    # channel counts that are multiples of 32 (one filter tap per K tile), strided input
+    # gradients split into stride classes, classes no tap reaches (1x1 stride 2), stride 3
+    (2, 11, 9, 32, 64, 3, 2, 1),
+    (2, 10, 7, 64, 32, 1, 2, 0),
+    (1, 9, 9, 64, 40, 3, 2, 1),
+    (2, 7, 7, 32, 36, 5, 2, 2),
+    (1, 8, 7, 4, 6, 3, 3, 1),
+    (1, 4, 4, 32, 32, 1, 3, 0),
 ]
 
 
