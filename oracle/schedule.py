@@ -164,7 +164,8 @@ def window_end(seq, sizes, l, window):
     return r
 
 
-def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C"):
+def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C", ahead=None,
+          threshold=None):
     """Schedule one training step.  Returns a dict:
 
     ``ops``      list of (fn, phase, kind, var) in emission order (fn = N at END);
@@ -174,6 +175,11 @@ def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C"):
     """
     if policy not in ("C", "L"):
         raise Invalid("policy must be 'C' or 'L'")
+    # fixed-distance rule of LMS (Section 2): swap in `ahead` functions before a use, keep a
+    # variable whose next use is at most `threshold` functions away
+    fixed = ahead is not None or threshold is not None
+    if fixed and (ahead is None or threshold is None or ahead < 0 or threshold < 0):
+        raise Invalid("the fixed-distance rule needs ahead >= 0 and threshold >= 0")
     if chunk <= 0:
         raise Invalid("chunk must be positive")
     fn_vars = normalize(fn_vars)
@@ -183,6 +189,7 @@ def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C"):
     a = [rounded(x, chunk) for x in var_bytes]
     seq, first, last = sequence(fn_vars)
     nxt = next_use(seq, first, last)
+    fn_of = [i for i in range(N) for _ in fn_vars[i]]
 
     state = [HOST if k in PERSISTENT else UNMAT for k in var_kinds]
     # pending swap-outs, oldest first; under policy L an entry is one device copy
@@ -198,8 +205,11 @@ def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C"):
 
     for i in range(N):
         l, e = first[i], last[i]
-        # 1. schedule-window
-        r = max(window_end(seq, b, l, window), e, r_prev)
+        # 1. schedule-window (bytes), or the functions up to f_{i + ahead}
+        if fixed:
+            r = max(last[min(i + ahead, N - 1)], e, r_prev)
+        else:
+            r = max(window_end(seq, b, l, window), e, r_prev)
         # 2. steps (a)+(b): admit positions r_prev+1 .. r
         p = r_prev + 1
         while p <= r:
@@ -243,8 +253,8 @@ def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C"):
                 state[u] = UNMAT
                 held -= a[u]
                 emit(i, POST, FREE, u)
-            elif n is not None and n <= r:
-                pass  # already reserved inside the window: keep it
+            elif n is not None and (n <= r or (fixed and fn_of[n] - i <= threshold)):
+                pass  # already reserved inside the window (or close enough): keep it
             else:
                 state[u] = PEND
                 fifo.append(u)

@@ -44,10 +44,13 @@ def parse_golden():
                 continue
             t = line.split()
             if t[0] == "windows":
-                out["windows"] = [int(x) for x in t[1:]]
+                (out[cur] if cur == "fixed" else out)["windows"] = [int(x) for x in t[1:]]
             elif t[0] == "policy":
                 cur = t[1]
                 out[cur] = {"ops": [], "held": []}
+            elif t[0] == "fixed":
+                cur = "fixed"
+                out[cur] = {"ops": [], "held": [], "ahead": int(t[1]), "threshold": int(t[2])}
             elif t[0] == "totals":
                 out[cur]["peak"], out[cur]["h2d"], out[cur]["d2h"] = int(t[2]), int(t[4]), int(t[6])
             else:
@@ -68,6 +71,53 @@ def test_golden_worked_example(policy):
     assert (out["peak"], out["h2d"], out["d2h"]) == (g[policy]["peak"], g[policy]["h2d"],
                                                       g[policy]["d2h"])
     check.replay(b, k, f, out["ops"], 24, policy=policy, held=out["held"])
+
+
+def test_golden_fixed_distance_example():
+    """The fixed-distance rule of LMS (Section 2) on the same sequence, worked out by hand."""
+    g = parse_golden()["fixed"]
+    b, k, f = golden_case()
+    out = S.build(b, k, f, budget=24, window=0, chunk=1, policy="C", ahead=g["ahead"],
+                  threshold=g["threshold"])
+    assert out["windows"] == g["windows"]
+    assert out["ops"] == g["ops"]
+    assert out["held"] == g["held"]
+    assert (out["peak"], out["h2d"], out["d2h"]) == (g["peak"], g["h2d"], g["d2h"])
+    check.replay(b, k, f, out["ops"], 24, policy="C", held=out["held"])
+
+
+@pytest.mark.parametrize("policy", ["C", "L"])
+def test_fixed_distance_schedules_replay(policy):
+    """Random registrations, every ahead up to 4 with a random threshold: the replayer accepts
+    every schedule that fits (variables kept by the threshold are not waited for, so, as with
+    LMS itself, a tight budget can be infeasible); a zero-ahead, zero-threshold schedule swaps
+    exactly like the zero byte window."""
+    rng = random.Random(11)
+    built = failed = 0
+    for _ in range(120):
+        b, k, f = random_registration(rng)
+        bud = S.working_set_max(b, f, 1) + rng.randint(0, 120)
+        for ahead in range(5):
+            thr = rng.randint(0, 4)
+            try:
+                out = S.build(b, k, f, budget=bud, window=0, chunk=1, policy=policy, ahead=ahead,
+                              threshold=thr)
+            except S.Infeasible:
+                failed += 1
+                continue
+            built += 1
+            check.replay(b, k, f, out["ops"], bud, policy=policy, held=out["held"])
+        z = S.build(b, k, f, budget=bud, window=0, chunk=1, policy=policy, ahead=0, threshold=0)
+        w0 = S.build(b, k, f, budget=bud, window=0, chunk=1, policy=policy)
+        assert z["ops"] == w0["ops"]
+    assert built > 2 * failed
+
+
+def test_fixed_distance_needs_both_parameters():
+    b, k, f = golden_case()
+    for kw in ({"ahead": 1}, {"threshold": 1}, {"ahead": -1, "threshold": 0}):
+        with pytest.raises(S.Invalid):
+            S.build(b, k, f, budget=24, window=0, **kw)
 
 
 # ---------------------------------------------------------------- registrations
