@@ -124,7 +124,7 @@ def measured_traffic(net, op):
 MAP_ENTRY_LIMIT = 40000   # chunks + mappings per plan; the process table holds ~65530
 
 
-def plan_for(net, frac, window_frac, chunk):
+def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None):
     """Budget, window and (chunks, mappings) of the out-of-core and in-core plans."""
     ctx = ooc.Context(-1)
     try:
@@ -144,6 +144,9 @@ def plan_for(net, frac, window_frac, chunk):
             ctx.set_budget(b)
             if w is not None:
                 ctx.set_window(w)
+                ctx.set_policy(policy)
+                if fixed is not None:
+                    ctx.set_fixed_distance(*fixed)
             ctx.build_schedule()
             counts.append(sum(ctx.plan_counts()))
         finally:
@@ -152,20 +155,24 @@ def plan_for(net, frac, window_frac, chunk):
             "map_entries": max(counts)}
 
 
-def choose_chunk(net, frac, window_frac):
+def choose_chunk(net, frac, window_frac, policy="C", fixed=None):
     """Smallest chunk (2 MiB .. 256 MiB) whose plans fit the memory-map table: the
     trade-off of Section 4 between mapping overhead and internal fragmentation."""
     for mib in (2, 4, 8, 16, 32, 64, 128, 256):
-        plan = plan_for(net, frac, window_frac, mib << 20)
+        plan = plan_for(net, frac, window_frac, mib << 20, policy, fixed)
         if plan["map_entries"] <= MAP_ENTRY_LIMIT:
             return mib << 20, plan
     return 256 << 20, plan
 
 
-def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup, depth=None):
+def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup, depth=None,
+             policy="C", fixed=None):
     ctx = ooc.Context(0)
     try:
         net.register(ctx)
+        ctx.set_policy(policy)
+        if fixed is not None and budget != ooc.UNLIMITED:
+            ctx.set_fixed_distance(*fixed)
         if depth is not None:
             ctx.set_swapout_depth(depth)
         ctx.set_chunk(chunk)
@@ -264,6 +271,13 @@ def main():
     ap.add_argument("--no-incore", action="store_true")
     ap.add_argument("--swapout-depth", type=int, default=None,
                     help="swap-outs in flight (library default when omitted; 0 = unbounded)")
+    ap.add_argument("--scheduler", default="adaptive", choices=("adaptive", "naive", "lms"),
+                    help="adaptive: the schedule-window algorithm with W = window-frac * B and "
+                         "cancelled swap-outs; naive: swap every variable in right before and "
+                         "out right after each use (W = 0, literal policy); lms: the "
+                         "fixed-distance rule with --swapin-ahead / --swapout-threshold")
+    ap.add_argument("--swapin-ahead", type=int, default=1, help="functions (lms)")
+    ap.add_argument("--swapout-threshold", type=int, default=1, help="functions (lms)")
     ap.add_argument("--timeline", default="",
                     help="write the last out-of-core step's kernel and copy spans (JSON) here")
     args = ap.parse_args()
@@ -275,10 +289,20 @@ def main():
     spec = synth.workload(args.workload, **({"batch": args.batch} if args.batch else {}))
     net = netdef.Net(spec)
     frac = args.budget_frac if args.budget_frac is not None else synth.budget_fraction(args.workload)
-    if args.chunk:
-        chunk, plan = args.chunk, plan_for(net, frac, args.window_frac, args.chunk)
-    else:
-        chunk, plan = choose_chunk(net, frac, args.window_frac)
+    policy = "L" if args.scheduler == "naive" else "C"
+    window_frac = args.window_frac if args.scheduler == "adaptive" else 0.0
+    fixed = (args.swapin_ahead, args.swapout_threshold) if args.scheduler == "lms" else None
+    try:
+        if args.chunk:
+            chunk, plan = args.chunk, plan_for(net, frac, window_frac, args.chunk, policy, fixed)
+        else:
+            chunk, plan = choose_chunk(net, frac, window_frac, policy, fixed)
+    except ooc.OocError as e:
+        if e.status != ooc.E_INFEASIBLE:
+            raise
+        print(json.dumps({"error": "infeasible", "scheduler": args.scheduler,
+                          "detail": str(e)}))
+        sys.exit(3)
     p_incore, budget, window = plan["p_incore"], plan["budget"], plan["window"]
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
@@ -290,7 +314,7 @@ def main():
         inc = run_mode(net, spec, x, labels, params, ooc.UNLIMITED, None, chunk, args.steps,
                        args.warmup)
     out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps, args.warmup,
-                   args.swapout_depth)
+                   args.swapout_depth, policy, fixed)
     if args.timeline:
         with open(args.timeline, "w") as fh:
             json.dump({"fns": net.fn_ops, "vars": net.names,
@@ -345,7 +369,9 @@ def main():
                    "budget_frac_of_incore_peak": round(budget / p_incore, 4),
                    "incore_peak_bytes": p_incore, "window_bytes": window, "chunk_bytes": chunk,
                    "map_entries": plan["map_entries"],
-                   "policy": "cancel",
+                   "scheduler": args.scheduler,
+                   **({"swapin_ahead": fixed[0], "swapout_threshold": fixed[1]} if fixed else {}),
+                   "policy": "cancel" if policy == "C" else "literal",
                    "swapout_depth": "library default" if args.swapout_depth is None
                    else args.swapout_depth},
         "roofline": roof,
@@ -369,6 +395,7 @@ def main():
                                               st["d2h_bytes"] / link["d2h"],
                                               moved / link["both"]) / 1e6, 2),
             "ceiling": ceiling,
+            "pinned_arena_bytes": st["host_bytes"],
         },
         "peak_device_bytes": {"pool": st["pool_bytes"], "max_chunks_in_use_bytes":
                               st["max_chunks_used"] * chunk, "peak_accounted": st["peak_accounted"],

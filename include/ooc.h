@@ -266,6 +266,18 @@ ooc_status ooc_set_window(ooc_ctx *ctx, uint64_t bytes);
  * allocation granularity once prepared; default 2 MiB. */
 ooc_status ooc_set_chunk(ooc_ctx *ctx, uint64_t bytes);
 
+/* Fixed-distance scheduling rule of LMS as Section 2 describes it, in place
+ * of the byte window: a variable is swapped in when it comes within
+ * `swapin_ahead` functions of its next use, and after a use it is kept on the
+ * device when its next use is at most `swapout_threshold` functions away,
+ * otherwise swapped out (the text prints this test as "<= threshold"; it is
+ * read as "> threshold", which keeps the variables needed soon).  Budget waits
+ * and policies are those of the adaptive scheduler.  Variables kept by the
+ * threshold are not waited for, so a tight budget can be infeasible, as with
+ * LMS.  Both -1 (default) selects the schedule-window rule; otherwise both
+ * must be >= 0.  Baseline for comparisons. */
+ooc_status ooc_set_fixed_distance(ooc_ctx *ctx, int64_t swapin_ahead, int64_t swapout_threshold);
+
 /* OOC_POLICY_CANCEL (default) or OOC_POLICY_LITERAL. */
 ooc_status ooc_set_policy(ooc_ctx *ctx, int32_t policy);
 

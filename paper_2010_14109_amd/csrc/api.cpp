@@ -157,6 +157,18 @@ ooc_status ooc_set_swapout_depth(ooc_ctx* ctx, int64_t depth) {
   return OOC_OK;
 }
 
+ooc_status ooc_set_fixed_distance(ooc_ctx* ctx, int64_t swapin_ahead, int64_t swapout_threshold) {
+  REQUIRE_CTX(ctx);
+  REQUIRE_STAGE(ctx, REGISTERING, "ooc_set_fixed_distance");
+  const bool off = swapin_ahead == -1 && swapout_threshold == -1;
+  if (!off && (swapin_ahead < 0 || swapout_threshold < 0))
+    return fail(ctx, OOC_E_INVALID, "swapin_ahead and swapout_threshold must both be >= 0, "
+                                    "or both -1");
+  ctx->ahead = swapin_ahead;
+  ctx->threshold = swapout_threshold;
+  return OOC_OK;
+}
+
 ooc_status ooc_build_schedule(ooc_ctx* ctx) {
   REQUIRE_CTX(ctx);
   REQUIRE_STAGE(ctx, REGISTERING, "ooc_build_schedule");
@@ -169,7 +181,7 @@ ooc_status ooc_build_schedule(ooc_ctx* ctx) {
     const uint64_t window = ctx->window_set ? ctx->window : ctx->budget / 2;
     std::string err;
     ooc_status st = build_schedule(ctx->vars, ctx->fns, ctx->budget, window, ctx->chunk,
-                                   ctx->policy, &s, &err);
+                                   ctx->policy, &s, &err, ctx->ahead, ctx->threshold);
     if (st) return fail(ctx, st, err);
   }
   ctx->sched = std::move(s);

@@ -48,6 +48,7 @@ struct ooc_ctx {
 
   uint64_t budget = OOC_UNLIMITED;
   uint64_t window = 0;
+  int64_t ahead = -1, threshold = -1;     // fixed-distance rule when ahead >= 0
   bool window_set = false;
   uint64_t chunk = 2ull << 20;
   int32_t policy = OOC_POLICY_CANCEL;

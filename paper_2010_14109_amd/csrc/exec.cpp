@@ -27,6 +27,8 @@
 #include <chrono>
 #include <cstdio>
 #include <cstring>
+#include <functional>
+#include <queue>
 #include <set>
 
 #include "ctx.h"
@@ -333,26 +335,111 @@ ooc_status prepare(ooc_ctx* ctx) {
     if (s) return s;
   }
 
-  // pinned host arena: every persistent variable, and every TEMP the step
-  // program actually copies out (cancelled and clean swap-outs need no slot)
+  // pinned host arena.  A persistent variable (INPUT, PARAM, STATE, OUTPUT)
+  // owns its slot for the whole step: the caller reads and writes it there.
+  // A TEMP needs host memory only from its first swap-out to its last
+  // swap-in, so TEMP slots are packed by lifetime: best fit over the holes
+  // left by TEMPs whose last swap-in was issued before.  The first swap-out
+  // into reused bytes waits for the last swap-in of every earlier occupant of
+  // those bytes; the variable's later swap-outs follow it on the same stream.
   const int64_t nv = (int64_t)ctx->vars.size();
   std::vector<uint8_t> backed(nv, 0);
-  for (int64_t v = 0; v < nv; ++v) backed[v] = ctx->vars[v].kind != OOC_TEMP;
-  for (const FnProgram& fp : ctx->prog)
-    for (const Copy& c : fp.d2h) backed[c.var] = 1;
-  for (const FnProgram& fp : ctx->prog)
-    for (const Copy& c : fp.h2d)
-      if (!backed[c.var]) {
-        ctx->err = "swap-in of variable " + std::to_string(c.var) + " with no host copy";
-        return OOC_E_INVALID;
-      }
-  uint64_t hb = 0;
   std::vector<uint64_t> hoff(nv, 0);
+  uint64_t hb = 0;
   for (int64_t v = 0; v < nv; ++v)
-    if (backed[v]) {
+    if (ctx->vars[v].kind != OOC_TEMP) {
+      backed[v] = 1;
       hoff[v] = hb;
       hb += round_up(ctx->vars[v].bytes, kSlotAlign);
     }
+  const uint64_t pers = hb;
+  // lifetimes in issue order: swap-ins of f_i at 3 i, swap-outs at 3 i + 2
+  std::vector<int64_t> born(nv, -1), dies(nv, -1);
+  std::vector<int32_t> last_in(nv, -1);
+  std::vector<Copy*> first_out(nv, nullptr);
+  for (size_t i = 0; i < ctx->prog.size(); ++i) {
+    for (Copy& c : ctx->prog[i].h2d) {
+      if (backed[c.var]) continue;
+      if (born[c.var] < 0) {
+        ctx->err = "swap-in of variable " + std::to_string(c.var) + " with no host copy";
+        return OOC_E_INVALID;
+      }
+      dies[c.var] = std::max<int64_t>(dies[c.var], 3 * (int64_t)i);
+      last_in[c.var] = c.ev_done;
+    }
+    for (Copy& c : ctx->prog[i].d2h) {
+      if (backed[c.var]) continue;
+      if (born[c.var] < 0) {
+        born[c.var] = 3 * (int64_t)i + 2;
+        first_out[c.var] = &c;
+      }
+      dies[c.var] = std::max<int64_t>(dies[c.var], 3 * (int64_t)i + 2);
+    }
+  }
+  std::vector<int64_t> order;
+  for (int64_t v = 0; v < nv; ++v)
+    if (born[v] >= 0) order.push_back(v);
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int64_t x, int64_t y) { return born[x] < born[y]; });
+  struct Span { uint64_t off, size; };
+  struct Freed { uint64_t off, size; int32_t ev; };
+  std::vector<Span> holes;     // sorted by offset, disjoint, not adjacent
+  std::vector<Freed> freed;    // released occupants whose last swap-in later copies wait for
+  std::priority_queue<std::pair<int64_t, int64_t>, std::vector<std::pair<int64_t, int64_t>>,
+                      std::greater<>> live;   // (dies, var)
+  uint64_t top = 0;
+  auto release = [&](int64_t u) {
+    const uint64_t off = hoff[u] - pers, size = round_up(ctx->vars[u].bytes, kSlotAlign);
+    if (last_in[u] >= 0) freed.push_back(Freed{off, size, last_in[u]});
+    auto it = std::lower_bound(holes.begin(), holes.end(), off,
+                               [](const Span& h, uint64_t o) { return h.off < o; });
+    it = holes.insert(it, Span{off, size});
+    if (it + 1 != holes.end() && it->off + it->size == (it + 1)->off) {
+      it->size += (it + 1)->size;
+      holes.erase(it + 1);
+    }
+    if (it != holes.begin() && (it - 1)->off + (it - 1)->size == it->off) {
+      (it - 1)->size += it->size;
+      holes.erase(it);
+    }
+  };
+  for (int64_t v : order) {
+    while (!live.empty() && live.top().first < born[v]) {
+      release(live.top().second);
+      live.pop();
+    }
+    const uint64_t size = round_up(ctx->vars[v].bytes, kSlotAlign);
+    size_t best = holes.size();
+    for (size_t h = 0; h < holes.size(); ++h)
+      if (holes[h].size >= size && (best == holes.size() || holes[h].size < holes[best].size))
+        best = h;
+    uint64_t off;
+    if (best < holes.size()) {
+      off = holes[best].off;
+      holes[best].off += size;
+      holes[best].size -= size;
+      if (holes[best].size == 0) holes.erase(holes.begin() + best);
+    } else {
+      off = top;
+      top += size;
+    }
+    backed[v] = 1;
+    hoff[v] = pers + off;
+    std::vector<int32_t>& w = first_out[v]->waits;
+    for (size_t f = 0; f < freed.size();) {
+      const Freed& fr = freed[f];
+      if (fr.off < off + size && off < fr.off + fr.size) {
+        if (std::find(w.begin(), w.end(), fr.ev) == w.end()) w.push_back(fr.ev);
+        if (fr.off >= off && fr.off + fr.size <= off + size) {
+          freed.erase(freed.begin() + f);
+          continue;
+        }
+      }
+      ++f;
+    }
+    live.push({dies[v], v});
+  }
+  hb = pers + top;
   ctx->host_slot.assign(nv, nullptr);
   if (hb > 0) {
     hipError_t e = hipHostMalloc((void**)&ctx->arena, hb, hipHostMallocDefault);

@@ -31,16 +31,20 @@ static bool persistent(int32_t kind) {
 
 ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& fns,
                           uint64_t budget, uint64_t window, uint64_t chunk, int policy,
-                          Schedule* out, std::string* err) {
+                          Schedule* out, std::string* err, int64_t ahead, int64_t threshold) {
+  const bool fixed = ahead >= 0;
   const int64_t N = (int64_t)fns.size();
   const int64_t nv = (int64_t)vars.size();
   std::vector<uint64_t> a(nv);
   for (int64_t v = 0; v < nv; ++v) a[v] = round_up(vars[v].bytes, chunk);
 
-  std::vector<int64_t> seq, first(N), last(N);
+  std::vector<int64_t> seq, first(N), last(N), fn_of;
   for (int64_t i = 0; i < N; ++i) {
     first[i] = (int64_t)seq.size();
-    for (const FnVar& fv : fns[i].vars) seq.push_back(fv.var);
+    for (const FnVar& fv : fns[i].vars) {
+      seq.push_back(fv.var);
+      fn_of.push_back(i);
+    }
     last[i] = (int64_t)seq.size() - 1;
   }
   const int64_t M = (int64_t)seq.size();
@@ -84,8 +88,12 @@ ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& f
   int64_t r_prev = -1, r_hat = -1;
   for (int64_t i = 0; i < N; ++i) {
     const int64_t l = first[i], e = last[i];
-    if (r_hat < l - 1) r_hat = l - 1;
-    while (r_hat + 1 < M && pre[r_hat + 2] - pre[l] <= window) ++r_hat;
+    if (fixed) {
+      r_hat = last[std::min(i + ahead, N - 1)];
+    } else {
+      if (r_hat < l - 1) r_hat = l - 1;
+      while (r_hat + 1 < M && pre[r_hat + 2] - pre[l] <= window) ++r_hat;
+    }
     int64_t r = std::max(std::max(r_hat, e), r_prev);
 
     for (int64_t p = r_prev + 1; p <= r; ++p) {
@@ -130,8 +138,8 @@ ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& f
         state[u] = UNMAT;
         held -= a[u];
         emit((int32_t)i, OOC_POST, OOC_FREE, u);
-      } else if (n >= 0 && n <= r) {
-        // already reserved inside the window: keep it on the device
+      } else if (n >= 0 && (n <= r || (fixed && fn_of[n] - i <= threshold))) {
+        // already reserved inside the window (or close enough): keep it on the device
       } else {
         state[u] = PEND;
         entry_of[u] = (int64_t)fifo.size();

@@ -162,6 +162,63 @@ def test_random_sequences_match_oracle(lib):
         ctx.close()
 
 
+def test_fixed_distance_matches_oracle(lib):
+    """The fixed-distance (LMS) rule: random registrations and the small networks, schedules
+    and chunk plans op for op, infeasible budgets reported on both sides."""
+    rng = random.Random(77)
+    cases = []
+    for _ in range(200):
+        b, k, f = random_registration(rng, nv=rng.randint(1, 12), nf=rng.randint(1, 20))
+        chunk = rng.choice([1, 8, 32])
+        ws = S.working_set_max(b, f, chunk)
+        cases.append((b, k, f, chunk, rng.choice([ws, ws + chunk, 2 * ws, 10 ** 6])))
+    for spec in specs_small():
+        b, k, f = as_schedule_input(lower(spec))
+        p = S.incore_peak(b, k, f, 4096)
+        ws = S.working_set_max(b, f, 4096)
+        for frac in (0.5, 0.25):
+            cases.append((b, k, f, 4096, max(S.budget_for(frac, p, 4096), ws)))
+    n_inf = 0
+    for trial, (b, k, f, chunk, B) in enumerate(cases):
+        ahead, thr = rng.randint(0, 6), rng.randint(0, 6)
+        policy = rng.choice("CL")
+        ctx = ooc.Context(-1)
+        for nb, kd in zip(b, k):
+            ctx.add_var(nb, kd)
+        for vs in f:
+            ctx.add_fn("noop", [v for v, _ in vs], [a for _, a in vs])
+        ctx.set_chunk(chunk)
+        ctx.set_budget(B)
+        ctx.set_policy(policy)
+        ctx.set_fixed_distance(ahead, thr)
+        try:
+            ref = S.build(b, k, f, B, 0, chunk, policy, ahead=ahead, threshold=thr)
+        except S.Infeasible:
+            n_inf += 1
+            with pytest.raises(ooc.OocError) as e:
+                ctx.build_schedule()
+            assert e.value.status == ooc.E_INFEASIBLE
+            ctx.close()
+            continue
+        ctx.build_schedule()
+        ops, held = ctx.schedule()
+        assert ops == ref["ops"], trial
+        assert held == ref["held"], trial
+        assert ctx.windows() == ref["windows"], trial
+        ivs, _ = opool.assign(ref["ops"], b, B // chunk, chunk)
+        assert [(g["var"], g["open"], g["close"], g["chunks"]) for g in ctx.plan()] == \
+            [(i["var"], i["open"], i["close"], i["chunks"]) for i in ivs]
+        ctx.close()
+    assert n_inf < len(cases) // 2
+    ctx = ooc.Context(-1)
+    for bad in ((1, -1), (-1, 2), (-2, -2)):
+        with pytest.raises(ooc.OocError) as e:
+            ctx.set_fixed_distance(*bad)
+        assert e.value.status == ooc.E_INVALID
+    ctx.set_fixed_distance(-1, -1)
+    ctx.close()
+
+
 def test_infeasible_budget_reports_error(lib):
     spec = specs_small()[0]
     net = netdef.Net(spec)

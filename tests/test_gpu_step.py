@@ -203,3 +203,50 @@ def test_swap_integrity_random_sequences(seed):
                         assert np.array_equal(ctx.host_view(v, "u32"), init[v])
             finally:
                 ctx.close()
+
+
+def test_host_slots_are_reused_without_corruption():
+    """Temporaries that are swapped out and back in one after another share pinned host slots
+    (a slot is reused once its last swap-in was issued); the values that flow through the
+    reused slots still match the integer reference word for word, with and without prefetch."""
+    n = 8
+    words = [1000, 1000] + [3000] * n + [6000]        # IN, OUT, T_0..T_{n-1}, FILL
+    kinds = [ooc.INPUT, ooc.OUTPUT] + [ooc.TEMP] * n + [ooc.TEMP]
+    IN, OUT, FILL = 0, 1, n + 2
+    fns = [([IN, OUT], [ooc.R, ooc.W], 7)]
+    for k in range(n):
+        fns.append(([IN, 2 + k], [ooc.R, ooc.W], 100 + k))              # produce T_k
+        fns.append(([IN, FILL], [ooc.R, ooc.W], 200 + k))               # pushes T_k out
+        if k:
+            fns.append(([2 + k - 1, OUT], [ooc.R, ooc.RW], 300 + k))    # consume T_{k-1}
+    fns.append(([2 + n - 1, OUT], [ooc.R, ooc.RW], 999))
+    rng = np.random.default_rng(5)
+    init = {IN: rng.integers(0, 2 ** 32, words[IN], dtype=np.uint64).astype(np.uint32)}
+    ref = mixop.run(words, kinds, fns, init)
+    chunk = 4096
+    b = [4 * w for w in words]
+    fv = [[(v, a) for v, a in zip(vs, acc)] for vs, acc, _ in fns]
+    ws = S.working_set_max(b, fv, chunk)
+    temp_bytes = sum(b[2:2 + n])
+    for policy in ("C", "L"):
+        for W in (0, 3 * ws):
+            print(f"slot reuse policy {policy} window {W}", flush=True)
+            ctx = ooc.Context(0)
+            try:
+                for w, kd in zip(words, kinds):
+                    ctx.add_var(4 * w, kd)
+                for vs, acc, sd in fns:
+                    ctx.add_fn("mix", vs, acc, [sd])
+                ctx.set_chunk(chunk)
+                ctx.set_budget(ws + chunk)
+                ctx.set_window(W)
+                ctx.set_policy(policy)
+                ctx.build_schedule()
+                ctx.prepare()
+                ctx.host_view(IN, "u32")[...] = init[IN]
+                for _ in range(2):
+                    ctx.step(0.0, 0.0)
+                    assert np.array_equal(ctx.host_view(OUT, "u32"), ref[OUT]), (policy, W)
+                assert ctx.stats()["host_bytes"] < temp_bytes
+            finally:
+                ctx.close()
