@@ -95,3 +95,80 @@ def assign(ops, var_bytes, n_chunks, chunk):
     for iv in intervals:
         del iv["rid"]
     return intervals, max_used
+
+
+def best_fit(ops, var_bytes, align=256, placements=None):
+    """Replay a schedule's device copies through one contiguous best-fit heap.
+
+    The comparison point of Section 4: an allocator that hands out contiguous
+    address ranges (as a caching allocator on top of one device allocation
+    does) suffers external fragmentation, so the address range it needs can
+    exceed the bytes live at any moment.  Each residency interval (the same
+    copies as ``assign``: SWAPIN / ALLOC open one, FREE closes the working
+    copy, WAIT_OUT the oldest pending one, CANCEL makes a pending copy the
+    working one again) asks for its size rounded up to ``align``.  A request
+    takes the smallest free hole that holds it (lowest address on ties); when
+    no hole does, it goes to the end of the heap, starting inside the free tail
+    if there is one.  Returns ``(extent, peak_live)``: the highest address ever
+    used and the most bytes live at once.  ``placements``, if a list, receives
+    ``(op index, offset, size)`` per request and ``(op index, None, size)`` per
+    release.
+    """
+    holes = []                 # [offset, size], sorted by offset, disjoint, not adjacent
+    heap_end = 0
+    live = peak = 0
+    blocks = {}                # interval id -> (offset, size, var)
+    working, pending = {}, deque()
+
+    def alloc(size):
+        nonlocal heap_end
+        fit = [h for h in holes if h[1] >= size]
+        if fit:
+            h = min(fit, key=lambda x: (x[1], x[0]))
+            off = h[0]
+            h[0] += size
+            h[1] -= size
+            if h[1] == 0:
+                holes.remove(h)
+            return off
+        if holes and holes[-1][0] + holes[-1][1] == heap_end:
+            off = holes.pop()[0]
+        else:
+            off = heap_end
+        heap_end = off + size
+        return off
+
+    def release(off, size):
+        holes.append([off, size])
+        holes.sort()
+        merged = []
+        for h in holes:
+            if merged and merged[-1][0] + merged[-1][1] == h[0]:
+                merged[-1][1] += h[1]
+            else:
+                merged.append(h)
+        holes[:] = merged
+
+    for k, (_, _, kind, u) in enumerate(ops):
+        if kind in (SWAPIN, ALLOC):
+            size = -(-var_bytes[u] // align) * align
+            blocks[k] = (alloc(size), size, u)
+            if placements is not None:
+                placements.append((k, blocks[k][0], size))
+            working[u] = k
+            live += size
+            peak = max(peak, live)
+        elif kind == SWAPOUT:
+            pending.append(working.pop(u))
+        elif kind == CANCEL:
+            j = next(j for j in pending if blocks[j][2] == u)
+            pending.remove(j)
+            working[u] = j
+        elif kind in (WAIT_OUT, FREE):
+            j = pending.popleft() if kind == WAIT_OUT else working.pop(u)
+            off, size, _ = blocks.pop(j)
+            release(off, size)
+            if placements is not None:
+                placements.append((k, None, off))
+            live -= size
+    return heap_end, peak

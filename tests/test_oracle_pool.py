@@ -1,4 +1,5 @@
-"""Pins of the oracle VA pool (Section 4): eq. 1, eq. 2, no external fragmentation."""
+"""Pins of the oracle VA pool (Section 4): eq. 1, eq. 2, no external fragmentation; and of the
+contiguous best-fit heap it is compared with."""
 
 import random
 
@@ -74,3 +75,81 @@ def test_schedule_assignment_fits_budget(policy):
                     owner[c] = j
                 else:
                     assert owner.pop(c) == j
+
+
+# ---------------------------------------------------------------- best-fit comparison heap
+def test_best_fit_hand_example():
+    """A = B = 4, C = 8 bytes: after A is freed its 4-byte hole cannot take C, so C goes above B
+    (extent 16 although at most 12 bytes are live); the next 4-byte request takes the smallest
+    hole that fits."""
+    ops = [(0, 0, S.ALLOC, 0), (0, 0, S.ALLOC, 1), (0, 1, S.FREE, 0), (1, 0, S.ALLOC, 2),
+           (1, 1, S.FREE, 1), (2, 0, S.ALLOC, 0)]
+    trace = []
+    assert P.best_fit(ops, [4, 4, 8], 1, trace) == (16, 12)
+    assert [t for t in trace if t[1] is not None] == [(0, 0, 4), (1, 4, 4), (3, 8, 8), (5, 0, 4)]
+
+
+def _check_best_fit(ops, sizes, align):
+    """Brute force: recompute the free intervals from the live blocks at every request and check
+    the placement against the best-fit rule; blocks never overlap; extent >= peak live."""
+    trace = []
+    extent, peak = P.best_fit(ops, sizes, align, trace)
+    live = {}                      # offset -> size
+    end = 0
+    peak_seen = 0
+    for k, off, size in trace:
+        if off is None:
+            del live[size]         # release: the third field holds the block's offset
+            continue
+        spans = sorted(live.items())
+        free, cur = [], 0
+        for o, sz in spans:
+            if o > cur:
+                free.append((cur, o - cur))
+            cur = max(cur, o + sz)
+        if cur < end:
+            free.append((cur, end - cur))      # the free tail is a hole like any other
+        fits = [f for f in free if f[1] >= size]
+        if fits:
+            assert off == min(fits, key=lambda f: (f[1], f[0]))[0]
+        else:
+            tail = cur if cur < end else end
+            assert off == tail
+        for o, sz in spans:
+            assert off + size <= o or o + sz <= off
+        live[off] = size
+        end = max(end, off + size)
+        peak_seen = max(peak_seen, sum(live.values()))
+    assert extent == end and peak == peak_seen and extent >= peak
+    return extent, peak
+
+
+@pytest.mark.parametrize("policy", ["C", "L"])
+def test_best_fit_replays_network_schedules(policy):
+    for spec in (synth.mlp(batch=4, width=16, depth=4, classes=5),
+                 synth.resnet(batch=2, hw=32, classes=7, blocks=(1, 2, 1, 1), width=4)):
+        b, k, f = as_schedule_input(lower(spec))
+        p = S.incore_peak(b, k, f, 1)
+        ws = S.working_set_max(b, f, 1)
+        for frac in (0.6, 0.3):
+            out = S.build(b, k, f, max(S.budget_for(frac, p, 1), ws), 0, 1, policy)
+            _check_best_fit(out["ops"], b, 256)
+
+
+def test_best_fit_equal_sizes_do_not_fragment():
+    rng = random.Random(3)
+    for _ in range(50):
+        n = rng.randint(2, 12)
+        kinds = [S.TEMP] * n
+        fns = []
+        produced = [False] * n
+        for _ in range(rng.randint(3, 20)):
+            vs = rng.sample(range(n), rng.randint(1, min(3, n)))
+            fns.append([(v, S.RW if produced[v] else S.W) for v in vs])
+            for v in vs:
+                produced[v] = True
+        sizes = [512] * n
+        ws = S.working_set_max(sizes, fns, 1)
+        out = S.build(sizes, kinds, fns, ws + rng.randint(0, 3) * 512, 0, 1, rng.choice("CL"))
+        extent, peak = _check_best_fit(out["ops"], sizes, 256)
+        assert extent == peak
