@@ -311,6 +311,18 @@ ooc_status ooc_working_set_max(const ooc_ctx *ctx, uint64_t *bytes);
  * concatenated chunk ids they map (lowest free chunk ids first).  Valid
  * after build_schedule; host only. */
 ooc_status ooc_plan_intervals(const ooc_ctx *ctx, ooc_interval *buf, uint64_t cap, uint64_t *n);
+
+/* The comparison of Section 4 (host only, after build_schedule): the same
+ * residency intervals served by one contiguous best-fit heap instead of the
+ * chunk pool.  Each request is the variable's size rounded up to `align` (a
+ * power of two); it takes the smallest free hole that holds it (lowest
+ * address on ties), else the end of the heap, starting in the free tail.
+ * *extent receives the highest address used (the device bytes such a heap
+ * needs), *peak_live the most bytes live at once; extent - peak_live is the
+ * external fragmentation the chunk pool avoids.  OOC_E_STATE before
+ * build_schedule, OOC_E_INVALID for a bad alignment. */
+ooc_status ooc_bestfit_extent(const ooc_ctx *ctx, uint64_t align, uint64_t *extent,
+                              uint64_t *peak_live);
 ooc_status ooc_plan_chunks(const ooc_ctx *ctx, int32_t *buf, uint64_t cap, uint64_t *n);
 
 /* Creates the physical chunks, maps every interval's chunks into its own

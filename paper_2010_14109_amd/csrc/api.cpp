@@ -236,6 +236,15 @@ ooc_status ooc_working_set_max(const ooc_ctx* ctx, uint64_t* bytes) {
   return OOC_OK;
 }
 
+ooc_status ooc_bestfit_extent(const ooc_ctx* ctx, uint64_t align, uint64_t* extent,
+                              uint64_t* peak_live) {
+  REQUIRE_CTX(ctx);
+  if (ctx->stage < BUILT || !extent || !peak_live) return OOC_E_STATE;
+  if (align == 0 || (align & (align - 1))) return OOC_E_INVALID;
+  bestfit_extent(ctx->vars, ctx->plan, align, extent, peak_live);
+  return OOC_OK;
+}
+
 ooc_status ooc_plan_intervals(const ooc_ctx* ctx, ooc_interval* buf, uint64_t cap, uint64_t* n) {
   REQUIRE_CTX(ctx);
   if (ctx->stage < BUILT || !n) return OOC_E_STATE;

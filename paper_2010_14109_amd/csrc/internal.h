@@ -57,6 +57,10 @@ struct Plan {
   uint64_t n_chunks = 0;              // chunks the pool must own
 };
 
+// The plan's intervals served by one contiguous best-fit heap (the allocator
+// the chunk pool is compared with): highest address used and peak live bytes.
+void bestfit_extent(const std::vector<Var>& vars, const Plan& plan, uint64_t align,
+                    uint64_t* extent, uint64_t* peak_live);
 // Scheduler (Section 3, Fig. 2).  Returns OOC_OK, OOC_E_INFEASIBLE.  With
 // ahead >= 0 the fixed-distance rule of LMS (Section 2) replaces the byte
 // window: the window ends with f_{i+ahead} and a variable whose next use is

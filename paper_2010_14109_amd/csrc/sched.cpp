@@ -19,7 +19,9 @@
 // (eq. 1), so the chunks the pool maps never exceed the budget.
 #include <algorithm>
 #include <functional>
+#include <map>
 #include <queue>
+#include <set>
 
 #include "internal.h"
 
@@ -298,6 +300,80 @@ void build_plan(const std::vector<Var>& vars, const Schedule& s, bool incore, ui
   plan.max_chunks_used = cache.max_in_use;
   plan.n_chunks = cache.max_in_use;
   *out = std::move(plan);
+}
+
+// The comparison point of Section 4: the plan's residency intervals served by
+// one contiguous best-fit heap instead of the chunk pool.  A request (size
+// rounded up to `align`) takes the smallest free hole that holds it, lowest
+// address on ties; when none does it goes to the end of the heap, starting in
+// the free tail if there is one.  Returns the highest address used and the
+// most bytes live at once.
+void bestfit_extent(const std::vector<Var>& vars, const Plan& plan, uint64_t align,
+                    uint64_t* extent, uint64_t* peak_live) {
+  std::map<uint64_t, uint64_t> by_off;             // hole offset -> size
+  std::set<std::pair<uint64_t, uint64_t>> by_size; // (size, offset)
+  uint64_t end = 0, live = 0, peak = 0;
+  std::vector<uint64_t> off(plan.intervals.size(), 0), size(plan.intervals.size(), 0);
+  auto erase_hole = [&](std::map<uint64_t, uint64_t>::iterator it) {
+    by_size.erase({it->second, it->first});
+    return by_off.erase(it);
+  };
+  auto alloc = [&](int64_t id) {
+    const uint64_t sz = round_up(vars[plan.intervals[id].var].bytes, align);
+    auto f = by_size.lower_bound({sz, 0});
+    uint64_t o;
+    if (f != by_size.end()) {
+      o = f->second;
+      const uint64_t hs = f->first;
+      erase_hole(by_off.find(o));
+      if (hs > sz) {
+        by_off[o + sz] = hs - sz;
+        by_size.insert({hs - sz, o + sz});
+      }
+    } else {
+      auto last = by_off.empty() ? by_off.end() : std::prev(by_off.end());
+      if (last != by_off.end() && last->first + last->second == end) {
+        o = last->first;
+        erase_hole(last);
+      } else {
+        o = end;
+      }
+      end = o + sz;
+    }
+    off[id] = o;
+    size[id] = sz;
+    live += sz;
+    peak = std::max(peak, live);
+  };
+  auto release = [&](int64_t id) {
+    uint64_t o = off[id], sz = size[id];
+    live -= sz;
+    auto nx = by_off.lower_bound(o);
+    if (nx != by_off.end() && o + sz == nx->first) {
+      sz += nx->second;
+      nx = erase_hole(nx);
+    }
+    if (nx != by_off.begin()) {
+      auto pv = std::prev(nx);
+      if (pv->first + pv->second == o) {
+        o = pv->first;
+        sz += pv->second;
+        erase_hole(pv);
+      }
+    }
+    by_off[o] = sz;
+    by_size.insert({sz, o});
+  };
+  for (int64_t id = 0; id < (int64_t)plan.intervals.size(); ++id)
+    if (plan.intervals[id].open < 0) alloc(id);
+  for (int64_t k = 0; k < (int64_t)plan.op_interval.size(); ++k) {
+    const int64_t id = plan.op_interval[k];
+    if (id < 0) continue;
+    if (plan.intervals[id].open == k) alloc(id);
+    else if (plan.intervals[id].close == k) release(id);
+  }
+  *extent = end;
+  *peak_live = peak;
 }
 
 }  // namespace ooc

@@ -40,7 +40,7 @@ EXPORTS = [
     "ooc_schedule_get", "ooc_schedule_windows", "ooc_incore_peak", "ooc_working_set_max",
     "ooc_plan_intervals", "ooc_plan_chunks", "ooc_prepare", "ooc_host_ptr", "ooc_upload",
     "ooc_download", "ooc_step", "ooc_get_stats", "ooc_fn_times", "ooc_link_probe",
-    "ooc_timeline", "ooc_set_swapout_depth", "ooc_set_fixed_distance",
+    "ooc_timeline", "ooc_set_swapout_depth", "ooc_set_fixed_distance", "ooc_bestfit_extent",
 ]
 
 
@@ -105,6 +105,8 @@ def load(path=LIB_PATH):
         "ooc_set_policy": ([P, c.c_int32], c.c_int32),
         "ooc_set_swapout_depth": ([P, c.c_int64], c.c_int32),
         "ooc_set_fixed_distance": ([P, c.c_int64, c.c_int64], c.c_int32),
+        "ooc_bestfit_extent": ([P, c.c_uint64, c.POINTER(c.c_uint64), c.POINTER(c.c_uint64)],
+                               c.c_int32),
         "ooc_build_schedule": ([P], c.c_int32),
         "ooc_schedule_get": ([P, c.POINTER(ooc_op), c.c_uint64, c.POINTER(c.c_uint64)], c.c_int32),
         "ooc_schedule_windows": ([P, c.POINTER(c.c_int64), c.c_uint64, c.POINTER(c.c_uint64)],
@@ -206,6 +208,13 @@ class Context:
 
     def set_policy(self, p):
         _check(self.lib.ooc_set_policy(self.h, {"C": 0, "L": 1}.get(p, p)), self.h)
+
+    def bestfit_extent(self, align=256):
+        """(extent, peak_live) of a contiguous best-fit heap serving this schedule."""
+        e, p = ctypes.c_uint64(), ctypes.c_uint64()
+        _check(self.lib.ooc_bestfit_extent(self.h, align, ctypes.byref(e), ctypes.byref(p)),
+               self.h)
+        return e.value, p.value
 
     def set_fixed_distance(self, swapin_ahead, swapout_threshold):
         _check(self.lib.ooc_set_fixed_distance(self.h, swapin_ahead, swapout_threshold), self.h)

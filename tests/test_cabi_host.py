@@ -219,6 +219,40 @@ def test_fixed_distance_matches_oracle(lib):
     ctx.close()
 
 
+def test_bestfit_extent_matches_oracle(lib):
+    """The contiguous best-fit comparison heap: extent and peak live bytes equal the oracle's on
+    random registrations and the small networks, for both policies and several alignments."""
+    rng = random.Random(5)
+    cases = []
+    for _ in range(150):
+        b, k, f = random_registration(rng, nv=rng.randint(1, 12), nf=rng.randint(1, 20))
+        ws = S.working_set_max(b, f, 1)
+        cases.append((b, k, f, rng.choice([ws, ws + 8, 2 * ws])))
+    for spec in specs_small():
+        b, k, f = as_schedule_input(lower(spec))
+        p = S.incore_peak(b, k, f, 1)
+        ws = S.working_set_max(b, f, 1)
+        for frac in (0.5, 0.25):
+            cases.append((b, k, f, max(S.budget_for(frac, p, 1), ws)))
+    for trial, (b, k, f, B) in enumerate(cases):
+        policy = rng.choice("CL")
+        W = rng.choice([0, B // 2, B])
+        align = rng.choice([1, 8, 256])
+        ref = S.build(b, k, f, B, W, 1, policy)
+        ctx = ooc.Context(-1)
+        for nb, kd in zip(b, k):
+            ctx.add_var(nb, kd)
+        for vs in f:
+            ctx.add_fn("noop", [v for v, _ in vs], [a for _, a in vs])
+        ctx.set_chunk(1)
+        ctx.set_budget(B)
+        ctx.set_window(W)
+        ctx.set_policy(policy)
+        ctx.build_schedule()
+        assert ctx.bestfit_extent(align) == opool.best_fit(ref["ops"], b, align), trial
+        ctx.close()
+
+
 def test_infeasible_budget_reports_error(lib):
     spec = specs_small()[0]
     net = netdef.Net(spec)
