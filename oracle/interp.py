@@ -63,7 +63,9 @@ def run(reg, x, labels, params, state=None, dtype=np.float64):
             env[Y] = g(A) + g(B)
         elif op == "softmax_ce":
             lg, lb, loss, dl = vs
-            rows, mean, env[dl] = ops.softmax_ce(g(lg), g(lb))
+            logits = g(lg)          # per-pixel logits: one row per position of the last axis
+            rows, mean, d = ops.softmax_ce(logits.reshape(-1, logits.shape[-1]), g(lb))
+            env[dl] = d.reshape(logits.shape)
             env[loss] = np.concatenate([rows, [mean]])
         elif op == "linear_bwd_w":
             X, dY, dW, db = vs[:4]
@@ -127,6 +129,18 @@ def run(reg, x, labels, params, state=None, dtype=np.float64):
         elif op == "gelu_bwd":
             X, dY, dX = vs
             env[dX] = ops.gelu_bwd(g(X), g(dY))
+        elif op == "concat_fwd":
+            env[vs[-1]] = ops.concat_fwd([g(v) for v in vs[:-1]])
+        elif op == "concat_bwd":
+            parts = ops.concat_bwd(g(vs[0]), a["cs"])
+            for v, part in zip(vs[1:], parts):
+                env[v] = part
+        elif op == "upsample_fwd":
+            X, Y = vs
+            env[Y] = ops.upsample_fwd(g(X))
+        elif op == "upsample_bwd":
+            dY, dX = vs
+            env[dX] = ops.upsample_bwd(g(dY))
         elif op == "attention_fwd":
             X, Pv, Y = vs
             env[Pv], env[Y] = ops.attention_fwd(g(X), a["B"], a["T"], a["H"], bool(a["causal"]))

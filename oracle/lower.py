@@ -41,6 +41,10 @@ gelu_fwd       X R, Y W
 gelu_bwd       X R, dY R, dX W            (X = the GELU input)
 attention_fwd  qkv R, P W, Y W            (P = the attention probabilities [B, H, T, T])
 attention_bwd  qkv R, P R, dY R, dqkv W, dS W   (dS = scratch of P's size)
+concat_fwd     X_1 R, ..., X_k R, Y W          (channel concatenation)
+concat_bwd     dY R, dX_1 W, ..., dX_k W
+upsample_fwd   X R, Y W                        (nearest, factor 2)
+upsample_bwd   dY R, dX W
 =============  ======================================================================
 
 The backward of an addition is the identity, so both inputs receive the
@@ -192,6 +196,19 @@ def lower(spec, keep_grads=False):
             shapes[name] = xs
             var(name, xs)
             fns.append(("gelu_fwd", [(X, R), (name, W)], {"n": math.prod(xs)}))
+        elif op == "concat":
+            lead = xs[:-1]
+            assert all(shapes[s][:-1] == lead for s in ins) and len(set(ins)) == len(ins)
+            cs = [shapes[s][-1] for s in ins]
+            shapes[name] = lead + (sum(cs),)
+            var(name, shapes[name])
+            fns.append(("concat_fwd", [(s, R) for s in ins] + [(name, W)],
+                        {"rows": math.prod(lead), "cs": cs}))
+        elif op == "upsample":
+            n, h, w, c = xs
+            shapes[name] = (n, 2 * h, 2 * w, c)
+            var(name, shapes[name])
+            fns.append(("upsample_fwd", [(X, R), (name, W)], {"N": n, "H": h, "W": w, "C": c}))
         elif op == "attention":
             rows, d3 = xs
             d, H = d3 // 3, L["heads"]
@@ -206,7 +223,7 @@ def lower(spec, keep_grads=False):
 
     # ---------------- loss
     logits = spec["logits"]
-    N, ncls = shapes[logits]
+    N, ncls = math.prod(shapes[logits][:-1]), shapes[logits][-1]   # rows of the last axis
     var("labels", (N,), dtype="i32", kind=INPUT)
     var("loss", (N + 1,), kind=OUTPUT)
     dlog = var("d:" + logits, shapes[logits])
@@ -337,6 +354,18 @@ def lower(spec, keep_grads=False):
         elif op == "gelu":
             dX = var(f"d:{X}@{name}", xs)
             fns.append(("gelu_bwd", [(X, R), (dY, R), (dX, W)], {"n": math.prod(xs)}))
+            contribute(X, dX, pending)
+        elif op == "concat":
+            cs = [shapes[s][-1] for s in L["in"]]
+            dXs = [var(f"d:{s}@{name}", shapes[s]) for s in L["in"]]
+            fns.append(("concat_bwd", [(dY, R)] + [(d, W) for d in dXs],
+                        {"rows": math.prod(xs[:-1]), "cs": cs}))
+            for s, d in zip(L["in"], dXs):
+                contribute(s, d, pending)
+        elif op == "upsample":
+            n, h, w, c = xs
+            dX = var(f"d:{X}@{name}", xs)
+            fns.append(("upsample_bwd", [(dY, R), (dX, W)], {"N": n, "H": h, "W": w, "C": c}))
             contribute(X, dX, pending)
         elif op == "attention":
             rows, d3 = xs

@@ -23,6 +23,10 @@ boundary: images NHWC, conv weights [K, R, S, C], dense weights [out, in].
                 column thirds of one [rows, 3 d] projection, head h owning
                 columns h dh .. (h + 1) dh of each third
 * embedding:    x[b, t] = E[id[b, t]] + pos[t]
+* concat:       channel (last axis) concatenation; its backward hands each input
+                its own channel range of the output gradient
+* upsample:     nearest, factor 2: y[n, 2h + i, 2w + j] = x[n, h, w]; backward sums
+                each 2 x 2 block of the output gradient
 """
 
 from __future__ import annotations
@@ -268,6 +272,24 @@ def attention_bwd(qkv, P, dctx, B, T, H):
 def embed_fwd(ids, E, pos):
     B, T = ids.shape
     return (E[ids] + pos[None, :T]).reshape(B * T, E.shape[1])
+
+
+def concat_fwd(Xs):
+    return np.concatenate(Xs, axis=-1)
+
+
+def concat_bwd(dY, channels):
+    edges = np.cumsum([0] + list(channels))
+    return [dY[..., edges[j]:edges[j + 1]].copy() for j in range(len(channels))]
+
+
+def upsample_fwd(X):
+    return X.repeat(2, axis=1).repeat(2, axis=2)
+
+
+def upsample_bwd(dY):
+    N, H2, W2, C = dY.shape
+    return dY.reshape(N, H2 // 2, 2, W2 // 2, 2, C).sum(axis=(2, 4))
 
 
 def embed_bwd(ids, dX, vocab):

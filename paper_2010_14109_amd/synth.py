@@ -147,21 +147,120 @@ def transformer(batch=64, seq=512, d=1024, heads=16, ffn=4096, layers=48, vocab=
             "optimizer": {"lr": lr, "momentum": momentum}}
 
 
-#: The five workloads: name -> (network description, budget as a fraction of
-#: the in-core peak).  Budget fractions follow the workload list of the build.
+def densenet(batch=64, hw=64, growth=32, blocks=(6, 12, 24, 16), stem=64, classes=10,
+             lr=0.01, momentum=0.9):
+    """DenseNet-shaped network (no bottleneck): inside a block every layer reads the channel
+    concatenation of the stem or transition output and of every earlier layer's output
+    (BN, ReLU, conv3x3 to ``growth`` channels), so each feature map is read by all later layers
+    of its block.  Between blocks: concatenation, BN, ReLU, conv1x1 to half the channels,
+    2x2 max pool.  Head: concatenation, BN, ReLU, global average pool, dense."""
+    layers = [{"name": "stem", "op": "conv", "in": ["x"], "cin": 3, "cout": stem, "k": 3,
+               "stride": 1, "pad": 1}]
+    feats, chans = ["stem"], [stem]
+
+    def gather(name):
+        if len(feats) == 1:
+            return feats[0]
+        layers.append({"name": name, "op": "concat", "in": list(feats)})
+        return name
+
+    for b, n in enumerate(blocks):
+        for i in range(n):
+            base = f"b{b + 1}l{i + 1}"
+            src = gather(f"{base}.cat")
+            layers += [
+                {"name": f"{base}.bn", "op": "bn", "in": [src], "c": sum(chans)},
+                {"name": f"{base}.relu", "op": "relu", "in": [f"{base}.bn"]},
+                {"name": f"{base}.conv", "op": "conv", "in": [f"{base}.relu"], "cin": sum(chans),
+                 "cout": growth, "k": 3, "stride": 1, "pad": 1},
+            ]
+            feats.append(f"{base}.conv")
+            chans.append(growth)
+        c = sum(chans)
+        base = f"t{b + 1}" if b + 1 < len(blocks) else "head"
+        src = gather(f"{base}.cat")
+        layers += [{"name": f"{base}.bn", "op": "bn", "in": [src], "c": c},
+                   {"name": f"{base}.relu", "op": "relu", "in": [f"{base}.bn"]}]
+        if b + 1 < len(blocks):
+            layers += [
+                {"name": f"{base}.conv", "op": "conv", "in": [f"{base}.relu"], "cin": c,
+                 "cout": c // 2, "k": 1, "stride": 1, "pad": 0},
+                {"name": f"{base}.pool", "op": "maxpool", "in": [f"{base}.conv"], "k": 2,
+                 "stride": 2, "pad": 0},
+            ]
+            feats, chans = [f"{base}.pool"], [c // 2]
+        else:
+            layers += [{"name": "gap", "op": "avgpool", "in": [f"{base}.relu"]},
+                       {"name": "fc", "op": "linear", "in": ["gap"], "in_features": c,
+                        "out_features": classes}]
+    return {"name": f"densenet{sum(blocks)}_g{growth}_b{batch}_{hw}",
+            "input": [batch, hw, hw, 3], "classes": classes, "layers": layers, "logits": "fc",
+            "optimizer": {"lr": lr, "momentum": momentum}}
+
+
+def unet(batch=16, hw=128, base=32, depth=4, classes=8, lr=0.01, momentum=0.9):
+    """U-Net-shaped segmentation network: ``depth`` encoder levels of two (conv3x3, BN, ReLU)
+    followed by a 2x2 max pool, a bottleneck, and decoder levels that upsample (nearest, 2x),
+    convolve to the level's width, concatenate the encoder output of the same level (a skip
+    across the whole network) and apply two (conv3x3, BN, ReLU); a conv1x1 gives per-pixel
+    logits, trained on per-pixel labels."""
+    layers = []
+
+    def cbr(name, src, cin, cout):
+        layers.extend([
+            {"name": f"{name}.conv", "op": "conv", "in": [src], "cin": cin, "cout": cout, "k": 3,
+             "stride": 1, "pad": 1},
+            {"name": f"{name}.bn", "op": "bn", "in": [f"{name}.conv"], "c": cout},
+            {"name": f"{name}.relu", "op": "relu", "in": [f"{name}.bn"]}])
+        return f"{name}.relu"
+
+    prev, cin, skips = "x", 3, []
+    for i in range(depth):
+        c = base * 2 ** i
+        prev = cbr(f"e{i + 1}a", prev, cin, c)
+        prev = cbr(f"e{i + 1}b", prev, c, c)
+        skips.append((prev, c))
+        layers.append({"name": f"e{i + 1}.pool", "op": "maxpool", "in": [prev], "k": 2,
+                       "stride": 2, "pad": 0})
+        prev, cin = f"e{i + 1}.pool", c
+    c = base * 2 ** depth
+    prev = cbr("mid.a", prev, cin, c)
+    prev = cbr("mid.b", prev, c, c)
+    cin = c
+    for i in reversed(range(depth)):
+        skip, c = skips[i]
+        layers.append({"name": f"d{i + 1}.up", "op": "upsample", "in": [prev]})
+        prev = cbr(f"d{i + 1}u", f"d{i + 1}.up", cin, c)
+        layers.append({"name": f"d{i + 1}.cat", "op": "concat", "in": [prev, skip]})
+        prev = cbr(f"d{i + 1}a", f"d{i + 1}.cat", 2 * c, c)
+        prev = cbr(f"d{i + 1}b", prev, c, c)
+        cin = c
+    layers.append({"name": "out", "op": "conv", "in": [prev], "cin": cin, "cout": classes, "k": 1,
+                   "stride": 1, "pad": 0})
+    return {"name": f"unet{depth}_c{base}_b{batch}_{hw}", "input": [batch, hw, hw, 3],
+            "classes": classes, "dense_labels": True, "layers": layers, "logits": "out",
+            "optimizer": {"lr": lr, "momentum": momentum}}
+
+
+#: The workloads: name -> (network description, budget as a fraction of the
+#: in-core peak).  The first five are the benchmark configurations; densenet
+#: and unet are long-skip networks whose feature maps are read many times.
 WORKLOADS = {
     "mlp": (lambda: mlp(), 0.40),
     "cnn": (lambda: plain_cnn(), 0.50),
     "resnet50_b256": (lambda: resnet(batch=256), 0.25),
     "resnet50_b1440": (lambda: resnet(batch=1440), 1.0 / 7.5),
     "transformer": (lambda: transformer(), 0.20),
+    "densenet": (lambda: densenet(), 0.25),
+    "unet": (lambda: unet(), 0.25),
 }
 
 
 def workload(name, **overrides):
     """Network description of a named workload, with keyword overrides (e.g. ``batch=8``)."""
     builders = {"mlp": mlp, "cnn": plain_cnn, "resnet50_b256": resnet,
-                "resnet50_b1440": resnet, "transformer": transformer}
+                "resnet50_b1440": resnet, "transformer": transformer, "densenet": densenet,
+                "unet": unet}
     defaults = {"resnet50_b256": {"batch": 256}, "resnet50_b1440": {"batch": 1440}}
     kw = dict(defaults.get(name, {}))
     kw.update(overrides)
@@ -208,7 +307,7 @@ def _width(spec, layer):
 
 def make_inputs(spec, seed=0):
     """``(x, labels)``.  Images: x float32 of the input shape, labels int32 [N] uniform over
-    the classes.  Tokens: ids [B, T + 1] uniform over the vocabulary; x = ids[:, :T] (int32)
+    the classes ([N H W], one per pixel, for per-pixel logits).  Tokens: ids [B, T + 1] uniform over the vocabulary; x = ids[:, :T] (int32)
     and the labels are the next tokens ids[:, 1:] flattened to [B T]."""
     g = np.random.Generator(np.random.PCG64(seed))
     if spec.get("tokens"):
@@ -216,7 +315,8 @@ def make_inputs(spec, seed=0):
         ids = g.integers(0, spec["classes"], size=(B, T + 1)).astype(np.int32)
         return np.ascontiguousarray(ids[:, :T]), np.ascontiguousarray(ids[:, 1:]).reshape(-1)
     x = g.standard_normal(size=tuple(spec["input"]), dtype=np.float32)
-    labels = g.integers(0, spec["classes"], size=spec["input"][0]).astype(np.int32)
+    n = int(np.prod(spec["input"][:3])) if spec.get("dense_labels") else spec["input"][0]
+    labels = g.integers(0, spec["classes"], size=n).astype(np.int32)
     return x, labels
 
 

@@ -149,6 +149,8 @@ def small_networks():
         synth.plain_cnn(batch=2, channels=4, depth=3, hw=8, classes=5),
         synth.resnet(batch=2, hw=32, classes=7, blocks=(1, 2, 1, 1), width=4),
         synth.resnet(batch=1, hw=32, classes=7, blocks=(1, 1, 1, 1), width=4, momentum=0.0),
+        synth.densenet(batch=2, hw=8, growth=4, blocks=(3, 3), stem=4, classes=5),
+        synth.unet(batch=1, hw=16, base=4, depth=3, classes=3),
     ]
 
 
