@@ -73,6 +73,11 @@ def fn_work(op, attrs):
         return "byte", 8 * a[0]
     if op == "gelu_bwd":
         return "byte", 12 * a[0]
+    if op in ("concat_fwd", "concat_bwd"):
+        return "byte", 8 * a[0] * sum(a[1:])
+    if op in ("upsample_fwd", "upsample_bwd"):
+        N, H, W, C = a
+        return "byte", 20 * N * H * W * C
     if op in ("attention_fwd", "attention_bwd"):
         # q k^T and P v forward, four products of the same size backward (dense,
         # as computed: the causal mask zeroes P but the products are full)
@@ -233,7 +238,7 @@ def cpu_baseline(name, budget_seconds=15.0):
     from oracle.interp import run as oracle_run
     from oracle.lower import lower
     small = {"mlp": 256, "cnn": 8, "resnet50_b256": 2, "resnet50_b1440": 2,
-             "transformer": 1}[name]
+             "transformer": 1, "densenet": 2, "unet": 1}[name]
     spec = synth.workload(name, batch=small)
     reg = lower(spec)
     x, labels = synth.make_inputs(spec, 0)

@@ -141,6 +141,16 @@ enum { OOC_PRE = 0, OOC_POST = 1, OOC_END = 2 };
  *                Y [B T][H dh] = P v                qkv[R] P[W] Y[W]    B T H dh causal
  *  ATTENTION_BWD dqkv of the above; dS is scratch of P's size
  *                                     qkv[R] P[R] dY[R] dqkv[W] dS[W]  B T H dh causal
+ *  CONCAT_FWD    channel concatenation of k = 1..64 row-major tensors with
+ *                the same rows: Y[r] = [X_1[r] | ... | X_k[r]]
+ *                                     X_1[R] .. X_k[R] Y[W]            rows c_1 .. c_k
+ *  CONCAT_BWD    dX_j[r] = the c_j columns of dY[r] that X_j filled
+ *                                     dY[R] dX_1[W] .. dX_k[W]         rows c_1 .. c_k
+ *  UPSAMPLE_FWD  nearest, factor 2: Y[n][2h+i][2w+j] = X[n][h][w]
+ *                                     X[R] Y[W]                        N H W C (of X)
+ *  UPSAMPLE_BWD  dX[n][h][w] = sum over i, j in {0, 1} of dY[n][2h+i][2w+j],
+ *                added in the order (0,0) (0,1) (1,0) (1,1)
+ *                                     dY[R] dX[W]                      N H W C (of dX)
  *  MIX           swap-integrity test op on uint32 words (sizes multiple of
  *                4): the last variable y is the only one written (W or RW),
  *                the others are read; y[j] = seed ^ (j * 2654435761) ^ sum
@@ -176,7 +186,11 @@ enum {
   OOC_OP_GELU_BWD = 24,
   OOC_OP_ATTENTION_FWD = 25,
   OOC_OP_ATTENTION_BWD = 26,
-  OOC_OP_COUNT = 27
+  OOC_OP_CONCAT_FWD = 27,
+  OOC_OP_CONCAT_BWD = 28,
+  OOC_OP_UPSAMPLE_FWD = 29,
+  OOC_OP_UPSAMPLE_BWD = 30,
+  OOC_OP_COUNT = 31
 };
 
 /* One schedule op.  fn = N for END ops; held = budget bytes held after it

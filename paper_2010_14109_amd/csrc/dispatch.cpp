@@ -83,6 +83,18 @@ hipError_t launch_fn(const Fn& fn, void* const* p, const uint64_t* bytes, float 
       return attention_fwd(F(0), F(1), F(2), a[0], a[1], a[2], a[3], a[4] != 0, s);
     case OOC_OP_ATTENTION_BWD:
       return attention_bwd(F(0), F(1), F(2), F(3), F(4), a[0], a[1], a[2], a[3], a[4] != 0, s);
+    case OOC_OP_CONCAT_FWD: {
+      const int k = (int)fn.vars.size() - 1;
+      return concat(true, F(k), p, a.data() + 1, k, a[0], s);
+    }
+    case OOC_OP_CONCAT_BWD: {
+      const int k = (int)fn.vars.size() - 1;
+      return concat(false, F(0), p + 1, a.data() + 1, k, a[0], s);
+    }
+    case OOC_OP_UPSAMPLE_FWD:
+      return upsample(true, F(0), F(1), a[0], a[1], a[2], a[3], s);
+    case OOC_OP_UPSAMPLE_BWD:
+      return upsample(false, F(0), F(1), a[0], a[1], a[2], a[3], s);
     default:
       return hipErrorInvalidValue;
   }

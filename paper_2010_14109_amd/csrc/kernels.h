@@ -58,6 +58,13 @@ struct PoolShape {
 hipError_t maxpool_fwd(const float* x, float* y, uint8_t* idx, const PoolShape& p, hipStream_t s);
 hipError_t maxpool_bwd(const uint8_t* idx, const float* dy, float* dx, const PoolShape& p,
                        hipStream_t s);
+// Channel concatenation (forward: parts -> cat; backward: cat -> parts) and
+// nearest 2x upsampling (forward: in [N H W C] -> out; backward: the gradient
+// of out -> in [N H W C]).
+hipError_t concat(bool forward, float* cat, void* const* parts, const int64_t* cs, int k,
+                  int64_t rows, hipStream_t s);
+hipError_t upsample(bool forward, const float* in, float* out, int64_t N, int64_t H, int64_t W,
+                    int64_t C, hipStream_t s);
 hipError_t avgpool_fwd(const float* x, float* y, int64_t N, int64_t HW, int64_t C, hipStream_t s);
 hipError_t avgpool_bwd(const float* dy, float* dx, int64_t N, int64_t HW, int64_t C,
                        hipStream_t s);

@@ -422,6 +422,84 @@ __global__ void mix_kernel(MixArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- concatenation, upsampling
+// One part of a channel concatenation: the rows x cp block of the part sits at
+// column `off` of the rows x ct concatenation.  TO_CAT copies part -> cat,
+// otherwise the concatenation's columns back into the part.  VEC moves float4
+// (cp, ct and off multiples of 4).
+template <bool TO_CAT, bool VEC>
+__global__ void concat_part_kernel(const float* __restrict__ src, float* __restrict__ dst,
+                                   int64_t rows, int64_t cp, int64_t ct, int64_t off) {
+  const int64_t per = VEC ? cp / 4 : cp;   // units per row
+  const int64_t n = rows * per;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int64_t r = i / per, u = (i - r * per) * (VEC ? 4 : 1);
+    const int64_t pi = r * cp + u, ci = r * ct + off + u;
+    if (VEC) {
+      if (TO_CAT)
+        *reinterpret_cast<float4*>(&dst[ci]) = *reinterpret_cast<const float4*>(&src[pi]);
+      else
+        *reinterpret_cast<float4*>(&dst[pi]) = *reinterpret_cast<const float4*>(&src[ci]);
+    } else {
+      if (TO_CAT)
+        dst[ci] = src[pi];
+      else
+        dst[pi] = src[ci];
+    }
+  }
+}
+
+// nearest 2x upsampling of NHWC x[N][H][W][C]: one thread per output unit
+template <bool VEC>
+__global__ void upsample_fwd_kernel(const float* __restrict__ x, float* __restrict__ y, int64_t N,
+                                    int64_t H, int64_t W, int64_t C) {
+  const int64_t per = VEC ? C / 4 : C;
+  const int64_t n = N * 4 * H * W * per;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    int64_t t = i / per;
+    const int64_t c = (i - t * per) * (VEC ? 4 : 1);
+    const int64_t w2 = t % (2 * W);
+    t /= 2 * W;
+    const int64_t h2 = t % (2 * H), b = t / (2 * H);
+    const int64_t src = ((b * H + h2 / 2) * W + w2 / 2) * C + c, dst = i * (VEC ? 4 : 1);
+    if (VEC)
+      *reinterpret_cast<float4*>(&y[dst]) = *reinterpret_cast<const float4*>(&x[src]);
+    else
+      y[dst] = x[src];
+  }
+}
+
+// its backward: one thread per input unit, the 2 x 2 block added in a fixed order
+template <bool VEC>
+__global__ void upsample_bwd_kernel(const float* __restrict__ dy, float* __restrict__ dx, int64_t N,
+                                    int64_t H, int64_t W, int64_t C) {
+  const int64_t per = VEC ? C / 4 : C;
+  const int64_t n = N * H * W * per;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    int64_t t = i / per;
+    const int64_t c = (i - t * per) * (VEC ? 4 : 1);
+    const int64_t w = t % W;
+    t /= W;
+    const int64_t h = t % H, b = t / H;
+    const int64_t row = 2 * W * C;   // one output row
+    const int64_t q = ((b * 2 * H + 2 * h) * 2 * W + 2 * w) * C + c;
+    if (VEC) {
+      const float4 a0 = *reinterpret_cast<const float4*>(&dy[q]);
+      const float4 a1 = *reinterpret_cast<const float4*>(&dy[q + C]);
+      const float4 a2 = *reinterpret_cast<const float4*>(&dy[q + row]);
+      const float4 a3 = *reinterpret_cast<const float4*>(&dy[q + row + C]);
+      *reinterpret_cast<float4*>(&dx[i * 4]) =
+          make_float4(((a0.x + a1.x) + a2.x) + a3.x, ((a0.y + a1.y) + a2.y) + a3.y,
+                      ((a0.z + a1.z) + a2.z) + a3.z, ((a0.w + a1.w) + a2.w) + a3.w);
+    } else {
+      dx[i] = ((dy[q] + dy[q + C]) + dy[q + row]) + dy[q + row + C];
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t relu_fwd(const float* x, float* y, int64_t n, hipStream_t s) {
@@ -531,6 +609,57 @@ hipError_t mix(void* const* ptrs, const uint64_t* words, int nvars, uint32_t see
   a.ylen = words[nvars - 1];
   a.seed = seed;
   hipLaunchKernelGGL(mix_kernel, dim3(grid_for((int64_t)a.ylen)), dim3(TPB), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t concat(bool forward, float* cat, void* const* parts, const int64_t* cs, int k,
+                  int64_t rows, hipStream_t s) {
+  int64_t ct = 0;
+  for (int j = 0; j < k; ++j) ct += cs[j];
+  int64_t off = 0;
+  for (int j = 0; j < k; ++j) {
+    float* part = static_cast<float*>(parts[j]);
+    const bool vec = cs[j] % 4 == 0 && ct % 4 == 0 && off % 4 == 0 && aligned16(cat) &&
+                     aligned16(part);
+    const unsigned g = grid_for(rows * (vec ? cs[j] / 4 : cs[j]));
+    if (forward) {
+      if (vec)
+        hipLaunchKernelGGL((concat_part_kernel<true, true>), dim3(g), dim3(TPB), 0, s, part, cat,
+                           rows, cs[j], ct, off);
+      else
+        hipLaunchKernelGGL((concat_part_kernel<true, false>), dim3(g), dim3(TPB), 0, s, part,
+                           cat, rows, cs[j], ct, off);
+    } else {
+      if (vec)
+        hipLaunchKernelGGL((concat_part_kernel<false, true>), dim3(g), dim3(TPB), 0, s, cat,
+                           part, rows, cs[j], ct, off);
+      else
+        hipLaunchKernelGGL((concat_part_kernel<false, false>), dim3(g), dim3(TPB), 0, s, cat,
+                           part, rows, cs[j], ct, off);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    off += cs[j];
+  }
+  return hipSuccess;
+}
+
+hipError_t upsample(bool forward, const float* in, float* out, int64_t N, int64_t H, int64_t W,
+                    int64_t C, hipStream_t s) {
+  const bool vec = C % 4 == 0 && aligned16(in) && aligned16(out);
+  const int64_t units = N * H * W * (vec ? C / 4 : C) * (forward ? 4 : 1);
+  const unsigned g = grid_for(units);
+  if (forward) {
+    if (vec)
+      hipLaunchKernelGGL(upsample_fwd_kernel<true>, dim3(g), dim3(TPB), 0, s, in, out, N, H, W, C);
+    else
+      hipLaunchKernelGGL(upsample_fwd_kernel<false>, dim3(g), dim3(TPB), 0, s, in, out, N, H, W, C);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL(upsample_bwd_kernel<true>, dim3(g), dim3(TPB), 0, s, in, out, N, H, W, C);
+    else
+      hipLaunchKernelGGL(upsample_bwd_kernel<false>, dim3(g), dim3(TPB), 0, s, in, out, N, H, W, C);
+  }
   return hipGetLastError();
 }
 

@@ -45,6 +45,10 @@ const Sig kSig[OOC_OP_COUNT] = {
     {"GELU_BWD", 3, 1, {OOC_R, OOC_R, OOC_W}},
     {"ATTENTION_FWD", 3, 5, {OOC_R, OOC_W, OOC_W}},
     {"ATTENTION_BWD", 5, 5, {OOC_R, OOC_R, OOC_R, OOC_W, OOC_W}},
+    {"CONCAT_FWD", -1, -1, {}},
+    {"CONCAT_BWD", -1, -1, {}},
+    {"UPSAMPLE_FWD", 2, 4, {OOC_R, OOC_W}},
+    {"UPSAMPLE_BWD", 2, 4, {OOC_R, OOC_W}},
 };
 
 const int64_t kMaxElems = int64_t(1) << 40;
@@ -288,6 +292,37 @@ std::string check_fn(const std::vector<Var>& vars, const Fn& fn) {
         NEED(3, qb, "dqkv");
         NEED(4, pb, "dS");
       }
+      return "";
+    }
+    case OOC_OP_CONCAT_FWD:
+    case OOC_OP_CONCAT_BWD: {
+      const int k = nv - 1;
+      if (k < 1 || k > 64 || (int)a.size() != 1 + k)
+        return nm + ": takes 1 + k variables and 1 + k attributes, k <= 64";
+      const bool fwd = fn.op == OOC_OP_CONCAT_FWD;
+      const int out = fwd ? k : 0;   // the concatenated tensor
+      for (int j = 0; j < nv; ++j) {
+        const uint8_t want = fwd ? (j == k ? OOC_W : OOC_R) : (j == 0 ? OOC_R : OOC_W);
+        if (v[j].access != want) return nm + ": wrong access";
+      }
+      const int64_t rows = a[0];
+      int64_t total = 0;
+      for (int j = 1; j <= k; ++j) {
+        if (a[j] <= 0) return nm + ": non-positive channel count";
+        total += a[j];
+      }
+      if (rows <= 0 || rows * total > kMaxElems) return nm + ": bad attributes";
+      for (int j = 0; j < k; ++j) NEED(fwd ? j : j + 1, rows * a[1 + j] * 4, "part");
+      NEED(out, rows * total * 4, "concatenation");
+      return "";
+    }
+    case OOC_OP_UPSAMPLE_FWD:
+    case OOC_OP_UPSAMPLE_BWD: {
+      const int64_t N = a[0], H = a[1], W = a[2], C = a[3];
+      if (N <= 0 || H <= 0 || W <= 0 || C <= 0) return nm + ": non-positive shape";
+      const int64_t small = N * H * W * C * 4, big = 4 * small;
+      NEED(0, fn.op == OOC_OP_UPSAMPLE_FWD ? small : big, "input");
+      NEED(1, fn.op == OOC_OP_UPSAMPLE_FWD ? big : small, "output");
       return "";
     }
     case OOC_OP_MIX: {

@@ -109,6 +109,25 @@ class Net:
                    [rows, c, S])
         return xs
 
+    def _fwd_concat(self, L, X):
+        srcs = L["in"]
+        lead = self.shape[srcs[0]][:-1]
+        if any(self.shape[s][:-1] != lead for s in srcs) or len(set(srcs)) != len(srcs):
+            raise ValueError(f"{L['name']}: concatenated tensors must differ and share all but "
+                             "their last axis")
+        cs = [self.shape[s][-1] for s in srcs]
+        ys = lead + (sum(cs),)
+        Y = self._decl(L["name"], ys)
+        self._call("concat_fwd", [(s, ooc.R) for s in srcs] + [(Y, ooc.W)], [prod(lead)] + cs)
+        return ys
+
+    def _fwd_upsample(self, L, X):
+        n, h, w, c = self.shape[X]
+        ys = (n, 2 * h, 2 * w, c)
+        Y = self._decl(L["name"], ys)
+        self._call("upsample_fwd", [(X, ooc.R), (Y, ooc.W)], [n, h, w, c])
+        return ys
+
     def _fwd_relu(self, L, X):
         xs = self.shape[X]
         Y = self._decl(L["name"], xs)
@@ -283,6 +302,18 @@ class Net:
             dX = self._decl(f"d:{X}@{name}", xs)
             self._call("gelu_bwd", [(X, ooc.R), (dY, ooc.R), (dX, ooc.W)], [prod(xs)])
             out.append((X, dX))
+        elif op == "concat":
+            srcs = L["in"]
+            cs = [self.shape[s][-1] for s in srcs]
+            dXs = [self._decl(f"d:{s}@{name}", self.shape[s]) for s in srcs]
+            self._call("concat_bwd", [(dY, ooc.R)] + [(d, ooc.W) for d in dXs],
+                       [prod(self.shape[name][:-1])] + cs)
+            out.extend(zip(srcs, dXs))
+        elif op == "upsample":
+            n, h, w, c = xs
+            dX = self._decl(f"d:{X}@{name}", xs)
+            self._call("upsample_bwd", [(dY, ooc.R), (dX, ooc.W)], [n, h, w, c])
+            out.append((X, dX))
         elif op == "attention":
             a = self._attn_attrs(L, X)
             B, T, H, dh, _ = a
@@ -302,14 +333,16 @@ class Net:
                "relu": self._fwd_relu, "maxpool": self._fwd_maxpool,
                "avgpool": self._fwd_avgpool, "add": self._fwd_add, "embed": self._fwd_embed,
                "layernorm": self._fwd_layernorm, "gelu": self._fwd_gelu,
-               "attention": self._fwd_attention}
+               "attention": self._fwd_attention, "concat": self._fwd_concat,
+               "upsample": self._fwd_upsample}
         for L in spec["layers"]:
             self.shape[L["name"]] = fwd[L["op"]](L, L["in"][0])
         logits = spec["logits"]
-        n, classes = self.shape[logits]
+        ls = self.shape[logits]
+        n, classes = prod(ls[:-1]), ls[-1]          # one row (and label) per position
         self._decl("labels", (n,), dtype="i32", kind=ooc.INPUT)
         self._decl("loss", (n + 1,), kind=ooc.OUTPUT)
-        dlogits = self._decl("d:" + logits, (n, classes))
+        dlogits = self._decl("d:" + logits, ls)
         self._call("softmax_ce", [(logits, ooc.R), ("labels", ooc.R), ("loss", ooc.W),
                                   (dlogits, ooc.W)], [n, classes])
         grads = {logits: dlogits}

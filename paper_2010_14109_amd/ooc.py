@@ -30,7 +30,8 @@ OPS = {
     "conv_bwd_x": 11, "bn_fwd": 12, "bn_bwd": 13, "maxpool_fwd": 14, "maxpool_bwd": 15,
     "avgpool_fwd": 16, "avgpool_bwd": 17, "mix": 18, "embed_fwd": 19, "embed_bwd": 20,
     "layernorm_fwd": 21, "layernorm_bwd": 22, "gelu_fwd": 23, "gelu_bwd": 24,
-    "attention_fwd": 25, "attention_bwd": 26,
+    "attention_fwd": 25, "attention_bwd": 26, "concat_fwd": 27, "concat_bwd": 28,
+    "upsample_fwd": 29, "upsample_bwd": 30,
 }
 
 #: every symbol ``include/ooc.h`` declares

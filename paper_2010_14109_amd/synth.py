@@ -198,7 +198,7 @@ def densenet(batch=64, hw=64, growth=32, blocks=(6, 12, 24, 16), stem=64, classe
             "optimizer": {"lr": lr, "momentum": momentum}}
 
 
-def unet(batch=16, hw=128, base=32, depth=4, classes=8, lr=0.01, momentum=0.9):
+def unet(batch=8, hw=256, base=64, depth=4, classes=8, lr=0.01, momentum=0.9):
     """U-Net-shaped segmentation network: ``depth`` encoder levels of two (conv3x3, BN, ReLU)
     followed by a 2x2 max pool, a bottleneck, and decoder levels that upsample (nearest, 2x),
     convolve to the level's width, concatenate the encoder output of the same level (a skip

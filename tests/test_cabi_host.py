@@ -35,12 +35,14 @@ def specs_small():
         synth.mlp(batch=3, width=8, depth=2, classes=3, momentum=0.9),
         synth.plain_cnn(batch=2, channels=4, depth=3, hw=8, classes=5),
         synth.resnet(batch=2, hw=32, classes=7, blocks=(1, 2, 1, 1), width=4),
+        synth.densenet(batch=2, hw=8, growth=4, blocks=(3, 2), stem=4, classes=5),
+        synth.unet(batch=1, hw=16, base=4, depth=3, classes=3),
     ]
 
 
 def specs_full():
     return [synth.workload(n) for n in ("mlp", "cnn", "resnet50_b256", "resnet50_b1440",
-                                        "transformer")]
+                                        "transformer", "densenet", "unet")]
 
 
 @pytest.mark.parametrize("spec", specs_small() + specs_full(), ids=lambda s: s["name"])

@@ -259,6 +259,36 @@ def test_mix_op():
     assert np.array_equal(y, mixop.mix([a], 33, 7))
 
 
+# ---------------------------------------------------------------- concatenation, upsampling
+@pytest.mark.parametrize("rows,cs", [(37, (8, 12)), (37, (3, 5, 1)), (1, (4,)), (1000, (64, 32, 32))])
+def test_concat(rows, cs):
+    parts = [f32(rows, c) for c in cs]
+    ct = sum(cs)
+    print(f"concat rows={rows} cs={cs}", flush=True)
+    out = run_fn("concat_fwd", [(p, ooc.R) for p in parts] + [(((rows, ct), "f32"), ooc.W)],
+                 [rows] + list(cs))
+    assert np.array_equal(out[-1], np.concatenate(parts, axis=1))
+    G = f32(rows, ct)
+    back = run_fn("concat_bwd", [(G, ooc.R)] + [(((rows, c), "f32"), ooc.W) for c in cs],
+                  [rows] + list(cs))
+    for got, ref in zip(back[1:], ops.concat_bwd(G, list(cs))):
+        assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("N,H,W,C", [(2, 3, 5, 8), (1, 4, 4, 3), (2, 16, 16, 64)])
+def test_upsample(N, H, W, C):
+    X = f32(N, H, W, C)
+    print(f"upsample {N}x{H}x{W}x{C}", flush=True)
+    (_, Y) = run_fn("upsample_fwd", [(X, ooc.R), (((N, 2 * H, 2 * W, C), "f32"), ooc.W)],
+                    [N, H, W, C])
+    assert np.array_equal(Y, ops.upsample_fwd(X))
+    G = f32(N, 2 * H, 2 * W, C)
+    (_, dX) = run_fn("upsample_bwd", [(G, ooc.R), (((N, H, W, C), "f32"), ooc.W)], [N, H, W, C])
+    g = G.reshape(N, H, 2, W, 2, C)
+    ref = ((g[:, :, 0, :, 0] + g[:, :, 0, :, 1]) + g[:, :, 1, :, 0]) + g[:, :, 1, :, 1]
+    assert np.array_equal(dX, ref)         # same fp32 order as the kernel: bit-exact
+
+
 # ---------------------------------------------------------------- transformer layers
 @pytest.mark.parametrize("rows,d,slices", [(37, 64, 1), (37, 100, 3), (130, 1024, 4), (5, 4096, 2),
                                           (2000, 1024, 63), (999, 100, 37)])

@@ -33,6 +33,10 @@ def tiny_specs():
         # the last BatchNorm sees 2 rows and even the oracle run in float32 is 4e-2 off float64.
         synth.resnet(batch=4, hw=64, classes=11, blocks=(1, 1, 1, 1), width=8, momentum=0.9),
         synth.transformer(batch=2, seq=16, d=64, heads=4, ffn=128, layers=2, vocab=97),
+        # long skips: every feature map of a block read by all later layers; encoder outputs
+        # concatenated into the decoder
+        synth.densenet(batch=4, hw=16, growth=8, blocks=(3, 3), stem=16, classes=6),
+        synth.unet(batch=2, hw=32, base=8, depth=2, classes=5),
     ]
 
 
