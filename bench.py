@@ -18,6 +18,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import platform
 import sys
 import time
 
@@ -141,6 +142,7 @@ def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None):
     budget = max(int(p_incore * frac) // chunk * chunk, ws_max)
     window = int(budget * window_frac)
     counts = []
+    build_ms = None
     for b, w in ((budget, window), (ooc.UNLIMITED, None)):
         ctx = ooc.Context(-1)
         try:
@@ -152,12 +154,15 @@ def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None):
                 ctx.set_policy(policy)
                 if fixed is not None:
                     ctx.set_fixed_distance(*fixed)
+            t0 = time.perf_counter()
             ctx.build_schedule()
+            if build_ms is None:
+                build_ms = (time.perf_counter() - t0) * 1e3
             counts.append(sum(ctx.plan_counts()))
         finally:
             ctx.close()
     return {"p_incore": p_incore, "ws_max": ws_max, "budget": budget, "window": window,
-            "map_entries": max(counts)}
+            "map_entries": max(counts), "build_ms": build_ms}
 
 
 def choose_chunk(net, frac, window_frac, policy="C", fixed=None):
@@ -233,6 +238,41 @@ def kernel_table(net, fn_ms):
     return table
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def _blas():
+    try:
+        from threadpoolctl import threadpool_info
+        libs = [f"{p.get('internal_api')} {p.get('version')}" for p in threadpool_info()
+                if p.get("user_api") == "blas"]
+        return ", ".join(libs) or "unknown"
+    except Exception:  # noqa: BLE001 - informational only
+        return "unknown"
+
+
+def oracle_schedule_ms(spec, budget, window, chunk, policy, fixed):
+    """Wall time of the oracle's scheduler on the full-size function sequence (median of 3)."""
+    from oracle import schedule as S
+    from oracle.lower import as_schedule_input, lower
+    b, k, f = as_schedule_input(lower(spec))
+    ahead, thr = fixed if fixed is not None else (None, None)
+    times = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        S.build(b, k, f, budget, window, chunk, policy, ahead, thr)
+        times.append((time.perf_counter() - t0) * 1e3)
+    return sorted(times)[1]
+
+
 def cpu_baseline(name, budget_seconds=15.0):
     """The float32 oracle step (``oracle.interp``) on a reduced batch of the same network."""
     from oracle.interp import run as oracle_run
@@ -259,7 +299,8 @@ def cpu_baseline(name, budget_seconds=15.0):
             break
     return {"value": n * small / el, "unit": "samples/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} float32 oracle steps of {spec['name']} (batch {small}) in "
-                      f"{el:.1f} s"}
+                      f"{el:.1f} s",
+            "cpu_model": _cpu_model(), "blas": _blas()}
 
 
 def main():
@@ -365,6 +406,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 3),
+        "median_ms_per_step": round(float(np.median(out["step_ms"])), 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -405,7 +447,9 @@ def main():
         "peak_device_bytes": {"pool": st["pool_bytes"], "max_chunks_in_use_bytes":
                               st["max_chunks_used"] * chunk, "peak_accounted": st["peak_accounted"],
                               "hipMemGetInfo_delta": st["device_bytes_delta"],
+                              "runtime_overhead": st["device_bytes_delta"] - st["pool_bytes"],
                               "budget": budget},
+        "schedule_build_ms": {"library": round(plan["build_ms"], 3), "oracle": None},
         "compute_busy_ms_per_step": round(st["compute_busy_ms"], 2),
         "loss": out["loss"],
         "kernels": {op: {"ms": round(e["ms"], 3), "launches": e["launches"],
@@ -415,6 +459,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args.workload)
+        res["schedule_build_ms"]["oracle"] = round(
+            oracle_schedule_ms(spec, budget, window, chunk, policy, fixed), 3)
     print(json.dumps(res), flush=True)
 
 

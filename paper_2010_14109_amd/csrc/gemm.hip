@@ -57,12 +57,36 @@ __device__ inline float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 // A loader feeds one operand tile of extent E (tile rows along m or n) by 32
 // along k.  init(mn0, MN) runs once per workgroup (mn0 = tile origin, MN =
 // extent of the matrix), fetch(k0, kend, r) loads this thread's E / 8 values
-// of the K tile starting at k0 as E / 32 float4 (zero at k >= kend),
-// store(lds, r) writes them.
+// of the K tile starting at k0 as E / 32 float4, store(lds, r) writes them.
+//
+// No load sits behind a branch, so that the address arithmetic of the next
+// tile can be scheduled between the MFMAs of the current one.  Values at
+// k >= kend must be zero (they enter every dot product): their lanes load
+// from a block of zeros instead.  Rows and columns past M or N only reach C
+// entries that are never stored, so their lanes read a clamped in-range
+// address and whatever they load is harmless.  Zero padding of a
+// convolution is masked like k >= kend.
 //
 // Row-of-k layout [E][32 + 4]: thread t loads rows (t >> 3) + 32 j, k offset
-// (t & 7) * 4.  Row-of-m layout [32][E + 4]: E / 4 threads per k row; thread
-// t loads k rows t / (E / 4) + (1024 / E) j, m offset (t % (E / 4)) * 4.
+// (t & 7) * 4.  Row-of-m layout [32][E + 4], two thread maps: RowM has E / 4
+// threads per k row, thread t loading k rows t / (E / 4) + (1024 / E) j at m
+// offset (t % (E / 4)) * 4, so that a wave reads whole rows; RowM1 gives
+// thread t the single k row t >> 3 and its E / 8 consecutive m values from
+// (t & 7) E / 8 on, so that one row address serves all of its loads (for
+// views whose row addresses are costly to form).
+
+// What masked lanes load (never written).
+__device__ __attribute__((aligned(16))) float g_zero[64] = {};
+
+__device__ inline float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+
+// Pins v in a register at this point.  The compiler would otherwise move an
+// address computation that only a masked select uses into a branch around
+// it, which is what the loaders avoid.
+template <class T>
+__device__ inline void keep(T& v) {
+  asm volatile("" : "+v"(v));
+}
 
 template <int E>
 struct RowK {
@@ -89,14 +113,30 @@ struct RowM {
     for (int j = 0; j < kN; ++j) *reinterpret_cast<float4*>(&lds[krow(j) * kLd + moff()]) = r[j];
   }
 };
+template <int E>
+struct RowM1 {
+  static constexpr bool kRowOfK = false;
+  static constexpr int kN = E / 32;
+  static constexpr int kLd = E + 4;
+  static constexpr int kLds = BK * kLd;
+  __device__ static int krow() { return (int)threadIdx.x >> 3; }
+  __device__ static int moff() { return ((int)threadIdx.x & 7) * (E / 8); }
+  __device__ static void store(float* lds, const float4 (&r)[kN]) {
+#pragma unroll
+    for (int j = 0; j < kN; ++j)
+      *reinterpret_cast<float4*>(&lds[krow() * kLd + moff() + 4 * j]) = r[j];
+  }
+};
 
 // x / d for 0 <= x < 2^31 and an invariant d >= 1 with one multiply-high
 // (Granlund and Montgomery, division by invariant integers using
 // multiplication, 1994): with l = ceil(log2 d) and m = floor(2^(31+l) / d) + 1,
 // 2^(31+l) < m d <= 2^(31+l) + 2^l, hence floor(x m / 2^(31+l)) = floor(x / d)
-// for every x < 2^31, and m < 2^32.
+// for every x < 2^31, and m < 2^32.  d = 1 takes m = 2^32 - 1 and adds one
+// to x first: floor((x + 1)(2^32 - 1) / 2^32) = x for x + 1 <= 2^32.  Both
+// cases are the same instructions, so a division never branches.
 struct FastDiv {
-  uint32_t d = 1, m = 0, s = 0;
+  uint32_t d = 1, m = 0xffffffffu, s = 0, a = 1;
   static FastDiv make(int64_t dv) {
     FastDiv f;
     f.d = (uint32_t)dv;
@@ -105,11 +145,10 @@ struct FastDiv {
     while ((1ull << l) < (uint64_t)dv) ++l;
     f.m = (uint32_t)((1ull << (31 + l)) / (uint64_t)dv + 1);
     f.s = l - 1;
+    f.a = 0;
     return f;
   }
-  __device__ int div(int x) const {
-    return d == 1 ? x : (int)(__umulhi((uint32_t)x, m) >> s);
-  }
+  __device__ int div(int x) const { return (int)(__umulhi((uint32_t)x + a, m) >> s); }
 };
 
 constexpr int kFar = -(1 << 29);   // coordinate of a row past the matrix: fails every bounds check
@@ -122,12 +161,12 @@ struct MatK : RowK<E> {
   using Base = RowK<E>;
   const float* p;
   int64_t ld;
-  int64_t off_[Base::kN];   // i * ld + this lane's k offset; -1 past the last row
+  int64_t off_[Base::kN];   // (row, clamped to the matrix) * ld + this lane's k offset
   __device__ void init(int64_t mn0, int64_t MN) {
 #pragma unroll
     for (int j = 0; j < Base::kN; ++j) {
       const int64_t i = mn0 + Base::row(j);
-      off_[j] = i < MN ? i * ld + Base::koff() : -1;
+      off_[j] = (i < MN ? i : 0) * ld + Base::koff();
     }
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
@@ -135,57 +174,60 @@ struct MatK : RowK<E> {
 #pragma unroll
     for (int j = 0; j < Base::kN; ++j) {
       const float* q = p + off_[j] + k0;
-      const bool ok = off_[j] >= 0;
       if (VEC) {
-        r[j] = (ok && k < kend) ? *reinterpret_cast<const float4*>(q) : zero4();
+        r[j] = ld4(k < kend ? q : g_zero);
       } else {
-        r[j].x = (ok && k + 0 < kend) ? q[0] : 0.f;
-        r[j].y = (ok && k + 1 < kend) ? q[1] : 0.f;
-        r[j].z = (ok && k + 2 < kend) ? q[2] : 0.f;
-        r[j].w = (ok && k + 3 < kend) ? q[3] : 0.f;
+        r[j].x = *(k + 0 < kend ? q + 0 : g_zero);
+        r[j].y = *(k + 1 < kend ? q + 1 : g_zero);
+        r[j].z = *(k + 2 < kend ? q + 2 : g_zero);
+        r[j].w = *(k + 3 < kend ? q + 3 : g_zero);
       }
     }
   }
 };
 
-// X[i][k] = p[k * ld + i]  (contiguous along m or n)
+// X[i][k] = p[k * ld + i]  (contiguous along m or n; VEC needs MN % 4 == 0)
 template <int E, bool VEC>
 struct MatM : RowM<E> {
   using Base = RowM<E>;
   const float* p;
   int64_t ld;
-  int64_t i0;
-  int64_t rows;
-  int64_t off_[Base::kN];   // this lane's k row * ld + i0
+  int64_t i0;                // this lane's first m
+  int64_t rows;              // MN
+  int64_t off_[Base::kN];    // k row * ld (+ the m offset clamped to the matrix, VEC)
   __device__ void init(int64_t mn0, int64_t MN) {
     i0 = mn0 + Base::moff();
     rows = MN;
 #pragma unroll
-    for (int j = 0; j < Base::kN; ++j) off_[j] = Base::krow(j) * ld + i0;
+    for (int j = 0; j < Base::kN; ++j)
+      off_[j] = Base::krow(j) * ld + (VEC ? (i0 < MN ? i0 : 0) : 0);
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
     const float* pk = p + k0 * ld;
 #pragma unroll
     for (int j = 0; j < Base::kN; ++j) {
-      const int64_t k = k0 + Base::krow(j);
-      const float* q = pk + off_[j];
+      const bool ok = k0 + Base::krow(j) < kend;
       if (VEC) {
-        r[j] = (k < kend && i0 < rows) ? *reinterpret_cast<const float4*>(q) : zero4();
+        r[j] = ld4(ok ? pk + off_[j] : g_zero);
       } else {
-        const bool ok = k < kend;
-        r[j].x = (ok && i0 + 0 < rows) ? q[0] : 0.f;
-        r[j].y = (ok && i0 + 1 < rows) ? q[1] : 0.f;
-        r[j].z = (ok && i0 + 2 < rows) ? q[2] : 0.f;
-        r[j].w = (ok && i0 + 3 < rows) ? q[3] : 0.f;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t i = i0 + e;
+          v[e] = *(ok ? pk + off_[j] + (i < rows ? i : 0) : g_zero);
+        }
+        r[j] = make_float4(v[0], v[1], v[2], v[3]);
       }
     }
   }
 };
 
-// Loader modes of the convolution views: TAP when the reduced channel count
-// is a multiple of 32 (a K tile lies inside one filter tap, uniform over the
-// workgroup), VEC when it is a multiple of 4 (each lane splits its own k
-// index, four consecutive channels per load), SCALAR otherwise.
+// Loader modes of the convolution views.  Row-of-k views: TAP when the
+// reduced channel count is a multiple of 32 (a K tile lies inside one filter
+// tap, uniform over the workgroup), VEC4 when it is a multiple of 4 (each lane
+// splits its own k index, four consecutive channels per load), SCALAR
+// otherwise.  Row-of-m views: TAP when all E / 8 values of a lane lie in one
+// tap (channels a multiple of 16), VEC4 when each float4 does.
 enum { SCALAR = 0, VEC4 = 1, TAP = 2 };
 
 // Convolution forward, A = input patches: A[m = (n, p, q)][kk = (r, s, c)] =
@@ -216,14 +258,15 @@ struct ConvPatch : RowK<E> {
       }
     }
   }
-  // value at (row j, column kk < kend) or 0
+  // value at (row j, column kk) or 0 when kk >= kend or outside the image
   __device__ float at(int j, int kk, int64_t kend) const {
-    if (kk >= kend) return 0.f;
-    const int r = dSC.div(kk);
-    const int rem = kk - r * (int)dSC.d;
+    const bool kin = kk < kend;
+    const int kc = kin ? kk : 0;
+    const int r = dSC.div(kc);
+    const int rem = kc - r * (int)dSC.d;
     const int s = dC.div(rem), c = rem - s * C;
-    if (!inside(h_[j] + r, H) || !inside(w_[j] + s, W)) return 0.f;
-    return x[base_[j] + ((int64_t)r * W + s) * C + c];
+    const bool ok = kin & inside(h_[j] + r, H) & inside(w_[j] + s, W);
+    return *(ok ? x + base_[j] + ((int64_t)r * W + s) * C + c : g_zero);
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
     const int kk = (int)k0 + Base::koff();
@@ -249,8 +292,8 @@ struct ConvPatch : RowK<E> {
       const bool kin = kk < kend;
 #pragma unroll
       for (int j = 0; j < Base::kN; ++j) {
-        const bool ok = kin && inside(h_[j] + rr, H) && inside(w_[j] + s, W);
-        r[j] = ok ? *reinterpret_cast<const float4*>(&x[base_[j] + toff]) : zero4();
+        const bool ok = kin & inside(h_[j] + rr, H) & inside(w_[j] + s, W);
+        r[j] = ld4(ok ? x + base_[j] + toff : g_zero);
       }
     }
   }
@@ -291,12 +334,13 @@ struct ConvGradTap : RowK<E> {
     }
   }
   __device__ float at(int j, int kk, int64_t kend) const {
-    if (kk >= kend) return 0.f;
-    const int i = dSK.div(kk);
-    const int rem = kk - i * (int)dSK.d;
+    const bool kin = kk < kend;
+    const int kc = kin ? kk : 0;
+    const int i = dSK.div(kc);
+    const int rem = kc - i * (int)dSK.d;
     const int jj = dK.div(rem), k = rem - jj * K;
-    if (!inside(p_[j] - i, P) || !inside(q_[j] - jj, Q)) return 0.f;
-    return dy[base_[j] - ((int64_t)i * Q + jj) * K + k];
+    const bool ok = kin & inside(p_[j] - i, P) & inside(q_[j] - jj, Q);
+    return *(ok ? dy + base_[j] - ((int64_t)i * Q + jj) * K + k : g_zero);
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
     const int kk = (int)k0 + Base::koff();
@@ -322,8 +366,8 @@ struct ConvGradTap : RowK<E> {
       const bool kin = kk < kend;
 #pragma unroll
       for (int j = 0; j < Base::kN; ++j) {
-        const bool ok = kin && inside(p_[j] - i, P) && inside(q_[j] - jj, Q);
-        r[j] = ok ? *reinterpret_cast<const float4*>(&dy[base_[j] + toff]) : zero4();
+        const bool ok = kin & inside(p_[j] - i, P) & inside(q_[j] - jj, Q);
+        r[j] = ld4(ok ? dy + base_[j] + toff : g_zero);
       }
     }
   }
@@ -338,33 +382,38 @@ struct ConvFilterTap : RowM<E> {
   int C, K, S, st, r0, s0, nS;
   int64_t RSC;
   FastDiv dK, dnS, dSK;
-  int c0;
-  __device__ void init(int64_t mn0, int64_t) { c0 = (int)mn0 + Base::moff(); }
+  int cc;                     // this lane's channel, clamped to the filter
+  int64_t roff_[Base::kN];    // this lane's k rows * RSC
+  __device__ void init(int64_t mn0, int64_t) {
+    const int c0 = (int)mn0 + Base::moff();
+    cc = c0 < C ? c0 : 0;
+#pragma unroll
+    for (int j = 0; j < Base::kN; ++j) roff_[j] = (int64_t)Base::krow(j) * RSC;
+  }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
     if constexpr (MODE == TAP) {   // uniform tap
       const int tap = dK.div((int)k0);
       const int i = dnS.div(tap), jj = tap - i * nS;
       const int kb = (int)k0 - tap * K;
-      const int64_t toff = ((int64_t)(r0 + st * i) * S + s0 + st * jj) * C + c0;
+      const float* base =
+          w + (int64_t)kb * RSC + ((int64_t)(r0 + st * i) * S + s0 + st * jj) * C + cc;
 #pragma unroll
       for (int j = 0; j < Base::kN; ++j) {
-        const bool ok = k0 + Base::krow(j) < kend && c0 < C;
-        r[j] = ok ? *reinterpret_cast<const float4*>(&w[(int64_t)(kb + Base::krow(j)) * RSC + toff])
-                  : zero4();
+        const bool ok = k0 + Base::krow(j) < kend;
+        r[j] = ld4(ok ? base + roff_[j] : g_zero);
       }
     } else {
 #pragma unroll
       for (int j = 0; j < Base::kN; ++j) {
         const int kk = (int)k0 + Base::krow(j);
-        if (kk < kend && c0 < C) {
-          const int i = dSK.div(kk);
-          const int rem = kk - i * (int)dSK.d;
-          const int jj = dK.div(rem), k = rem - jj * K;
-          r[j] = *reinterpret_cast<const float4*>(
-              &w[(int64_t)k * RSC + ((int64_t)(r0 + st * i) * S + s0 + st * jj) * C + c0]);
-        } else {
-          r[j] = zero4();
-        }
+        const bool ok = kk < kend;
+        const int kc = ok ? kk : 0;
+        const int i = dSK.div(kc);
+        const int rem = kc - i * (int)dSK.d;
+        const int jj = dK.div(rem), k = rem - jj * K;
+        int64_t off = (int64_t)k * RSC + ((int64_t)(r0 + st * i) * S + s0 + st * jj) * C + cc;
+        keep(off);
+        r[j] = ld4(ok ? w + off : g_zero);
       }
     }
   }
@@ -372,53 +421,64 @@ struct ConvFilterTap : RowM<E> {
 
 // Convolution filter gradient, B = input patches along the pixel axis:
 // B[kk = (n, p, q)][col = (r, s, c)] = X[n][p st - pad + r][q st - pad + s][c]
-// (row-of-m; VEC needs C % 4 == 0)
-template <int E, bool VEC>
-struct ConvPixelPatch : RowM<E> {
-  using Base = RowM<E>;
+// (row-of-m).  A lane's columns are clamped to the matrix, then split into
+// taps at set-up: one tap for all of them (TAP), one per float4 (VEC4) or one
+// per value (SCALAR).
+template <int E, int MODE>
+struct ConvPixelPatch : RowM1<E> {
+  using Base = RowM1<E>;
+  static constexpr int kT = MODE == TAP ? 1 : MODE == VEC4 ? Base::kN : 4 * Base::kN;
   const float* x;
   int H, W, C, st, pad;
   FastDiv dQ, dPQ, dC, dSC;
-  int64_t toff_[4];   // per column of this lane: (r W + s) C + c
-  int r_[4], s_[4];   // kFar: no column
+  int toff_[kT];          // (r W + s) C + c of each tap entry
+  int r_[kT], s_[kT];
   __device__ void init(int64_t mn0, int64_t RSC) {
-    const int col = (int)mn0 + Base::moff();
+    const int col0 = (int)mn0 + Base::moff();
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int cc = col + e;
-      if (cc < RSC && (VEC ? e == 0 : true)) {
-        const int r = dSC.div(cc);
-        const int rem = cc - r * (int)dSC.d;
-        const int s = dC.div(rem), c = rem - s * C;
-        r_[e] = r;
-        s_[e] = s;
-        toff_[e] = ((int64_t)r * W + s) * C + c;
-      } else {
-        r_[e] = kFar;
-        s_[e] = 0;
-        toff_[e] = 0;
-      }
+    for (int e = 0; e < kT; ++e) {
+      const int step = MODE == VEC4 ? 4 : 1;
+      const int cc = col0 + step * e < RSC ? col0 + step * e : 0;
+      const int r = dSC.div(cc);
+      const int rem = cc - r * (int)dSC.d;
+      const int s = dC.div(rem), c = rem - s * C;
+      r_[e] = r;
+      s_[e] = s;
+      toff_[e] = (r * W + s) * C + c;
     }
   }
   __device__ void fetch(int64_t k0, int64_t kend, float4 (&r)[Base::kN]) const {
+    const int kk = (int)k0 + Base::krow();
+    const bool kin = kk < kend;
+    const int kc = kin ? kk : 0;
+    const int n = dPQ.div(kc);
+    const int rem = kc - n * (int)dPQ.d;
+    const int p = dQ.div(rem), q = rem - p * (int)dQ.d;
+    const int hb = p * st - pad, wb = q * st - pad;
+    int64_t po = (((int64_t)n * H + hb) * W + wb) * C;
+    keep(po);
+    const float* pix = x + po;
+    if constexpr (MODE == TAP) {
+      const bool ok = kin & inside(hb + r_[0], H) & inside(wb + s_[0], W);
+      const float* src = ok ? pix + toff_[0] : g_zero;
 #pragma unroll
-    for (int j = 0; j < Base::kN; ++j) {
-      const int kk = (int)k0 + Base::krow(j);
-      r[j] = zero4();
-      if (kk >= kend) continue;
-      const int n = dPQ.div(kk);
-      const int rem = kk - n * (int)dPQ.d;
-      const int p = dQ.div(rem), q = rem - p * (int)dQ.d;
-      const int hb = p * st - pad, wb = q * st - pad;
-      const int64_t base = (((int64_t)n * H + hb) * W + wb) * C;
-      if (VEC) {
-        if (inside(hb + r_[0], H) && inside(wb + s_[0], W))
-          r[j] = *reinterpret_cast<const float4*>(&x[base + toff_[0]]);
-      } else {
+      for (int j = 0; j < Base::kN; ++j) r[j] = ld4(src + 4 * j);
+    } else if constexpr (MODE == VEC4) {
+#pragma unroll
+      for (int j = 0; j < Base::kN; ++j) {
+        const bool ok = kin & inside(hb + r_[j], H) & inside(wb + s_[j], W);
+        r[j] = ld4(ok ? pix + toff_[j] : g_zero);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < Base::kN; ++j) {
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          v[e] = (inside(hb + r_[e], H) && inside(wb + s_[e], W)) ? x[base + toff_[e]] : 0.f;
+        for (int e = 0; e < 4; ++e) {
+          const int u = 4 * j + e;
+          const bool ok = kin & inside(hb + r_[u], H) & inside(wb + s_[u], W);
+          v[e] = *(ok ? pix + toff_[u] : g_zero);
+        }
         r[j] = make_float4(v[0], v[1], v[2], v[3]);
       }
     }
@@ -468,8 +528,8 @@ __device__ inline void shift(L& l, int64_t d) {
   l.p += d;
 }
 
-// rowsum (optional): rowsum[slice][m] = sum over this slice's k of A[m][k]
-template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED>
+// ROWSUM: rowsum[slice][m] = sum over this slice's k of A[m][k]
+template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED, bool ROWSUM>
 __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __restrict__ c, OM om,
                                                        int64_t slice_stride,
                                                        const float* __restrict__ bias, int64_t M,
@@ -520,7 +580,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  const bool sums = rowsum != nullptr && tn == 0 && (int)threadIdx.x < BM;
+  const bool sums = ROWSUM && tn == 0 && (int)threadIdx.x < BM;
   float rs = 0.f;
 
   const int lane = threadIdx.x & 63;
@@ -529,29 +589,19 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
   const int half = lane >> 5;
   const int li = lane & 31;
 
-  if (kb < ke) {
-    la.fetch(kb, ke, ra);
-    lb.fetch(kb, ke, rb);
-    LA::store(As[0], ra);
-    LB::store(Bs[0], rb);
-  }
+  la.fetch(kb, ke, ra);
+  lb.fetch(kb, ke, rb);
+  LA::store(As[0], ra);
+  LB::store(Bs[0], rb);
   __syncthreads();
   int buf = 0;
   for (int64_t k0 = kb; k0 < ke; k0 += BK) {
-    const bool more = k0 + BK < ke;
-    if (more) {
-      la.fetch(k0 + BK, ke, ra);
-      lb.fetch(k0 + BK, ke, rb);
-    }
+    // the tile after the last one is all zeros: fetching and storing it anyway
+    // keeps the loop body free of branches
+    la.fetch(k0 + BK, ke, ra);
+    lb.fetch(k0 + BK, ke, rb);
     const float* A = As[buf];
     const float* B = Bs[buf];
-    if (sums) {
-#pragma unroll
-      for (int k = 0; k < BK; ++k) {
-        if constexpr (LA::kRowOfK) rs += A[threadIdx.x * LDK + k];
-        else rs += A[k * (LA::kLds / BK) + threadIdx.x];
-      }
-    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int kq = half * 16 + 4 * j;
@@ -569,10 +619,25 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
             acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a[mb], s), comp(b[nb], s),
                                                               acc[mb][nb], 0, 0, 0);
     }
-    if (more) {
-      LA::store(As[buf ^ 1], ra);
-      LB::store(Bs[buf ^ 1], rb);
+    if constexpr (ROWSUM) {
+      if (sums) {
+#pragma unroll
+        for (int k = 0; k < BK; ++k) {
+          if constexpr (LA::kRowOfK) rs += A[threadIdx.x * LDK + k];
+          else rs += A[k * (LA::kLds / BK) + threadIdx.x];
+        }
+      }
     }
+    // Issue the next tile's global loads one per two MFMAs from the start of
+    // the body, so that the MFMAs cover their latency; left alone, the
+    // scheduler sinks them next to the LDS stores that consume them.
+#pragma unroll
+    for (int g = 0; g < LA::kN + LB::kN; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // one global load
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // two MFMAs
+    }
+    LA::store(As[buf ^ 1], ra);
+    LB::store(Bs[buf ^ 1], rb);
     __syncthreads();
     buf ^= 1;
   }
@@ -594,7 +659,8 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
     }
 }
 
-template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED = false>
+template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED = false,
+          bool ROWSUM = false>
 hipError_t run_gemm(const LA& la, const LB& lb, float* c, OM om, int64_t slice_stride,
                     const float* bias, int64_t M, int64_t N, int64_t K, int64_t slices,
                     hipStream_t s, int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
@@ -606,7 +672,8 @@ hipError_t run_gemm(const LA& la, const LB& lb, float* c, OM om, int64_t slice_s
   int64_t k_slice = (K + slices - 1) / slices;
   k_slice = (k_slice + BK - 1) / BK * BK;
   dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices, (unsigned)batches);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, OM, BIAS, BATCHED>), grid, dim3(THREADS), 0, s,
+  if (ROWSUM != (rowsum != nullptr)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, OM, BIAS, BATCHED, ROWSUM>), grid, dim3(THREADS), 0, s,
                      la, lb, c, om, slice_stride, bias, M, N, K, k_slice, (int)tiles_m,
                      (int)tiles_n, bt, rowsum);
   return hipGetLastError();
@@ -627,7 +694,7 @@ Shape pick_shape(int64_t M, int64_t N) {
 // tile shape; `fa(a)` / `fb(b)` fill them in.  Row m of C starts at om.row(m);
 // split-K slices of C are slice_stride floats apart.
 template <template <int> class LAT, template <int> class LBT, bool BIAS, bool BATCHED = false,
-          class FA, class FB, class OM>
+          bool ROWSUM = false, class FA, class FB, class OM>
 hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const float* bias,
                     int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s,
                     int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
@@ -638,7 +705,7 @@ hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const f
       LBT<64> b{};
       fa(a);
       fb(b);
-      return run_gemm<128, 64, LAT<128>, LBT<64>, OM, BIAS, BATCHED>(
+      return run_gemm<128, 64, LAT<128>, LBT<64>, OM, BIAS, BATCHED, ROWSUM>(
           a, b, c, om, slice_stride, bias, M, N, K, slices, s, batches, bt, rowsum);
     }
     case S64x128: {
@@ -646,7 +713,7 @@ hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const f
       LBT<128> b{};
       fa(a);
       fb(b);
-      return run_gemm<64, 128, LAT<64>, LBT<128>, OM, BIAS, BATCHED>(
+      return run_gemm<64, 128, LAT<64>, LBT<128>, OM, BIAS, BATCHED, ROWSUM>(
           a, b, c, om, slice_stride, bias, M, N, K, slices, s, batches, bt, rowsum);
     }
     default: {
@@ -654,7 +721,7 @@ hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const f
       LBT<128> b{};
       fa(a);
       fb(b);
-      return run_gemm<128, 128, LAT<128>, LBT<128>, OM, BIAS, BATCHED>(
+      return run_gemm<128, 128, LAT<128>, LBT<128>, OM, BIAS, BATCHED, ROWSUM>(
           a, b, c, om, slice_stride, bias, M, N, K, slices, s, batches, bt, rowsum);
     }
   }
@@ -662,13 +729,13 @@ hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const f
 
 // row-major C with leading dimension ldc
 template <template <int> class LAT, template <int> class LBT, bool BIAS, bool BATCHED = false,
-          class FA, class FB>
+          bool ROWSUM = false, class FA, class FB>
 hipError_t dispatch_dense(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int64_t M,
                           int64_t N, int64_t K, int64_t slices, hipStream_t s,
                           int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
                           float* rowsum = nullptr) {
-  return dispatch<LAT, LBT, BIAS, BATCHED>(fa, fb, c, DenseOut{ldc}, M * ldc, bias, M, N, K, slices,
-                                           s, batches, bt, rowsum);
+  return dispatch<LAT, LBT, BIAS, BATCHED, ROWSUM>(fa, fb, c, DenseOut{ldc}, M * ldc, bias, M, N, K,
+                                                   slices, s, batches, bt, rowsum);
 }
 
 template <int E> using MatKv = MatK<E, true>;
@@ -683,8 +750,9 @@ template <int E> using ConvGradTapV = ConvGradTap<E, VEC4>;
 template <int E> using ConvGradTapS = ConvGradTap<E, SCALAR>;
 template <int E> using ConvFilterTapT = ConvFilterTap<E, TAP>;
 template <int E> using ConvFilterTapG = ConvFilterTap<E, VEC4>;
-template <int E> using ConvPixelPatchV = ConvPixelPatch<E, true>;
-template <int E> using ConvPixelPatchS = ConvPixelPatch<E, false>;
+template <int E> using ConvPixelPatchT = ConvPixelPatch<E, TAP>;
+template <int E> using ConvPixelPatchV = ConvPixelPatch<E, VEC4>;
+template <int E> using ConvPixelPatchS = ConvPixelPatch<E, SCALAR>;
 
 // the GEMM sizes of the convolution views index with 32-bit arithmetic
 bool fits31(int64_t v) { return v >= 0 && v < (int64_t(1) << 31) - 64; }
@@ -740,9 +808,11 @@ hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, f
   const Batch one{1, 0, 0, 0, 0, 0, 0};
   hipError_t e;
   if (N % 4 == 0 && K % 4 == 0 && aligned16(X) && aligned16(dY))
-    e = dispatch_dense<MatMv, MatMv, false>(fa, fb, out, K, nullptr, N, K, M, slices, s, 1, one, sums);
+    e = dispatch_dense<MatMv, MatMv, false, false, true>(fa, fb, out, K, nullptr, N, K, M, slices,
+                                                         s, 1, one, sums);
   else
-    e = dispatch_dense<MatMs, MatMs, false>(fa, fb, out, K, nullptr, N, K, M, slices, s, 1, one, sums);
+    e = dispatch_dense<MatMs, MatMs, false, false, true>(fa, fb, out, K, nullptr, N, K, M, slices,
+                                                         s, 1, one, sums);
   if (e != hipSuccess || slices <= 1) return e;
   hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((N * K + 255) / 256)), dim3(256), 0, s,
                      part, dW, N * K, slices);
@@ -841,7 +911,7 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
                       const ConvShape& c, hipStream_t s) {
   // dW[K][RSC] = sum over pixels of dY[pixel][k] * patch[pixel][rsc]
   const int64_t M = c.K, N = c.R * c.S * c.C, K = c.N * c.P * c.Q;
-  if (!fits31(K) || !fits31(N)) return hipErrorInvalidValue;
+  if (!fits31(K) || !fits31(N) || !fits31((c.R * c.W + c.S) * c.C)) return hipErrorInvalidValue;
   if (slices > 1 && part == nullptr) return hipErrorInvalidValue;
   float* out = slices > 1 ? part : dW;
   auto fa = [&](auto& a) { a.p = dY; a.ld = c.K; };
@@ -852,7 +922,10 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
   };
   hipError_t e;
   if (c.K % 4 == 0) {
-    if (c.C % 4 == 0)
+    if (c.C % 16 == 0)
+      e = dispatch_dense<MatMv, ConvPixelPatchT, false>(fa, fb, out, N, nullptr, M, N, K, slices,
+                                                        s);
+    else if (c.C % 4 == 0)
       e = dispatch_dense<MatMv, ConvPixelPatchV, false>(fa, fb, out, N, nullptr, M, N, K, slices,
                                                         s);
     else
