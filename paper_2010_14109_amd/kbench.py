@@ -5,7 +5,7 @@ with seeded inputs, runs it in-core REPS times through the library and prints
 its event-timed duration; under ``rocprofv3`` it gives clean per-kernel
 statistics and counters.  CASE is ``op:n1,n2,...``:
 
-* ``conv_fwd | conv_bwd_x | conv_bwd_w : N,H,W,C,K,k,stride,pad``
+* ``conv_fwd | conv_bwd_x | conv_bwd_w : N,H,W,C,K,k,stride,pad[,slices]``
 * ``linear_fwd | linear_bwd_x | linear_bwd_w : M,K,N``
 * ``relu_fwd : n``  (reads 4 n bytes, writes 4 n bytes: the calibration kernel)
 
@@ -45,14 +45,14 @@ def case(spec):
     if op == "relu_fwd":
         return op, [(v[0] * 4, I, R), (v[0] * 4, O, Wr)], [v[0]]
     if op.startswith("conv"):
-        N, H, W, C, K, k, st, pd = v
+        N, H, W, C, K, k, st, pd = v[:8]
         a, P, Q = _conv_attrs(N, H, W, C, K, k, st, pd)
         xb, wb, yb = N * H * W * C * 4, K * k * k * C * 4, N * P * Q * K * 4
         if op == "conv_fwd":
             return op, [(xb, I, R), (wb, I, R), (yb, O, Wr)], a
         if op == "conv_bwd_x":
             return op, [(wb, I, R), (yb, I, R), (xb, O, Wr)], a
-        s = netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q)
+        s = v[8] if len(v) > 8 else netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q)
         vs = [(xb, I, R), (yb, I, R), (wb, O, Wr)] + ([(s * wb, O, Wr)] if s > 1 else [])
         return op, vs, a + [s]
     M, K, N = v
