@@ -86,8 +86,18 @@ def ln_slices(rows):
 
 
 def conv_wgrad_slices(K, RSC, L):
-    tiles = math.ceil(K / 128) * math.ceil(RSC / 128)
-    return max(1, min(math.ceil(1024 / tiles), math.ceil(L / 1024)))
+    """Partial-sum copies of a weight gradient (K x RSC outputs reduced over L rows).  The count
+    is a blocking choice of the GPU kernels that the function sequence carries (it sizes the
+    partials variable), so the lowering reproduces it: 256 compute units times the workgroups
+    each holds (3 when one side of the output is at most 64, else 2) divided by the output tiles
+    (128-wide, 64 on a side of at most 64), at least 256 rows per slice."""
+    if K <= 64:
+        tiles, per_cu = math.ceil(RSC / 128), 3
+    elif RSC <= 64:
+        tiles, per_cu = math.ceil(K / 128), 3
+    else:
+        tiles, per_cu = math.ceil(K / 128) * math.ceil(RSC / 128), 2
+    return max(1, min(256 * per_cu // tiles, math.ceil(L / 256)))
 
 
 def lower(spec, keep_grads=False):

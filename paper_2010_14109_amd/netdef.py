@@ -44,9 +44,23 @@ def ln_row_slices(rows):
     return min(ceil(rows / 32), 2048)
 
 
+GPU_CUS = 256   # compute units of an MI355X
+
+
 def wgrad_pixel_slices(k_out, rsc, pixels):
-    tiles = ceil(k_out / 128) * ceil(rsc / 128)
-    return max(1, min(ceil(1024 / tiles), ceil(pixels / 1024)))
+    """Split-K slices of a weight-gradient GEMM (k_out x rsc outputs, reduced over ``pixels``).
+
+    As many as make the workgroups fill exactly one round of the GPU: 256 CUs holding three
+    workgroups each for the 64-wide tile shapes, two for 128 x 128 tiles (LDS bounds the
+    residency).  A partly filled second round would leave most CUs idle behind a few.  Slices
+    keep at least 256 pixels each."""
+    if k_out <= 64:
+        tiles, resident = ceil(rsc / 128), 3
+    elif rsc <= 64:
+        tiles, resident = ceil(k_out / 128), 3
+    else:
+        tiles, resident = ceil(k_out / 128) * ceil(rsc / 128), 2
+    return max(1, min(GPU_CUS * resident // tiles, ceil(pixels / 256)))
 
 
 class Net:
