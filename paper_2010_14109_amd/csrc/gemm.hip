@@ -758,20 +758,41 @@ template <int E> using ConvPixelPatchS = ConvPixelPatch<E, SCALAR>;
 bool fits31(int64_t v) { return v >= 0 && v < (int64_t(1) << 31) - 64; }
 
 // ---------------------------------------------------------------- small kernels
-// out[j] = sum over slices of part[s][j]: four interleaved accumulators
-// (slices s = u mod 4), added in a fixed order
-__global__ void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
-                                 int64_t n, int64_t slices) {
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= n) return;
-  float a[4] = {0.f, 0.f, 0.f, 0.f};
-  int64_t s = 0;
-  for (; s + 4 <= slices; s += 4) {
+// out[j] = sum over slices of part[s][j].  A workgroup covers 64 consecutive
+// j, one per lane; wave w takes the slices s = w mod 4 in eight interleaved
+// chains (s / 4 mod 8), so that each lane has eight loads in flight, and the
+// partial sums are added in a fixed order: the result does not depend on
+// timing.
+constexpr int SUM_J = 64;
+__global__ __launch_bounds__(256) void slice_sum_kernel(const float* __restrict__ part,
+                                                        float* __restrict__ out, int64_t n,
+                                                        int64_t slices) {
+  __shared__ float red[4][SUM_J];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t j = (int64_t)blockIdx.x * SUM_J + lane;
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (j < n) {
+    int64_t s = w;
+    for (; s + 28 < slices; s += 32) {
+      float v[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) a[u] += part[(s + u) * n + j];
+      for (int u = 0; u < 8; ++u) v[u] = part[(s + 4 * u) * n + j];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) a[u] += v[u];
+    }
+#pragma unroll
+    for (int u = 0; u < 7; ++u)
+      if (s + 4 * u < slices) a[u] += part[(s + 4 * u) * n + j];
   }
-  for (; s < slices; ++s) a[0] += part[s * n + j];
-  out[j] = (a[0] + a[1]) + (a[2] + a[3]);
+  red[w][lane] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+  __syncthreads();
+  if (w == 0 && j < n) out[j] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+}
+
+hipError_t slice_sum(const float* part, float* out, int64_t n, int64_t slices, hipStream_t s) {
+  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((n + SUM_J - 1) / SUM_J)), dim3(256), 0, s,
+                     part, out, n, slices);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -814,11 +835,9 @@ hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, f
     e = dispatch_dense<MatMs, MatMs, false, false, true>(fa, fb, out, K, nullptr, N, K, M, slices,
                                                          s, 1, one, sums);
   if (e != hipSuccess || slices <= 1) return e;
-  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((N * K + 255) / 256)), dim3(256), 0, s,
-                     part, dW, N * K, slices);
-  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s, sums, db,
-                     N, slices);
-  return hipGetLastError();
+  e = slice_sum(part, dW, N * K, slices, s);
+  if (e != hipSuccess) return e;
+  return slice_sum(sums, db, N, slices, s);
 }
 
 hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, const float* B,
@@ -935,10 +954,7 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
     e = dispatch_dense<MatMs, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
   }
   if (e != hipSuccess || slices <= 1) return e;
-  const int64_t n = M * N;
-  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part,
-                     dW, n, slices);
-  return hipGetLastError();
+  return slice_sum(part, dW, M * N, slices, s);
 }
 
 }  // namespace ooc
