@@ -85,13 +85,19 @@ def ln_slices(rows):
     return min(math.ceil(rows / 32), 2048)
 
 
-def conv_wgrad_slices(K, RSC, L):
-    """Partial-sum copies of a weight gradient (K x RSC outputs reduced over L rows).  The count
-    is a blocking choice of the GPU kernels that the function sequence carries (it sizes the
-    partials variable), so the lowering reproduces it: 256 compute units times the workgroups
-    each holds (3 when one side of the output is at most 64, else 2) divided by the output tiles
-    (128-wide, 64 on a side of at most 64), at least 256 rows per slice."""
-    if K <= 64:
+def conv_wgrad_slices(K, RSC, L, C=None):
+    """Partial-sum copies of a weight gradient (K x RSC outputs reduced over L rows; C input
+    channels of a convolution, None for a dense layer).  The count is a blocking choice of the
+    GPU kernels that the function sequence carries (it sizes the partials variable), so the
+    lowering reproduces it: 256 compute units times the workgroups each holds divided by the
+    output tiles, at least 256 rows per slice.  Tiles are 64 x 192 (2 per CU) for a convolution
+    with K <= 64, K and C multiples of 4 and fewer padded RSC columns that way than with
+    128-wide tiles; else 64 on a side of at most 64 (3 per CU) and 128 x 128 otherwise (2)."""
+    pad128 = math.ceil(RSC / 128) * 128 - RSC
+    pad192 = math.ceil(RSC / 192) * 192 - RSC
+    if C is not None and K <= 64 and K % 4 == 0 and C % 4 == 0 and pad192 < pad128:
+        tiles, per_cu = math.ceil(RSC / 192), 2
+    elif K <= 64:
         tiles, per_cu = math.ceil(RSC / 128), 3
     elif RSC <= 64:
         tiles, per_cu = math.ceil(K / 128), 3
@@ -302,7 +308,7 @@ def lower(spec, keep_grads=False):
             attrs = {"N": n, "H": h, "W": w, "C": c, "K": K, "R": k, "S": k,
                      "stride": L["stride"], "pad": L["pad"], "P": P, "Q": Q}
             dW = var("d:" + Wn, decl[Wn][0], kind=grad_kind)
-            Sw = conv_wgrad_slices(K, k * k * c, n * P * Q)
+            Sw = conv_wgrad_slices(K, k * k * c, n * P * Q, c)
             vs = [(X, R), (dY, R), (dW, W)]
             if Sw > 1:
                 vs.append((var(name + ".part", (Sw * K * k * k * c,)), W))

@@ -537,6 +537,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
                                                        int tiles_m, int tiles_n, Batch bt,
                                                        float* __restrict__ rowsum) {
   constexpr int MB = BM / 64, NB = BN / 64;
+  constexpr bool kLoadsFirst = BN > 128;
   // Workgroup (tile, slice, batch) from an XCD-aware order: the hardware hands
   // linear workgroup h to XCD h mod 8, so logical ids are laid out so that each
   // XCD (with its own L2) gets one contiguous run of them, and neighbouring
@@ -600,6 +601,10 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
     // keeps the loop body free of branches
     la.fetch(k0 + BK, ke, ra);
     lb.fetch(k0 + BK, ke, rb);
+    // 192-wide tiles issue all their loads before the MFMAs: their address
+    // arithmetic is long enough that the interleave below would place the
+    // loads late (measured 2-4 % slower)
+    if constexpr (kLoadsFirst) __builtin_amdgcn_sched_barrier(0);
     const float* A = As[buf];
     const float* B = Bs[buf];
 #pragma unroll
@@ -631,10 +636,12 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
     // Issue the next tile's global loads one per two MFMAs from the start of
     // the body, so that the MFMAs cover their latency; left alone, the
     // scheduler sinks them next to the LDS stores that consume them.
+    if constexpr (!kLoadsFirst) {
 #pragma unroll
-    for (int g = 0; g < LA::kN + LB::kN; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // one global load
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // two MFMAs
+      for (int g = 0; g < LA::kN + LB::kN; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // one global load
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // two MFMAs
+      }
     }
     LA::store(As[buf ^ 1], ra);
     LB::store(Bs[buf ^ 1], rb);
@@ -756,6 +763,15 @@ template <int E> using ConvPixelPatchS = ConvPixelPatch<E, SCALAR>;
 
 // the GEMM sizes of the convolution views index with 32-bit arithmetic
 bool fits31(int64_t v) { return v >= 0 && v < (int64_t(1) << 31) - 64; }
+
+// A filter gradient with at most 64 output channels (M) runs on 64 x 192 tiles
+// when those leave fewer padded columns of RSC (N) than 64 x 128 tiles do
+// (RSC = 576 for a 3 x 3 x 64 filter: 3 full tiles instead of 4.5); it needs
+// four-aligned channels.
+bool wgrad_wide_tile(int64_t M, int64_t N, int64_t C) {
+  const int64_t pad128 = (N + 127) / 128 * 128 - N, pad192 = (N + 191) / 192 * 192 - N;
+  return M <= 64 && M % 4 == 0 && C % 4 == 0 && pad192 < pad128;
+}
 
 // ---------------------------------------------------------------- small kernels
 // out[j] = sum over slices of part[s][j].  A workgroup covers 64 consecutive
@@ -940,7 +956,15 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
     b.dC = FastDiv::make(c.C); b.dSC = FastDiv::make(c.S * c.C);
   };
   hipError_t e;
-  if (c.K % 4 == 0) {
+  if (wgrad_wide_tile(M, N, c.C)) {
+    // 64 x 192 tiles: no tile column half empty when RSC is an odd multiple of 64
+    MatM<64, true> a{};
+    ConvPixelPatch<192, VEC4> b{};
+    fa(a);
+    fb(b);
+    e = run_gemm<64, 192, MatM<64, true>, ConvPixelPatch<192, VEC4>, DenseOut, false>(
+        a, b, out, DenseOut{N}, M * N, nullptr, M, N, K, slices, s);
+  } else if (c.K % 4 == 0) {
     if (c.C % 16 == 0)
       e = dispatch_dense<MatMv, ConvPixelPatchT, false>(fa, fb, out, N, nullptr, M, N, K, slices,
                                                         s);

@@ -6,7 +6,7 @@ its event-timed duration; under ``rocprofv3`` it gives clean per-kernel
 statistics and counters.  CASE is ``op:n1,n2,...``:
 
 * ``conv_fwd | conv_bwd_x | conv_bwd_w : N,H,W,C,K,k,stride,pad[,slices]``
-* ``linear_fwd | linear_bwd_x | linear_bwd_w : M,K,N``
+* ``linear_fwd | linear_bwd_x : M,K,N``, ``linear_bwd_w : M,K,N[,slices]``
 * ``relu_fwd : n``  (reads 4 n bytes, writes 4 n bytes: the calibration kernel)
 
 ``python -m paper_2010_14109_amd.kbench --traffic FETCH_DIR WRITE_DIR CAL_DIR``
@@ -52,19 +52,19 @@ def case(spec):
             return op, [(xb, I, R), (wb, I, R), (yb, O, Wr)], a
         if op == "conv_bwd_x":
             return op, [(wb, I, R), (yb, I, R), (xb, O, Wr)], a
-        s = v[8] if len(v) > 8 else netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q)
+        s = v[8] if len(v) > 8 else netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q, C)
         vs = [(xb, I, R), (yb, I, R), (wb, O, Wr)] + ([(s * wb, O, Wr)] if s > 1 else [])
         return op, vs, a + [s]
-    M, K, N = v
+    M, K, N = v[:3]
     if op == "linear_fwd":
         return op, [(M * K * 4, I, R), (N * K * 4, I, R), (N * 4, I, R), (M * N * 4, O, Wr)], v
     if op == "linear_bwd_x":
         return op, [(N * K * 4, I, R), (M * N * 4, I, R), (M * K * 4, O, Wr)], v
-    s = netdef.wgrad_pixel_slices(N, K, M)
+    s = v[3] if len(v) > 3 else netdef.wgrad_pixel_slices(N, K, M)
     vs = [(M * K * 4, I, R), (M * N * 4, I, R), (N * K * 4, O, Wr), (N * 4, O, Wr)]
     if s > 1:
         vs.append((s * (N * K + N) * 4, O, Wr))
-    return op, vs, v + [s]
+    return op, vs, [M, K, N, s]
 
 
 def run(spec, reps=20):

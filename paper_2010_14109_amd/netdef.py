@@ -47,14 +47,25 @@ def ln_row_slices(rows):
 GPU_CUS = 256   # compute units of an MI355X
 
 
-def wgrad_pixel_slices(k_out, rsc, pixels):
-    """Split-K slices of a weight-gradient GEMM (k_out x rsc outputs, reduced over ``pixels``).
+def wgrad_wide_tile(k_out, rsc, channels):
+    """Whether a filter gradient runs on 64 x 192 tiles (the GEMM library's rule): at most 64
+    four-aligned output channels, four-aligned input channels, and fewer padded RSC columns
+    than with 128-wide tiles."""
+    pad128, pad192 = ceil(rsc / 128) * 128 - rsc, ceil(rsc / 192) * 192 - rsc
+    return k_out <= 64 and k_out % 4 == 0 and channels % 4 == 0 and pad192 < pad128
+
+
+def wgrad_pixel_slices(k_out, rsc, pixels, channels=None):
+    """Split-K slices of a weight-gradient GEMM (k_out x rsc outputs, reduced over ``pixels``;
+    ``channels`` is the input channel count of a filter gradient, None for a dense layer).
 
     As many as make the workgroups fill exactly one round of the GPU: 256 CUs holding three
-    workgroups each for the 64-wide tile shapes, two for 128 x 128 tiles (LDS bounds the
-    residency).  A partly filled second round would leave most CUs idle behind a few.  Slices
-    keep at least 256 pixels each."""
-    if k_out <= 64:
+    workgroups each for the 64-wide tile shapes, two for 128 x 128 and 64 x 192 tiles (LDS
+    bounds the residency).  A partly filled second round would leave most CUs idle behind a
+    few.  Slices keep at least 256 pixels each."""
+    if channels is not None and wgrad_wide_tile(k_out, rsc, channels):
+        tiles, resident = ceil(rsc / 192), 2
+    elif k_out <= 64:
         tiles, resident = ceil(rsc / 128), 3
     elif rsc <= 64:
         tiles, resident = ceil(k_out / 128), 3
@@ -258,7 +269,7 @@ class Net:
             (W,) = self.params[name]
             a = self._conv_attrs(L, xs)
             n, _, _, c, K, R, S, _, _, P, Q = a
-            sw = wgrad_pixel_slices(K, R * S * c, n * P * Q)
+            sw = wgrad_pixel_slices(K, R * S * c, n * P * Q, c)
             pairs = [(X, ooc.R), (dY, ooc.R), (self._grad_of_param(W), ooc.W)]
             if sw > 1:
                 pairs.append((self._decl(name + ".part", (sw * K * R * S * c,)), ooc.W))

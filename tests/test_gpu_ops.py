@@ -111,6 +111,9 @@ CONVS = [  # N, H, W, C, K, k, stride, pad
     (2, 7, 7, 32, 36, 5, 2, 2),
     (1, 8, 7, 4, 6, 3, 3, 1),
     (1, 4, 4, 32, 32, 1, 3, 0),
+    # filter gradients on 64 x 192 tiles whose last tile is ragged (RSC 540 and 180)
+    (2, 9, 9, 60, 20, 3, 1, 1),
+    (1, 7, 6, 20, 64, 3, 2, 1),
 ]
 
 
@@ -124,7 +127,7 @@ def test_conv(shape):
     (_, _, Y) = run_fn("conv_fwd", [(X, ooc.R), (Wt, ooc.R), (((N, P, Q, K), "f32"), ooc.W)], a)
     assert rel_l2(Y, ops.conv_fwd(d(X), d(Wt), st, pd)) < TOL
     ref_dW = ops.conv_bwd_w(d(X), d(G), Wt.shape, st, pd)
-    for slices in sorted({1, netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q), 3, 7}):
+    for slices in sorted({1, netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q, C), 3, 7}):
         slices = min(slices, N * P * Q)
         args = [(X, ooc.R), (G, ooc.R), (((K, k, k, C), "f32"), ooc.W)]
         if slices > 1:
