@@ -89,10 +89,12 @@ def conv_wgrad_slices(K, RSC, L, C=None):
     """Partial-sum copies of a weight gradient (K x RSC outputs reduced over L rows; C input
     channels of a convolution, None for a dense layer).  The count is a blocking choice of the
     GPU kernels that the function sequence carries (it sizes the partials variable), so the
-    lowering reproduces it: 256 compute units times the workgroups each holds divided by the
-    output tiles, at least 256 rows per slice.  Tiles are 64 x 192 (2 per CU) for a convolution
-    with K <= 64, K and C multiples of 4 and fewer padded RSC columns that way than with
-    128-wide tiles; else 64 on a side of at most 64 (3 per CU) and 128 x 128 otherwise (2)."""
+    lowering reproduces it.  With slots = 256 compute units times the workgroups each holds,
+    the count s minimises ceil(tiles s / slots) / s over 1 <= s <= min(4 slots / tiles,
+    L / 256 rounded up), taking the smallest s within 1 % of the minimum.  Tiles are 64 x 192
+    (2 per CU) for a convolution with K <= 64, K and C multiples of 4 and fewer padded RSC
+    columns that way than with 128-wide tiles; else 64 on a side of at most 64 (3 per CU) and
+    128 x 128 otherwise (2)."""
     pad128 = math.ceil(RSC / 128) * 128 - RSC
     pad192 = math.ceil(RSC / 192) * 192 - RSC
     if C is not None and K <= 64 and K % 4 == 0 and C % 4 == 0 and pad192 < pad128:
@@ -103,7 +105,13 @@ def conv_wgrad_slices(K, RSC, L, C=None):
         tiles, per_cu = math.ceil(K / 128), 3
     else:
         tiles, per_cu = math.ceil(K / 128) * math.ceil(RSC / 128), 2
-    return max(1, min(256 * per_cu // tiles, math.ceil(L / 256)))
+    slots = 256 * per_cu
+    smax = max(1, min(4 * slots // tiles, math.ceil(L / 256)))
+    ratio = [math.ceil(tiles * s / slots) / s for s in range(1, smax + 1)]
+    lowest = min(ratio)
+    for s in range(1, smax + 1):
+        if ratio[s - 1] <= lowest * 1.01:
+            return s
 
 
 def lower(spec, keep_grads=False):

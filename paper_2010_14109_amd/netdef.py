@@ -59,10 +59,11 @@ def wgrad_pixel_slices(k_out, rsc, pixels, channels=None):
     """Split-K slices of a weight-gradient GEMM (k_out x rsc outputs, reduced over ``pixels``;
     ``channels`` is the input channel count of a filter gradient, None for a dense layer).
 
-    As many as make the workgroups fill exactly one round of the GPU: 256 CUs holding three
-    workgroups each for the 64-wide tile shapes, two for 128 x 128 and 64 x 192 tiles (LDS
-    bounds the residency).  A partly filled second round would leave most CUs idle behind a
-    few.  Slices keep at least 256 pixels each."""
+    The GPU holds 256 CUs x (3 workgroups for the 64-wide tile shapes, 2 for 128 x 128 and
+    64 x 192 tiles; LDS bounds the residency) at once.  A launch of tiles x s workgroups takes
+    ceil(tiles s / slots) rounds of K / s pixels each, so s minimises rounds / s: a partly
+    filled last round leaves most CUs idle behind a few.  The smallest s within 1 % of the best
+    is taken (fewer partial sums), with at most four rounds and at least 256 pixels a slice."""
     if channels is not None and wgrad_wide_tile(k_out, rsc, channels):
         tiles, resident = ceil(rsc / 192), 2
     elif k_out <= 64:
@@ -71,7 +72,11 @@ def wgrad_pixel_slices(k_out, rsc, pixels, channels=None):
         tiles, resident = ceil(k_out / 128), 3
     else:
         tiles, resident = ceil(k_out / 128) * ceil(rsc / 128), 2
-    return max(1, min(GPU_CUS * resident // tiles, ceil(pixels / 256)))
+    slots = GPU_CUS * resident
+    smax = max(1, min(4 * slots // tiles, ceil(pixels / 256)))
+    cost = [ceil(tiles * s / slots) / s for s in range(1, smax + 1)]
+    best = min(cost)
+    return next(s for s, c in enumerate(cost, 1) if c <= best * 1.01)
 
 
 class Net:
