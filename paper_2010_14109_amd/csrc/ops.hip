@@ -8,6 +8,7 @@
 // depend on scheduling or on where a variable lives.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "kernels.h"
@@ -221,23 +222,25 @@ __global__ void bn_partials(const float* __restrict__ x, const float* __restrict
   }
 }
 
-// combine slice partials (double) in a fixed order: wave w of the workgroup
-// sums slices w, w + 4, ... with four interleaved accumulators, then the four
-// waves are added in order.  Forward -> mean, invstd; backward -> dgamma, dbeta.
-template <int MODE>
-__global__ __launch_bounds__(TPB) void bn_finalize(const float* __restrict__ x,
-                                                   const float* __restrict__ part,
-                                                   float* __restrict__ head,
-                                                   float* __restrict__ dgamma,
-                                                   float* __restrict__ dbeta, int64_t rows,
-                                                   int64_t C, int64_t slices) {
+// Slice partials are combined in fp64 and in a fixed order, in two passes so
+// that a layer with few channels and many slices still spreads over the GPU.
+// Pass 1 (more than 256 slices): workgroup (channel group, slice group g) sums its
+// group's slices for 64 channels, wave w taking the slices w, w + 4, ... of
+// the group in four interleaved chains, the waves added in order.  The group
+// owns at least two slices; once all its waves have read them, it stores the
+// two fp64 sums of each channel as bit halves in that channel's own columns of
+// its first two slices, which no other workgroup reads.
+__global__ __launch_bounds__(TPB) void bn_group_sums(float* __restrict__ part, int64_t C,
+                                                     int64_t slices, int64_t per, int64_t groups) {
   __shared__ double sa[4][64], sb[4][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+  const int64_t g = blockIdx.y;
+  const int64_t s0 = g * per, s1 = g + 1 == groups ? slices : s0 + per;
   double a[4] = {0, 0, 0, 0}, b[4] = {0, 0, 0, 0};
   if (c < C) {
-    int64_t s = w;
-    for (; s + 12 < slices; s += 16) {
+    int64_t s = s0 + w;
+    for (; s + 12 < s1; s += 16) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const float* p = part + (s + 4 * u) * 2 * C;
@@ -245,10 +248,73 @@ __global__ __launch_bounds__(TPB) void bn_finalize(const float* __restrict__ x,
         b[u] += p[C + c];
       }
     }
-    for (; s < slices; s += 4) {
+    for (int u = 0; s < s1; s += 4, ++u) {
       const float* p = part + s * 2 * C;
-      a[0] += p[c];
-      b[0] += p[C + c];
+      a[u] += p[c];
+      b[u] += p[C + c];
+    }
+  }
+  sa[w][lane] = (a[0] + a[1]) + (a[2] + a[3]);
+  sb[w][lane] = (b[0] + b[1]) + (b[2] + b[3]);
+  __syncthreads();
+  if (w != 0 || c >= C) return;
+  const double ta = ((sa[0][lane] + sa[1][lane]) + sa[2][lane]) + sa[3][lane];
+  const double tb = ((sb[0][lane] + sb[1][lane]) + sb[2][lane]) + sb[3][lane];
+  float* p0 = part + s0 * 2 * C;
+  float* p1 = p0 + 2 * C;
+  p0[c] = __int_as_float(__double2loint(ta));
+  p0[C + c] = __int_as_float(__double2hiint(ta));
+  p1[c] = __int_as_float(__double2loint(tb));
+  p1[C + c] = __int_as_float(__double2hiint(tb));
+}
+
+// Pass 2 adds, per channel, either the fp64 sums of the slice groups
+// (GROUPED) or the slices' float partials.  Wave w takes the terms w, w + 4,
+// ... in four interleaved chains (term w + 4 u + 16 i goes to chain u), the
+// chains and then the four waves are added in order.  Forward -> mean, invstd;
+// backward -> dgamma, dbeta.
+template <bool GROUPED>
+__device__ inline void bn_term(const float* part, int64_t C, int64_t per, int64_t t, int64_t c,
+                               double& a, double& b) {
+  const float* p0 = part + t * per * 2 * C;
+  if (GROUPED) {
+    const float* p1 = p0 + 2 * C;
+    a = __hiloint2double(__float_as_int(p0[C + c]), __float_as_int(p0[c]));
+    b = __hiloint2double(__float_as_int(p1[C + c]), __float_as_int(p1[c]));
+  } else {
+    a = p0[c];
+    b = p0[C + c];
+  }
+}
+
+template <int MODE, bool GROUPED>
+__global__ __launch_bounds__(TPB) void bn_finalize(const float* __restrict__ x,
+                                                   const float* __restrict__ part,
+                                                   float* __restrict__ head,
+                                                   float* __restrict__ dgamma,
+                                                   float* __restrict__ dbeta, int64_t rows,
+                                                   int64_t C, int64_t per, int64_t terms) {
+  __shared__ double sa[4][64], sb[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+  double a[4] = {0, 0, 0, 0}, b[4] = {0, 0, 0, 0};
+  if (c < C) {
+    int64_t t = w;
+    for (; t + 12 < terms; t += 16) {
+      double va[4], vb[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) bn_term<GROUPED>(part, C, per, t + 4 * u, c, va[u], vb[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a[u] += va[u];
+        b[u] += vb[u];
+      }
+    }
+    for (int u = 0; t < terms; t += 4, ++u) {
+      double va, vb;
+      bn_term<GROUPED>(part, C, per, t, c, va, vb);
+      a[u] += va;
+      b[u] += vb;
     }
   }
   sa[w][lane] = (a[0] + a[1]) + (a[2] + a[3]);
@@ -267,6 +333,30 @@ __global__ __launch_bounds__(TPB) void bn_finalize(const float* __restrict__ x,
     dbeta[c] = (float)ta;
     dgamma[c] = (float)tb;
   }
+}
+
+// The slice reduction over stats' partials (after the 2 C head): one pass up
+// to 256 slices, else pass 1 into at most 64 groups of at least two slices
+// (the last group takes the remainder) and pass 2 over the groups.
+constexpr int64_t kOnePassSlices = 256;
+template <int MODE>
+hipError_t bn_reduce(const float* x, float* stats, float* dgamma, float* dbeta, int64_t rows,
+                     int64_t C, int64_t slices, hipStream_t s) {
+  const unsigned cg = (unsigned)((C + 63) / 64);
+  float* part = stats + 2 * C;
+  if (slices <= kOnePassSlices) {
+    hipLaunchKernelGGL((bn_finalize<MODE, false>), dim3(cg), dim3(TPB), 0, s, x, part, stats,
+                       dgamma, dbeta, rows, C, (int64_t)1, slices);
+    return hipGetLastError();
+  }
+  const int64_t groups = std::min<int64_t>(64, slices / 2), per = slices / groups;
+  hipLaunchKernelGGL(bn_group_sums, dim3(cg, (unsigned)groups), dim3(TPB), 0, s, part, C, slices,
+                     per, groups);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((bn_finalize<MODE, true>), dim3(cg), dim3(TPB), 0, s, x, part, stats, dgamma,
+                     dbeta, rows, C, per, groups);
+  return hipGetLastError();
 }
 
 // forward: y = (x - mean) invstd gamma + beta; backward:
@@ -538,9 +628,7 @@ hipError_t bn_fwd(const float* x, const float* gamma, const float* beta, float* 
                      stats, sm, C);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(bn_finalize<0>, dim3(cg), dim3(TPB), 0, s, x, stats + 2 * C, stats, nullptr,
-                     nullptr, rows, C, slices);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = bn_reduce<0>(x, stats, nullptr, nullptr, rows, C, slices, s)) != hipSuccess) return e;
   const bool vec = C % 4 == 0 && aligned16(x) && aligned16(y);
   hipLaunchKernelGGL(bn_apply<0>, dim3(grid_for((rows * C + 3) / 4)), dim3(TPB), 0, s, x, nullptr,
                      stats, gamma, beta, nullptr, y, rows, C, vec);
@@ -556,9 +644,7 @@ hipError_t bn_bwd(const float* x, const float* gamma, float* stats, const float*
                      C);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(bn_finalize<1>, dim3(cg), dim3(TPB), 0, s, x, stats + 2 * C, stats, dgamma,
-                     dbeta, rows, C, slices);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = bn_reduce<1>(x, stats, dgamma, dbeta, rows, C, slices, s)) != hipSuccess) return e;
   const bool vec = C % 4 == 0 && aligned16(x) && aligned16(dy) && aligned16(dx);
   // backward uses beta's slot for dbeta: dx = gamma invstd (dy - dbeta/rows - xhat dgamma/rows)
   hipLaunchKernelGGL(bn_apply<1>, dim3(grid_for((rows * C + 3) / 4)), dim3(TPB), 0, s, x, dy,

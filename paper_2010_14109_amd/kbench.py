@@ -8,6 +8,7 @@ statistics and counters.  CASE is ``op:n1,n2,...``:
 * ``conv_fwd | conv_bwd_x | conv_bwd_w : N,H,W,C,K,k,stride,pad[,slices]``
 * ``linear_fwd | linear_bwd_x : M,K,N``, ``linear_bwd_w : M,K,N[,slices]``
 * ``relu_fwd : n``  (reads 4 n bytes, writes 4 n bytes: the calibration kernel)
+* ``bn_fwd | bn_bwd : rows,C``  (training-mode batch normalisation over ``rows`` NHWC pixels)
 
 ``python -m paper_2010_14109_amd.kbench --traffic FETCH_DIR WRITE_DIR CAL_DIR``
 turns ``rocprofv3 --pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` output of a case
@@ -44,6 +45,14 @@ def case(spec):
     I, O, R, Wr = ooc.INPUT, ooc.OUTPUT, ooc.R, ooc.W
     if op == "relu_fwd":
         return op, [(v[0] * 4, I, R), (v[0] * 4, O, Wr)], [v[0]]
+    if op in ("bn_fwd", "bn_bwd"):
+        rows, C = v
+        s = netdef.bn_row_slices(rows)
+        xb, cb, sb = rows * C * 4, C * 4, (2 + 2 * s) * C * 4
+        if op == "bn_fwd":
+            return op, [(xb, I, R), (cb, I, R), (cb, I, R), (xb, O, Wr), (sb, O, Wr)], [rows, C, s]
+        return op, [(xb, I, R), (cb, I, R), (sb, ooc.STATE, ooc.RW), (xb, I, R), (xb, O, Wr),
+                    (cb, O, Wr), (cb, O, Wr)], [rows, C, s]
     if op.startswith("conv"):
         N, H, W, C, K, k, st, pd = v[:8]
         a, P, Q = _conv_attrs(N, H, W, C, K, k, st, pd)
@@ -78,8 +87,10 @@ def run(spec, reps=20):
         ctx.prepare()
         rng = np.random.default_rng(0)
         for (b, k, _), v in zip(vs, ids):
-            if k == ooc.INPUT:
-                ctx.host_view(v, np.float32)[...] = rng.standard_normal(b // 4).astype(np.float32)
+            if k in (ooc.INPUT, ooc.STATE):
+                # |N(0,1)| keeps a batch-norm inverse deviation positive
+                ctx.host_view(v, np.float32)[...] = np.abs(rng.standard_normal(b // 4)).astype(
+                    np.float32) if k == ooc.STATE else rng.standard_normal(b // 4).astype(np.float32)
         ctx.upload()
         ctx.step(0.0, 0.0)
         t0 = time.perf_counter()
