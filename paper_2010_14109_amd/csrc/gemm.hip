@@ -23,9 +23,10 @@
 // The input gradient of a strided convolution is computed per stride class
 // of input pixels (h mod st, w mod st), each class a GEMM over only the taps
 // that reach it.  LDS layout follows the contiguous direction: "row of k" tiles
-// ([rows][32 + 4]) are written and read with 16-byte accesses, "row of m"
-// tiles ([32][rows + 4]) are written with 16-byte accesses and read with
-// 4-byte ones; the +4 pads keep half-wave reads free of bank conflicts.
+// ([rows][32], k quads XOR-swizzled by row against bank conflicts) are
+// written and read with 16-byte accesses, "row of m" tiles ([32][rows]) are
+// written with 16-byte accesses and read with 4-byte ones.  No padding: the
+// 128 x 64 tiles then fit three workgroups in a CU's 160 KB of LDS.
 //
 // Split-K: the filter gradients reduce over N P Q pixels or over the rows of
 // a dense layer (up to millions), so the grid's second dimension cuts that
@@ -45,7 +46,6 @@ namespace ooc {
 namespace {
 
 constexpr int BK = 32;
-constexpr int LDK = BK + 4;    // row-of-k tile stride (floats)
 constexpr int THREADS = 256;
 constexpr uint32_t kXcds = 8;   // accelerator complex dies of an MI355X, one L2 each
 
@@ -67,8 +67,8 @@ __device__ inline float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 // address and whatever they load is harmless.  Zero padding of a
 // convolution is masked like k >= kend.
 //
-// Row-of-k layout [E][32 + 4]: thread t loads rows (t >> 3) + 32 j, k offset
-// (t & 7) * 4.  Row-of-m layout [32][E + 4], two thread maps: RowM has E / 4
+// Row-of-k layout [E][32] (swizzled, below): thread t loads rows (t >> 3) + 32 j,
+// k offset (t & 7) * 4.  Row-of-m layout [32][E], two thread maps: RowM has E / 4
 // threads per k row, thread t loading k rows t / (E / 4) + (1024 / E) j at m
 // offset (t % (E / 4)) * 4, so that a wave reads whole rows; RowM1 gives
 // thread t the single k row t >> 3 and its E / 8 consecutive m values from
@@ -88,23 +88,29 @@ __device__ inline void keep(T& v) {
   asm volatile("" : "+v"(v));
 }
 
+// Row-of-k tiles [E][32] keep k quad q of row i in slot q ^ (i mod 8): the
+// lanes of a 16-byte read take 8 consecutive rows at one quad, which then
+// cover all banks, without padding the rows.
+__device__ inline int rowk_index(int i, int k) { return i * BK + ((((k >> 2) ^ i) & 7) << 2) + (k & 3); }
+
 template <int E>
 struct RowK {
   static constexpr bool kRowOfK = true;
   static constexpr int kN = E / 32;
-  static constexpr int kLds = E * LDK;
+  static constexpr int kLds = E * BK;
   __device__ static int row(int j) { return (threadIdx.x >> 3) + 32 * j; }
   __device__ static int koff() { return (threadIdx.x & 7) * 4; }
   __device__ static void store(float* lds, const float4 (&r)[kN]) {
 #pragma unroll
-    for (int j = 0; j < kN; ++j) *reinterpret_cast<float4*>(&lds[row(j) * LDK + koff()]) = r[j];
+    for (int j = 0; j < kN; ++j)
+      *reinterpret_cast<float4*>(&lds[rowk_index(row(j), koff())]) = r[j];
   }
 };
 template <int E>
 struct RowM {
   static constexpr bool kRowOfK = false;
   static constexpr int kN = E / 32;
-  static constexpr int kLd = E + 4;
+  static constexpr int kLd = E;
   static constexpr int kLds = BK * kLd;
   __device__ static int krow(int j) { return (int)threadIdx.x / (E / 4) + (1024 / E) * j; }
   __device__ static int moff() { return ((int)threadIdx.x % (E / 4)) * 4; }
@@ -117,7 +123,7 @@ template <int E>
 struct RowM1 {
   static constexpr bool kRowOfK = false;
   static constexpr int kN = E / 32;
-  static constexpr int kLd = E + 4;
+  static constexpr int kLd = E;
   static constexpr int kLds = BK * kLd;
   __device__ static int krow() { return (int)threadIdx.x >> 3; }
   __device__ static int moff() { return ((int)threadIdx.x & 7) * (E / 8); }
@@ -504,8 +510,8 @@ struct ClassOut {
 // ---------------------------------------------------------------- kernel
 template <class L>
 __device__ inline float4 read_op(const float* lds, int i, int k) {
-  if (L::kRowOfK) return *reinterpret_cast<const float4*>(&lds[i * LDK + k]);
-  constexpr int ld = L::kRowOfK ? LDK : (L::kLds / BK);
+  if (L::kRowOfK) return *reinterpret_cast<const float4*>(&lds[rowk_index(i, k)]);
+  constexpr int ld = L::kLds / BK;
   return make_float4(lds[(k + 0) * ld + i], lds[(k + 1) * ld + i], lds[(k + 2) * ld + i],
                      lds[(k + 3) * ld + i]);
 }
@@ -628,7 +634,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
       if (sums) {
 #pragma unroll
         for (int k = 0; k < BK; ++k) {
-          if constexpr (LA::kRowOfK) rs += A[threadIdx.x * LDK + k];
+          if constexpr (LA::kRowOfK) rs += A[rowk_index(threadIdx.x, k)];
           else rs += A[k * (LA::kLds / BK) + threadIdx.x];
         }
       }
