@@ -142,7 +142,10 @@ def test_conv(shape):
 
 # ---------------------------------------------------------------- BatchNorm
 @pytest.mark.parametrize("rows,C,slices", [(162, 12, 1), (162, 12, 5), (162, 6, 4), (4096, 64, 8),
-                                           (3, 128, 3)])
+                                           (3, 128, 3),
+                                           # above 256 slices the reduction runs in two passes:
+                                           # empty trailing slices, a ragged last slice group
+                                           (4096, 64, 300), (5000, 12, 513), (3000, 5, 257)])
 def test_batchnorm(rows, C, slices):
     X = f32(rows, C, scale=2.0) + 0.5
     g, b, G = f32(C), f32(C), f32(rows, C)
