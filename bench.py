@@ -130,7 +130,7 @@ def measured_traffic(net, op):
 MAP_ENTRY_LIMIT = 40000   # chunks + mappings per plan; the process table holds ~65530
 
 
-def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None):
+def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None, wait="oldest"):
     """Budget, window and (chunks, mappings) of the out-of-core and in-core plans."""
     ctx = ooc.Context(-1)
     try:
@@ -152,6 +152,7 @@ def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None):
             if w is not None:
                 ctx.set_window(w)
                 ctx.set_policy(policy)
+                ctx.set_wait_order(wait)
                 if fixed is not None:
                     ctx.set_fixed_distance(*fixed)
             t0 = time.perf_counter()
@@ -165,22 +166,23 @@ def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None):
             "map_entries": max(counts), "build_ms": build_ms}
 
 
-def choose_chunk(net, frac, window_frac, policy="C", fixed=None):
+def choose_chunk(net, frac, window_frac, policy="C", fixed=None, wait="oldest"):
     """Smallest chunk (2 MiB .. 256 MiB) whose plans fit the memory-map table: the
     trade-off of Section 4 between mapping overhead and internal fragmentation."""
     for mib in (2, 4, 8, 16, 32, 64, 128, 256):
-        plan = plan_for(net, frac, window_frac, mib << 20, policy, fixed)
+        plan = plan_for(net, frac, window_frac, mib << 20, policy, fixed, wait)
         if plan["map_entries"] <= MAP_ENTRY_LIMIT:
             return mib << 20, plan
     return 256 << 20, plan
 
 
 def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup, depth=None,
-             policy="C", fixed=None):
+             policy="C", fixed=None, wait="oldest"):
     ctx = ooc.Context(0)
     try:
         net.register(ctx)
         ctx.set_policy(policy)
+        ctx.set_wait_order(wait)
         if fixed is not None and budget != ooc.UNLIMITED:
             ctx.set_fixed_distance(*fixed)
         if depth is not None:
@@ -259,7 +261,7 @@ def _blas():
         return "unknown"
 
 
-def oracle_schedule_ms(spec, budget, window, chunk, policy, fixed):
+def oracle_schedule_ms(spec, budget, window, chunk, policy, fixed, wait="oldest"):
     """Wall time of the oracle's scheduler on the full-size function sequence (median of 3)."""
     from oracle import schedule as S
     from oracle.lower import as_schedule_input, lower
@@ -268,7 +270,7 @@ def oracle_schedule_ms(spec, budget, window, chunk, policy, fixed):
     times = []
     for _ in range(3):
         t0 = time.perf_counter()
-        S.build(b, k, f, budget, window, chunk, policy, ahead, thr)
+        S.build(b, k, f, budget, window, chunk, policy, ahead, thr, wait=wait)
         times.append((time.perf_counter() - t0) * 1e3)
     return sorted(times)[1]
 
@@ -322,6 +324,10 @@ def main():
                          "cancelled swap-outs; naive: swap every variable in right before and "
                          "out right after each use (W = 0, literal policy); lms: the "
                          "fixed-distance rule with --swapin-ahead / --swapout-threshold")
+    ap.add_argument("--wait-order", default="oldest", choices=("oldest", "furthest"),
+                    help="which pending swap-out a budget wait completes: the oldest (the "
+                         "paper's procedure) or the one whose variable is used again furthest "
+                         "ahead")
     ap.add_argument("--swapin-ahead", type=int, default=1, help="functions (lms)")
     ap.add_argument("--swapout-threshold", type=int, default=1, help="functions (lms)")
     ap.add_argument("--timeline", default="",
@@ -340,9 +346,10 @@ def main():
     fixed = (args.swapin_ahead, args.swapout_threshold) if args.scheduler == "lms" else None
     try:
         if args.chunk:
-            chunk, plan = args.chunk, plan_for(net, frac, window_frac, args.chunk, policy, fixed)
+            chunk, plan = args.chunk, plan_for(net, frac, window_frac, args.chunk, policy, fixed,
+                                               args.wait_order)
         else:
-            chunk, plan = choose_chunk(net, frac, window_frac, policy, fixed)
+            chunk, plan = choose_chunk(net, frac, window_frac, policy, fixed, args.wait_order)
     except ooc.OocError as e:
         if e.status != ooc.E_INFEASIBLE:
             raise
@@ -360,7 +367,7 @@ def main():
         inc = run_mode(net, spec, x, labels, params, ooc.UNLIMITED, None, chunk, args.steps,
                        args.warmup)
     out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps, args.warmup,
-                   args.swapout_depth, policy, fixed)
+                   args.swapout_depth, policy, fixed, args.wait_order)
     if args.timeline:
         with open(args.timeline, "w") as fh:
             json.dump({"fns": net.fn_ops, "vars": net.names,
@@ -419,6 +426,7 @@ def main():
                    "scheduler": args.scheduler,
                    **({"swapin_ahead": fixed[0], "swapout_threshold": fixed[1]} if fixed else {}),
                    "policy": "cancel" if policy == "C" else "literal",
+                   "wait_order": args.wait_order,
                    "swapout_depth": "library default" if args.swapout_depth is None
                    else args.swapout_depth},
         "roofline": roof,
@@ -460,7 +468,7 @@ def main():
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args.workload)
         res["schedule_build_ms"]["oracle"] = round(
-            oracle_schedule_ms(spec, budget, window, chunk, policy, fixed), 3)
+            oracle_schedule_ms(spec, budget, window, chunk, policy, fixed, args.wait_order), 3)
     print(json.dumps(res), flush=True)
 
 

@@ -67,6 +67,7 @@ enum { OOC_R = 1, OOC_W = 2, OOC_RW = 3 };
  * copy; LITERAL treats the variable as already on the host (binary state of
  * Section 3) and swaps it in again into fresh memory. */
 enum { OOC_POLICY_CANCEL = 0, OOC_POLICY_LITERAL = 1 };
+enum { OOC_WAIT_OLDEST = 0, OOC_WAIT_FURTHEST = 1 };
 
 /* Schedule ops and the phase of f_i they belong to (PRE: before f_i runs;
  * POST: after it; END: after f_N). */
@@ -294,6 +295,17 @@ ooc_status ooc_set_fixed_distance(ooc_ctx *ctx, int64_t swapin_ahead, int64_t sw
 
 /* OOC_POLICY_CANCEL (default) or OOC_POLICY_LITERAL. */
 ooc_status ooc_set_policy(ooc_ctx *ctx, int32_t policy);
+
+/* Which pending swap-out a budget wait completes (step (b) of Section 3).
+ * OOC_WAIT_OLDEST (default): the oldest, as the paper's Fig. 2 does.
+ * OOC_WAIT_FURTHEST: the one whose variable is used again furthest ahead in
+ * the variable-sequence (write-backs of variables never used again first,
+ * ties to the oldest), so that swap-outs of variables needed sooner stay
+ * pending and can still be cancelled when the window reaches them.  The
+ * paper leaves the order of swap-outs as future work (Section 6); this is one
+ * answer to it.  The waits at the end of the step stay oldest first.
+ * Registering stage only; OOC_E_INVALID for another value. */
+ooc_status ooc_set_wait_order(ooc_ctx *ctx, int32_t order);
 
 /* Most swap-outs in flight on the device-to-host stream during a step: before
  * issuing another one, the host waits for the oldest.  0 = no bound; default

@@ -8,7 +8,9 @@ Fig. 2; Section 4 for the budget):
 * the device never holds more than the budget (chunk-rounded bytes, eq. 1);
 * before ``f_i`` runs, every variable it uses is on the device and holds the
   newest value of that variable (swap-ins read host copies that are current);
-* swap-outs are completed oldest first;
+* swap-outs are completed oldest first (or, with ``wait="furthest"``, a budget
+  wait completes the earliest pending swap-out whose variable is used again
+  furthest ahead, positions counted in the variable-sequence);
 * at the end of the step nothing is left on the device and every PARAM, STATE
   and OUTPUT variable has its final value on the host.
 
@@ -42,18 +44,29 @@ def _merge(vs):
     return [(v, acc[v]) for v in order]
 
 
-def replay(var_bytes, var_kinds, fn_vars, ops, budget, chunk=1, policy="C", held=None):
+def replay(var_bytes, var_kinds, fn_vars, ops, budget, chunk=1, policy="C", held=None,
+           wait="oldest"):
     """Check an op list; returns ``{"peak", "h2d", "d2h", "max_live"}`` or raises ScheduleError."""
     fns = [_merge(vs) for vs in fn_vars]
     N = len(fns)
     nv = len(var_bytes)
     size = [-(-b // chunk) * chunk for b in var_bytes]
     uses = [[i for i, vs in enumerate(fns) if any(v == u for v, _ in vs)] for u in range(nv)]
+    start = [0] * (N + 1)              # position of each function's first variable
+    for i, vs in enumerate(fns):
+        start[i + 1] = start[i] + len(vs)
+
+    def next_position(u, i):
+        """Position of the first use of u by a function after f_i (infinity if none)."""
+        for j in uses[u]:
+            if j > i:
+                return start[j] + [v for v, _ in fns[j]].index(u)
+        return float("inf")
 
     version = [0] * nv                 # newest value of each variable
     host_ver = [0 if var_kinds[u] in (INPUT, PARAM, STATE) else None for u in range(nv)]
     working = [None] * nv              # version held by the working device copy, or None
-    pending = deque()                  # (var, version) of issued swap-outs, oldest first
+    pending = deque()                  # (var, version, next use) of issued swap-outs, oldest first
     cur = 0
     h2d = d2h = 0
     peak = 0
@@ -130,7 +143,7 @@ def replay(var_bytes, var_kinds, fn_vars, ops, budget, chunk=1, policy="C", held
             idx = [j for j, p in enumerate(pending) if p[0] == u]
             if not idx or working[u] is not None:
                 fail(k, "cancel of a variable without a pending swap-out")
-            _, ver = pending[idx[0]]
+            _, ver, _ = pending[idx[0]]
             del pending[idx[0]]
             working[u] = ver
         elif kind == WAIT_OUT:
@@ -138,16 +151,21 @@ def replay(var_bytes, var_kinds, fn_vars, ops, budget, chunk=1, policy="C", held
                 fail(k, "wait in a POST phase")
             if not pending:
                 fail(k, "wait with no pending swap-out")
-            w, _ = pending.popleft()
+            j = 0
+            if wait == "furthest" and phase == PRE:
+                far = max(p[2] for p in pending)
+                j = next(q for q, p in enumerate(pending) if p[2] == far)
+            w = pending[j][0]
+            del pending[j]
             if w != u:
-                fail(k, f"wait for {u} but the oldest pending swap-out is {w}")
+                fail(k, f"wait for {u} but the pending swap-out to complete is {w}")
             cur -= size[u]
         elif kind == SWAPOUT:
             if phase != POST:
                 fail(k, "swap-out outside a POST phase")
             if working[u] is None:
                 fail(k, "swap-out of a variable not on the device")
-            pending.append((u, working[u]))
+            pending.append((u, working[u], next_position(u, i)))
             host_ver[u] = working[u]
             working[u] = None
             d2h += var_bytes[u]

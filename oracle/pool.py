@@ -60,9 +60,8 @@ def assign(ops, var_bytes, n_chunks, chunk):
     """Replay a schedule's ops through the pool.
 
     Every SWAPIN or ALLOC opens a residency interval of one device copy; FREE
-    closes the variable's working copy, WAIT_OUT the oldest pending copy (the
-    swap-out queue order), CANCEL turns a pending copy back into the working
-    one.  Returns the intervals in opening order as dicts
+    closes the variable's working copy, WAIT_OUT the variable's oldest pending
+    copy, CANCEL turns a pending copy back into the working one.  Returns the intervals in opening order as dicts
     ``{"var", "open", "close", "chunks"}`` (op indices; close = None if never
     closed) and the most chunks in use at once.
     """
@@ -83,8 +82,8 @@ def assign(ops, var_bytes, n_chunks, chunk):
             pending.remove(j)
             working[u] = j
         elif kind == WAIT_OUT:
-            j = pending.popleft()
-            assert intervals[j]["var"] == u
+            j = next(j for j in pending if intervals[j]["var"] == u)
+            pending.remove(j)
             intervals[j]["close"] = k
             pool.release(intervals[j]["rid"])
         elif kind == FREE:
@@ -105,7 +104,7 @@ def best_fit(ops, var_bytes, align=256, placements=None):
     does) suffers external fragmentation, so the address range it needs can
     exceed the bytes live at any moment.  Each residency interval (the same
     copies as ``assign``: SWAPIN / ALLOC open one, FREE closes the working
-    copy, WAIT_OUT the oldest pending one, CANCEL makes a pending copy the
+    copy, WAIT_OUT the variable's oldest pending one, CANCEL makes a pending copy the
     working one again) asks for its size rounded up to ``align``.  A request
     takes the smallest free hole that holds it (lowest address on ties); when
     no hole does, it goes to the end of the heap, starting inside the free tail
@@ -165,7 +164,11 @@ def best_fit(ops, var_bytes, align=256, placements=None):
             pending.remove(j)
             working[u] = j
         elif kind in (WAIT_OUT, FREE):
-            j = pending.popleft() if kind == WAIT_OUT else working.pop(u)
+            if kind == WAIT_OUT:
+                j = next(j for j in pending if blocks[j][2] == u)
+                pending.remove(j)
+            else:
+                j = working.pop(u)
             off, size, _ = blocks.pop(j)
             release(off, size)
             if placements is not None:

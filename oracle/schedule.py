@@ -49,6 +49,7 @@ Readings of the paper where it is silent (stated once, used throughout):
 
 from __future__ import annotations
 
+import math
 from collections import deque
 
 # access flags
@@ -165,16 +166,24 @@ def window_end(seq, sizes, l, window):
 
 
 def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C", ahead=None,
-          threshold=None):
+          threshold=None, wait="oldest"):
     """Schedule one training step.  Returns a dict:
 
     ``ops``      list of (fn, phase, kind, var) in emission order (fn = N at END);
     ``held``     budget bytes held after each op;
     ``windows``  r_i per function;
     ``peak``     max held; ``h2d`` / ``d2h`` bytes moved by SWAPIN / SWAPOUT.
+
+    ``wait`` chooses which pending swap-out a budget wait in step (b) completes:
+    ``"oldest"`` as in Fig. 2, or ``"furthest"``: the one whose variable's next
+    use lies furthest ahead in the variable-sequence (never used again counts
+    as furthest; the earliest reserved among equals).  The paper leaves the
+    order of swap-outs open (Section 6).  The waits at END are oldest first.
     """
     if policy not in ("C", "L"):
         raise Invalid("policy must be 'C' or 'L'")
+    if wait not in ("oldest", "furthest"):
+        raise Invalid("wait must be 'oldest' or 'furthest'")
     # fixed-distance rule of LMS (Section 2): swap in `ahead` functions before a use, keep a
     # variable whose next use is at most `threshold` functions away
     fixed = ahead is not None or threshold is not None
@@ -192,8 +201,11 @@ def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C", ah
     fn_of = [i for i in range(N) for _ in fn_vars[i]]
 
     state = [HOST if k in PERSISTENT else UNMAT for k in var_kinds]
-    # pending swap-outs, oldest first; under policy L an entry is one device copy
+    # pending swap-outs, oldest first; under policy L an entry is one device copy.
+    # fifo_next[k] is the position of the next use of fifo[k]'s variable
+    # (infinity when it has none).
     fifo = deque()
+    fifo_next = deque()
     held = 0
     ops, trace, windows = [], [], []
     h2d = d2h = 0
@@ -218,14 +230,21 @@ def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C", ah
                 p += 1
                 continue
             if state[u] == PEND and policy == "C":
-                fifo.remove(u)
+                k = fifo.index(u)
+                del fifo[k]
+                del fifo_next[k]
                 state[u] = DEV
                 emit(i, PRE, CANCEL, u)
                 p += 1
                 continue
             need = a[u]
             while held + need > budget and fifo:
-                w = fifo.popleft()
+                k = 0
+                if wait == "furthest":
+                    k = max(range(len(fifo)), key=lambda q: (fifo_next[q], -q))
+                w = fifo[k]
+                del fifo[k]
+                del fifo_next[k]
                 held -= a[w]
                 _swapped_out(w, fifo, state)
                 emit(i, PRE, WAIT_OUT, w)
@@ -258,12 +277,14 @@ def build(var_bytes, var_kinds, fn_vars, budget, window, chunk=1, policy="C", ah
             else:
                 state[u] = PEND
                 fifo.append(u)
+                fifo_next.append(math.inf if n is None else n)
                 d2h += b[u]
                 emit(i, POST, SWAPOUT, u)
         r_prev = r
 
     while fifo:
         w = fifo.popleft()
+        fifo_next.popleft()
         held -= a[w]
         _swapped_out(w, fifo, state)
         emit(N, END, WAIT_OUT, w)

@@ -150,6 +150,15 @@ ooc_status ooc_set_policy(ooc_ctx* ctx, int32_t policy) {
   return OOC_OK;
 }
 
+ooc_status ooc_set_wait_order(ooc_ctx* ctx, int32_t order) {
+  REQUIRE_CTX(ctx);
+  REQUIRE_STAGE(ctx, REGISTERING, "ooc_set_wait_order");
+  if (order != OOC_WAIT_OLDEST && order != OOC_WAIT_FURTHEST)
+    return fail(ctx, OOC_E_INVALID, "unknown wait order");
+  ctx->wait_order = order;
+  return OOC_OK;
+}
+
 ooc_status ooc_set_swapout_depth(ooc_ctx* ctx, int64_t depth) {
   REQUIRE_CTX(ctx);
   if (depth < 0) return fail(ctx, OOC_E_INVALID, "negative swap-out depth");
@@ -181,7 +190,8 @@ ooc_status ooc_build_schedule(ooc_ctx* ctx) {
     const uint64_t window = ctx->window_set ? ctx->window : ctx->budget / 2;
     std::string err;
     ooc_status st = build_schedule(ctx->vars, ctx->fns, ctx->budget, window, ctx->chunk,
-                                   ctx->policy, &s, &err, ctx->ahead, ctx->threshold);
+                                   ctx->policy, &s, &err, ctx->ahead, ctx->threshold,
+                                   ctx->wait_order);
     if (st) return fail(ctx, st, err);
   }
   ctx->sched = std::move(s);

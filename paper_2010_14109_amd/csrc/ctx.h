@@ -52,6 +52,7 @@ struct ooc_ctx {
   bool window_set = false;
   uint64_t chunk = 2ull << 20;
   int32_t policy = OOC_POLICY_CANCEL;
+  int32_t wait_order = OOC_WAIT_OLDEST;    // see ooc_set_wait_order
   int64_t swapout_depth = 4;               // see ooc_set_swapout_depth
   bool incore = true;
 

@@ -64,11 +64,12 @@ void bestfit_extent(const std::vector<Var>& vars, const Plan& plan, uint64_t ali
 // Scheduler (Section 3, Fig. 2).  Returns OOC_OK, OOC_E_INFEASIBLE.  With
 // ahead >= 0 the fixed-distance rule of LMS (Section 2) replaces the byte
 // window: the window ends with f_{i+ahead} and a variable whose next use is
-// at most `threshold` functions away is kept.
+// at most `threshold` functions away is kept.  wait_order: OOC_WAIT_OLDEST or
+// OOC_WAIT_FURTHEST (which pending swap-out a budget wait completes).
 ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& fns,
                           uint64_t budget, uint64_t window, uint64_t chunk, int policy,
                           Schedule* out, std::string* err, int64_t ahead = -1,
-                          int64_t threshold = -1);
+                          int64_t threshold = -1, int wait_order = OOC_WAIT_OLDEST);
 // In-core plan: persistent variables resident for the whole step, TEMPs from
 // first to last use, no transfers.
 void build_incore(const std::vector<Var>& vars, const std::vector<Fn>& fns, uint64_t chunk,

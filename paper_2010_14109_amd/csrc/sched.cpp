@@ -15,6 +15,10 @@
 //   (c)+(d) after f_i: a variable never used again is freed (INPUT, TEMP) or
 //           written back (PARAM, STATE, OUTPUT); one used again inside the
 //           window is kept; any other is swapped out.
+// Which pending swap-out a budget wait completes: the oldest (Fig. 2), or
+// with OOC_WAIT_FURTHEST the one whose variable is used again furthest ahead
+// (write-backs first, ties to the oldest), so that swap-outs of variables
+// needed sooner stay pending and can still be cancelled.
 // Budget accounting uses chunk-rounded sizes a_v = ceil(b_v / m_c) m_c
 // (eq. 1), so the chunks the pool maps never exceed the budget.
 #include <algorithm>
@@ -33,7 +37,8 @@ static bool persistent(int32_t kind) {
 
 ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& fns,
                           uint64_t budget, uint64_t window, uint64_t chunk, int policy,
-                          Schedule* out, std::string* err, int64_t ahead, int64_t threshold) {
+                          Schedule* out, std::string* err, int64_t ahead, int64_t threshold,
+                          int wait_order) {
   const bool fixed = ahead >= 0;
   const int64_t N = (int64_t)fns.size();
   const int64_t nv = (int64_t)vars.size();
@@ -62,7 +67,11 @@ ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& f
   for (int64_t v = 0; v < nv; ++v) state[v] = persistent(vars[v].kind) ? HOST : UNMAT;
 
   // pending swap-outs, oldest first; cancelled entries are skipped lazily
-  struct Entry { int64_t var; bool alive; };
+  struct Entry {
+    int64_t var;
+    bool alive;
+    int64_t next;   // position of the variable's next use, INT64_MAX for none
+  };
   std::vector<Entry> fifo;
   size_t head = 0, alive = 0;
   std::vector<int64_t> entry_of(nv, -1);   // CANCEL policy: the variable's pending entry
@@ -73,11 +82,15 @@ ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& f
   auto emit = [&](int32_t i, uint8_t phase, uint8_t kind, int64_t v) {
     s.ops.push_back(Op{i, phase, kind, v, held});
   };
-  auto pop_oldest = [&](int32_t i, uint8_t phase) {
+  auto pop = [&](int32_t i, uint8_t phase, bool furthest) {
     while (!fifo[head].alive) ++head;
-    const int64_t w = fifo[head].var;
-    fifo[head].alive = false;
-    ++head;
+    size_t pick = head;
+    if (furthest)
+      for (size_t q = head + 1; q < fifo.size(); ++q)
+        if (fifo[q].alive && fifo[q].next > fifo[pick].next) pick = q;
+    const int64_t w = fifo[pick].var;
+    fifo[pick].alive = false;
+    if (pick == head) ++head;
     --alive;
     --queued[w];
     entry_of[w] = -1;
@@ -111,7 +124,8 @@ ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& f
         continue;
       }
       const uint64_t need = a[u];
-      while (held + need > budget && alive > 0) pop_oldest((int32_t)i, OOC_PRE);
+      while (held + need > budget && alive > 0)
+        pop((int32_t)i, OOC_PRE, wait_order == OOC_WAIT_FURTHEST);
       if (held + need <= budget) {
         uint8_t kind = OOC_ALLOC;
         if (state[u] != UNMAT) {
@@ -145,7 +159,7 @@ ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& f
       } else {
         state[u] = PEND;
         entry_of[u] = (int64_t)fifo.size();
-        fifo.push_back(Entry{u, true});
+        fifo.push_back(Entry{u, true, n >= 0 ? n : INT64_MAX});
         ++alive;
         ++queued[u];
         s.d2h += vars[u].bytes;
@@ -154,7 +168,7 @@ ooc_status build_schedule(const std::vector<Var>& vars, const std::vector<Fn>& f
     }
     r_prev = r;
   }
-  while (alive > 0) pop_oldest((int32_t)N, OOC_END);
+  while (alive > 0) pop((int32_t)N, OOC_END, false);
   for (const Op& o : s.ops) s.peak = std::max(s.peak, o.held);
   *out = std::move(s);
   return OOC_OK;
@@ -276,18 +290,20 @@ void build_plan(const std::vector<Var>& vars, const Schedule& s, bool incore, ui
         working[o.var] = -1;
         break;
       case OOC_CANCEL:
+      case OOC_WAIT_OUT:
+        // the variable's oldest pending copy (a budget wait need not complete
+        // the oldest swap-out overall, see ooc_set_wait_order)
         for (size_t j = head; j < pending.size(); ++j)
           if (pending[j] >= 0 && plan.intervals[pending[j]].var == o.var) {
             id = pending[j];
             pending[j] = -1;
             break;
           }
-        working[o.var] = id;
-        break;
-      case OOC_WAIT_OUT:
-        while (pending[head] < 0) ++head;
-        id = pending[head++];
-        close(id, k);
+        while (head < pending.size() && pending[head] < 0) ++head;
+        if (o.kind == OOC_CANCEL)
+          working[o.var] = id;
+        else
+          close(id, k);
         break;
       case OOC_FREE:
         id = working[o.var];

@@ -20,6 +20,7 @@ OK, E_INVALID, E_STATE, E_INFEASIBLE, E_HOST_OOM, E_DEVICE, E_UNSUPPORTED = 0, -
 INPUT, PARAM, STATE, OUTPUT, TEMP = 0, 1, 2, 3, 4
 R, W, RW = 1, 2, 3
 POLICY_CANCEL, POLICY_LITERAL = 0, 1
+WAIT_OLDEST, WAIT_FURTHEST = 0, 1
 SWAPIN, ALLOC, CANCEL, WAIT_OUT, SWAPOUT, FREE = 0, 1, 2, 3, 4, 5
 PRE, POST, END = 0, 1, 2
 UNLIMITED = 2 ** 64 - 1
@@ -42,6 +43,7 @@ EXPORTS = [
     "ooc_plan_intervals", "ooc_plan_chunks", "ooc_prepare", "ooc_host_ptr", "ooc_upload",
     "ooc_download", "ooc_step", "ooc_get_stats", "ooc_fn_times", "ooc_link_probe",
     "ooc_timeline", "ooc_set_swapout_depth", "ooc_set_fixed_distance", "ooc_bestfit_extent",
+    "ooc_set_wait_order",
 ]
 
 
@@ -106,6 +108,7 @@ def load(path=LIB_PATH):
         "ooc_set_policy": ([P, c.c_int32], c.c_int32),
         "ooc_set_swapout_depth": ([P, c.c_int64], c.c_int32),
         "ooc_set_fixed_distance": ([P, c.c_int64, c.c_int64], c.c_int32),
+        "ooc_set_wait_order": ([P, c.c_int32], c.c_int32),
         "ooc_bestfit_extent": ([P, c.c_uint64, c.POINTER(c.c_uint64), c.POINTER(c.c_uint64)],
                                c.c_int32),
         "ooc_build_schedule": ([P], c.c_int32),
@@ -216,6 +219,11 @@ class Context:
         _check(self.lib.ooc_bestfit_extent(self.h, align, ctypes.byref(e), ctypes.byref(p)),
                self.h)
         return e.value, p.value
+
+    def set_wait_order(self, order):
+        """``"oldest"`` / WAIT_OLDEST or ``"furthest"`` / WAIT_FURTHEST (see ooc_set_wait_order)."""
+        order = {"oldest": WAIT_OLDEST, "furthest": WAIT_FURTHEST}.get(order, order)
+        _check(self.lib.ooc_set_wait_order(self.h, order), self.h)
 
     def set_fixed_distance(self, swapin_ahead, swapout_threshold):
         _check(self.lib.ooc_set_fixed_distance(self.h, swapin_ahead, swapout_threshold), self.h)

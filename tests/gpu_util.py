@@ -6,7 +6,8 @@ from paper_2010_14109_amd import netdef, ooc
 
 
 def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk=2 << 20,
-            policy="C", keep_grads=True, momentum_state=None, steps=1, inspect=None):
+            policy="C", keep_grads=True, momentum_state=None, steps=1, inspect=None,
+            wait="oldest"):
     """One (or more) training steps on device 0.  Returns (loss, outputs, stats) with
     outputs = {name: array} for every PARAM, STATE and OUTPUT variable.  ``inspect(ctx,
     net)``, when given, runs after the steps."""
@@ -19,6 +20,7 @@ def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk
         if window is not None:
             ctx.set_window(window)
         ctx.set_policy(policy)
+        ctx.set_wait_order(wait)
         ctx.build_schedule()
         ctx.prepare()
         net.view(ctx, "x")[...] = x

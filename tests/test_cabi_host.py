@@ -221,6 +221,65 @@ def test_fixed_distance_matches_oracle(lib):
     ctx.close()
 
 
+def test_wait_order_matches_oracle(lib):
+    """The furthest-next-use wait order: random registrations and the small networks, both
+    policies, with the window or the fixed-distance rule; schedules and chunk plans op for op."""
+    rng = random.Random(91)
+    cases = []
+    for _ in range(200):
+        b, k, f = random_registration(rng, nv=rng.randint(1, 12), nf=rng.randint(1, 20))
+        chunk = rng.choice([1, 8, 32])
+        ws = S.working_set_max(b, f, chunk)
+        cases.append((b, k, f, chunk, rng.choice([ws, ws + chunk, 2 * ws, 10 ** 6]),
+                      rng.choice([0, 8, 64, 512, S.INCORE])))
+    for spec in specs_small():
+        b, k, f = as_schedule_input(lower(spec))
+        p = S.incore_peak(b, k, f, 4096)
+        ws = S.working_set_max(b, f, 4096)
+        for frac in (0.5, 0.25, 0.0):
+            B = max(S.budget_for(frac, p, 4096), ws)
+            cases.append((b, k, f, 4096, B, B // 2))
+    for trial, (b, k, f, chunk, B, W) in enumerate(cases):
+        policy = rng.choice("CL")
+        fixed = (rng.randint(0, 4), rng.randint(0, 4)) if rng.random() < 0.25 else None
+        ctx = ooc.Context(-1)
+        for nb, kd in zip(b, k):
+            ctx.add_var(nb, kd)
+        for vs in f:
+            ctx.add_fn("noop", [v for v, _ in vs], [a for _, a in vs])
+        ctx.set_chunk(chunk)
+        ctx.set_budget(B)
+        ctx.set_window(W)
+        ctx.set_policy(policy)
+        ctx.set_wait_order("furthest")
+        if fixed:
+            ctx.set_fixed_distance(*fixed)
+        kw = {"ahead": fixed[0], "threshold": fixed[1]} if fixed else {}
+        try:
+            ref = S.build(b, k, f, B, W, chunk, policy, wait="furthest", **kw)
+        except S.Infeasible:
+            with pytest.raises(ooc.OocError) as e:
+                ctx.build_schedule()
+            assert e.value.status == ooc.E_INFEASIBLE
+            ctx.close()
+            continue
+        ctx.build_schedule()
+        ops, held = ctx.schedule()
+        assert ops == ref["ops"], trial
+        assert held == ref["held"], trial
+        assert ctx.windows() == ref["windows"], trial
+        ivs, _ = opool.assign(ref["ops"], b, B // chunk, chunk)
+        assert [(g["var"], g["open"], g["close"], g["chunks"]) for g in ctx.plan()] == \
+            [(i["var"], i["open"], i["close"], i["chunks"]) for i in ivs]
+        ctx.close()
+    ctx = ooc.Context(-1)
+    with pytest.raises(ooc.OocError) as e:
+        ctx.set_wait_order(2)
+    assert e.value.status == ooc.E_INVALID
+    ctx.set_wait_order("oldest")
+    ctx.close()
+
+
 def test_bestfit_extent_matches_oracle(lib):
     """The contiguous best-fit comparison heap: extent and peak live bytes equal the oracle's on
     random registrations and the small networks, for both policies and several alignments."""
@@ -238,9 +297,10 @@ def test_bestfit_extent_matches_oracle(lib):
             cases.append((b, k, f, max(S.budget_for(frac, p, 1), ws)))
     for trial, (b, k, f, B) in enumerate(cases):
         policy = rng.choice("CL")
+        wait = rng.choice(["oldest", "furthest"])
         W = rng.choice([0, B // 2, B])
         align = rng.choice([1, 8, 256])
-        ref = S.build(b, k, f, B, W, 1, policy)
+        ref = S.build(b, k, f, B, W, 1, policy, wait=wait)
         ctx = ooc.Context(-1)
         for nb, kd in zip(b, k):
             ctx.add_var(nb, kd)
@@ -250,6 +310,7 @@ def test_bestfit_extent_matches_oracle(lib):
         ctx.set_budget(B)
         ctx.set_window(W)
         ctx.set_policy(policy)
+        ctx.set_wait_order(wait)
         ctx.build_schedule()
         assert ctx.bestfit_extent(align) == opool.best_fit(ref["ops"], b, align), trial
         ctx.close()

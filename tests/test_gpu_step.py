@@ -72,15 +72,17 @@ def test_step_matches_oracle_and_is_budget_independent(spec):
     ws = S.working_set_max(b, f, chunk)
     for frac in (0.5, 0.25, 0.0):
         B = max(S.budget_for(frac, p, chunk), ws)
-        for W, policy in ((B // 2, "C"), (0, "C"), (B, "L"), (0, "L")):
-            print(f"{spec['name']}: budget {B} window {W} policy {policy}", flush=True)
+        for W, policy, wait in ((B // 2, "C", "oldest"), (B // 2, "C", "furthest"),
+                                (0, "C", "oldest"), (B, "L", "oldest"), (0, "L", "oldest"),
+                                (0, "L", "furthest")):
+            print(f"{spec['name']}: budget {B} window {W} policy {policy} wait {wait}", flush=True)
             loss, outs, st = run_net(spec, x, labels, params, budget=B, window=W, chunk=chunk,
-                                     policy=policy)
+                                     policy=policy, wait=wait)
             assert st["pool_bytes"] <= B
             assert st["h2d_bytes"] > 0
             assert np.float32(loss).tobytes() == np.float32(loss0).tobytes()
             for name in outs0:
-                assert outs[name].tobytes() == outs0[name].tobytes(), (name, B, W, policy)
+                assert outs[name].tobytes() == outs0[name].tobytes(), (name, B, W, policy, wait)
 
 
 def test_full_size_mlp_matches_oracle():

@@ -362,3 +362,61 @@ def test_fuzz_chains_with_skips(seed, nv, nf, wsel, bsel, policy, chunk):
     _, first, last = S.sequence(fn)
     assert all(r[i] >= last[i] for i in range(len(r)))
     assert all(r[i] >= r[i - 1] for i in range(1, len(r)))
+
+
+# ---------------------------------------------------------------- wait order of pending swap-outs
+def test_wait_order_hand_example():
+    """Three unit TEMPs, budget 2, W = 0, policy C: f0 writes A, f1 writes B, f2 writes C, then
+    f3, f4, f5 read A, B, C.  Admitting C at f2 needs one pending swap-out completed.  Oldest
+    first completes A, which f3 then swaps back in (after completing B); furthest first completes
+    B (next used at f4, after A's use at f3), and A's pending swap-out is cancelled at f3.  Derived
+    by hand from the procedure of Section 3."""
+    A, B_, C = 0, 1, 2
+    b, k = [1, 1, 1], [S.TEMP] * 3
+    f = [[(A, S.W)], [(B_, S.W)], [(C, S.W)], [(A, S.R)], [(B_, S.R)], [(C, S.R)]]
+    pre, post = S.PRE, S.POST
+    common = [(0, pre, S.ALLOC, A), (0, post, S.SWAPOUT, A), (1, pre, S.ALLOC, B_),
+              (1, post, S.SWAPOUT, B_)]
+    oldest = common + [(2, pre, S.WAIT_OUT, A), (2, pre, S.ALLOC, C), (2, post, S.SWAPOUT, C),
+                       (3, pre, S.WAIT_OUT, B_), (3, pre, S.SWAPIN, A), (3, post, S.FREE, A),
+                       (4, pre, S.SWAPIN, B_), (4, post, S.FREE, B_),
+                       (5, pre, S.CANCEL, C), (5, post, S.FREE, C)]
+    furthest = common + [(2, pre, S.WAIT_OUT, B_), (2, pre, S.ALLOC, C), (2, post, S.SWAPOUT, C),
+                         (3, pre, S.CANCEL, A), (3, post, S.FREE, A),
+                         (4, pre, S.SWAPIN, B_), (4, post, S.FREE, B_),
+                         (5, pre, S.CANCEL, C), (5, post, S.FREE, C)]
+    out_o = S.build(b, k, f, 2, 0, 1, "C")
+    out_f = S.build(b, k, f, 2, 0, 1, "C", wait="furthest")
+    assert out_o["ops"] == oldest and out_f["ops"] == furthest
+    assert (out_o["h2d"], out_f["h2d"]) == (2, 1)
+    check.replay(b, k, f, out_f["ops"], 2, wait="furthest")
+    with pytest.raises(check.ScheduleError):        # the replayer tells the two rules apart
+        check.replay(b, k, f, out_f["ops"], 2)
+    with pytest.raises(check.ScheduleError):
+        check.replay(b, k, f, out_o["ops"], 2, wait="furthest")
+    with pytest.raises(S.Invalid):
+        S.build(b, k, f, 2, 0, 1, "C", wait="newest")
+
+
+@pytest.mark.parametrize("policy", ["C", "L"])
+def test_furthest_wait_schedules_replay(policy):
+    """Random registrations and the small networks under the furthest-next-use wait order:
+    budget, residency, data versions and the wait rule hold (independent replayer)."""
+    rng = random.Random(31 if policy == "C" else 32)
+    for _ in range(150):
+        b, k, f = random_registration(rng)
+        ws = S.working_set_max(b, f)
+        B = rng.randint(ws, ws * 3)
+        W = rng.choice([0, 16, 64, 256, S.INCORE])
+        out = S.build(b, k, f, budget=B, window=W, policy=policy, wait="furthest")
+        res = check.replay(b, k, f, out["ops"], B, policy=policy, held=out["held"], wait="furthest")
+        assert res["peak"] == out["peak"] <= B
+        assert (res["h2d"], res["d2h"]) == (out["h2d"], out["d2h"])
+    for spec in small_networks():
+        b, k, f = as_schedule_input(lower(spec))
+        p = S.incore_peak(b, k, f, 256)
+        ws = S.working_set_max(b, f, 256)
+        for frac in (0.5, 0.25, 0.0):
+            B = max(S.budget_for(frac, p, 256), ws)
+            out = S.build(b, k, f, B, B // 2, 256, policy, wait="furthest")
+            check.replay(b, k, f, out["ops"], B, 256, policy, held=out["held"], wait="furthest")
