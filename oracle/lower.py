@@ -91,14 +91,20 @@ def conv_wgrad_slices(K, RSC, L, C=None):
     GPU kernels that the function sequence carries (it sizes the partials variable), so the
     lowering reproduces it.  With slots = 256 compute units times the workgroups each holds,
     the count s minimises ceil(tiles s / slots) / s over 1 <= s <= min(4 slots / tiles,
-    L / 256 rounded up), taking the smallest s within 1 % of the minimum.  Tiles are 64 x 192
-    (2 per CU) for a convolution with K <= 64, K and C multiples of 4 and fewer padded RSC
-    columns that way than with 128-wide tiles; else 64 on a side of at most 64 (3 per CU) and
-    128 x 128 otherwise (2)."""
+    L / 256 rounded up), taking the smallest s within 1 % of the minimum.  Tiles of a
+    convolution with K % 4 == 0, first rule that applies: 32 x 256 (2 per CU) for K <= 32 and
+    C % 4 == 0; 64 x 192 (2 per CU) for K <= 64, C % 4 == 0 and fewer padded RSC columns that
+    way than with 128-wide tiles; 64 x 64 for K <= 64 and RSC <= 64 (5 per CU, 4 when
+    C % 4 != 0).  Otherwise 64 on a side of at most 64 (3 per CU) and 128 x 128 (2)."""
     pad128 = math.ceil(RSC / 128) * 128 - RSC
     pad192 = math.ceil(RSC / 192) * 192 - RSC
-    if C is not None and K <= 64 and K % 4 == 0 and C % 4 == 0 and pad192 < pad128:
+    conv = C is not None and K % 4 == 0
+    if conv and K <= 32 and C % 4 == 0:
+        tiles, per_cu = math.ceil(RSC / 256), 2
+    elif conv and K <= 64 and C % 4 == 0 and pad192 < pad128:
         tiles, per_cu = math.ceil(RSC / 192), 2
+    elif conv and K <= 64 and RSC <= 64:
+        tiles, per_cu = 1, (5 if C % 4 == 0 else 4)
     elif K <= 64:
         tiles, per_cu = math.ceil(RSC / 128), 3
     elif RSC <= 64:

@@ -520,8 +520,8 @@ __device__ inline float comp(const float4& v, int t) {
   return t == 0 ? v.x : t == 1 ? v.y : t == 2 ? v.z : v.w;
 }
 
-// BM x BN tile; the four waves form a 2 x 2 grid of (BM/2) x (BN/2) sub-tiles,
-// each made of (BM/64) x (BN/64) MFMA 32 x 32 blocks.
+// BM x BN tile; the four waves form a grid of sub-tiles made of MFMA 32 x 32
+// blocks (2 x 2 waves, or 4 x 1 / 1 x 4 for tiles 32 wide / 32 tall).
 // Batched problems (grid z): batch z = (zo, zi) with zi = z mod inner; operand
 // and result pointers move by zo * outer stride + zi * inner stride.
 struct Batch {
@@ -542,7 +542,11 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
                                                        int64_t N, int64_t K, int64_t k_slice,
                                                        int tiles_m, int tiles_n, Batch bt,
                                                        float* __restrict__ rowsum) {
-  constexpr int MB = BM / 64, NB = BN / 64;
+  // the four waves form a WM x WN grid: 4 x 1 for 32-wide tiles, 1 x 4 for
+  // 32-tall ones, else 2 x 2; each wave owns MB x NB MFMA 32 x 32 blocks
+  constexpr int WM = BN == 32 ? 4 : BM == 32 ? 1 : 2, WN = 4 / WM;
+  constexpr int MB = BM / (32 * WM), NB = BN / (32 * WN);
+  static_assert(MB >= 1 && NB >= 1 && MB * 32 * WM == BM && NB * 32 * WN == BN, "tile shape");
   constexpr bool kLoadsFirst = BN > 128;
   // Workgroup (tile, slice, batch) from an XCD-aware order: the hardware hands
   // linear workgroup h to XCD h mod 8, so logical ids are laid out so that each
@@ -592,7 +596,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % WM, wn = wave / WM;
   const int half = lane >> 5;
   const int li = lane & 31;
 
@@ -618,9 +622,9 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
       const int kq = half * 16 + 4 * j;
       float4 a[MB], b[NB];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) a[mb] = read_op<LA>(A, wm * (BM / 2) + mb * 32 + li, kq);
+      for (int mb = 0; mb < MB; ++mb) a[mb] = read_op<LA>(A, wm * (BM / WM) + mb * 32 + li, kq);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) b[nb] = read_op<LB>(B, wn * (BN / 2) + nb * 32 + li, kq);
+      for (int nb = 0; nb < NB; ++nb) b[nb] = read_op<LB>(B, wn * (BN / WN) + nb * 32 + li, kq);
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -661,12 +665,12 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      const int64_t col = n0 + wn * (BN / 2) + nb * 32 + li;
+      const int64_t col = n0 + wn * (BN / WN) + nb * 32 + li;
       if (col >= N) continue;
       const float bv = BIAS ? bias[col] : 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * (BM / 2) + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const int64_t row = m0 + wm * (BM / WM) + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
         if (row < M) out[om.row(row) + col] = acc[mb][nb][r] + bv;
       }
     }
@@ -751,6 +755,19 @@ hipError_t dispatch_dense(FA fa, FB fb, float* c, int64_t ldc, const float* bias
                                                    slices, s, batches, bt, rowsum);
 }
 
+// one explicit tile shape, loaders instantiated at its extents
+template <int BM, int BN, template <int> class LAT, template <int> class LBT, class FA, class FB,
+          class OM>
+hipError_t dispatch_shape(FA fa, FB fb, float* c, OM om, int64_t slice_stride, int64_t M,
+                          int64_t N, int64_t K, int64_t slices, hipStream_t s) {
+  LAT<BM> a{};
+  LBT<BN> b{};
+  fa(a);
+  fb(b);
+  return run_gemm<BM, BN, LAT<BM>, LBT<BN>, OM, false>(a, b, c, om, slice_stride, nullptr, M, N, K,
+                                                       slices, s);
+}
+
 template <int E> using MatKv = MatK<E, true>;
 template <int E> using MatKs = MatK<E, false>;
 template <int E> using MatMv = MatM<E, true>;
@@ -770,13 +787,23 @@ template <int E> using ConvPixelPatchS = ConvPixelPatch<E, SCALAR>;
 // the GEMM sizes of the convolution views index with 32-bit arithmetic
 bool fits31(int64_t v) { return v >= 0 && v < (int64_t(1) << 31) - 64; }
 
-// A filter gradient with at most 64 output channels (M) runs on 64 x 192 tiles
-// when those leave fewer padded columns of RSC (N) than 64 x 128 tiles do
-// (RSC = 576 for a 3 x 3 x 64 filter: 3 full tiles instead of 4.5); it needs
-// four-aligned channels.
-bool wgrad_wide_tile(int64_t M, int64_t N, int64_t C) {
+// Tile of a filter gradient (M = output channels, N = RSC), first rule that
+// applies; the lowering's split-K slice count follows the same rule:
+//   32 x 256 for M <= 32 (no empty tile rows; 32 columns of one tap a thread
+//            when C % 32 == 0);
+//   64 x 192 for M <= 64 when that leaves fewer padded RSC columns than
+//            64 x 128 (RSC = 576 for a 3 x 3 x 64 filter: 3 full tiles, not 4.5);
+//   64 x 64  for M <= 64 and RSC <= 64 (1 x 1 filters, 3-channel inputs);
+//   otherwise the general shapes.
+// The first three need M % 4 == 0 (and C % 4 == 0 for the first two).
+enum class WgradTile { k32x256, k64x192, k64x64, kGeneral };
+WgradTile wgrad_tile(int64_t M, int64_t N, int64_t C) {
+  if (M % 4 != 0) return WgradTile::kGeneral;
+  if (M <= 32 && C % 4 == 0) return WgradTile::k32x256;
   const int64_t pad128 = (N + 127) / 128 * 128 - N, pad192 = (N + 191) / 192 * 192 - N;
-  return M <= 64 && M % 4 == 0 && C % 4 == 0 && pad192 < pad128;
+  if (M <= 64 && C % 4 == 0 && pad192 < pad128) return WgradTile::k64x192;
+  if (M <= 64 && N <= 64) return WgradTile::k64x64;
+  return WgradTile::kGeneral;
 }
 
 // ---------------------------------------------------------------- small kernels
@@ -898,6 +925,11 @@ hipError_t conv_fwd(const float* X, const float* W, float* Y, const ConvShape& c
     a.dS = FastDiv::make(c.S); a.dSC = FastDiv::make(c.S * c.C);
   };
   auto fb = [&](auto& b) { b.p = W; b.ld = K; };
+  if (N <= 32 && c.C % 4 == 0) {   // at most 32 output channels: 256 x 32 tiles, no empty columns
+    if (c.C % 32 == 0)
+      return dispatch_shape<256, 32, ConvPatchT, MatKv>(fa, fb, Y, DenseOut{N}, 0, M, N, K, 1, s);
+    return dispatch_shape<256, 32, ConvPatchV, MatKv>(fa, fb, Y, DenseOut{N}, 0, M, N, K, 1, s);
+  }
   if (c.C % 32 == 0)
     return dispatch_dense<ConvPatchT, MatKv, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
   if (c.C % 4 == 0)
@@ -961,27 +993,41 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
     b.pad = (int)c.pad; b.dQ = FastDiv::make(c.Q); b.dPQ = FastDiv::make(c.P * c.Q);
     b.dC = FastDiv::make(c.C); b.dSC = FastDiv::make(c.S * c.C);
   };
+  const DenseOut om{N};
   hipError_t e;
-  if (wgrad_wide_tile(M, N, c.C)) {
-    // 64 x 192 tiles: no tile column half empty when RSC is an odd multiple of 64
-    MatM<64, true> a{};
-    ConvPixelPatch<192, VEC4> b{};
-    fa(a);
-    fb(b);
-    e = run_gemm<64, 192, MatM<64, true>, ConvPixelPatch<192, VEC4>, DenseOut, false>(
-        a, b, out, DenseOut{N}, M * N, nullptr, M, N, K, slices, s);
-  } else if (c.K % 4 == 0) {
-    if (c.C % 16 == 0)
-      e = dispatch_dense<MatMv, ConvPixelPatchT, false>(fa, fb, out, N, nullptr, M, N, K, slices,
-                                                        s);
-    else if (c.C % 4 == 0)
-      e = dispatch_dense<MatMv, ConvPixelPatchV, false>(fa, fb, out, N, nullptr, M, N, K, slices,
-                                                        s);
-    else
-      e = dispatch_dense<MatMv, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices,
-                                                        s);
-  } else {
-    e = dispatch_dense<MatMs, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices, s);
+  switch (wgrad_tile(M, N, c.C)) {
+    case WgradTile::k32x256:   // at most 32 output channels: no empty tile rows
+      e = c.C % 32 == 0
+              ? dispatch_shape<32, 256, MatMv, ConvPixelPatchT>(fa, fb, out, om, M * N, M, N, K,
+                                                                slices, s)
+              : dispatch_shape<32, 256, MatMv, ConvPixelPatchV>(fa, fb, out, om, M * N, M, N, K,
+                                                                slices, s);
+      break;
+    case WgradTile::k64x192:   // no tile column half empty when RSC is an odd multiple of 64
+      e = dispatch_shape<64, 192, MatMv, ConvPixelPatchV>(fa, fb, out, om, M * N, M, N, K, slices,
+                                                          s);
+      break;
+    case WgradTile::k64x64:    // RSC of at most 64 (1 x 1 filters, the 3-channel first layer)
+      e = c.C % 16 == 0 ? dispatch_shape<64, 64, MatMv, ConvPixelPatchT>(fa, fb, out, om, M * N, M,
+                                                                         N, K, slices, s)
+          : c.C % 4 == 0 ? dispatch_shape<64, 64, MatMv, ConvPixelPatchV>(fa, fb, out, om, M * N,
+                                                                          M, N, K, slices, s)
+                         : dispatch_shape<64, 64, MatMv, ConvPixelPatchS>(fa, fb, out, om, M * N,
+                                                                          M, N, K, slices, s);
+      break;
+    default:
+      if (c.K % 4 != 0)
+        e = dispatch_dense<MatMs, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices,
+                                                          s);
+      else if (c.C % 16 == 0)
+        e = dispatch_dense<MatMv, ConvPixelPatchT, false>(fa, fb, out, N, nullptr, M, N, K, slices,
+                                                          s);
+      else if (c.C % 4 == 0)
+        e = dispatch_dense<MatMv, ConvPixelPatchV, false>(fa, fb, out, N, nullptr, M, N, K, slices,
+                                                          s);
+      else
+        e = dispatch_dense<MatMv, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices,
+                                                          s);
   }
   if (e != hipSuccess || slices <= 1) return e;
   return slice_sum(part, dW, M * N, slices, s);

@@ -47,25 +47,36 @@ def ln_row_slices(rows):
 GPU_CUS = 256   # compute units of an MI355X
 
 
-def wgrad_wide_tile(k_out, rsc, channels):
-    """Whether a filter gradient runs on 64 x 192 tiles (the GEMM library's rule): at most 64
-    four-aligned output channels, four-aligned input channels, and fewer padded RSC columns
-    than with 128-wide tiles."""
+def wgrad_tile(k_out, rsc, channels):
+    """Tile of a filter gradient (the GEMM library's rule, first that applies), as
+    (rows, columns, workgroups per CU): 32 x 256 for at most 32 output channels, 64 x 192 for at
+    most 64 when that pads fewer RSC columns than 128-wide tiles, 64 x 64 for at most 64 output
+    channels and RSC <= 64; all three need output channels % 4 == 0, the first two input
+    channels % 4 == 0.  None for the general shapes."""
+    if k_out % 4:
+        return None
+    if k_out <= 32 and channels % 4 == 0:
+        return 32, 256, 2
     pad128, pad192 = ceil(rsc / 128) * 128 - rsc, ceil(rsc / 192) * 192 - rsc
-    return k_out <= 64 and k_out % 4 == 0 and channels % 4 == 0 and pad192 < pad128
+    if k_out <= 64 and channels % 4 == 0 and pad192 < pad128:
+        return 64, 192, 2
+    if k_out <= 64 and rsc <= 64:
+        return 64, 64, 5 if channels % 4 == 0 else 4
+    return None
 
 
 def wgrad_pixel_slices(k_out, rsc, pixels, channels=None):
     """Split-K slices of a weight-gradient GEMM (k_out x rsc outputs, reduced over ``pixels``;
     ``channels`` is the input channel count of a filter gradient, None for a dense layer).
 
-    The GPU holds 256 CUs x (3 workgroups for the 64-wide tile shapes, 2 for 128 x 128 and
-    64 x 192 tiles; LDS bounds the residency) at once.  A launch of tiles x s workgroups takes
+    The GPU holds 256 CUs x (3 workgroups for the 64-wide general tile shapes, 2 for 128 x 128;
+    filter-gradient tiles as ``wgrad_tile`` says; LDS bounds the residency) at once.  A launch of tiles x s workgroups takes
     ceil(tiles s / slots) rounds of K / s pixels each, so s minimises rounds / s: a partly
     filled last round leaves most CUs idle behind a few.  The smallest s within 1 % of the best
     is taken (fewer partial sums), with at most four rounds and at least 256 pixels a slice."""
-    if channels is not None and wgrad_wide_tile(k_out, rsc, channels):
-        tiles, resident = ceil(rsc / 192), 2
+    tile = wgrad_tile(k_out, rsc, channels) if channels is not None else None
+    if tile is not None:
+        tiles, resident = ceil(rsc / tile[1]), tile[2]
     elif k_out <= 64:
         tiles, resident = ceil(rsc / 128), 3
     elif rsc <= 64:

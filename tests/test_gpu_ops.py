@@ -114,6 +114,11 @@ CONVS = [  # N, H, W, C, K, k, stride, pad
     # filter gradients on 64 x 192 tiles whose last tile is ragged (RSC 540 and 180)
     (2, 9, 9, 60, 20, 3, 1, 1),
     (1, 7, 6, 20, 64, 3, 2, 1),
+    # filter gradients on 64 x 64 tiles (3 input channels, RSC 27; a 1 x 1 64 -> 64 filter) and on
+    # 32 x 256 tiles with a ragged last tile (128 -> 32 channels, RSC 1152); forward on 256 x 32
+    (2, 10, 9, 3, 64, 3, 1, 1),
+    (2, 6, 5, 64, 64, 1, 1, 0),
+    (1, 6, 6, 128, 32, 3, 1, 1),
 ]
 
 

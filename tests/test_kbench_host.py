@@ -45,8 +45,9 @@ def test_slice_rule_agrees_with_oracle_and_fills_rounds():
         for ch in (None, c):
             s = netdef.wgrad_pixel_slices(k_out, rsc, pixels, ch)
             assert s == oracle_lower.conv_wgrad_slices(k_out, rsc, pixels, ch)
-            if ch is not None and netdef.wgrad_wide_tile(k_out, rsc, ch):
-                tiles, per_cu = math.ceil(rsc / 192), 2
+            tile = netdef.wgrad_tile(k_out, rsc, ch) if ch is not None else None
+            if tile is not None:
+                tiles, per_cu = math.ceil(rsc / tile[1]), tile[2]
             elif k_out <= 64:
                 tiles, per_cu = math.ceil(rsc / 128), 3
             elif rsc <= 64:
@@ -65,6 +66,10 @@ def test_slice_rule_known_shapes():
     # for 192 tiles at 8 slices; the 3 x 3 x 64 filter gradient on 64 x 192 tiles
     assert netdef.wgrad_pixel_slices(64, 576, 131072) == 152
     assert netdef.wgrad_pixel_slices(3072, 1024, 12288) == 8
-    assert netdef.wgrad_wide_tile(64, 576, 64) and not netdef.wgrad_wide_tile(64, 1152, 128)
+    assert netdef.wgrad_tile(64, 576, 64) == (64, 192, 2)
+    assert netdef.wgrad_tile(64, 1152, 128) is None
+    assert netdef.wgrad_tile(32, 1152, 128) == (32, 256, 2)
+    assert netdef.wgrad_tile(64, 27, 3) == (64, 64, 4) and netdef.wgrad_tile(64, 64, 64) == (64, 64, 5)
+    assert netdef.wgrad_tile(6, 27, 3) is None
     assert netdef.wgrad_pixel_slices(64, 576, 131072, 64) == 169
     assert netdef.wgrad_pixel_slices(1024, 1024, 256) == 1
