@@ -241,6 +241,9 @@ typedef struct {
   double compute_busy_ms;     /* sum of kernel-phase durations, last step */
   int32_t incore;
   int32_t policy;
+  uint64_t spill_bytes;       /* pageable host homes of TEMPs beyond the host limit */
+  uint64_t staged_h2d_bytes;  /* of h2d_bytes: copied through the staging slots */
+  uint64_t staged_d2h_bytes;  /* of d2h_bytes: copied through the staging slots */
 } ooc_stats;
 
 /* Creates a context bound to HIP device `hip_device`, or a host-only
@@ -314,6 +317,20 @@ ooc_status ooc_set_wait_order(ooc_ctx *ctx, int32_t order);
  * 57 GB/s; a short queue keeps the full rate.  Any stage; takes effect at the
  * next step. */
 ooc_status ooc_set_swapout_depth(ooc_ctx *ctx, int64_t depth);
+
+/* Most bytes of pinned host memory the host arena may take (the CPU-memory
+ * cache of Section 1; pinning is what lets the copies run asynchronously at
+ * the link's rate).  Persistent slots (INPUT, PARAM, STATE, OUTPUT) are
+ * always pinned.  TEMP slots are pinned while they fit under the limit less
+ * 1 GiB of staging slots; the others get homes in pageable memory, and their
+ * copies move in 32 MiB pieces through the staging slots, host threads
+ * copying each piece between slot and home.  Results are identical; only the
+ * transfer rate of the staged bytes changes.  For hosts that pin less memory
+ * than a tight budget leaves on the host.  Default OOC_UNLIMITED (everything
+ * pinned).  OOC_E_INVALID for 0, OOC_E_STATE after ooc_prepare; ooc_prepare
+ * returns OOC_E_HOST_OOM when the persistent slots and the staging slots alone
+ * exceed the limit. */
+ooc_status ooc_set_host_limit(ooc_ctx *ctx, uint64_t bytes);
 
 /* Runs the scheduler of Section 3 (host only).  OOC_E_INFEASIBLE if one
  * function's variables do not fit in the budget. */

@@ -159,6 +159,14 @@ ooc_status ooc_set_wait_order(ooc_ctx* ctx, int32_t order) {
   return OOC_OK;
 }
 
+ooc_status ooc_set_host_limit(ooc_ctx* ctx, uint64_t bytes) {
+  REQUIRE_CTX(ctx);
+  if (ctx->stage == PREPARED) return fail(ctx, OOC_E_STATE, "ooc_set_host_limit after ooc_prepare");
+  if (bytes == 0) return fail(ctx, OOC_E_INVALID, "host limit of 0 bytes");
+  ctx->host_limit = bytes;
+  return OOC_OK;
+}
+
 ooc_status ooc_set_swapout_depth(ooc_ctx* ctx, int64_t depth) {
   REQUIRE_CTX(ctx);
   if (depth < 0) return fail(ctx, OOC_E_INVALID, "negative swap-out depth");

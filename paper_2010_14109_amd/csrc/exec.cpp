@@ -23,13 +23,18 @@
 // cancelled (its host copy is never read: the variable is kept on the device
 // and any later swap-out writes a newer copy) and one of a variable whose
 // host copy is still current (not written since it was swapped in).
+#include <sys/mman.h>
+
 #include <algorithm>
 #include <chrono>
+#include <condition_variable>
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <mutex>
 #include <queue>
 #include <set>
+#include <thread>
 
 #include "ctx.h"
 #include "kernels.h"
@@ -37,6 +42,12 @@
 namespace ooc {
 
 static const uint64_t kSlotAlign = 4096;
+// Pageable overflow (see ooc_set_host_limit): pieces of at most kPiece bytes
+// move through kSlots pinned staging slots per direction, copied between slot
+// and pageable home by kThreads host threads per direction.
+static const uint64_t kPiece = 32ull << 20;
+static const int64_t kSlots = 16;
+static const int kThreads = 4;
 
 #define HIPCK(call)                                                               \
   do {                                                                            \
@@ -53,12 +64,14 @@ void release_device(ooc_ctx* ctx) {
   if (ctx->cs) hipStreamSynchronize(ctx->cs);
   if (ctx->hs) hipStreamSynchronize(ctx->hs);
   if (ctx->ds) hipStreamSynchronize(ctx->ds);
+  if (ctx->ss) hipStreamSynchronize(ctx->ss);
   for (hipEvent_t e : ctx->events) hipEventDestroy(e);
   ctx->events.clear();
   if (ctx->cs) hipStreamDestroy(ctx->cs);
   if (ctx->hs) hipStreamDestroy(ctx->hs);
   if (ctx->ds) hipStreamDestroy(ctx->ds);
-  ctx->cs = ctx->hs = ctx->ds = nullptr;
+  if (ctx->ss) hipStreamDestroy(ctx->ss);
+  ctx->cs = ctx->hs = ctx->ds = ctx->ss = nullptr;
   if (ctx->va_base) {
     hipMemUnmap(ctx->va_base, ctx->va_bytes);
     hipMemAddressFree(ctx->va_base, ctx->va_bytes);
@@ -68,6 +81,9 @@ void release_device(ooc_ctx* ctx) {
   ctx->chunks.clear();
   if (ctx->arena) hipHostFree(ctx->arena);
   ctx->arena = nullptr;
+  if (ctx->spill) munmap(ctx->spill, ctx->spill_bytes);
+  ctx->spill = nullptr;
+  ctx->spill_bytes = 0;
 }
 
 // Entries of the process memory-map table still free (-1 if unknown).
@@ -144,6 +160,7 @@ static ooc_status compile(ooc_ctx* ctx) {
     release[J].clear();
     if (last_fn[J] >= 0) release[J].push_back(ctx->prog[last_fn[J]].ev_fn);
     if (last_d2h[J] >= 0) release[J].push_back((int32_t)last_d2h[J]);
+    if (in_ev[J] >= 0) release[J].push_back((int32_t)in_ev[J]);   // its swap-in copy, if unused
   };
   auto add_waits = [&](std::vector<int32_t>* w, const std::vector<int32_t>& evs, int8_t stream) {
     for (int32_t e : evs)
@@ -172,8 +189,10 @@ static ooc_status compile(ooc_ctx* ctx) {
           opened(J);
           working[o.var] = J;
           Copy c{o.var, J, nullptr, nullptr, ctx->vars[o.var].bytes, {}, 0, 0};
-          add_waits(&c.waits, preds[J], 1);
-          if (var_d2h[o.var] >= 0) add_waits(&c.waits, {(int32_t)var_d2h[o.var]}, 1);
+          // every release event, same stream included: a swap-in whose variable ends up with
+          // a pageable home moves to the staged stream
+          add_waits(&c.waits, preds[J], -1);
+          if (var_d2h[o.var] >= 0) add_waits(&c.waits, {(int32_t)var_d2h[o.var]}, -1);
           c.ev_start = new_event(ctx, 1);
           c.ev_done = new_event(ctx, 1);
           in_ev[J] = c.ev_done;
@@ -329,6 +348,7 @@ ooc_status prepare(ooc_ctx* ctx) {
   HIPCK(hipStreamCreateWithFlags(&ctx->cs, hipStreamNonBlocking));
   HIPCK(hipStreamCreateWithFlags(&ctx->hs, hipStreamNonBlocking));
   HIPCK(hipStreamCreateWithFlags(&ctx->ds, hipStreamNonBlocking));
+  HIPCK(hipStreamCreateWithFlags(&ctx->ss, hipStreamNonBlocking));
 
   {
     ooc_status s = compile(ctx);
@@ -353,6 +373,22 @@ ooc_status prepare(ooc_ctx* ctx) {
       hb += round_up(ctx->vars[v].bytes, kSlotAlign);
     }
   const uint64_t pers = hb;
+  // With a host limit, TEMP slots get pinned bytes up to the limit (less the
+  // staging slots); the rest get pageable homes, one each, no reuse.
+  const uint64_t stage_bytes = 2 * kSlots * kPiece;
+  uint64_t cap = UINT64_MAX;
+  if (ctx->host_limit != OOC_UNLIMITED) {
+    if (ctx->host_limit < pers + stage_bytes) {
+      ctx->err = "host limit " + std::to_string(ctx->host_limit) + " is below the " +
+                 std::to_string(pers) + " bytes of persistent slots plus " +
+                 std::to_string(stage_bytes) + " bytes of staging slots";
+      return OOC_E_HOST_OOM;
+    }
+    cap = ctx->host_limit - pers - stage_bytes;
+  }
+  std::vector<uint8_t> spilled(nv, 0);
+  std::vector<uint64_t> soff(nv, 0);
+  uint64_t spill_top = 0;
   // lifetimes in issue order: swap-ins of f_i at 3 i, swap-outs at 3 i + 2
   std::vector<int64_t> born(nv, -1), dies(nv, -1);
   std::vector<int32_t> last_in(nv, -1);
@@ -419,9 +455,15 @@ ooc_status prepare(ooc_ctx* ctx) {
       holes[best].off += size;
       holes[best].size -= size;
       if (holes[best].size == 0) holes.erase(holes.begin() + best);
-    } else {
+    } else if (size <= cap && top <= cap - size) {
       off = top;
       top += size;
+    } else {
+      spilled[v] = 1;
+      soff[v] = spill_top;
+      spill_top += size;
+      backed[v] = 1;
+      continue;
     }
     backed[v] = 1;
     hoff[v] = pers + off;
@@ -440,6 +482,8 @@ ooc_status prepare(ooc_ctx* ctx) {
     live.push({dies[v], v});
   }
   hb = pers + top;
+  const uint64_t stage_off = hb;
+  if (spill_top > 0) hb += stage_bytes;
   ctx->host_slot.assign(nv, nullptr);
   if (hb > 0) {
     hipError_t e = hipHostMalloc((void**)&ctx->arena, hb, hipHostMallocDefault);
@@ -450,7 +494,75 @@ ooc_status prepare(ooc_ctx* ctx) {
     }
     ctx->arena_bytes = hb;
     for (int64_t v = 0; v < nv; ++v)
-      if (backed[v]) ctx->host_slot[v] = ctx->arena + hoff[v];
+      if (backed[v] && !spilled[v]) ctx->host_slot[v] = ctx->arena + hoff[v];
+  }
+  ctx->in_copy.clear();
+  ctx->out_copy.clear();
+  ctx->ev_staged_in.clear();
+  ctx->in_piece.clear();
+  ctx->out_piece.clear();
+  ctx->staged_h2d = ctx->staged_d2h = 0;
+  if (spill_top > 0) {
+    // pageable homes: populated now (transparent huge pages where the kernel
+    // gives them), so that no page fault lands inside a step
+    void* m = mmap(nullptr, spill_top, PROT_READ | PROT_WRITE, MAP_PRIVATE | MAP_ANONYMOUS, -1, 0);
+    if (m == MAP_FAILED) {
+      ctx->err = "pageable host overflow of " + std::to_string(spill_top) + " bytes: mmap failed";
+      return OOC_E_HOST_OOM;
+    }
+    ctx->spill = (char*)m;
+    ctx->spill_bytes = spill_top;
+    madvise(m, spill_top, MADV_HUGEPAGE);
+    {
+      std::vector<std::thread> ts;
+      const uint64_t part = round_up((spill_top + 7) / 8, kSlotAlign);
+      for (uint64_t o = 0; o < spill_top; o += part)
+        ts.emplace_back([=] { std::memset(ctx->spill + o, 0, std::min(part, spill_top - o)); });
+      for (auto& t : ts) t.join();
+    }
+    ctx->stage_in = ctx->arena + stage_off;
+    ctx->stage_out = ctx->stage_in + kSlots * kPiece;
+    for (int64_t v = 0; v < nv; ++v)
+      if (spilled[v]) ctx->host_slot[v] = ctx->spill + soff[v];
+    // staged copies in pieces, numbered per direction in issue order; a
+    // swap-in needs the host copy written by the latest swap-out before it
+    std::vector<int64_t> outs(nv, 0);
+    auto split = [&](Copy& c, int8_t stream, std::vector<const Copy*>* owner,
+                     std::vector<int32_t>* index) {
+      c.staged = true;
+      const uint64_t n = (c.bytes + kPiece - 1) / kPiece;
+      for (uint64_t k = 0; k < n; ++k) {
+        Piece pc;
+        pc.off = k * kPiece;
+        pc.bytes = std::min(kPiece, c.bytes - pc.off);
+        pc.ev_start = k == 0 ? c.ev_start : new_event(ctx, stream);
+        pc.ev_done = k + 1 == n ? c.ev_done : new_event(ctx, stream);
+        pc.seq = (int64_t)owner->size();
+        owner->push_back(&c);
+        index->push_back((int32_t)k);
+        c.pieces.push_back(pc);
+      }
+    };
+    int64_t staged_in = 0;
+    for (FnProgram& fp : ctx->prog) {
+      for (Copy& c : fp.h2d)
+        if (spilled[c.var]) {
+          c.gen = outs[c.var];
+          // staged swap-ins run on their own stream (3)
+          ctx->event_stream[c.ev_start] = ctx->event_stream[c.ev_done] = 3;
+          split(c, 3, &ctx->in_copy, &ctx->in_piece);
+          ctx->staged_h2d += c.bytes;
+          if ((int64_t)ctx->ev_staged_in.size() < (int64_t)ctx->event_stream.size())
+            ctx->ev_staged_in.resize(ctx->event_stream.size(), -1);
+          ctx->ev_staged_in[c.ev_done] = staged_in++;
+        }
+      for (Copy& c : fp.d2h)
+        if (spilled[c.var]) {
+          c.gen = ++outs[c.var];
+          split(c, 2, &ctx->out_copy, &ctx->out_piece);
+          ctx->staged_d2h += c.bytes;
+        }
+    }
   }
   for (FnProgram& fp : ctx->prog) {
     for (Copy& c : fp.h2d) {
@@ -463,6 +575,7 @@ ooc_status prepare(ooc_ctx* ctx) {
     }
   }
 
+  ctx->ev_staged_in.resize(ctx->event_stream.size(), -1);
   ctx->events.resize(ctx->event_stream.size(), nullptr);
   for (size_t j = 0; j < ctx->events.size(); ++j) {
     hipError_t e = hipEventCreate(&ctx->events[j]);
@@ -485,6 +598,9 @@ ooc_status prepare(ooc_ctx* ctx) {
   st.max_chunks_used = plan.max_chunks_used;
   st.device_bytes_delta = free0 > free1 ? (uint64_t)(free0 - free1) : 0;
   st.host_bytes = hb;
+  st.spill_bytes = ctx->spill_bytes;
+  st.staged_h2d_bytes = ctx->staged_h2d;
+  st.staged_d2h_bytes = ctx->staged_d2h;
   st.n_intervals = (uint64_t)NI;
   st.prepare_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
   return OOC_OK;
@@ -531,9 +647,193 @@ ooc_status timeline(ooc_ctx* ctx, std::vector<ooc_span>* out) {
   return OOC_OK;
 }
 
+namespace {
+
+// Host side of the staged copies of one step (pageable homes, see
+// ooc_set_host_limit).
+//  * Swap-in piece p: a fill thread copies the pageable home into staging
+//    slot p mod kSlots once the slot's previous piece has reached the device
+//    and the variable's host copy has been written; an issuer thread, in
+//    program order, enqueues each staged swap-in on its own stream once the
+//    step loop has reached it, piece by piece as the slots fill.  The step
+//    loop only waits for the issuer when a kernel needs a staged swap-in
+//    whose copy is not enqueued yet, so it keeps running ahead of the device.
+//  * Swap-out piece q: the step loop enqueues the device copy into slot
+//    q mod kSlots once a drain thread has emptied the slot's previous piece
+//    into its pageable home.
+// Every wait is for work that comes earlier in the step's order, so all of
+// them end.
+struct Stager {
+  ooc_ctx* ctx;
+  hipStream_t s;                    // stream of the staged swap-ins
+  std::mutex m;
+  std::condition_variable cv;
+  std::vector<uint8_t> in_ready, out_free;
+  std::vector<int64_t> written;     // per variable: host copies completed this step
+  std::vector<int32_t> left;        // per swap-out copy (seq of its first piece): pieces to drain
+  int64_t in_enq = 0;               // swap-in pieces enqueued by the issuer
+  int64_t out_pushed = 0;           // swap-out pieces enqueued by the step loop
+  int64_t posted = 0;               // staged swap-in copies the step loop has reached
+  int64_t recorded = 0;             // staged swap-in copies the issuer has enqueued
+  bool failed = false, finished = false;
+  std::string err;
+  std::vector<std::thread> threads;
+
+  Stager(ooc_ctx* c, hipStream_t stream) : ctx(c), s(stream) {
+    const int64_t ni = (int64_t)ctx->in_copy.size(), no = (int64_t)ctx->out_copy.size();
+    if (ni == 0 && no == 0) return;
+    in_ready.assign(ni, 0);
+    out_free.assign(no, 0);
+    written.assign(ctx->vars.size(), 0);
+    left.assign(no, 0);
+    for (int64_t q = 0; q < no; ++q) {
+      const Copy& cp = *ctx->out_copy[q];
+      left[cp.pieces[0].seq] = (int32_t)cp.pieces.size();
+    }
+    for (int t = 0; t < kThreads; ++t) {
+      if (t < ni) threads.emplace_back([this, t] { fill(t); });
+      if (t < no) threads.emplace_back([this, t] { drain(t); });
+    }
+    if (ni > 0) threads.emplace_back([this] { issue(); });
+  }
+  ~Stager() { finish(true); }
+
+  char* in_slot(int64_t p) const { return ctx->stage_in + (p % kSlots) * kPiece; }
+  char* out_slot(int64_t q) const { return ctx->stage_out + (q % kSlots) * kPiece; }
+
+  void fail(const std::string& e) {
+    {
+      std::lock_guard<std::mutex> lk(m);
+      if (!failed) err = e;
+      failed = true;
+    }
+    cv.notify_all();
+  }
+  template <class Pred>
+  bool wait(Pred pred) {
+    std::unique_lock<std::mutex> lk(m);
+    cv.wait(lk, [&] { return failed || pred(); });
+    return !failed;
+  }
+  void bump(int64_t* counter, int64_t v) {
+    {
+      std::lock_guard<std::mutex> lk(m);
+      *counter = v;
+    }
+    cv.notify_all();
+  }
+  // joins the threads; abort: make every wait end first
+  void finish(bool abort) {
+    if (finished) return;
+    finished = true;
+    if (abort) {
+      {
+        std::lock_guard<std::mutex> lk(m);
+        if (!failed) err = "step aborted";
+        failed = true;
+      }
+      cv.notify_all();
+    }
+    for (auto& t : threads) t.join();
+  }
+
+  void fill(int t) {
+    hipSetDevice(ctx->device);
+    const int64_t n = (int64_t)ctx->in_copy.size();
+    for (int64_t p = t; p < n; p += kThreads) {
+      const Copy& c = *ctx->in_copy[p];
+      const Piece& pc = c.pieces[ctx->in_piece[p]];
+      if (p >= kSlots) {
+        if (!wait([&] { return in_enq > p - kSlots; })) return;
+        const Copy& prev = *ctx->in_copy[p - kSlots];
+        const hipError_t e =
+            hipEventSynchronize(ctx->events[prev.pieces[ctx->in_piece[p - kSlots]].ev_done]);
+        if (e != hipSuccess) return fail(std::string("staging: ") + hipGetErrorString(e));
+      }
+      if (!wait([&] { return written[c.var] >= c.gen; })) return;
+      std::memcpy(in_slot(p), ctx->host_slot[c.var] + pc.off, pc.bytes);
+      {
+        std::lock_guard<std::mutex> lk(m);
+        in_ready[p] = 1;
+      }
+      cv.notify_all();
+    }
+  }
+
+  void issue() {
+    hipSetDevice(ctx->device);
+    const int64_t n = (int64_t)ctx->in_copy.size();
+    int64_t ci = 0;
+    for (int64_t p = 0; p < n; ++ci) {
+      const Copy& c = *ctx->in_copy[p];
+      if (!wait([&] { return posted > ci; })) return;
+      for (int32_t w : c.waits) {
+        const hipError_t e = hipStreamWaitEvent(s, ctx->events[w], 0);
+        if (e != hipSuccess) return fail(std::string("staging: ") + hipGetErrorString(e));
+      }
+      for (const Piece& pc : c.pieces) {
+        if (!wait([&] { return in_ready[pc.seq] != 0; })) return;
+        hipError_t e = hipEventRecord(ctx->events[pc.ev_start], s);
+        if (e == hipSuccess)
+          e = hipMemcpyAsync((char*)c.dst + pc.off, in_slot(pc.seq), pc.bytes,
+                             hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipEventRecord(ctx->events[pc.ev_done], s);
+        if (e != hipSuccess) return fail(std::string("staging: ") + hipGetErrorString(e));
+        bump(&in_enq, pc.seq + 1);
+      }
+      p += (int64_t)c.pieces.size();
+      bump(&recorded, ci + 1);
+    }
+  }
+
+  void drain(int t) {
+    hipSetDevice(ctx->device);
+    const int64_t n = (int64_t)ctx->out_copy.size();
+    for (int64_t q = t; q < n; q += kThreads) {
+      const Copy& c = *ctx->out_copy[q];
+      const Piece& pc = c.pieces[ctx->out_piece[q]];
+      if (!wait([&] { return out_pushed > q; })) return;
+      const hipError_t e = hipEventSynchronize(ctx->events[pc.ev_done]);
+      if (e != hipSuccess) return fail(std::string("staging: ") + hipGetErrorString(e));
+      std::memcpy(ctx->host_slot[c.var] + pc.off, out_slot(q), pc.bytes);
+      {
+        std::lock_guard<std::mutex> lk(m);
+        out_free[q] = 1;
+        if (--left[c.pieces[0].seq] == 0) written[c.var] = std::max(written[c.var], c.gen);
+      }
+      cv.notify_all();
+    }
+  }
+};
+
+}  // namespace
+
+// Enqueues a staged swap-out piece by piece (see Stager).
+static ooc_status enqueue_staged_out(ooc_ctx* ctx, Stager* sg, const Copy& c) {
+  hipStream_t s = ctx->ds;
+  for (size_t k = 0; k < c.pieces.size(); ++k) {
+    const Piece& pc = c.pieces[k];
+    const int64_t q = pc.seq;
+    if (q >= kSlots && !sg->wait([&] { return sg->out_free[q - kSlots] != 0; })) {
+      ctx->err = sg->err;
+      return OOC_E_DEVICE;
+    }
+    if (k == 0)
+      for (int32_t w : c.waits) HIPCK(hipStreamWaitEvent(s, ctx->events[w], 0));
+    HIPCK(hipEventRecord(ctx->events[pc.ev_start], s));
+    HIPCK(hipMemcpyAsync(sg->out_slot(q), (const char*)c.src + pc.off, pc.bytes,
+                         hipMemcpyDeviceToHost, s));
+    HIPCK(hipEventRecord(ctx->events[pc.ev_done], s));
+    sg->bump(&sg->out_pushed, q + 1);
+  }
+  return OOC_OK;
+}
+
 ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out) {
   HIPCK(hipSetDevice(ctx->device));
   auto t0 = std::chrono::steady_clock::now();
+  Stager stager(ctx, ctx->ss);
+  int64_t staged_in = 0;         // staged swap-in copies reached so far
   hipStream_t cs = ctx->cs;
   HIPCK(hipEventRecord(ctx->events[ctx->ev_begin], cs));
   const int64_t N = (int64_t)ctx->fns.size();
@@ -542,10 +842,21 @@ ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out) {
   for (int64_t i = 0; i < N; ++i) {
     const FnProgram& fp = ctx->prog[i];
     for (const Copy& c : fp.h2d) {
+      if (c.staged) {
+        stager.bump(&stager.posted, ++staged_in);
+        continue;
+      }
       ooc_status s = enqueue_copy(ctx, c, ctx->hs, hipMemcpyHostToDevice);
       if (s) return s;
     }
-    for (int32_t w : fp.cwaits) HIPCK(hipStreamWaitEvent(cs, ctx->events[w], 0));
+    for (int32_t w : fp.cwaits) {
+      const int64_t sc = ctx->ev_staged_in[w];   // staged swap-in it completes, or -1
+      if (sc >= 0 && !stager.wait([&] { return stager.recorded > sc; })) {
+        ctx->err = stager.err;
+        return OOC_E_DEVICE;
+      }
+      HIPCK(hipStreamWaitEvent(cs, ctx->events[w], 0));
+    }
     HIPCK(hipEventRecord(ctx->events[fp.ev_pre], cs));
     hipError_t e = launch_fn(ctx->fns[i], fp.ptrs.data(), fp.sizes.data(), lr, mu, cs);
     if (e != hipSuccess) {
@@ -559,7 +870,8 @@ ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out) {
       // stream already holds the work up to f_i, so it keeps running meanwhile
       if (depth > 0 && (int64_t)issued.size() >= depth)
         HIPCK(hipEventSynchronize(ctx->events[issued[issued.size() - depth]]));
-      ooc_status s = enqueue_copy(ctx, c, ctx->ds, hipMemcpyDeviceToHost);
+      ooc_status s = c.staged ? enqueue_staged_out(ctx, &stager, c)
+                              : enqueue_copy(ctx, c, ctx->ds, hipMemcpyDeviceToHost);
       if (s) return s;
       issued.push_back(c.ev_done);
     }
@@ -568,6 +880,12 @@ ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out) {
   HIPCK(hipStreamSynchronize(cs));
   HIPCK(hipStreamSynchronize(ctx->hs));
   HIPCK(hipStreamSynchronize(ctx->ds));
+  stager.finish(false);
+  HIPCK(hipStreamSynchronize(ctx->ss));
+  if (stager.failed) {
+    ctx->err = stager.err;
+    return OOC_E_DEVICE;
+  }
   auto t1 = std::chrono::steady_clock::now();
 
   ooc_stats& st = ctx->stats;

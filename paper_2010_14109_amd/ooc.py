@@ -43,7 +43,7 @@ EXPORTS = [
     "ooc_plan_intervals", "ooc_plan_chunks", "ooc_prepare", "ooc_host_ptr", "ooc_upload",
     "ooc_download", "ooc_step", "ooc_get_stats", "ooc_fn_times", "ooc_link_probe",
     "ooc_timeline", "ooc_set_swapout_depth", "ooc_set_fixed_distance", "ooc_bestfit_extent",
-    "ooc_set_wait_order",
+    "ooc_set_wait_order", "ooc_set_host_limit",
 ]
 
 
@@ -68,7 +68,8 @@ class ooc_stats(ctypes.Structure):
         "device_bytes_delta", "host_bytes", "sched_h2d_bytes", "sched_d2h_bytes", "h2d_bytes",
         "d2h_bytes", "n_intervals", "n_mappings")] + [(n, ctypes.c_double) for n in (
         "prepare_ms", "step_ms", "step_gpu_ms", "h2d_busy_ms", "d2h_busy_ms",
-        "compute_busy_ms")] + [("incore", ctypes.c_int32), ("policy", ctypes.c_int32)]
+        "compute_busy_ms")] + [("incore", ctypes.c_int32), ("policy", ctypes.c_int32)] + [
+        (n, ctypes.c_uint64) for n in ("spill_bytes", "staged_h2d_bytes", "staged_d2h_bytes")]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
@@ -109,6 +110,7 @@ def load(path=LIB_PATH):
         "ooc_set_swapout_depth": ([P, c.c_int64], c.c_int32),
         "ooc_set_fixed_distance": ([P, c.c_int64, c.c_int64], c.c_int32),
         "ooc_set_wait_order": ([P, c.c_int32], c.c_int32),
+        "ooc_set_host_limit": ([P, c.c_uint64], c.c_int32),
         "ooc_bestfit_extent": ([P, c.c_uint64, c.POINTER(c.c_uint64), c.POINTER(c.c_uint64)],
                                c.c_int32),
         "ooc_build_schedule": ([P], c.c_int32),
@@ -227,6 +229,10 @@ class Context:
 
     def set_fixed_distance(self, swapin_ahead, swapout_threshold):
         _check(self.lib.ooc_set_fixed_distance(self.h, swapin_ahead, swapout_threshold), self.h)
+
+    def set_host_limit(self, nbytes):
+        """Most pinned host bytes for the arena (see ooc_set_host_limit)."""
+        _check(self.lib.ooc_set_host_limit(self.h, nbytes), self.h)
 
     def set_swapout_depth(self, depth):
         _check(self.lib.ooc_set_swapout_depth(self.h, depth), self.h)

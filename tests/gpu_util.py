@@ -7,7 +7,7 @@ from paper_2010_14109_amd import netdef, ooc
 
 def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk=2 << 20,
             policy="C", keep_grads=True, momentum_state=None, steps=1, inspect=None,
-            wait="oldest"):
+            wait="oldest", host_limit=None):
     """One (or more) training steps on device 0.  Returns (loss, outputs, stats) with
     outputs = {name: array} for every PARAM, STATE and OUTPUT variable.  ``inspect(ctx,
     net)``, when given, runs after the steps."""
@@ -21,6 +21,8 @@ def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk
             ctx.set_window(window)
         ctx.set_policy(policy)
         ctx.set_wait_order(wait)
+        if host_limit is not None:
+            ctx.set_host_limit(host_limit)
         ctx.build_schedule()
         ctx.prepare()
         net.view(ctx, "x")[...] = x
@@ -44,6 +46,16 @@ def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk
         return losses[-1], outs, ctx.stats()
     finally:
         ctx.close()
+
+
+def persistent_host_bytes(spec, keep_grads=True):
+    """Bytes of the pinned slots of the persistent variables (4 KiB-aligned each)."""
+    net = netdef.Net(spec, keep_grads=keep_grads)
+    return sum((b + 4095) // 4096 * 4096 for b, k in zip(net.var_bytes, net.var_kinds)
+               if k != ooc.TEMP)
+
+
+STAGING_BYTES = 1 << 30   # the staging slots a host limit reserves
 
 
 def rel_l2(a, b):

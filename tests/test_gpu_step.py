@@ -19,7 +19,7 @@ from oracle import schedule as S
 from oracle.interp import run as oracle_run
 from oracle.lower import lower, as_schedule_input
 from paper_2010_14109_amd import netdef, ooc, synth
-from tests.gpu_util import rel_l2, run_net
+from tests.gpu_util import STAGING_BYTES, persistent_host_bytes, rel_l2, run_net
 
 pytestmark = pytest.mark.gpu
 TOL = 1e-4
@@ -170,6 +170,61 @@ def test_full_size_out_of_core_equals_in_core(name, kw, chunk_mib):
     assert np.float32(loss).tobytes() == np.float32(loss0).tobytes()
     for nm in outs0:
         assert outs[nm].tobytes() == outs0[nm].tobytes(), nm
+
+
+@pytest.mark.parametrize("idx,policy", [(i, p) for i in range(6) for p in ("C", "L")])
+def test_pageable_overflow_equals_in_core(idx, policy):
+    """A host limit that leaves no pinned bytes for TEMPs: every swapped activation has a
+    pageable home and moves through the staging slots.  Two steps (the second starts from
+    the state the first wrote back) equal two in-core steps bit for bit."""
+    spec = tiny_specs()[idx]
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    b, k, f = as_schedule_input(lower(spec, keep_grads=True))
+    chunk = 4096
+    B = max(S.budget_for(0.25, S.incore_peak(b, k, f, chunk), chunk), S.working_set_max(b, f, chunk))
+    W = B // 2 if policy == "C" else 0
+    limit = persistent_host_bytes(spec) + STAGING_BYTES
+    print(f"{spec['name']}: budget {B} window {W} policy {policy} host limit {limit}", flush=True)
+    loss0, outs0, _ = run_net(spec, x, labels, params, chunk=chunk, steps=2)
+    loss, outs, st = run_net(spec, x, labels, params, budget=B, window=W, chunk=chunk,
+                             policy=policy, steps=2, host_limit=limit)
+    assert st["spill_bytes"] > 0 and st["staged_h2d_bytes"] > 0 and st["staged_d2h_bytes"] > 0
+    assert st["staged_h2d_bytes"] <= st["h2d_bytes"] and st["staged_d2h_bytes"] <= st["d2h_bytes"]
+    assert st["pool_bytes"] <= B and st["host_bytes"] <= limit
+    assert np.float32(loss).tobytes() == np.float32(loss0).tobytes()
+    for name in outs0:
+        assert outs[name].tobytes() == outs0[name].tobytes(), name
+
+
+def test_pageable_overflow_multi_piece():
+    """Plain CNN at batch 256 (64 MiB activations: two 32 MiB pieces each) with half of the
+    TEMP host bytes pinned and half pageable: bit-identical to the in-core step."""
+    spec = synth.plain_cnn(batch=256, channels=64, depth=4, hw=32, classes=10)
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    net = netdef.Net(spec, keep_grads=False)
+    chunk = 2 << 20
+    p = S.incore_peak(net.var_bytes, net.var_kinds, net.fn_vars, chunk)
+    ws = S.working_set_max(net.var_bytes, net.fn_vars, chunk)
+    B = max(ws, (p // 2) // chunk * chunk)
+    loss0, outs0, _ = run_net(spec, x, labels, params, chunk=chunk, keep_grads=False)
+    _, _, full = run_net(spec, x, labels, params, budget=B, chunk=chunk, keep_grads=False)
+    pers = persistent_host_bytes(spec, keep_grads=False)
+    temps = full["host_bytes"] - pers
+    limit = pers + STAGING_BYTES + temps // 2
+    loss, outs, st = run_net(spec, x, labels, params, budget=B, chunk=chunk, keep_grads=False,
+                             host_limit=limit)
+    print(f"cnn b256: pinned TEMP bytes {temps}, spilled {st['spill_bytes']}, staged "
+          f"{st['staged_h2d_bytes']} / {st['h2d_bytes']} in, {st['staged_d2h_bytes']} / "
+          f"{st['d2h_bytes']} out", flush=True)
+    assert 0 < st["spill_bytes"] < temps + STAGING_BYTES
+    assert 0 < st["staged_h2d_bytes"] < st["h2d_bytes"]
+    assert st["host_bytes"] <= limit
+    assert st["h2d_bytes"] == full["h2d_bytes"] and st["d2h_bytes"] == full["d2h_bytes"]
+    assert np.float32(loss).tobytes() == np.float32(loss0).tobytes()
+    for name in outs0:
+        assert outs[name].tobytes() == outs0[name].tobytes(), name
 
 
 def test_two_steps_keep_state_on_the_host():
