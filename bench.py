@@ -177,10 +177,12 @@ def choose_chunk(net, frac, window_frac, policy="C", fixed=None, wait="oldest"):
 
 
 def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup, depth=None,
-             policy="C", fixed=None, wait="oldest"):
+             policy="C", fixed=None, wait="oldest", host_limit=None):
     ctx = ooc.Context(0)
     try:
         net.register(ctx)
+        if host_limit is not None and budget != ooc.UNLIMITED:
+            ctx.set_host_limit(host_limit)
         ctx.set_policy(policy)
         ctx.set_wait_order(wait)
         if fixed is not None and budget != ooc.UNLIMITED:
@@ -202,8 +204,12 @@ def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup,
                 net.view(ctx, name)[...] = 0
         ctx.upload()
         lr, mu = spec["optimizer"]["lr"], spec["optimizer"]["momentum"]
-        for _ in range(warmup):
+        mode = "in-core" if budget == ooc.UNLIMITED else "out-of-core"
+        for i in range(warmup):
+            s0 = time.perf_counter()
             ctx.step(lr, mu)
+            print(f"{mode} warm-up step {i}: {(time.perf_counter() - s0) * 1e3:.1f} ms",
+                  file=sys.stderr, flush=True)
         # ooc_step returns after all three streams are synchronized
         t0 = time.perf_counter()
         loss = None
@@ -212,6 +218,8 @@ def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup,
             s0 = time.perf_counter()
             loss = ctx.step(lr, mu)
             step_ms.append((time.perf_counter() - s0) * 1e3)
+            if step_ms[-1] > 1000:   # long steps report as they go
+                print(f"{mode} step: {step_ms[-1]:.1f} ms", file=sys.stderr, flush=True)
         elapsed = time.perf_counter() - t0
         return {"elapsed": elapsed, "loss": loss, "stats": ctx.stats(), "fn_ms": ctx.fn_times(),
                 "step_ms": step_ms, "timeline": ctx.timeline()}
@@ -330,6 +338,9 @@ def main():
                          "ahead")
     ap.add_argument("--swapin-ahead", type=int, default=1, help="functions (lms)")
     ap.add_argument("--swapout-threshold", type=int, default=1, help="functions (lms)")
+    ap.add_argument("--host-limit-gib", type=float, default=None,
+                    help="most pinned host memory for the arena (GiB); TEMPs beyond it get "
+                         "pageable homes copied through pinned staging slots")
     ap.add_argument("--timeline", default="",
                     help="write the last out-of-core step's kernel and copy spans (JSON) here")
     args = ap.parse_args()
@@ -366,8 +377,9 @@ def main():
     if not args.no_incore:
         inc = run_mode(net, spec, x, labels, params, ooc.UNLIMITED, None, chunk, args.steps,
                        args.warmup)
+    host_limit = None if args.host_limit_gib is None else int(args.host_limit_gib * (1 << 30))
     out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps, args.warmup,
-                   args.swapout_depth, policy, fixed, args.wait_order)
+                   args.swapout_depth, policy, fixed, args.wait_order, host_limit)
     if args.timeline:
         with open(args.timeline, "w") as fh:
             json.dump({"fns": net.fn_ops, "vars": net.names,
@@ -451,6 +463,10 @@ def main():
                                               moved / link["both"]) / 1e6, 2),
             "ceiling": ceiling,
             "pinned_arena_bytes": st["host_bytes"],
+            "host_limit_bytes": host_limit,
+            "pageable_overflow_bytes": st["spill_bytes"],
+            "staged_h2d_bytes_per_step": st["staged_h2d_bytes"],
+            "staged_d2h_bytes_per_step": st["staged_d2h_bytes"],
         },
         "peak_device_bytes": {"pool": st["pool_bytes"], "max_chunks_in_use_bytes":
                               st["max_chunks_used"] * chunk, "peak_accounted": st["peak_accounted"],
