@@ -322,7 +322,7 @@ ooc_status ooc_set_swapout_depth(ooc_ctx *ctx, int64_t depth);
  * cache of Section 1; pinning is what lets the copies run asynchronously at
  * the link's rate).  Persistent slots (INPUT, PARAM, STATE, OUTPUT) are
  * always pinned.  TEMP slots are pinned while they fit under the limit less
- * 1 GiB of staging slots; the others get homes in pageable memory, and their
+ * 2 GiB of staging slots; the others get homes in pageable memory, and their
  * copies move in 32 MiB pieces through the staging slots, host threads
  * copying each piece between slot and home.  Results are identical; only the
  * transfer rate of the staged bytes changes.  For hosts that pin less memory

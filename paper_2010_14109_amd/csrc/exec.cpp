@@ -46,8 +46,8 @@ static const uint64_t kSlotAlign = 4096;
 // move through kSlots pinned staging slots per direction, copied between slot
 // and pageable home by kThreads host threads per direction.
 static const uint64_t kPiece = 32ull << 20;
-static const int64_t kSlots = 16;
-static const int kThreads = 4;
+static const int64_t kSlots = 32;
+static const int kThreads = 8;
 
 #define HIPCK(call)                                                               \
   do {                                                                            \

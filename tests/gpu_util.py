@@ -55,7 +55,7 @@ def persistent_host_bytes(spec, keep_grads=True):
                if k != ooc.TEMP)
 
 
-STAGING_BYTES = 1 << 30   # the staging slots a host limit reserves
+STAGING_BYTES = 2 << 30   # the staging slots a host limit reserves
 
 
 def rel_l2(a, b):
