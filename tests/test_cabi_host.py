@@ -393,3 +393,22 @@ def test_conv_and_bn_signatures_are_checked(lib):
         ctx.add_fn("bn_fwd", [y, g, bt, yb, st], [ooc.R] * 3 + [ooc.W] * 2, [128, 6, 4])
     ctx.add_fn("bn_fwd", [y, g, bt, yb, st], [ooc.R] * 3 + [ooc.W] * 2, [128, 6, 3])
     ctx.close()
+
+
+def test_host_limit_validation(lib):
+    """A host limit of 0 is rejected; any positive limit is accepted until prepare (the
+    placement itself needs a device)."""
+    ctx = ooc.Context(-1)
+    try:
+        with pytest.raises(ooc.OocError) as e:
+            ctx.set_host_limit(0)
+        assert e.value.status == ooc.E_INVALID
+        ctx.set_host_limit(1)
+        ctx.set_host_limit(56 << 30)
+        x = ctx.add_var(64, ooc.INPUT)
+        t = ctx.add_var(64, ooc.TEMP)
+        ctx.add_fn("relu_fwd", [x, t], [ooc.R, ooc.W], [16])
+        ctx.build_schedule()
+        ctx.set_host_limit(ooc.UNLIMITED)           # still allowed after the schedule
+    finally:
+        ctx.close()

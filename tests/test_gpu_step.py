@@ -233,6 +233,25 @@ def test_pageable_overflow_multi_piece():
         assert outs[name].tobytes() == outs0[name].tobytes(), name
 
 
+def test_host_limit_below_persistent_slots_is_refused():
+    """prepare fails with OOC_E_HOST_OOM when the persistent slots and the staging slots alone
+    exceed the host limit (nothing else can move to pageable memory)."""
+    spec = tiny_specs()[0]
+    net = netdef.Net(spec, keep_grads=True)
+    ctx = ooc.Context(0)
+    try:
+        net.register(ctx)
+        ctx.set_chunk(4096)
+        ctx.set_budget(ctx.working_set_max())
+        ctx.set_host_limit(persistent_host_bytes(spec) + STAGING_BYTES - 1)
+        ctx.build_schedule()
+        with pytest.raises(ooc.OocError) as e:
+            ctx.prepare()
+        assert e.value.status == ooc.E_HOST_OOM
+    finally:
+        ctx.close()
+
+
 def test_two_steps_keep_state_on_the_host():
     """Parameters and momentum written back by step 1 are what step 2 starts from."""
     spec = tiny_specs()[2]
