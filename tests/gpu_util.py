@@ -7,7 +7,7 @@ from paper_2010_14109_amd import netdef, ooc
 
 def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk=2 << 20,
             policy="C", keep_grads=True, momentum_state=None, steps=1, inspect=None,
-            wait="oldest", host_limit=None):
+            wait="oldest", host_limit=None, fixed=None):
     """One (or more) training steps on device 0.  Returns (loss, outputs, stats) with
     outputs = {name: array} for every PARAM, STATE and OUTPUT variable.  ``inspect(ctx,
     net)``, when given, runs after the steps."""
@@ -23,6 +23,8 @@ def run_net(spec, x, labels, params, *, budget=ooc.UNLIMITED, window=None, chunk
         ctx.set_wait_order(wait)
         if host_limit is not None:
             ctx.set_host_limit(host_limit)
+        if fixed is not None:
+            ctx.set_fixed_distance(*fixed)
         ctx.build_schedule()
         ctx.prepare()
         net.view(ctx, "x")[...] = x

@@ -178,11 +178,16 @@ def test_full_size_out_of_core_equals_in_core(name, kw, chunk_mib, limit_gib):
         assert outs[nm].tobytes() == outs0[nm].tobytes(), nm
 
 
-@pytest.mark.parametrize("idx,policy", [(i, p) for i in range(6) for p in ("C", "L")])
-def test_pageable_overflow_equals_in_core(idx, policy):
+OVERFLOW = [(i, p, "oldest", None) for i in range(6) for p in ("C", "L")] + \
+    [(i, "C", "furthest", None) for i in (2, 5)] + [(i, "C", "oldest", (1, 1)) for i in (1, 3)]
+
+
+@pytest.mark.parametrize("idx,policy,wait,fixed", OVERFLOW)
+def test_pageable_overflow_equals_in_core(idx, policy, wait, fixed):
     """A host limit that leaves no pinned bytes for TEMPs: every swapped activation has a
     pageable home and moves through the staging slots.  Two steps (the second starts from
-    the state the first wrote back) equal two in-core steps bit for bit."""
+    the state the first wrote back) equal two in-core steps bit for bit, under both policies,
+    both wait orders and the fixed-distance scheduler."""
     spec = tiny_specs()[idx]
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
@@ -191,10 +196,13 @@ def test_pageable_overflow_equals_in_core(idx, policy):
     B = max(S.budget_for(0.25, S.incore_peak(b, k, f, chunk), chunk), S.working_set_max(b, f, chunk))
     W = B // 2 if policy == "C" else 0
     limit = persistent_host_bytes(spec) + STAGING_BYTES
-    print(f"{spec['name']}: budget {B} window {W} policy {policy} host limit {limit}", flush=True)
+    if fixed is not None:   # the fixed-distance rule keeps what it keeps: give it room
+        B = max(B, S.budget_for(0.5, S.incore_peak(b, k, f, chunk), chunk))
+    print(f"{spec['name']}: budget {B} window {W} policy {policy} wait {wait} fixed {fixed} "
+          f"host limit {limit}", flush=True)
     loss0, outs0, _ = run_net(spec, x, labels, params, chunk=chunk, steps=2)
     loss, outs, st = run_net(spec, x, labels, params, budget=B, window=W, chunk=chunk,
-                             policy=policy, steps=2, host_limit=limit)
+                             policy=policy, steps=2, host_limit=limit, wait=wait, fixed=fixed)
     assert st["spill_bytes"] > 0 and st["staged_h2d_bytes"] > 0 and st["staged_d2h_bytes"] > 0
     assert st["staged_h2d_bytes"] <= st["h2d_bytes"] and st["staged_d2h_bytes"] <= st["d2h_bytes"]
     assert st["pool_bytes"] <= B and st["host_bytes"] <= limit
