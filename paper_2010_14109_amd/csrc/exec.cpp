@@ -841,22 +841,29 @@ ooc_status step(ooc_ctx* ctx, float lr, float mu, float* loss_out) {
   std::vector<int32_t> issued;   // done events of the swap-outs issued so far
   for (int64_t i = 0; i < N; ++i) {
     const FnProgram& fp = ctx->prog[i];
+    // an event of a staged swap-in is recorded by the issuer thread: wait until it has
+    // been, before a stream of this loop waits for it
+    auto issued_by_stager = [&](const std::vector<int32_t>& evs) -> bool {
+      for (int32_t w : evs) {
+        const int64_t sc = ctx->ev_staged_in[w];   // staged swap-in it completes, or -1
+        if (sc >= 0 && !stager.wait([&] { return stager.recorded > sc; })) {
+          ctx->err = stager.err;
+          return false;
+        }
+      }
+      return true;
+    };
     for (const Copy& c : fp.h2d) {
       if (c.staged) {
         stager.bump(&stager.posted, ++staged_in);
         continue;
       }
+      if (!issued_by_stager(c.waits)) return OOC_E_DEVICE;
       ooc_status s = enqueue_copy(ctx, c, ctx->hs, hipMemcpyHostToDevice);
       if (s) return s;
     }
-    for (int32_t w : fp.cwaits) {
-      const int64_t sc = ctx->ev_staged_in[w];   // staged swap-in it completes, or -1
-      if (sc >= 0 && !stager.wait([&] { return stager.recorded > sc; })) {
-        ctx->err = stager.err;
-        return OOC_E_DEVICE;
-      }
-      HIPCK(hipStreamWaitEvent(cs, ctx->events[w], 0));
-    }
+    if (!issued_by_stager(fp.cwaits)) return OOC_E_DEVICE;
+    for (int32_t w : fp.cwaits) HIPCK(hipStreamWaitEvent(cs, ctx->events[w], 0));
     HIPCK(hipEventRecord(ctx->events[fp.ev_pre], cs));
     hipError_t e = launch_fn(ctx->fns[i], fp.ptrs.data(), fp.sizes.data(), lr, mu, cs);
     if (e != hipSuccess) {
