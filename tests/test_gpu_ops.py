@@ -369,6 +369,8 @@ def test_attention(B, T, H, dh, causal):
                                          (((B * T, dmod), "f32"), ooc.W)], [B, T, H, dh, causal])
     rP, rY = ops.attention_fwd(qkv.astype(np.float64), B, T, H, bool(causal))
     assert rel_l2(P, rP) < TOL and rel_l2(Y, rY) < TOL
+    if causal:   # masked scores are exact zeros, also in tiles the products skip
+        assert not np.triu(P.reshape(B * H, T, T), 1).any()
     out = run_fn("attention_bwd", [(qkv, ooc.R), (P, ooc.R), (G, ooc.R),
                                    (((B * T, 3 * dmod), "f32"), ooc.W),
                                    (((B, H, T, T), "f32"), ooc.W)], [B, T, H, dh, causal])
