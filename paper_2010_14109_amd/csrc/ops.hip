@@ -269,10 +269,12 @@ __global__ __launch_bounds__(TPB) void bn_group_sums(float* __restrict__ part, i
 }
 
 // Pass 2 adds, per channel, either the fp64 sums of the slice groups
-// (GROUPED) or the slices' float partials.  Wave w takes the terms w, w + 4,
-// ... in four interleaved chains (term w + 4 u + 16 i goes to chain u), the
-// chains and then the four waves are added in order.  Forward -> mean, invstd;
-// backward -> dgamma, dbeta.
+// (GROUPED) or the slices' float partials.  Its workgroup has 16 waves (the
+// pass is a short chain of dependent loads per lane, so more waves shorten
+// it); wave w takes the terms w, w + 16, ... in four interleaved chains (term
+// w + 16 u + 64 i goes to chain u), the chains and then the 16 waves are added
+// in order.  Forward -> mean, invstd; backward -> dgamma, dbeta.
+constexpr int FIN_W = 16;
 template <bool GROUPED>
 __device__ inline void bn_term(const float* part, int64_t C, int64_t per, int64_t t, int64_t c,
                                double& a, double& b) {
@@ -288,29 +290,29 @@ __device__ inline void bn_term(const float* part, int64_t C, int64_t per, int64_
 }
 
 template <int MODE, bool GROUPED>
-__global__ __launch_bounds__(TPB) void bn_finalize(const float* __restrict__ x,
-                                                   const float* __restrict__ part,
-                                                   float* __restrict__ head,
-                                                   float* __restrict__ dgamma,
-                                                   float* __restrict__ dbeta, int64_t rows,
-                                                   int64_t C, int64_t per, int64_t terms) {
-  __shared__ double sa[4][64], sb[4][64];
+__global__ __launch_bounds__(64 * FIN_W) void bn_finalize(const float* __restrict__ x,
+                                                          const float* __restrict__ part,
+                                                          float* __restrict__ head,
+                                                          float* __restrict__ dgamma,
+                                                          float* __restrict__ dbeta, int64_t rows,
+                                                          int64_t C, int64_t per, int64_t terms) {
+  __shared__ double sa[FIN_W][64], sb[FIN_W][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t c = (int64_t)blockIdx.x * 64 + lane;
   double a[4] = {0, 0, 0, 0}, b[4] = {0, 0, 0, 0};
   if (c < C) {
     int64_t t = w;
-    for (; t + 12 < terms; t += 16) {
+    for (; t + 3 * FIN_W < terms; t += 4 * FIN_W) {
       double va[4], vb[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) bn_term<GROUPED>(part, C, per, t + 4 * u, c, va[u], vb[u]);
+      for (int u = 0; u < 4; ++u) bn_term<GROUPED>(part, C, per, t + FIN_W * u, c, va[u], vb[u]);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         a[u] += va[u];
         b[u] += vb[u];
       }
     }
-    for (int u = 0; t < terms; t += 4, ++u) {
+    for (int u = 0; t < terms; t += FIN_W, ++u) {
       double va, vb;
       bn_term<GROUPED>(part, C, per, t, c, va, vb);
       a[u] += va;
@@ -321,8 +323,12 @@ __global__ __launch_bounds__(TPB) void bn_finalize(const float* __restrict__ x,
   sb[w][lane] = (b[0] + b[1]) + (b[2] + b[3]);
   __syncthreads();
   if (w != 0 || c >= C) return;
-  const double ta = ((sa[0][lane] + sa[1][lane]) + sa[2][lane]) + sa[3][lane];
-  const double tb = ((sb[0][lane] + sb[1][lane]) + sb[2][lane]) + sb[3][lane];
+  double ta = 0, tb = 0;
+#pragma unroll
+  for (int k = 0; k < FIN_W; ++k) {
+    ta += sa[k][lane];
+    tb += sb[k][lane];
+  }
   if (MODE == 0) {
     const double m1 = ta / (double)rows;
     double var = tb / (double)rows - m1 * m1;
@@ -345,7 +351,7 @@ hipError_t bn_reduce(const float* x, float* stats, float* dgamma, float* dbeta, 
   const unsigned cg = (unsigned)((C + 63) / 64);
   float* part = stats + 2 * C;
   if (slices <= kOnePassSlices) {
-    hipLaunchKernelGGL((bn_finalize<MODE, false>), dim3(cg), dim3(TPB), 0, s, x, part, stats,
+    hipLaunchKernelGGL((bn_finalize<MODE, false>), dim3(cg), dim3(64 * FIN_W), 0, s, x, part, stats,
                        dgamma, dbeta, rows, C, (int64_t)1, slices);
     return hipGetLastError();
   }
@@ -354,7 +360,7 @@ hipError_t bn_reduce(const float* x, float* stats, float* dgamma, float* dbeta, 
                      per, groups);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((bn_finalize<MODE, true>), dim3(cg), dim3(TPB), 0, s, x, part, stats, dgamma,
+  hipLaunchKernelGGL((bn_finalize<MODE, true>), dim3(cg), dim3(64 * FIN_W), 0, s, x, part, stats, dgamma,
                      dbeta, rows, C, per, groups);
   return hipGetLastError();
 }
