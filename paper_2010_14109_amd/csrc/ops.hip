@@ -174,7 +174,42 @@ __global__ void bn_partials(const float* __restrict__ x, const float* __restrict
     }
   }
   const bool vec = (C % 4 == 0) && c0 + 3 < C;
-  for (int64_t r = sm.begin(s) + rl; r < sm.end(s); r += 16) {
+  auto add = [&](const float (&xv)[4], const float (&gv)[4]) {
+    for (int e = 0; e < 4; ++e) {
+      if (MODE == 0) {
+        const float d = xv[e] - sh[e];
+        a[e] += d;
+        b[e] += d * d;
+      } else {
+        const float xh = (xv[e] - sh[e]) * inv[e];
+        a[e] += gv[e];
+        b[e] += gv[e] * xh;
+      }
+    }
+  };
+  int64_t r = sm.begin(s) + rl;
+  const int64_t r_end = sm.end(s);
+  if (vec) {
+    // four rows' loads in flight per lane, then added in row order as below
+    for (; r + 48 < r_end; r += 64) {
+      float4 t[4], u[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        t[k] = *reinterpret_cast<const float4*>(&x[(r + 16 * k) * C + c0]);
+        if (MODE == 1) u[k] = *reinterpret_cast<const float4*>(&dy[(r + 16 * k) * C + c0]);
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float xv[4] = {t[k].x, t[k].y, t[k].z, t[k].w};
+        float gv[4] = {0, 0, 0, 0};
+        if (MODE == 1) {
+          gv[0] = u[k].x; gv[1] = u[k].y; gv[2] = u[k].z; gv[3] = u[k].w;
+        }
+        add(xv, gv);
+      }
+    }
+  }
+  for (; r < r_end; r += 16) {
     float xv[4], gv[4] = {0, 0, 0, 0};
     if (vec) {
       const float4 t = *reinterpret_cast<const float4*>(&x[r * C + c0]);
@@ -190,17 +225,7 @@ __global__ void bn_partials(const float* __restrict__ x, const float* __restrict
         if (MODE == 1) gv[e] = c < C ? dy[r * C + c] : 0.f;
       }
     }
-    for (int e = 0; e < 4; ++e) {
-      if (MODE == 0) {
-        const float d = xv[e] - sh[e];
-        a[e] += d;
-        b[e] += d * d;
-      } else {
-        const float xh = (xv[e] - sh[e]) * inv[e];
-        a[e] += gv[e];
-        b[e] += gv[e] * xh;
-      }
-    }
+    add(xv, gv);
   }
   for (int e = 0; e < 4; ++e) {
     sa[rl][cl * 4 + e] = a[e];
