@@ -487,29 +487,120 @@ __global__ void maxpool_bwd_kernel(const uint8_t* __restrict__ idx, const float*
   }
 }
 
-// workgroup per (image, 64 channels): lane = channel, wave w sums pixels
-// w, w + 4, ...; the four wave sums are added in order
-__global__ __launch_bounds__(TPB) void avgpool_fwd_kernel(const float* __restrict__ x,
-                                                          float* __restrict__ y, int64_t HW,
-                                                          int64_t C) {
-  __shared__ float part[4][64];
+// The same two pooling passes for four channels per thread (C % 4 == 0) with
+// 32-bit index arithmetic (fewer than 2^31 elements): float4 data, uchar4
+// indices.  Per channel the taps are visited in the same order, so results
+// and ties are those of the kernels above.
+struct Pool32 {
+  int H, W, C4, k, st, pad, P, Q;
+};
+__device__ inline float comp4(const float4& v, int e) {
+  return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w;
+}
+
+__global__ void maxpool_fwd4_kernel(const float4* __restrict__ x, float4* __restrict__ y,
+                                    uchar4* __restrict__ idx, Pool32 p, int total) {
+  const int stride = gridDim.x * blockDim.x;
+  for (int o = blockIdx.x * blockDim.x + threadIdx.x; o < total; o += stride) {
+    const int c4 = o % p.C4;
+    int t = o / p.C4;
+    const int q = t % p.Q;
+    t /= p.Q;
+    const int pp = t % p.P;
+    const int n = t / p.P;
+    float best[4] = {0.f, 0.f, 0.f, 0.f};
+    int bi[4] = {-1, -1, -1, -1};
+    for (int r = 0; r < p.k; ++r) {
+      const int h = pp * p.st + r - p.pad;
+      if (h < 0 || h >= p.H) continue;
+      for (int s = 0; s < p.k; ++s) {
+        const int w = q * p.st + s - p.pad;
+        if (w < 0 || w >= p.W) continue;
+        const float4 v = x[((n * p.H + h) * p.W + w) * p.C4 + c4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float ve = comp4(v, e);
+          if (bi[e] < 0 || ve > best[e]) {
+            best[e] = ve;
+            bi[e] = r * p.k + s;
+          }
+        }
+      }
+    }
+    y[o] = make_float4(best[0], best[1], best[2], best[3]);
+    idx[o] = make_uchar4((unsigned char)(bi[0] < 0 ? 0 : bi[0]), (unsigned char)(bi[1] < 0 ? 0 : bi[1]),
+                         (unsigned char)(bi[2] < 0 ? 0 : bi[2]), (unsigned char)(bi[3] < 0 ? 0 : bi[3]));
+  }
+}
+
+__global__ void maxpool_bwd4_kernel(const uchar4* __restrict__ idx, const float4* __restrict__ dy,
+                                    float4* __restrict__ dx, Pool32 p, int total) {
+  const int stride = gridDim.x * blockDim.x;
+  for (int o = blockIdx.x * blockDim.x + threadIdx.x; o < total; o += stride) {
+    const int c4 = o % p.C4;
+    int t = o / p.C4;
+    const int w = t % p.W;
+    t /= p.W;
+    const int h = t % p.H;
+    const int n = t / p.H;
+    int plo = h + p.pad - p.k + 1;
+    plo = plo <= 0 ? 0 : (plo + p.st - 1) / p.st;
+    int phi = (h + p.pad) / p.st;
+    if (phi > p.P - 1) phi = p.P - 1;
+    int qlo = w + p.pad - p.k + 1;
+    qlo = qlo <= 0 ? 0 : (qlo + p.st - 1) / p.st;
+    int qhi = (w + p.pad) / p.st;
+    if (qhi > p.Q - 1) qhi = p.Q - 1;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int pp = plo; pp <= phi; ++pp)
+      for (int q = qlo; q <= qhi; ++q) {
+        const int tap = (h - (pp * p.st - p.pad)) * p.k + (w - (q * p.st - p.pad));
+        const int oi = ((n * p.P + pp) * p.Q + q) * p.C4 + c4;
+        const uchar4 ix = idx[oi];
+        const float4 g = dy[oi];
+        acc[0] += ix.x == tap ? g.x : 0.f;
+        acc[1] += ix.y == tap ? g.y : 0.f;
+        acc[2] += ix.z == tap ? g.z : 0.f;
+        acc[3] += ix.w == tap ? g.w : 0.f;
+      }
+    dx[o] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  }
+}
+
+// workgroup of nw waves (16 for large images, 4 for small ones) per (image, 64
+// channels): lane = channel, wave w sums the pixels w, w + nw, ... in four
+// interleaved chains (pixel w + nw u + 4 nw i goes to chain u), so that each
+// lane has four loads in flight; the chains and then the wave sums are added
+// in order
+constexpr int POOL_W = 16;
+__global__ __launch_bounds__(64 * POOL_W) void avgpool_fwd_kernel(const float* __restrict__ x,
+                                                                 float* __restrict__ y,
+                                                                 int64_t HW, int64_t C) {
+  __shared__ float part[POOL_W][64];
+  const int nw = (int)blockDim.x >> 6;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t n = blockIdx.y;
   const int64_t c = (int64_t)blockIdx.x * 64 + lane;
-  float acc[2] = {0.f, 0.f};
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
   if (c < C) {
     const float* xn = x + n * HW * C + c;
     int64_t j = w;
-    for (; j + 4 < HW; j += 8) {
-      acc[0] += xn[j * C];
-      acc[1] += xn[(j + 4) * C];
+    for (; j + 3 * nw < HW; j += 4 * nw) {
+      float v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = xn[(j + nw * u) * C];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] += v[u];
     }
-    for (; j < HW; j += 4) acc[0] += xn[j * C];
+    for (int u = 0; j < HW; j += nw, ++u) acc[u] += xn[j * C];
   }
-  part[w][lane] = acc[0] + acc[1];
+  part[w][lane] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   __syncthreads();
-  if (w == 0 && c < C)
-    y[n * C + c] = (((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane]) / (float)HW;
+  if (w == 0 && c < C) {
+    float t = 0.f;
+    for (int k = 0; k < nw; ++k) t += part[k][lane];
+    y[n * C + c] = t / (float)HW;
+  }
 }
 
 __global__ void avgpool_bwd_kernel(const float* __restrict__ dy, float* __restrict__ dx, int64_t N,
@@ -683,7 +774,25 @@ hipError_t bn_bwd(const float* x, const float* gamma, float* stats, const float*
   return hipGetLastError();
 }
 
+// four channels per thread with 32-bit indices when every element index fits
+static bool pool_vec(const PoolShape& p, const void* a, const void* b, const void* i) {
+  const int64_t big = std::max(p.N * p.H * p.W * p.C, p.N * p.P * p.Q * p.C);
+  return p.C % 4 == 0 && big < (int64_t(1) << 31) && aligned16(a) && aligned16(b) &&
+         ((uintptr_t)i & 3) == 0;
+}
+static Pool32 pool32(const PoolShape& p) {
+  return Pool32{(int)p.H, (int)p.W, (int)(p.C / 4), (int)p.k, (int)p.stride, (int)p.pad, (int)p.P,
+                (int)p.Q};
+}
+
 hipError_t maxpool_fwd(const float* x, float* y, uint8_t* idx, const PoolShape& p, hipStream_t s) {
+  if (pool_vec(p, x, y, idx)) {
+    const int total = (int)(p.N * p.P * p.Q * p.C / 4);
+    hipLaunchKernelGGL(maxpool_fwd4_kernel, dim3(grid_for(total)), dim3(TPB), 0, s,
+                       reinterpret_cast<const float4*>(x), reinterpret_cast<float4*>(y),
+                       reinterpret_cast<uchar4*>(idx), pool32(p), total);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(grid_for(p.N * p.P * p.Q * p.C)), dim3(TPB), 0, s, x,
                      y, idx, p);
   return hipGetLastError();
@@ -691,14 +800,22 @@ hipError_t maxpool_fwd(const float* x, float* y, uint8_t* idx, const PoolShape& 
 
 hipError_t maxpool_bwd(const uint8_t* idx, const float* dy, float* dx, const PoolShape& p,
                        hipStream_t s) {
+  if (pool_vec(p, dy, dx, idx)) {
+    const int total = (int)(p.N * p.H * p.W * p.C / 4);
+    hipLaunchKernelGGL(maxpool_bwd4_kernel, dim3(grid_for(total)), dim3(TPB), 0, s,
+                       reinterpret_cast<const uchar4*>(idx), reinterpret_cast<const float4*>(dy),
+                       reinterpret_cast<float4*>(dx), pool32(p), total);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(grid_for(p.N * p.H * p.W * p.C)), dim3(TPB), 0, s,
                      idx, dy, dx, p);
   return hipGetLastError();
 }
 
 hipError_t avgpool_fwd(const float* x, float* y, int64_t N, int64_t HW, int64_t C, hipStream_t s) {
-  hipLaunchKernelGGL(avgpool_fwd_kernel, dim3((unsigned)((C + 63) / 64), (unsigned)N), dim3(TPB), 0,
-                     s, x, y, HW, C);
+  const int nw = HW >= 256 ? POOL_W : 4;
+  hipLaunchKernelGGL(avgpool_fwd_kernel, dim3((unsigned)((C + 63) / 64), (unsigned)N),
+                     dim3(64 * nw), 0, s, x, y, HW, C);
   return hipGetLastError();
 }
 

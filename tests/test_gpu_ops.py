@@ -209,8 +209,9 @@ def test_sgd_plain_and_momentum():
 
 
 # ---------------------------------------------------------------- pooling
-def test_maxpool_with_ties():
-    N, H, Wd, C, k, st, pd = 2, 9, 8, 8, 3, 2, 1
+@pytest.mark.parametrize("C", [8, 6, 64])   # four channels per thread; one per thread (C % 4)
+def test_maxpool_with_ties(C):
+    N, H, Wd, k, st, pd = 2, 9, 8, 3, 2, 1
     P, Q = (H + 2 * pd - k) // st + 1, (Wd + 2 * pd - k) // st + 1
     X = f32(N, H, Wd, C)
     X[0, 0, 0, :] = X[0, 0, 1, :] = 7.0
@@ -226,8 +227,9 @@ def test_maxpool_with_ties():
     assert rel_l2(dX, ops.maxpool_bwd(ridx, d(G), X.shape, k, st, pd)) < 1e-6
 
 
-def test_avgpool():
-    N, H, Wd, C = 3, 7, 5, 12
+@pytest.mark.parametrize("H,Wd,C", [(7, 5, 12), (17, 19, 70)])   # 4 and 16 waves per workgroup
+def test_avgpool(H, Wd, C):
+    N = 3
     X, G = f32(N, H, Wd, C), f32(N, C)
     (_, Y) = run_fn("avgpool_fwd", [(X, ooc.R), (((N, C), "f32"), ooc.W)], [N, H, Wd, C])
     assert rel_l2(Y, ops.avgpool_fwd(d(X))) < TOL
