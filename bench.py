@@ -128,6 +128,9 @@ def measured_traffic(net, op):
     return round(sum(got) / len(got)) if got else None
 
 
+# pinned host memory asked for when the whole arena cannot be pinned (the MI355X boxes here pin
+# at most 64 GiB per process)
+DEFAULT_HOST_LIMIT = 56 << 30
 MAP_ENTRY_LIMIT = 40000   # chunks + mappings per plan; the process table holds ~65530
 
 
@@ -379,8 +382,18 @@ def main():
         inc = run_mode(net, spec, x, labels, params, ooc.UNLIMITED, None, chunk, args.steps,
                        args.warmup)
     host_limit = None if args.host_limit_gib is None else int(args.host_limit_gib * (1 << 30))
-    out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps, args.warmup,
-                   args.swapout_depth, policy, fixed, args.wait_order, host_limit)
+    try:
+        out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps,
+                       args.warmup, args.swapout_depth, policy, fixed, args.wait_order, host_limit)
+    except ooc.OocError as e:
+        # the host could not pin the whole arena: give the TEMPs beyond a limit pageable homes
+        if e.status != ooc.E_HOST_OOM or host_limit is not None:
+            raise
+        host_limit = DEFAULT_HOST_LIMIT
+        print(f"pinned arena refused ({e}); retrying with --host-limit-gib "
+              f"{host_limit / (1 << 30):g}", file=sys.stderr, flush=True)
+        out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps,
+                       args.warmup, args.swapout_depth, policy, fixed, args.wait_order, host_limit)
     if args.timeline:
         with open(args.timeline, "w") as fh:
             json.dump({"fns": net.fn_ops, "vars": net.names,
