@@ -488,6 +488,7 @@ ooc_status prepare(ooc_ctx* ctx) {
   if (hb > 0) {
     hipError_t e = hipHostMalloc((void**)&ctx->arena, hb, hipHostMallocDefault);
     if (e != hipSuccess) {
+      (void)hipGetLastError();   // the refusal must not surface at a later launch check
       ctx->arena = nullptr;
       ctx->err = "pinned host arena of " + std::to_string(hb) + " bytes: " + hipGetErrorString(e);
       return OOC_E_HOST_OOM;
