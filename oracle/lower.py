@@ -57,10 +57,10 @@ channel for each of S row slices, S = min(ceil(rows / 512), 2048) with rows =
 N H W; a LayerNorm's ``stats`` holds mean and 1/std per row followed by two
 partial sums per feature for each of S row slices, S = min(ceil(rows / 32),
 2048); a convolution's
-``part`` holds S_w slices of dW, S_w = min(ceil(1024 / T), ceil(L / 1024))
-with T = ceil(K / 128) ceil(R S C / 128) output tiles and L = N P Q; a dense
-layer's ``part`` holds S_w slices of dW then S_w slices of db, with the same
-S_w formula over K = out, R S C = in and L = rows.
+``part`` holds S_w slices of dW, S_w from ``conv_wgrad_slices`` over K output
+channels, R S C and L = N P Q; a dense layer's ``part`` holds S_w slices of dW
+then S_w slices of db, with the same rule over K = out, R S C = in and
+L = rows.
 
 Kinds: x and labels INPUT, parameters PARAM, momentum buffers STATE, loss
 OUTPUT (parameter gradients too when ``keep_grads``), everything else TEMP.
