@@ -577,9 +577,24 @@ ooc_status prepare(ooc_ctx* ctx) {
   }
 
   ctx->ev_staged_in.resize(ctx->event_stream.size(), -1);
+  // Compute-stream events that no stream waits for only time the step: they are
+  // created without the system-scope fence that recording an event otherwise
+  // performs (a cache writeback and invalidation after every function, measured
+  // at ~6 % of the plain CNN's in-core step).  Events another stream waits for
+  // keep it.
+  std::vector<uint8_t> waited(ctx->event_stream.size(), 0);
+  for (const FnProgram& fp : ctx->prog) {
+    for (int32_t w : fp.cwaits) waited[w] = 1;
+    for (const Copy& c : fp.h2d)
+      for (int32_t w : c.waits) waited[w] = 1;
+    for (const Copy& c : fp.d2h)
+      for (int32_t w : c.waits) waited[w] = 1;
+  }
   ctx->events.resize(ctx->event_stream.size(), nullptr);
   for (size_t j = 0; j < ctx->events.size(); ++j) {
-    hipError_t e = hipEventCreate(&ctx->events[j]);
+    const bool timing_only = ctx->event_stream[j] == 0 && !waited[j];
+    hipError_t e = timing_only ? hipEventCreateWithFlags(&ctx->events[j], hipEventDisableSystemFence)
+                               : hipEventCreate(&ctx->events[j]);
     if (e != hipSuccess) {
       ctx->events.resize(j);
       ctx->err = std::string("hipEventCreate failed: ") + hipGetErrorString(e);
