@@ -248,6 +248,25 @@ __global__ void gelu_kernel(const float* __restrict__ x, const float* __restrict
   }
 }
 
+// the same arithmetic four elements at a time (n % 4 == 0, 16-byte aligned pointers)
+__device__ inline float gelu_at(float v, float g, bool backward) {
+  const float cdf = 0.5f * erfcf(-v * 0.70710678118654752f);
+  if (!backward) return v * cdf;
+  const float pdf = expf(-0.5f * v * v) * 0.39894228040143268f;
+  return g * (cdf + v * pdf);
+}
+
+__global__ void gelu4_kernel(const float4* __restrict__ x, const float4* __restrict__ dy,
+                             float4* __restrict__ out, int64_t n4, bool backward) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    const float4 v = x[i];
+    const float4 g = backward ? dy[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    out[i] = make_float4(gelu_at(v.x, g.x, backward), gelu_at(v.y, g.y, backward),
+                         gelu_at(v.z, g.z, backward), gelu_at(v.w, g.w, backward));
+  }
+}
+
 // ---------------------------------------------------------------- attention rows
 // P row (b, h, i) in place: scale, causal mask (keys j > i get 0), softmax
 __global__ void attn_softmax(float* __restrict__ P, int64_t nrows, int64_t T, float scale,
@@ -268,6 +287,78 @@ __global__ void attn_softmax(float* __restrict__ P, int64_t nrows, int64_t T, fl
   for (int64_t j = lane; j < T; j += 64) p[j] = j < n ? expf(p[j] * scale - mx) * inv : 0.f;
 }
 
+// The same two row operations with the row held in registers: lane l owns the float4s
+// l, l + 64, ..., so a row of T <= 256 K floats (T % 4 == 0) is read once.  Under the causal
+// mask, keys j >= n are not read: their P is 0, and so is their dS.
+template <int K>
+__global__ void attn_softmax_regs(float* __restrict__ P, int64_t nrows, int64_t T, float scale,
+                                  bool causal) {
+  const int64_t row = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= nrows) return;
+  const int64_t n = causal ? row % T + 1 : T;
+  float4* p = reinterpret_cast<float4*>(P + row * T);
+  float v[K][4];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int64_t j0 = 4 * (lane + 64 * k);
+    float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (j0 < n) t = p[lane + 64 * k];
+    v[k][0] = t.x; v[k][1] = t.y; v[k][2] = t.z; v[k][3] = t.w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (j0 + e < n) mx = fmaxf(mx, v[k][e] * scale);
+  }
+  mx = wave_max(mx);
+  float sum = 0.f;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int64_t j0 = 4 * (lane + 64 * k);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[k][e] = j0 + e < n ? expf(v[k][e] * scale - mx) : 0.f;
+      sum += v[k][e];
+    }
+  }
+  sum = wave_sum(sum);
+  const float inv = 1.f / sum;
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+    if (4 * (lane + 64 * k) < T)
+      p[lane + 64 * k] = make_float4(v[k][0] * inv, v[k][1] * inv, v[k][2] * inv, v[k][3] * inv);
+}
+
+template <int K>
+__global__ void attn_softmax_bwd_regs(const float* __restrict__ P, float* __restrict__ dS,
+                                      int64_t nrows, int64_t T, float scale, bool causal) {
+  const int64_t row = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= nrows) return;
+  const int64_t n = causal ? row % T + 1 : T;
+  const float4* p = reinterpret_cast<const float4*>(P + row * T);
+  float4* g = reinterpret_cast<float4*>(dS + row * T);
+  float4 pv[K], gv[K];
+  float dot = 0.f;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    pv[k] = gv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (4 * (lane + 64 * k) < n) {
+      pv[k] = p[lane + 64 * k];
+      gv[k] = g[lane + 64 * k];
+    }
+    dot += gv[k].x * pv[k].x + gv[k].y * pv[k].y + gv[k].z * pv[k].z + gv[k].w * pv[k].w;
+  }
+  dot = wave_sum(dot);
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+    if (4 * (lane + 64 * k) < T)
+      g[lane + 64 * k] = make_float4(scale * pv[k].x * (gv[k].x - dot),
+                                     scale * pv[k].y * (gv[k].y - dot),
+                                     scale * pv[k].z * (gv[k].z - dot),
+                                     scale * pv[k].w * (gv[k].w - dot));
+}
+
 // dS row in place: dS = scale P (dP - sum_j dP P)
 __global__ void attn_softmax_bwd(const float* __restrict__ P, float* __restrict__ dS,
                                  int64_t nrows, int64_t T, float scale) {
@@ -280,6 +371,49 @@ __global__ void attn_softmax_bwd(const float* __restrict__ P, float* __restrict_
   for (int64_t j = lane; j < T; j += 64) dot += g[j] * p[j];
   dot = wave_sum(dot);
   for (int64_t j = lane; j < T; j += 64) g[j] = scale * p[j] * (g[j] - dot);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+hipError_t gelu_launch(const float* x, const float* dy, float* out, int64_t n, bool backward,
+                       hipStream_t s) {
+  if (n % 4 == 0 && aligned16(x) && aligned16(out) && (!backward || aligned16(dy)))
+    hipLaunchKernelGGL(gelu4_kernel, dim3(grid_for(n / 4)), dim3(TPB), 0, s,
+                       reinterpret_cast<const float4*>(x), reinterpret_cast<const float4*>(dy),
+                       reinterpret_cast<float4*>(out), n / 4, backward);
+  else
+    hipLaunchKernelGGL(gelu_kernel, dim3(grid_for(n)), dim3(TPB), 0, s, x, dy, out, n, backward);
+  return hipGetLastError();
+}
+
+// rows of T floats: the register kernels need T % 4 == 0, T <= 1024 and an aligned base
+int softmax_regs(const float* base, int64_t T) {
+  if (T % 4 != 0 || T > 1024 || !aligned16(base)) return 0;
+  return T <= 256 ? 1 : T <= 512 ? 2 : 4;
+}
+
+hipError_t softmax_rows(float* P, int64_t nrows, int64_t T, float scale, bool causal,
+                        hipStream_t s) {
+  const dim3 grid((unsigned)((nrows + 3) / 4));
+  switch (softmax_regs(P, T)) {
+    case 1: hipLaunchKernelGGL(attn_softmax_regs<1>, grid, dim3(TPB), 0, s, P, nrows, T, scale, causal); break;
+    case 2: hipLaunchKernelGGL(attn_softmax_regs<2>, grid, dim3(TPB), 0, s, P, nrows, T, scale, causal); break;
+    case 4: hipLaunchKernelGGL(attn_softmax_regs<4>, grid, dim3(TPB), 0, s, P, nrows, T, scale, causal); break;
+    default: hipLaunchKernelGGL(attn_softmax, grid, dim3(TPB), 0, s, P, nrows, T, scale, causal);
+  }
+  return hipGetLastError();
+}
+
+hipError_t softmax_rows_bwd(const float* P, float* dS, int64_t nrows, int64_t T, float scale,
+                            bool causal, hipStream_t s) {
+  const dim3 grid((unsigned)((nrows + 3) / 4));
+  switch (aligned16(dS) ? softmax_regs(P, T) : 0) {
+    case 1: hipLaunchKernelGGL(attn_softmax_bwd_regs<1>, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale, causal); break;
+    case 2: hipLaunchKernelGGL(attn_softmax_bwd_regs<2>, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale, causal); break;
+    case 4: hipLaunchKernelGGL(attn_softmax_bwd_regs<4>, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale, causal); break;
+    default: hipLaunchKernelGGL(attn_softmax_bwd, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale);
+  }
+  return hipGetLastError();
 }
 
 template <int J>
@@ -351,14 +485,13 @@ hipError_t layernorm_bwd(const float* x, const float* gamma, float* stats, const
   return hipGetLastError();
 }
 
+
 hipError_t gelu_fwd(const float* x, float* y, int64_t n, hipStream_t s) {
-  hipLaunchKernelGGL(gelu_kernel, dim3(grid_for(n)), dim3(TPB), 0, s, x, nullptr, y, n, false);
-  return hipGetLastError();
+  return gelu_launch(x, nullptr, y, n, false, s);
 }
 
 hipError_t gelu_bwd(const float* x, const float* dy, float* dx, int64_t n, hipStream_t s) {
-  hipLaunchKernelGGL(gelu_kernel, dim3(grid_for(n)), dim3(TPB), 0, s, x, dy, dx, n, true);
-  return hipGetLastError();
+  return gelu_launch(x, dy, dx, n, true, s);
 }
 
 hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_t T, int64_t H,
@@ -368,9 +501,8 @@ hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_
   BatchStrides st{H, T * d3, dh, T * d3, dh, H * TT, TT};
   hipError_t e = gemm_batched(true, qkv, d3, true, qkv + d, d3, P, T, T, T, dh, B * H, st, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_softmax, dim3((unsigned)((B * H * T + 3) / 4)), dim3(TPB), 0, s, P,
-                     B * H * T, T, 1.f / sqrtf((float)dh), causal);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = softmax_rows(P, B * H * T, T, 1.f / sqrtf((float)dh), causal, s)) != hipSuccess)
+    return e;
   // context = P v
   BatchStrides sv{H, H * TT, TT, T * d3, dh, T * d, dh};
   return gemm_batched(true, P, T, false, qkv + 2 * d, d3, y, d, T, dh, T, B * H, sv, s);
@@ -378,7 +510,6 @@ hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_
 
 hipError_t attention_bwd(const float* qkv, const float* P, const float* dy, float* dqkv, float* dS,
                          int64_t B, int64_t T, int64_t H, int64_t dh, bool causal, hipStream_t s) {
-  (void)causal;   // P is zero above the diagonal, so dS is too
   const int64_t d = H * dh, d3 = 3 * d, TT = T * T;
   hipError_t e;
   // dv = P^T dO
@@ -391,9 +522,9 @@ hipError_t attention_bwd(const float* qkv, const float* P, const float* dy, floa
   if ((e = gemm_batched(true, dy, d, true, qkv + 2 * d, d3, dS, T, T, T, dh, B * H, s2, s)) !=
       hipSuccess)
     return e;
-  hipLaunchKernelGGL(attn_softmax_bwd, dim3((unsigned)((B * H * T + 3) / 4)), dim3(TPB), 0, s, P,
-                     dS, B * H * T, T, 1.f / sqrtf((float)dh));
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = softmax_rows_bwd(P, dS, B * H * T, T, 1.f / sqrtf((float)dh), causal, s)) !=
+      hipSuccess)
+    return e;
   // dq = dS k
   BatchStrides s3{H, H * TT, TT, T * d3, dh, T * d3, dh};
   if ((e = gemm_batched(true, dS, T, false, qkv + d, d3, dqkv, d3, T, dh, T, B * H, s3, s)) !=

@@ -26,9 +26,10 @@ rng = np.random.default_rng(77)
 NPT = {"f32": np.float32, "i32": np.int32, "u8": np.uint8, "u32": np.uint32}
 
 
-def run_fn(op, args, attrs):
+def run_fn(op, args, attrs, chunk=4096):
     """args: list of (array or (shape, dtype), access); arrays are inputs, tuples outputs.
-    Returns the final value of every variable, in order."""
+    Returns the final value of every variable, in order.  Variables of tens of MiB need a
+    chunk larger than the 4 KiB default: tens of thousands of 4 KiB mappings are refused."""
     ctx = ooc.Context(0)
     try:
         ids, dts = [], []
@@ -43,7 +44,7 @@ def run_fn(op, args, attrs):
                 ids.append(ctx.add_var(nb, ooc.OUTPUT))
                 dts.append((shape, np.dtype(NPT[dt])))
         ctx.add_fn(op, ids, [acc for _, acc in args], attrs)
-        ctx.set_chunk(4096)
+        ctx.set_chunk(chunk)
         ctx.build_schedule()
         ctx.prepare()
         for (a, _), v, (shape, dt) in zip(args, ids, dts):
@@ -326,15 +327,17 @@ def test_layernorm(rows, d, slices):
     assert rel_l2(out[4], rdX) < TOL and rel_l2(out[5], rdg) < TOL and rel_l2(out[6], rdb) < TOL
 
 
-@pytest.mark.parametrize("n", [1003, 1, 64])
+@pytest.mark.parametrize("n", [1003, 1, 64, 4 * (16384 * 256 + 5)])
 def test_gelu(n):
-    """n = 64 spans the lower tail (x down to -12), where GELU is tiny but not 0."""
+    """n = 64 spans the lower tail (x down to -12), where GELU is tiny but not 0.  Sizes that are
+    multiples of 4 take the four-wide kernel; the largest needs two grid-stride passes."""
     x, g = f32(n, scale=3.0), f32(n)
     if n == 64:
         x = np.linspace(-12.0, 4.0, n).astype(np.float32)
-    (_, y) = run_fn("gelu_fwd", [(x, ooc.R), (((n,), "f32"), ooc.W)], [n])
+    chunk = 4096 if n < 1 << 20 else 2 << 20
+    (_, y) = run_fn("gelu_fwd", [(x, ooc.R), (((n,), "f32"), ooc.W)], [n], chunk)
     assert rel_l2(y, ops.gelu_fwd(x.astype(np.float64))) < TOL
-    (_, _, dx) = run_fn("gelu_bwd", [(x, ooc.R), (g, ooc.R), (((n,), "f32"), ooc.W)], [n])
+    (_, _, dx) = run_fn("gelu_bwd", [(x, ooc.R), (g, ooc.R), (((n,), "f32"), ooc.W)], [n], chunk)
     assert rel_l2(dx, ops.gelu_bwd(x.astype(np.float64), g.astype(np.float64))) < TOL
 
 
@@ -362,7 +365,9 @@ def test_embedding_out_of_range_id():
 
 
 @pytest.mark.parametrize("B,T,H,dh,causal", [(2, 6, 2, 8, 1), (2, 64, 4, 16, 1), (1, 130, 2, 64, 1),
-                                            (2, 33, 3, 8, 0), (1, 512, 2, 64, 1)])
+                                            (2, 33, 3, 8, 0), (1, 512, 2, 64, 1),
+                                            (1, 260, 2, 8, 1), (2, 256, 2, 16, 0),
+                                            (1, 392, 1, 16, 0), (1, 1024, 1, 32, 1)])
 def test_attention(B, T, H, dh, causal):
     dmod = H * dh
     qkv, G = f32(B * T, 3 * dmod), f32(B * T, dmod)
