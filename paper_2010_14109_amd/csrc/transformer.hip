@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <initializer_list>
 
 #include "kernels.h"
 
@@ -197,6 +198,123 @@ __global__ __launch_bounds__(TPB) void ln_bwd_kernel(const float* __restrict__ x
     __syncthreads();
   }
   for (int64_t c = threadIdx.x; c < 2 * d; c += TPB) part[s * 2 * d + c] = lds[c];
+}
+
+// The same two LayerNorm passes for d % 4 == 0 with 16-byte aligned rows: a lane owns the
+// float4s lane, lane + 64, ... of a row.  The backward runs 8 waves per slice.
+template <int J4>
+__global__ __launch_bounds__(TPB) void ln_fwd4_kernel(const float4* __restrict__ x,
+                                                      const float4* __restrict__ gamma,
+                                                      const float4* __restrict__ beta,
+                                                      float4* __restrict__ y,
+                                                      float* __restrict__ stats, int64_t rows,
+                                                      int64_t d) {
+  const int64_t r = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const int64_t d4 = d / 4;
+  const float4* xr = x + r * d4;
+  float4 v[J4];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < J4; ++j) {
+    const int64_t c = lane + 64 * j;
+    v[j] = c < d4 ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    s += v[j].x + v[j].y + v[j].z + v[j].w;
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < J4; ++j) {
+    if (lane + 64 * j < d4) {
+      const float4 t = make_float4(v[j].x - mean, v[j].y - mean, v[j].z - mean, v[j].w - mean);
+      q += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
+    }
+  }
+  const float rstd = 1.f / sqrtf(wave_sum(q) / (float)d + 1e-5f);
+  float4* yr = y + r * d4;
+#pragma unroll
+  for (int j = 0; j < J4; ++j) {
+    const int64_t c = lane + 64 * j;
+    if (c < d4) {
+      const float4 g = gamma[c], b = beta[c];
+      yr[c] = make_float4((v[j].x - mean) * rstd * g.x + b.x, (v[j].y - mean) * rstd * g.y + b.y,
+                          (v[j].z - mean) * rstd * g.z + b.z, (v[j].w - mean) * rstd * g.w + b.w);
+    }
+  }
+  if (lane == 0) {
+    stats[r] = mean;
+    stats[rows + r] = rstd;
+  }
+}
+
+constexpr int LNB_WAVES = 8;
+
+template <int J4>
+__global__ __launch_bounds__(64 * LNB_WAVES) void ln_bwd4_kernel(
+    const float4* __restrict__ x, const float4* __restrict__ gamma, const float* __restrict__ st,
+    const float4* __restrict__ dy, float4* __restrict__ dx, float* __restrict__ part, int64_t rows,
+    int64_t d, int64_t len) {
+  extern __shared__ float4 lds4[];   // [2][d / 4]
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t s = blockIdx.x, d4 = d / 4;
+  const int64_t r0 = s * len, r1 = min(rows, r0 + len);
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 ag[J4], ab[J4], gm[J4];
+#pragma unroll
+  for (int j = 0; j < J4; ++j) {
+    const int64_t c = lane + 64 * j;
+    ag[j] = ab[j] = z;
+    gm[j] = c < d4 ? gamma[c] : z;
+  }
+  for (int64_t r = r0 + w; r < r1; r += LNB_WAVES) {
+    const float mean = st[r], rstd = st[rows + r];
+    float4 xh[J4], g[J4];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < J4; ++j) {
+      const int64_t c = lane + 64 * j;
+      const float4 dv = c < d4 ? dy[r * d4 + c] : z;
+      const float4 xv = c < d4 ? x[r * d4 + c] : z;
+      xh[j] = c < d4 ? make_float4((xv.x - mean) * rstd, (xv.y - mean) * rstd,
+                                   (xv.z - mean) * rstd, (xv.w - mean) * rstd)
+                     : z;
+      g[j] = make_float4(dv.x * gm[j].x, dv.y * gm[j].y, dv.z * gm[j].z, dv.w * gm[j].w);
+      s1 += g[j].x + g[j].y + g[j].z + g[j].w;
+      s2 += g[j].x * xh[j].x + g[j].y * xh[j].y + g[j].z * xh[j].z + g[j].w * xh[j].w;
+      ag[j].x += dv.x * xh[j].x; ag[j].y += dv.y * xh[j].y;
+      ag[j].z += dv.z * xh[j].z; ag[j].w += dv.w * xh[j].w;
+      ab[j].x += dv.x; ab[j].y += dv.y; ab[j].z += dv.z; ab[j].w += dv.w;
+    }
+    const float m1 = wave_sum(s1) / (float)d, m2 = wave_sum(s2) / (float)d;
+#pragma unroll
+    for (int j = 0; j < J4; ++j) {
+      const int64_t c = lane + 64 * j;
+      if (c < d4)
+        dx[r * d4 + c] = make_float4(rstd * (g[j].x - m1 - xh[j].x * m2),
+                                     rstd * (g[j].y - m1 - xh[j].y * m2),
+                                     rstd * (g[j].z - m1 - xh[j].z * m2),
+                                     rstd * (g[j].w - m1 - xh[j].w * m2));
+    }
+  }
+  // per-feature partials of the slice, the waves added in wave order
+  for (int k = 0; k < LNB_WAVES; ++k) {
+    if (w == k) {
+#pragma unroll
+      for (int j = 0; j < J4; ++j) {
+        const int64_t c = lane + 64 * j;
+        if (c < d4) {
+          const float4 pa = k == 0 ? z : lds4[c], pb = k == 0 ? z : lds4[d4 + c];
+          lds4[c] = make_float4(pa.x + ag[j].x, pa.y + ag[j].y, pa.z + ag[j].z, pa.w + ag[j].w);
+          lds4[d4 + c] =
+              make_float4(pb.x + ab[j].x, pb.y + ab[j].y, pb.z + ab[j].z, pb.w + ab[j].w);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  const float* l = reinterpret_cast<const float*>(lds4);
+  for (int64_t c = threadIdx.x; c < 2 * d; c += 64 * LNB_WAVES) part[s * 2 * d + c] = l[c];
 }
 
 // dgamma[c] / dbeta[c] = sum over slices of the partials.  A workgroup owns
@@ -454,6 +572,43 @@ hipError_t embed_bwd(const int32_t* ids, const float* dy, float* dE, float* dpos
   return hipGetLastError();
 }
 
+template <int J4>
+hipError_t ln_fwd4_j(const float* x, const float* g, const float* b, float* y, float* st,
+                     int64_t rows, int64_t d, hipStream_t s) {
+  hipLaunchKernelGGL(ln_fwd4_kernel<J4>, dim3((unsigned)((rows + 3) / 4)), dim3(TPB), 0, s,
+                     reinterpret_cast<const float4*>(x), reinterpret_cast<const float4*>(g),
+                     reinterpret_cast<const float4*>(b), reinterpret_cast<float4*>(y), st, rows, d);
+  return hipGetLastError();
+}
+
+template <int J4>
+hipError_t ln_bwd4_j(const float* x, const float* g, float* st, const float* dy, float* dx,
+                     int64_t rows, int64_t d, int64_t slices, hipStream_t s) {
+  const int64_t len = (rows + slices - 1) / slices;
+  hipLaunchKernelGGL(ln_bwd4_kernel<J4>, dim3((unsigned)slices), dim3(64 * LNB_WAVES),
+                     (unsigned)(2 * d * sizeof(float)), s, reinterpret_cast<const float4*>(x),
+                     reinterpret_cast<const float4*>(g), st, reinterpret_cast<const float4*>(dy),
+                     reinterpret_cast<float4*>(dx), st + 2 * rows, rows, d, len);
+  return hipGetLastError();
+}
+
+// float4 rows: d % 4 == 0, d <= dmax and every row pointer 16-byte aligned (the backward
+// stops at 2048: wider rows would spill its five float4 arrays per lane)
+static bool ln_vec(int64_t d, int64_t dmax, std::initializer_list<const void*> ptrs) {
+  if (d % 4 != 0 || d > dmax) return false;
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return false;
+  return true;
+}
+
+#define LN4_DISPATCH(CALL)                \
+  if (d <= 256) return CALL(1);           \
+  if (d <= 512) return CALL(2);           \
+  if (d <= 1024) return CALL(4);          \
+  if (d <= 2048) return CALL(8);          \
+  if (d <= 4096) return CALL(16);         \
+  return hipErrorInvalidValue
+
 #define LN_DISPATCH(CALL)                 \
   if (d <= 64) return CALL(1);            \
   if (d <= 128) return CALL(2);           \
@@ -467,6 +622,11 @@ hipError_t embed_bwd(const int32_t* ids, const float* dy, float* dE, float* dpos
 hipError_t layernorm_fwd(const float* x, const float* gamma, const float* beta, float* y,
                          float* stats, int64_t rows, int64_t d, int64_t slices, hipStream_t s) {
   (void)slices;
+  if (ln_vec(d, 4096, {x, gamma, beta, y})) {
+#define LN_F4(J) ln_fwd4_j<J>(x, gamma, beta, y, stats, rows, d, s)
+    LN4_DISPATCH(LN_F4);
+#undef LN_F4
+  }
 #define LN_F(J) ln_fwd_j<J>(x, gamma, beta, y, stats, rows, d, s)
   LN_DISPATCH(LN_F);
 #undef LN_F
@@ -477,7 +637,17 @@ hipError_t layernorm_bwd(const float* x, const float* gamma, float* stats, const
                          int64_t slices, hipStream_t s) {
   hipError_t e;
 #define LN_B(J) ln_bwd_j<J>(x, gamma, stats, dy, dx, rows, d, slices, s)
-  e = [&]() -> hipError_t { LN_DISPATCH(LN_B); }();
+#define LN_B4(J) ln_bwd4_j<J>(x, gamma, stats, dy, dx, rows, d, slices, s)
+  if (ln_vec(d, 2048, {x, gamma, dy, dx}))
+    e = [&]() -> hipError_t {
+      if (d <= 256) return LN_B4(1);
+      if (d <= 512) return LN_B4(2);
+      if (d <= 1024) return LN_B4(4);
+      return LN_B4(8);
+    }();
+  else
+    e = [&]() -> hipError_t { LN_DISPATCH(LN_B); }();
+#undef LN_B4
 #undef LN_B
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(ln_finalize, dim3((unsigned)((d + 63) / 64)), dim3(64 * FIN_WAVES), 0, s,

@@ -305,7 +305,8 @@ def test_upsample(N, H, W, C):
 
 # ---------------------------------------------------------------- transformer layers
 @pytest.mark.parametrize("rows,d,slices", [(37, 64, 1), (37, 100, 3), (130, 1024, 4), (5, 4096, 2),
-                                          (2000, 1024, 63), (999, 100, 37)])
+                                          (2000, 1024, 63), (999, 100, 37), (40, 66, 2),
+                                          (300, 2048, 9)])
 def test_layernorm(rows, d, slices):
     X = f32(rows, d, scale=2.0) + 0.3
     g, b, G = f32(d), f32(d), f32(rows, d)
