@@ -523,10 +523,12 @@ __device__ inline float comp(const float4& v, int t) {
 // BM x BN tile; the four waves form a grid of sub-tiles made of MFMA 32 x 32
 // blocks (2 x 2 waves, or 4 x 1 / 1 x 4 for tiles 32 wide / 32 tall).
 // Batched problems (grid z): batch z = (zo, zi) with zi = z mod inner; operand
-// and result pointers move by zo * outer stride + zi * inner stride.
+// and result pointers move by zo * outer stride + zi * inner stride.  With
+// skip_upper, tiles strictly above the diagonal return without writing.
 struct Batch {
   int64_t inner;
   int64_t a_o, a_i, b_o, b_i, c_o, c_i;
+  int64_t skip_upper;
 };
 
 template <class L>
@@ -577,6 +579,9 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
   const int tm = first_m + (t % per_group) % gsize;
   const int tn = (t % per_group) / gsize;
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  if constexpr (BATCHED) {
+    if (bt.skip_upper && n0 >= m0 + BM) return;   // the whole workgroup leaves together
+  }
   const int64_t kb = slice * k_slice;
   const int64_t ke = min(K, kb + k_slice);
 
@@ -680,7 +685,7 @@ template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED 
           bool ROWSUM = false>
 hipError_t run_gemm(const LA& la, const LB& lb, float* c, OM om, int64_t slice_stride,
                     const float* bias, int64_t M, int64_t N, int64_t K, int64_t slices,
-                    hipStream_t s, int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
+                    hipStream_t s, int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0, 0},
                     float* rowsum = nullptr) {
   const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   if (tiles_m * tiles_n > INT32_MAX / 2 || slices > 65535 || batches > 65535 || batches < 1 ||
@@ -714,7 +719,7 @@ template <template <int> class LAT, template <int> class LBT, bool BIAS, bool BA
           bool ROWSUM = false, class FA, class FB, class OM>
 hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const float* bias,
                     int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s,
-                    int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
+                    int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0, 0},
                     float* rowsum = nullptr) {
   switch (pick_shape(M, N)) {
     case S128x64: {
@@ -749,7 +754,7 @@ template <template <int> class LAT, template <int> class LBT, bool BIAS, bool BA
           bool ROWSUM = false, class FA, class FB>
 hipError_t dispatch_dense(FA fa, FB fb, float* c, int64_t ldc, const float* bias, int64_t M,
                           int64_t N, int64_t K, int64_t slices, hipStream_t s,
-                          int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0},
+                          int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0, 0},
                           float* rowsum = nullptr) {
   return dispatch<LAT, LBT, BIAS, BATCHED, ROWSUM>(fa, fb, c, DenseOut{ldc}, M * ldc, bias, M, N, K,
                                                    slices, s, batches, bt, rowsum);
@@ -892,8 +897,8 @@ hipError_t linear_bwd_w(const float* X, const float* dY, float* dW, float* db, f
 hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, const float* B,
                         int64_t ldb, float* C, int64_t ldc, int64_t M, int64_t N, int64_t K,
                         int64_t batches, const BatchStrides& st, hipStream_t s) {
-  const Batch bt{st.inner, st.a_outer, st.a_inner, st.b_outer, st.b_inner, st.c_outer,
-                 st.c_inner};
+  const Batch bt{st.inner,   st.a_outer, st.a_inner, st.b_outer,
+                 st.b_inner, st.c_outer, st.c_inner, st.skip_upper};
   auto fa = [&](auto& a) { a.p = A; a.ld = lda; };
   auto fb = [&](auto& b) { b.p = B; b.ld = ldb; };
   const bool vec = lda % 4 == 0 && ldb % 4 == 0 && aligned16(A) && aligned16(B) &&

@@ -26,6 +26,8 @@ hipError_t linear_bwd_x(const float* W, const float* dY, float* dX, int64_t M, i
 struct BatchStrides {
   int64_t inner;
   int64_t a_outer, a_inner, b_outer, b_inner, c_outer, c_inner;
+  // nonzero: C tiles whose every entry lies above the diagonal (column > row) are left unwritten
+  int64_t skip_upper = 0;
 };
 hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, const float* B,
                         int64_t ldb, float* C, int64_t ldc, int64_t M, int64_t N, int64_t K,

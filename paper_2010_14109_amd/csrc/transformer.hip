@@ -477,18 +477,20 @@ __global__ void attn_softmax_bwd_regs(const float* __restrict__ P, float* __rest
                                      scale * pv[k].w * (gv[k].w - dot));
 }
 
-// dS row in place: dS = scale P (dP - sum_j dP P)
+// dS row in place: dS = scale P (dP - sum_j dP P).  Under the causal mask the keys
+// j >= n are neither read (dP there may be unwritten) nor kept: their dS is 0.
 __global__ void attn_softmax_bwd(const float* __restrict__ P, float* __restrict__ dS,
-                                 int64_t nrows, int64_t T, float scale) {
+                                 int64_t nrows, int64_t T, float scale, bool causal) {
   const int64_t row = (int64_t)blockIdx.x * (TPB / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= nrows) return;
+  const int64_t n = causal ? row % T + 1 : T;
   const float* p = P + row * T;
   float* g = dS + row * T;
   float dot = 0.f;
-  for (int64_t j = lane; j < T; j += 64) dot += g[j] * p[j];
+  for (int64_t j = lane; j < n; j += 64) dot += g[j] * p[j];
   dot = wave_sum(dot);
-  for (int64_t j = lane; j < T; j += 64) g[j] = scale * p[j] * (g[j] - dot);
+  for (int64_t j = lane; j < T; j += 64) g[j] = j < n ? scale * p[j] * (g[j] - dot) : 0.f;
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -529,7 +531,7 @@ hipError_t softmax_rows_bwd(const float* P, float* dS, int64_t nrows, int64_t T,
     case 1: hipLaunchKernelGGL(attn_softmax_bwd_regs<1>, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale, causal); break;
     case 2: hipLaunchKernelGGL(attn_softmax_bwd_regs<2>, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale, causal); break;
     case 4: hipLaunchKernelGGL(attn_softmax_bwd_regs<4>, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale, causal); break;
-    default: hipLaunchKernelGGL(attn_softmax_bwd, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale);
+    default: hipLaunchKernelGGL(attn_softmax_bwd, grid, dim3(TPB), 0, s, P, dS, nrows, T, scale, causal);
   }
   return hipGetLastError();
 }
@@ -667,8 +669,9 @@ hipError_t gelu_bwd(const float* x, const float* dy, float* dx, int64_t n, hipSt
 hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_t T, int64_t H,
                          int64_t dh, bool causal, hipStream_t s) {
   const int64_t d = H * dh, d3 = 3 * d, TT = T * T;
-  // S = q k^T into P
-  BatchStrides st{H, T * d3, dh, T * d3, dh, H * TT, TT};
+  // S = q k^T into P; under the causal mask the tiles above the diagonal are left to the
+  // softmax, which writes them as 0 without reading them
+  BatchStrides st{H, T * d3, dh, T * d3, dh, H * TT, TT, causal ? 1 : 0};
   hipError_t e = gemm_batched(true, qkv, d3, true, qkv + d, d3, P, T, T, T, dh, B * H, st, s);
   if (e != hipSuccess) return e;
   if ((e = softmax_rows(P, B * H * T, T, 1.f / sqrtf((float)dh), causal, s)) != hipSuccess)
@@ -687,8 +690,8 @@ hipError_t attention_bwd(const float* qkv, const float* P, const float* dy, floa
   if ((e = gemm_batched(false, P, T, false, dy, d, dqkv + 2 * d, d3, T, dh, T, B * H, s1, s)) !=
       hipSuccess)
     return e;
-  // dP = dO v^T into dS
-  BatchStrides s2{H, T * d, dh, T * d3, dh, H * TT, TT};
+  // dP = dO v^T into dS (tiles above the diagonal likewise left to the softmax backward)
+  BatchStrides s2{H, T * d, dh, T * d3, dh, H * TT, TT, causal ? 1 : 0};
   if ((e = gemm_batched(true, dy, d, true, qkv + 2 * d, d3, dS, T, T, T, dh, B * H, s2, s)) !=
       hipSuccess)
     return e;
