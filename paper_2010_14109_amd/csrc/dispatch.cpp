@@ -1,5 +1,7 @@
 // Maps a registered function to its kernel launches.  Shapes come from the
 // attributes, which ooc_add_fn has checked against every variable's size.
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace ooc {
@@ -32,10 +34,20 @@ hipError_t launch_fn(const Fn& fn, void* const* p, const uint64_t* bytes, float 
       return softmax_ce(F(0), static_cast<const int32_t*>(p[1]), F(2), F(3), a[0], a[1], s);
     case OOC_OP_SGD: {
       const int per = a[1] ? 3 : 2;
-      for (int64_t k = 0; k < a[0]; ++k) {
-        const int j = (int)(k * per);
-        hipError_t e = sgd(F(j), F(j + 1), a[1] ? F(j + 2) : nullptr, (int64_t)(bytes[j] / 4), lr,
-                           mu, s);
+      float* w[64];
+      const float* g[64];
+      float* v[64];
+      int64_t n[64];
+      for (int64_t k0 = 0; k0 < a[0]; k0 += 64) {
+        const int m = (int)std::min<int64_t>(64, a[0] - k0);
+        for (int k = 0; k < m; ++k) {
+          const int j = (int)((k0 + k) * per);
+          w[k] = F(j);
+          g[k] = F(j + 1);
+          v[k] = a[1] ? F(j + 2) : nullptr;
+          n[k] = (int64_t)(bytes[j] / 4);
+        }
+        hipError_t e = sgd(m, w, g, v, n, lr, mu, s);
         if (e != hipSuccess) return e;
       }
       return hipSuccess;

@@ -46,7 +46,9 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
 hipError_t relu_fwd(const float* x, float* y, int64_t n, hipStream_t s);
 hipError_t relu_bwd(const float* y, const float* dy, float* dx, int64_t n, hipStream_t s);
 hipError_t add(const float* a, const float* b, float* y, int64_t n, hipStream_t s);
-hipError_t sgd(float* w, const float* g, float* v, int64_t n, float lr, float mu, hipStream_t s);
+// count parameter tensors: w[k] -= lr * (v[k] = mu v[k] + g[k]), or lr * g[k] where v[k] is null
+hipError_t sgd(int count, float* const* w, const float* const* g, float* const* v,
+               const int64_t* n, float lr, float mu, hipStream_t s);
 hipError_t softmax_ce(const float* logits, const int32_t* labels, float* loss, float* dlogits,
                       int64_t N, int64_t classes, hipStream_t s);
 hipError_t bn_fwd(const float* x, const float* gamma, const float* beta, float* y, float* stats,

@@ -60,12 +60,27 @@ hipError_t ew(const float* a, const float* b, float* y, int64_t n, hipStream_t s
   return hipGetLastError();
 }
 
-__global__ void sgd_kernel(float* __restrict__ w, const float* __restrict__ g,
-                           float* __restrict__ v, int64_t n, float lr, float mu, bool vec) {
+// Up to kSgdSet parameter tensors of one update function in one launch: grid row y
+// updates tensor y, each element with the same arithmetic as a launch of its own.
+constexpr int kSgdSet = 8;
+struct SgdSet {
+  float* w[kSgdSet];
+  const float* g[kSgdSet];
+  float* v[kSgdSet];
+  int64_t n[kSgdSet];
+  int32_t vec[kSgdSet];
+};
+
+__global__ void sgd_kernel(SgdSet set, float lr, float mu) {
+  const int k = blockIdx.y;
+  float* __restrict__ w = set.w[k];
+  const float* __restrict__ g = set.g[k];
+  float* __restrict__ v = set.v[k];
+  const int64_t n = set.n[k];
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t done = 0;
-  if (vec) {
+  if (set.vec[k]) {
     const int64_t n4 = n / 4;
     for (int64_t j = i; j < n4; j += stride) {
       float4 ww = reinterpret_cast<float4*>(w)[j];
@@ -724,11 +739,25 @@ hipError_t add(const float* a, const float* b, float* y, int64_t n, hipStream_t 
   return ew<2>(a, b, y, n, s);
 }
 
-hipError_t sgd(float* w, const float* g, float* v, int64_t n, float lr, float mu, hipStream_t s) {
-  const bool vec = aligned16(w) && aligned16(g) && (!v || aligned16(v));
-  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for((n + 3) / 4)), dim3(TPB), 0, s, w, g, v, n, lr, mu,
-                     vec);
-  return hipGetLastError();
+hipError_t sgd(int count, float* const* w, const float* const* g, float* const* v,
+               const int64_t* n, float lr, float mu, hipStream_t s) {
+  for (int k0 = 0; k0 < count; k0 += kSgdSet) {
+    SgdSet set{};
+    const int m = std::min(kSgdSet, count - k0);
+    unsigned gx = 1;
+    for (int k = 0; k < m; ++k) {
+      set.w[k] = w[k0 + k];
+      set.g[k] = g[k0 + k];
+      set.v[k] = v[k0 + k];
+      set.n[k] = n[k0 + k];
+      set.vec[k] = aligned16(set.w[k]) && aligned16(set.g[k]) && (!set.v[k] || aligned16(set.v[k]));
+      gx = std::max(gx, grid_for((set.n[k] + 3) / 4));
+    }
+    hipLaunchKernelGGL(sgd_kernel, dim3(gx, (unsigned)m), dim3(TPB), 0, s, set, lr, mu);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t softmax_ce(const float* logits, const int32_t* labels, float* loss, float* dlogits,

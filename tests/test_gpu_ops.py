@@ -209,6 +209,47 @@ def test_sgd_plain_and_momentum():
     del ctx_args
 
 
+@pytest.mark.parametrize("mom", [1, 0])
+def test_sgd_many_tensors_in_one_function(mom):
+    """One update function over 11 tensors (more than one launch's set of 8), sizes from 1 to
+    70001 elements, so that each tensor's grid row differs from the launch's widest."""
+    sizes = [1, 3, 4, 5000, 70001, 64, 7, 12288, 2, 999, 4096]
+    lr, mu = 0.05, 0.9 if mom else 0.0
+    ws, gs, vs = [f32(n) for n in sizes], [f32(n) for n in sizes], [f32(n) for n in sizes]
+    ctx = ooc.Context(0)
+    try:
+        ids, acc = [], []
+        for n in sizes:
+            ids.append(ctx.add_var(n * 4, ooc.PARAM))
+            ids.append(ctx.add_var(n * 4, ooc.INPUT))
+            acc += [ooc.RW, ooc.R]
+            if mom:
+                ids.append(ctx.add_var(n * 4, ooc.STATE))
+                acc.append(ooc.RW)
+        ctx.add_fn("sgd", ids, acc, [len(sizes), mom])
+        ctx.set_chunk(4096)
+        ctx.build_schedule()
+        ctx.prepare()
+        per = 3 if mom else 2
+        for k in range(len(sizes)):
+            ctx.host_view(ids[per * k])[...] = ws[k]
+            ctx.host_view(ids[per * k + 1])[...] = gs[k]
+            if mom:
+                ctx.host_view(ids[per * k + 2])[...] = vs[k]
+        ctx.upload()
+        ctx.step(lr, mu)
+        ctx.download()
+        for k in range(len(sizes)):
+            if mom:
+                rw, rv = ops.sgd_momentum(d(ws[k]), d(gs[k]), d(vs[k]), lr, mu)
+                assert rel_l2(ctx.host_view(ids[per * k + 2]), rv) < 1e-6
+            else:
+                rw = ops.sgd(d(ws[k]), d(gs[k]), lr)
+            assert rel_l2(ctx.host_view(ids[per * k]), rw) < 1e-6, k
+    finally:
+        ctx.close()
+
+
 # ---------------------------------------------------------------- pooling
 @pytest.mark.parametrize("C", [8, 6, 64])   # four channels per thread; one per thread (C % 4)
 def test_maxpool_with_ties(C):
