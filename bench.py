@@ -309,7 +309,7 @@ def cpu_baseline(name, budget_seconds=15.0):
         oracle_run(reg, x, labels, params, dtype=np.float32)
         n += 1
         el = time.perf_counter() - t0
-        if el >= budget_seconds or n >= 50:
+        if el >= budget_seconds or n >= 1000:
             break
     return {"value": n * small / el, "unit": "samples/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} float32 oracle steps of {spec['name']} (batch {small}) in "
