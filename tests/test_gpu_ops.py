@@ -280,7 +280,7 @@ def test_avgpool(H, Wd, C):
 
 
 # ---------------------------------------------------------------- loss
-@pytest.mark.parametrize("N,C", [(37, 10), (5, 1000), (1, 1)])
+@pytest.mark.parametrize("N,C", [(37, 10), (5, 1000), (1, 1), (70001, 3), (16387, 2)])
 def test_softmax_ce(N, C):
     Z = f32(N, C, scale=3.0)
     y = rng.integers(0, C, N).astype(np.int32)
