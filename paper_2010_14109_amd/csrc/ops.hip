@@ -677,7 +677,7 @@ __global__ void mix_kernel(MixArgs a) {
 // otherwise the concatenation's columns back into the part.  VEC moves float4
 // (cp, ct and off multiples of 4).
 template <bool TO_CAT, bool VEC>
-__global__ void concat_part_kernel(const float* __restrict__ src, float* __restrict__ dst,
+__device__ inline void concat_part(const float* __restrict__ src, float* __restrict__ dst,
                                    int64_t rows, int64_t cp, int64_t ct, int64_t off) {
   const int64_t per = VEC ? cp / 4 : cp;   // units per row
   const int64_t n = rows * per;
@@ -697,6 +697,26 @@ __global__ void concat_part_kernel(const float* __restrict__ src, float* __restr
         dst[pi] = src[ci];
     }
   }
+}
+
+// Up to kCatSet parts in one launch: grid row y moves part y.
+constexpr int kCatSet = 16;
+struct CatSet {
+  float* part[kCatSet];
+  int64_t cp[kCatSet], off[kCatSet];
+  int32_t vec[kCatSet];
+};
+
+template <bool TO_CAT>
+__global__ void concat_part_kernel(float* cat, CatSet set, int64_t rows, int64_t ct) {
+  const int k = blockIdx.y;
+  float* part = set.part[k];
+  const float* src = TO_CAT ? part : cat;
+  float* dst = TO_CAT ? cat : part;
+  if (set.vec[k])
+    concat_part<TO_CAT, true>(src, dst, rows, set.cp[k], ct, set.off[k]);
+  else
+    concat_part<TO_CAT, false>(src, dst, rows, set.cp[k], ct, set.off[k]);
 }
 
 // nearest 2x upsampling of NHWC x[N][H][W][C]: one thread per output unit
@@ -902,29 +922,29 @@ hipError_t concat(bool forward, float* cat, void* const* parts, const int64_t* c
   int64_t ct = 0;
   for (int j = 0; j < k; ++j) ct += cs[j];
   int64_t off = 0;
-  for (int j = 0; j < k; ++j) {
-    float* part = static_cast<float*>(parts[j]);
-    const bool vec = cs[j] % 4 == 0 && ct % 4 == 0 && off % 4 == 0 && aligned16(cat) &&
-                     aligned16(part);
-    const unsigned g = grid_for(rows * (vec ? cs[j] / 4 : cs[j]));
-    if (forward) {
-      if (vec)
-        hipLaunchKernelGGL((concat_part_kernel<true, true>), dim3(g), dim3(TPB), 0, s, part, cat,
-                           rows, cs[j], ct, off);
-      else
-        hipLaunchKernelGGL((concat_part_kernel<true, false>), dim3(g), dim3(TPB), 0, s, part,
-                           cat, rows, cs[j], ct, off);
-    } else {
-      if (vec)
-        hipLaunchKernelGGL((concat_part_kernel<false, true>), dim3(g), dim3(TPB), 0, s, cat,
-                           part, rows, cs[j], ct, off);
-      else
-        hipLaunchKernelGGL((concat_part_kernel<false, false>), dim3(g), dim3(TPB), 0, s, cat,
-                           part, rows, cs[j], ct, off);
+  for (int j0 = 0; j0 < k; j0 += kCatSet) {
+    CatSet set{};
+    const int m = std::min(kCatSet, k - j0);
+    unsigned g = 1;
+    for (int j = 0; j < m; ++j) {
+      float* part = static_cast<float*>(parts[j0 + j]);
+      const int64_t cp = cs[j0 + j];
+      set.part[j] = part;
+      set.cp[j] = cp;
+      set.off[j] = off;
+      set.vec[j] = cp % 4 == 0 && ct % 4 == 0 && off % 4 == 0 && aligned16(cat) &&
+                   aligned16(part);
+      g = std::max(g, grid_for(rows * (set.vec[j] ? cp / 4 : cp)));
+      off += cp;
     }
+    if (forward)
+      hipLaunchKernelGGL(concat_part_kernel<true>, dim3(g, (unsigned)m), dim3(TPB), 0, s, cat, set,
+                         rows, ct);
+    else
+      hipLaunchKernelGGL(concat_part_kernel<false>, dim3(g, (unsigned)m), dim3(TPB), 0, s, cat,
+                         set, rows, ct);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    off += cs[j];
   }
   return hipSuccess;
 }

@@ -315,7 +315,8 @@ def test_mix_op():
 
 
 # ---------------------------------------------------------------- concatenation, upsampling
-@pytest.mark.parametrize("rows,cs", [(37, (8, 12)), (37, (3, 5, 1)), (1, (4,)), (1000, (64, 32, 32))])
+@pytest.mark.parametrize("rows,cs", [(37, (8, 12)), (37, (3, 5, 1)), (1, (4,)), (1000, (64, 32, 32)),
+                                     (50, (64,) + (32,) * 14 + (3, 4, 5, 32))])
 def test_concat(rows, cs):
     parts = [f32(rows, c) for c in cs]
     ct = sum(cs)
