@@ -273,11 +273,12 @@ def _blas():
         return "unknown"
 
 
-def oracle_schedule_ms(spec, budget, window, chunk, policy, fixed, wait="oldest"):
-    """Wall time of the oracle's scheduler on the full-size function sequence (median of 3)."""
+def oracle_schedule_ms(spec, slices, budget, window, chunk, policy, fixed, wait="oldest"):
+    """Wall time of the oracle's scheduler on the full-size function sequence (median of 3);
+    ``slices``: the split-K counts of the weight gradients, as registered."""
     from oracle import schedule as S
     from oracle.lower import as_schedule_input, lower
-    b, k, f = as_schedule_input(lower(spec))
+    b, k, f = as_schedule_input(lower(spec, slices=slices))
     ahead, thr = fixed if fixed is not None else (None, None)
     times = []
     for _ in range(3):
@@ -498,7 +499,8 @@ def main():
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args.workload)
         res["schedule_build_ms"]["oracle"] = round(
-            oracle_schedule_ms(spec, budget, window, chunk, policy, fixed, args.wait_order), 3)
+            oracle_schedule_ms(spec, net.slices, budget, window, chunk, policy, fixed,
+                               args.wait_order), 3)
     print(json.dumps(res), flush=True)
 
 

@@ -15,7 +15,12 @@
  *
  * Conventions (every call):
  *  - No exception or signal crosses this interface.  Every failure returns a
- *    negative ooc_status and sets a message readable with ooc_last_error().
+ *    negative ooc_status and sets a message readable with ooc_last_error():
+ *    on the context for calls that take one (const queries included), else
+ *    (a NULL context, ooc_create, ooc_link_probe, ooc_wgrad_slices) on
+ *    ooc_last_error(NULL).  A NULL out-pointer, or a NULL buffer with a
+ *    nonzero capacity, is OOC_E_INVALID; a query made before the stage it
+ *    needs is OOC_E_STATE.
  *  - A context is driven in this order: create -> add_var / add_fn ->
  *    set_* -> build_schedule -> prepare -> (host_ptr, upload, step,
  *    download, get_stats)* -> destroy.  A call out of order returns
@@ -336,17 +341,25 @@ ooc_status ooc_set_host_limit(ooc_ctx *ctx, uint64_t bytes);
  * function's variables do not fit in the budget. */
 ooc_status ooc_build_schedule(ooc_ctx *ctx);
 
-/* Copies up to `cap` ops into `buf` (caller-owned; may be NULL when cap is
- * 0); *n receives the total count. */
+/* The schedule of Section 3 (Fig. 2, steps (a)-(d)) as an op list, in
+ * emission order: per function its PRE ops (swap-ins, allocations,
+ * cancelled swap-outs, budget waits), then its POST ops (frees and
+ * swap-outs), then the END waits.  Copies up to `cap` ops into `buf`
+ * (caller-owned; may be NULL when cap is 0); *n receives the total count.
+ * OOC_E_STATE before ooc_build_schedule. */
 ooc_status ooc_schedule_get(const ooc_ctx *ctx, ooc_op *buf, uint64_t cap, uint64_t *n);
 
-/* Window end r_i (0-based position of the variable-sequence) per function. */
+/* Window end r_i (0-based position of the variable-sequence, Section 3) per
+ * function.  OOC_E_STATE before ooc_build_schedule. */
 ooc_status ooc_schedule_windows(const ooc_ctx *ctx, int64_t *buf, uint64_t cap, uint64_t *n);
 
 /* P_incore: most chunk-rounded bytes live at one function in the in-core
- * plan; WS_max: largest chunk-rounded footprint of one function (no budget
- * below it is feasible).  Valid after registration (the chunk size in effect
- * is used). */
+ * plan, the memory an ordinary step needs (the "in-core" baseline the
+ * budgets and speeds of Section 5 are measured against); INPUT, PARAM,
+ * STATE and OUTPUT count for the whole step, a TEMP from its first to its
+ * last use.  WS_max: largest chunk-rounded footprint of one function (no
+ * budget below it is feasible, Section 3).  Valid after registration (the
+ * chunk size in effect is used). */
 ooc_status ooc_incore_peak(const ooc_ctx *ctx, uint64_t *bytes);
 ooc_status ooc_working_set_max(const ooc_ctx *ctx, uint64_t *bytes);
 
@@ -368,15 +381,19 @@ ooc_status ooc_bestfit_extent(const ooc_ctx *ctx, uint64_t align, uint64_t *exte
                               uint64_t *peak_live);
 ooc_status ooc_plan_chunks(const ooc_ctx *ctx, int32_t *buf, uint64_t cap, uint64_t *n);
 
-/* Creates the physical chunks, maps every interval's chunks into its own
- * virtual range, allocates the pinned host arena, streams and events.
+/* Sets up the memory of Section 4: creates the physical chunks (at most
+ * budget / m_c of them), maps every residency interval's chunks into its own
+ * contiguous virtual range (eq. 1: at most one partly used chunk per
+ * interval), and allocates the pinned host arena of Section 1, the streams
+ * and the events.  All mapping happens here, once; a step maps nothing.
  * Each chunk and each mapping of a chunk takes one entry of the process's
  * memory-map table (vm.max_map_count, typically 65530): a plan needing more
  * than the entries left returns OOC_E_UNSUPPORTED (choose a larger chunk). */
 ooc_status ooc_prepare(ooc_ctx *ctx);
 
 /* Pinned host slot of a host-backed variable (INPUT, PARAM, STATE, OUTPUT;
- * a TEMP has none: OOC_E_INVALID).  The caller writes INPUT/PARAM/STATE
+ * a TEMP has none: OOC_E_INVALID) in the CPU memory that serves as the
+ * swap target of Section 1.  The caller writes INPUT/PARAM/STATE
  * slots before a step and reads PARAM/STATE/OUTPUT slots after it; the
  * slot stays owned by the library and valid until ooc_destroy. */
 ooc_status ooc_host_ptr(ooc_ctx *ctx, int64_t var, void **p);
@@ -388,13 +405,18 @@ ooc_status ooc_host_ptr(ooc_ctx *ctx, int64_t var, void **p);
 ooc_status ooc_upload(ooc_ctx *ctx);
 ooc_status ooc_download(ooc_ctx *ctx);
 
-/* One blocking training step: all functions in order on the compute
- * stream, the schedule's swaps on the copy streams.  lr and momentum feed
+/* One blocking training step (the iteration whose time Section 5 reports):
+ * all functions in order on the compute stream, the swaps of the Section 3
+ * schedule (Fig. 2) on the copy streams, each function started only once
+ * its variables are resident and each chunk reused only once its previous
+ * occupant's kernels and copies are done.  lr and momentum feed
  * the SGD functions; *loss_out (may be NULL) receives the mean loss of the
  * last SOFTMAX_CE function (NaN if none). */
 ooc_status ooc_step(ooc_ctx *ctx, float lr, float momentum, float *loss_out);
 
-/* Statistics of the schedule, the pool and the last step. */
+/* Statistics of the schedule, the pool and the last step: the quantities
+ * Section 5 reports (budget, actual device usage against it as in Fig. 3,
+ * bytes swapped, step time).  OOC_E_STATE before ooc_build_schedule. */
 ooc_status ooc_get_stats(const ooc_ctx *ctx, ooc_stats *out);
 
 /* Measures the host link the swaps use (the CPU-memory cache of Section 1
@@ -405,6 +427,19 @@ ooc_status ooc_get_stats(const ooc_ctx *ctx, ooc_stats *out);
  * Allocates and frees its own buffers. */
 ooc_status ooc_link_probe(int32_t hip_device, uint64_t bytes, int32_t reps, double *h2d_gbs,
                           double *d2h_gbs, double *both_gbs);
+
+/* Split-K slice count the library's weight-gradient kernels run best with
+ * for one function, for the caller to size its partial-sum variable and to
+ * pass as the function's `slices` attribute (Section 3: every byte a
+ * function touches is one of its variables, so the budget accounts for the
+ * partial sums).  `op` is OOC_OP_CONV_BWD_W with the 11 attributes
+ * N H W C K R S stride pad P Q, or OOC_OP_LINEAR_BWD_W with M K N (a
+ * trailing slices attribute is ignored).  Any count >= 1 gives the same
+ * gradient up to the order of its sums; this one fills whole rounds of
+ * resident workgroups on the device.  Host only; no context.  OOC_E_INVALID
+ * for another op, too few or negative attributes, or an empty shape
+ * (message on ooc_last_error(NULL)). */
+ooc_status ooc_wgrad_slices(int32_t op, const int64_t *attrs, int32_t n_attrs, int64_t *slices);
 
 /* Duration in milliseconds of each function's kernels in the last step,
  * measured with events on the compute stream right before and after its

@@ -57,10 +57,9 @@ channel for each of S row slices, S = min(ceil(rows / 512), 2048) with rows =
 N H W; a LayerNorm's ``stats`` holds mean and 1/std per row followed by two
 partial sums per feature for each of S row slices, S = min(ceil(rows / 32),
 2048); a convolution's
-``part`` holds S_w slices of dW, S_w from ``conv_wgrad_slices`` over K output
-channels, R S C and L = N P Q; a dense layer's ``part`` holds S_w slices of dW
-then S_w slices of db, with the same rule over K = out, R S C = in and
-L = rows.
+``part`` holds S_w slices of dW and a dense layer's S_w slices of dW then
+S_w slices of db, S_w being given per layer by the caller (``lower``'s
+``slices``).
 
 Kinds: x and labels INPUT, parameters PARAM, momentum buffers STATE, loss
 OUTPUT (parameter gradients too when ``keep_grads``), everything else TEMP.
@@ -85,43 +84,14 @@ def ln_slices(rows):
     return min(math.ceil(rows / 32), 2048)
 
 
-def conv_wgrad_slices(K, RSC, L, C=None):
-    """Partial-sum copies of a weight gradient (K x RSC outputs reduced over L rows; C input
-    channels of a convolution, None for a dense layer).  The count is a blocking choice of the
-    GPU kernels that the function sequence carries (it sizes the partials variable), so the
-    lowering reproduces it.  With slots = 256 compute units times the workgroups each holds,
-    the count s minimises ceil(tiles s / slots) / s over 1 <= s <= min(4 slots / tiles,
-    L / 256 rounded up), taking the smallest s within 1 % of the minimum.  Tiles of a
-    convolution with K % 4 == 0, first rule that applies: 32 x 256 (2 per CU) for K <= 32 and
-    C % 4 == 0; 64 x 192 (2 per CU) for K <= 64, C % 4 == 0 and fewer padded RSC columns that
-    way than with 128-wide tiles; 64 x 64 for K <= 64 and RSC <= 64 (5 per CU, 4 when
-    C % 4 != 0).  Otherwise 64 on a side of at most 64 (3 per CU) and 128 x 128 (2)."""
-    pad128 = math.ceil(RSC / 128) * 128 - RSC
-    pad192 = math.ceil(RSC / 192) * 192 - RSC
-    conv = C is not None and K % 4 == 0
-    if conv and K <= 32 and C % 4 == 0:
-        tiles, per_cu = math.ceil(RSC / 256), 2
-    elif conv and K <= 64 and C % 4 == 0 and pad192 < pad128:
-        tiles, per_cu = math.ceil(RSC / 192), 2
-    elif conv and K <= 64 and RSC <= 64:
-        tiles, per_cu = 1, (5 if C % 4 == 0 else 4)
-    elif K <= 64:
-        tiles, per_cu = math.ceil(RSC / 128), 3
-    elif RSC <= 64:
-        tiles, per_cu = math.ceil(K / 128), 3
-    else:
-        tiles, per_cu = math.ceil(K / 128) * math.ceil(RSC / 128), 2
-    slots = 256 * per_cu
-    smax = max(1, min(4 * slots // tiles, math.ceil(L / 256)))
-    ratio = [math.ceil(tiles * s / slots) / s for s in range(1, smax + 1)]
-    lowest = min(ratio)
-    for s in range(1, smax + 1):
-        if ratio[s - 1] <= lowest * 1.01:
-            return s
-
-
-def lower(spec, keep_grads=False):
+def lower(spec, keep_grads=False, slices=None):
     """Returns ``{"vars": [...], "fns": [...]}``.
+
+    ``slices`` maps a convolution or dense layer's name to the number S_w of
+    partial sums its weight gradient is split into (1 when absent).  The count
+    is a blocking choice of whoever computes the gradient, taken as an input:
+    it only sizes the ``part`` variable, since the gradient is the same sum
+    for every S_w.
 
     ``vars[i] = {"name", "shape", "dtype", "kind", "bytes"}``;
     ``fns[j] = {"op", "vars": [(id, access)], "attrs": {...}}``.
@@ -304,7 +274,7 @@ def lower(spec, keep_grads=False):
             dW = var("d:" + Wn, decl[Wn][0], kind=grad_kind)
             db = var("d:" + bn_, decl[bn_][0], kind=grad_kind)
             attrs = {"M": xs[0], "K": xs[1], "N": L["out_features"]}
-            Sw = conv_wgrad_slices(attrs["N"], attrs["K"], attrs["M"])
+            Sw = int((slices or {}).get(name, 1))
             vs = [(X, R), (dY, R), (dW, W), (db, W)]
             if Sw > 1:
                 vs.append((var(name + ".part", (Sw * (attrs["N"] * attrs["K"] + attrs["N"]),)), W))
@@ -322,7 +292,7 @@ def lower(spec, keep_grads=False):
             attrs = {"N": n, "H": h, "W": w, "C": c, "K": K, "R": k, "S": k,
                      "stride": L["stride"], "pad": L["pad"], "P": P, "Q": Q}
             dW = var("d:" + Wn, decl[Wn][0], kind=grad_kind)
-            Sw = conv_wgrad_slices(K, k * k * c, n * P * Q, c)
+            Sw = int((slices or {}).get(name, 1))
             vs = [(X, R), (dY, R), (dW, W)]
             if Sw > 1:
                 vs.append((var(name + ".part", (Sw * K * k * k * c,)), W))

@@ -5,6 +5,7 @@
 #include <new>
 
 #include "ctx.h"
+#include "kernels.h"
 
 namespace ooc {
 ooc_status prepare(ooc_ctx* ctx);
@@ -20,13 +21,28 @@ using namespace ooc;
 
 static thread_local std::string g_create_error;
 
-static ooc_status fail(ooc_ctx* ctx, ooc_status s, const std::string& msg) {
+// Records msg as the context's last error (readable with ooc_last_error) and
+// returns s.  The message lives in the context, so const queries set it too.
+static ooc_status fail(const ooc_ctx* ctx, ooc_status s, const std::string& msg) {
   ctx->err = msg;
   return s;
 }
 
-#define REQUIRE_CTX(ctx) \
-  if (!(ctx)) return OOC_E_INVALID
+#define REQUIRE_CTX(ctx)                                 \
+  if (!(ctx)) {                                          \
+    g_create_error = std::string(__func__) + ": NULL context"; \
+    return OOC_E_INVALID;                                \
+  }
+// queries valid once the schedule is built
+#define REQUIRE_BUILT(ctx)                                                          \
+  if ((ctx)->stage < BUILT)                                                         \
+  return fail((ctx), OOC_E_STATE, std::string(__func__) + " before ooc_build_schedule")
+#define REQUIRE_OUT(ctx, p)                                                        \
+  if (!(p))                                                                          \
+  return fail((ctx), OOC_E_INVALID, std::string(__func__) + ": " #p " is NULL")
+#define REQUIRE_BUF(ctx, buf, cap)                                                 \
+  if ((cap) > 0 && !(buf))                                                           \
+  return fail((ctx), OOC_E_INVALID, std::string(__func__) + ": " #buf " is NULL with cap > 0")
 #define REQUIRE_STAGE(ctx, st, what)                                              \
   if ((ctx)->stage != (st)) return fail((ctx), OOC_E_STATE, std::string(what) +   \
                                          " is not allowed at this point")
@@ -34,7 +50,10 @@ static ooc_status fail(ooc_ctx* ctx, ooc_status s, const std::string& msg) {
 extern "C" {
 
 ooc_status ooc_create(int32_t hip_device, ooc_ctx** out) {
-  if (!out) return OOC_E_INVALID;
+  if (!out) {
+    g_create_error = "ooc_create: out is NULL";
+    return OOC_E_INVALID;
+  }
   *out = nullptr;
   if (hip_device < -1) {
     g_create_error = "device id must be >= -1";
@@ -51,7 +70,10 @@ ooc_status ooc_create(int32_t hip_device, ooc_ctx** out) {
     }
   }
   ooc_ctx* ctx = new (std::nothrow) ooc_ctx();
-  if (!ctx) return OOC_E_HOST_OOM;
+  if (!ctx) {
+    g_create_error = "ooc_create: out of host memory";
+    return OOC_E_HOST_OOM;
+  }
   ctx->device = hip_device;
   *out = ctx;
   return OOC_OK;
@@ -221,9 +243,10 @@ ooc_status ooc_build_schedule(ooc_ctx* ctx) {
 
 ooc_status ooc_schedule_get(const ooc_ctx* ctx, ooc_op* buf, uint64_t cap, uint64_t* n) {
   REQUIRE_CTX(ctx);
-  if (ctx->stage < BUILT || !n) return OOC_E_STATE;
+  REQUIRE_OUT(ctx, n);
+  REQUIRE_BUF(ctx, buf, cap);
+  REQUIRE_BUILT(ctx);
   *n = ctx->sched.ops.size();
-  if (cap > 0 && !buf) return OOC_E_INVALID;
   for (uint64_t k = 0; k < cap && k < *n; ++k) {
     const Op& o = ctx->sched.ops[k];
     buf[k] = ooc_op{o.fn, o.phase, o.kind, 0, o.var, o.held};
@@ -233,23 +256,24 @@ ooc_status ooc_schedule_get(const ooc_ctx* ctx, ooc_op* buf, uint64_t cap, uint6
 
 ooc_status ooc_schedule_windows(const ooc_ctx* ctx, int64_t* buf, uint64_t cap, uint64_t* n) {
   REQUIRE_CTX(ctx);
-  if (ctx->stage < BUILT || !n) return OOC_E_STATE;
+  REQUIRE_OUT(ctx, n);
+  REQUIRE_BUF(ctx, buf, cap);
+  REQUIRE_BUILT(ctx);
   *n = ctx->sched.windows.size();
-  if (cap > 0 && !buf) return OOC_E_INVALID;
   for (uint64_t k = 0; k < cap && k < *n; ++k) buf[k] = ctx->sched.windows[k];
   return OOC_OK;
 }
 
 ooc_status ooc_incore_peak(const ooc_ctx* ctx, uint64_t* bytes) {
   REQUIRE_CTX(ctx);
-  if (!bytes) return OOC_E_INVALID;
+  REQUIRE_OUT(ctx, bytes);
   *bytes = incore_peak(ctx->vars, ctx->fns, ctx->chunk);
   return OOC_OK;
 }
 
 ooc_status ooc_working_set_max(const ooc_ctx* ctx, uint64_t* bytes) {
   REQUIRE_CTX(ctx);
-  if (!bytes) return OOC_E_INVALID;
+  REQUIRE_OUT(ctx, bytes);
   *bytes = working_set_max(ctx->vars, ctx->fns, ctx->chunk);
   return OOC_OK;
 }
@@ -257,17 +281,21 @@ ooc_status ooc_working_set_max(const ooc_ctx* ctx, uint64_t* bytes) {
 ooc_status ooc_bestfit_extent(const ooc_ctx* ctx, uint64_t align, uint64_t* extent,
                               uint64_t* peak_live) {
   REQUIRE_CTX(ctx);
-  if (ctx->stage < BUILT || !extent || !peak_live) return OOC_E_STATE;
-  if (align == 0 || (align & (align - 1))) return OOC_E_INVALID;
+  REQUIRE_OUT(ctx, extent);
+  REQUIRE_OUT(ctx, peak_live);
+  REQUIRE_BUILT(ctx);
+  if (align == 0 || (align & (align - 1)))
+    return fail(ctx, OOC_E_INVALID, "ooc_bestfit_extent: align must be a power of two");
   bestfit_extent(ctx->vars, ctx->plan, align, extent, peak_live);
   return OOC_OK;
 }
 
 ooc_status ooc_plan_intervals(const ooc_ctx* ctx, ooc_interval* buf, uint64_t cap, uint64_t* n) {
   REQUIRE_CTX(ctx);
-  if (ctx->stage < BUILT || !n) return OOC_E_STATE;
+  REQUIRE_OUT(ctx, n);
+  REQUIRE_BUF(ctx, buf, cap);
+  REQUIRE_BUILT(ctx);
   *n = ctx->plan.intervals.size();
-  if (cap > 0 && !buf) return OOC_E_INVALID;
   int64_t first = 0;
   for (uint64_t k = 0; k < *n; ++k) {
     const Interval& iv = ctx->plan.intervals[k];
@@ -280,14 +308,13 @@ ooc_status ooc_plan_intervals(const ooc_ctx* ctx, ooc_interval* buf, uint64_t ca
 
 ooc_status ooc_plan_chunks(const ooc_ctx* ctx, int32_t* buf, uint64_t cap, uint64_t* n) {
   REQUIRE_CTX(ctx);
-  if (ctx->stage < BUILT || !n) return OOC_E_STATE;
+  REQUIRE_OUT(ctx, n);
+  REQUIRE_BUF(ctx, buf, cap);
+  REQUIRE_BUILT(ctx);
   uint64_t k = 0;
   for (const Interval& iv : ctx->plan.intervals)
     for (int32_t c : iv.chunks) {
-      if (k < cap) {
-        if (!buf) return OOC_E_INVALID;
-        buf[k] = c;
-      }
+      if (k < cap) buf[k] = c;
       ++k;
     }
   *n = k;
@@ -313,8 +340,9 @@ ooc_status ooc_prepare(ooc_ctx* ctx) {
 ooc_status ooc_host_ptr(ooc_ctx* ctx, int64_t var, void** p) {
   REQUIRE_CTX(ctx);
   REQUIRE_STAGE(ctx, PREPARED, "ooc_host_ptr");
-  if (!p || var < 0 || var >= (int64_t)ctx->vars.size())
-    return fail(ctx, OOC_E_INVALID, "unknown variable");
+  REQUIRE_OUT(ctx, p);
+  if (var < 0 || var >= (int64_t)ctx->vars.size())
+    return fail(ctx, OOC_E_INVALID, "ooc_host_ptr: unknown variable " + std::to_string(var));
   if (ctx->vars[var].kind == OOC_TEMP)
     return fail(ctx, OOC_E_INVALID, "a TEMP variable has no host slot");
   *p = ctx->host_slot[var];
@@ -343,8 +371,8 @@ ooc_status ooc_step(ooc_ctx* ctx, float lr, float momentum, float* loss_out) {
 
 ooc_status ooc_get_stats(const ooc_ctx* ctx, ooc_stats* out) {
   REQUIRE_CTX(ctx);
-  if (!out) return OOC_E_INVALID;
-  if (ctx->stage < BUILT) return OOC_E_STATE;
+  REQUIRE_OUT(ctx, out);
+  REQUIRE_BUILT(ctx);
   *out = ctx->stats;
   return OOC_OK;
 }
@@ -366,19 +394,52 @@ ooc_status ooc_link_probe(int32_t hip_device, uint64_t bytes, int32_t reps, doub
   return s;
 }
 
+ooc_status ooc_wgrad_slices(int32_t op, const int64_t* attrs, int32_t n_attrs, int64_t* slices) {
+  if (!slices || !attrs) {
+    g_create_error = "ooc_wgrad_slices: NULL argument";
+    return OOC_E_INVALID;
+  }
+  for (int32_t j = 0; j < n_attrs; ++j)
+    if (attrs[j] < 0 || attrs[j] > (int64_t(1) << 40)) {
+      g_create_error = "ooc_wgrad_slices: attribute out of range";
+      return OOC_E_INVALID;
+    }
+  if (op == OOC_OP_CONV_BWD_W && n_attrs >= 11) {
+    const int64_t* a = attrs;   // N H W C K R S stride pad P Q
+    if (a[0] < 1 || a[3] < 1 || a[4] < 1 || a[5] < 1 || a[6] < 1 || a[9] < 1 || a[10] < 1) {
+      g_create_error = "ooc_wgrad_slices: empty convolution";
+      return OOC_E_INVALID;
+    }
+    *slices = wgrad_slices(a[4], a[5] * a[6] * a[3], a[0] * a[9] * a[10], a[3]);
+    return OOC_OK;
+  }
+  if (op == OOC_OP_LINEAR_BWD_W && n_attrs >= 3) {
+    const int64_t* a = attrs;   // M K N: dW [N][K] reduced over M rows
+    if (a[0] < 1 || a[1] < 1 || a[2] < 1) {
+      g_create_error = "ooc_wgrad_slices: empty dense layer";
+      return OOC_E_INVALID;
+    }
+    *slices = wgrad_slices(a[2], a[1], a[0], -1);
+    return OOC_OK;
+  }
+  g_create_error = "ooc_wgrad_slices: op must be CONV_BWD_W (11 attributes) or LINEAR_BWD_W (3)";
+  return OOC_E_INVALID;
+}
+
 ooc_status ooc_fn_times(const ooc_ctx* ctx, double* buf, uint64_t cap, uint64_t* n) {
   REQUIRE_CTX(ctx);
-  if (!n || ctx->fn_ms.empty()) return OOC_E_STATE;
+  REQUIRE_OUT(ctx, n);
+  REQUIRE_BUF(ctx, buf, cap);
+  if (ctx->fn_ms.empty()) return fail(ctx, OOC_E_STATE, "ooc_fn_times before the first step");
   *n = ctx->fn_ms.size();
-  if (cap > 0 && !buf) return OOC_E_INVALID;
   for (uint64_t k = 0; k < cap && k < *n; ++k) buf[k] = ctx->fn_ms[k];
   return OOC_OK;
 }
 
 ooc_status ooc_timeline(ooc_ctx* ctx, ooc_span* buf, uint64_t cap, uint64_t* n) {
   REQUIRE_CTX(ctx);
-  if (!n) return fail(ctx, OOC_E_INVALID, "ooc_timeline: n is NULL");
-  if (cap > 0 && !buf) return fail(ctx, OOC_E_INVALID, "ooc_timeline: buf is NULL");
+  REQUIRE_OUT(ctx, n);
+  REQUIRE_BUF(ctx, buf, cap);
   std::vector<ooc_span> t;
   ooc_status st = timeline(ctx, &t);
   if (st) return st;

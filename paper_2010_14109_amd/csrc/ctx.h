@@ -54,7 +54,7 @@ enum Stage { REGISTERING = 0, BUILT = 1, PREPARED = 2 };
 
 struct ooc_ctx {
   int32_t device = -1;
-  std::string err;
+  mutable std::string err;                // message of the last failing call
   ooc::Stage stage = ooc::REGISTERING;
 
   std::vector<ooc::Var> vars;

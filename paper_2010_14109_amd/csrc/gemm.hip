@@ -37,6 +37,7 @@
 // do not depend on scheduling or addresses.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "kernels.h"
@@ -1036,6 +1037,42 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
   }
   if (e != hipSuccess || slices <= 1) return e;
   return slice_sum(part, dW, M * N, slices, s);
+}
+
+// Split-K slice count of a weight gradient with M x N outputs reduced over K
+// rows (C = input channels of a filter gradient, -1 for a dense layer).  The
+// launchers above run tiles x s workgroups; a CU holds kResident of them at
+// once (LDS bounds it: 2 for 128 x 128, 64 x 192 and 32 x 256 tiles, 3 for the
+// general 64-wide ones, 4-5 for the small 64 x 64 filter tiles), so a launch
+// takes ceil(tiles s / slots) rounds of K / s rows.  s minimises rounds / s
+// (a partly filled last round leaves most CUs idle behind a few), with at most
+// four rounds and at least 256 rows a slice; the smallest s within 1 % of the
+// best is taken, since every slice adds one partial dW to write and read back.
+int64_t wgrad_slices(int64_t M, int64_t N, int64_t K, int64_t C) {
+  constexpr int64_t kCUs = 256;
+  int64_t tiles, resident;
+  const WgradTile t = C >= 0 ? wgrad_tile(M, N, C) : WgradTile::kGeneral;
+  if (t == WgradTile::k32x256) {
+    tiles = (N + 255) / 256, resident = 2;
+  } else if (t == WgradTile::k64x192) {
+    tiles = (N + 191) / 192, resident = 2;
+  } else if (t == WgradTile::k64x64) {
+    tiles = 1, resident = C % 4 == 0 ? 5 : 4;
+  } else {
+    switch (pick_shape(M, N)) {
+      case S128x64: tiles = (M + 127) / 128, resident = 3; break;
+      case S64x128: tiles = (N + 127) / 128, resident = 3; break;
+      default: tiles = ((M + 127) / 128) * ((N + 127) / 128), resident = 2;
+    }
+  }
+  const int64_t slots = kCUs * resident;
+  const int64_t smax = std::max<int64_t>(1, std::min(4 * slots / tiles, (K + 255) / 256));
+  double best = 1e300;
+  for (int64_t s = 1; s <= smax; ++s)
+    best = std::min(best, (double)((tiles * s + slots - 1) / slots) / (double)s);
+  for (int64_t s = 1; s <= smax; ++s)
+    if ((double)((tiles * s + slots - 1) / slots) / (double)s <= best * 1.01) return s;
+  return 1;
 }
 
 }  // namespace ooc

@@ -41,6 +41,10 @@ hipError_t conv_bwd_x(const float* W, const float* dY, float* dX, const ConvShap
                       hipStream_t s);
 hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, int64_t slices,
                       const ConvShape& c, hipStream_t s);
+// Split-K slice count the weight-gradient launchers run best with: M x N
+// outputs reduced over K rows; C = input channels of a filter gradient, -1 for
+// a dense layer.
+int64_t wgrad_slices(int64_t M, int64_t N, int64_t K, int64_t C);
 
 // Elementwise, loss, update, normalisation and pooling (ops.hip).
 hipError_t relu_fwd(const float* x, float* y, int64_t n, hipStream_t s);

@@ -61,7 +61,7 @@ def case(spec):
             return op, [(xb, I, R), (wb, I, R), (yb, O, Wr)], a
         if op == "conv_bwd_x":
             return op, [(wb, I, R), (yb, I, R), (xb, O, Wr)], a
-        s = v[8] if len(v) > 8 else netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q, C)
+        s = v[8] if len(v) > 8 else ooc.wgrad_slices(op, a)
         vs = [(xb, I, R), (yb, I, R), (wb, O, Wr)] + ([(s * wb, O, Wr)] if s > 1 else [])
         return op, vs, a + [s]
     M, K, N = v[:3]
@@ -69,7 +69,7 @@ def case(spec):
         return op, [(M * K * 4, I, R), (N * K * 4, I, R), (N * 4, I, R), (M * N * 4, O, Wr)], v
     if op == "linear_bwd_x":
         return op, [(N * K * 4, I, R), (M * N * 4, I, R), (M * K * 4, O, Wr)], v
-    s = v[3] if len(v) > 3 else netdef.wgrad_pixel_slices(N, K, M)
+    s = v[3] if len(v) > 3 else ooc.wgrad_slices(op, v[:3])
     vs = [(M * K * 4, I, R), (M * N * 4, I, R), (N * K * 4, O, Wr), (N * 4, O, Wr)]
     if s > 1:
         vs.append((s * (N * K + N) * 4, O, Wr))

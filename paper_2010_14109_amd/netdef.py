@@ -15,16 +15,14 @@ registers it through the C interface:
 Variables are numbered by first appearance.  Variable lists, sizes and
 kinds follow the operation table of ``include/ooc.h``; the auxiliary sizes are
 fixed per shape: a BatchNorm keeps 2 + 2 S floats per channel with S =
-min(ceil(rows / 512), 2048) row slices, and a convolution's filter gradient
-is split over S_w = min(ceil(1024 / T), ceil(L / 1024)) pixel slices (at
-least 1) with T = ceil(K / 128) ceil(R S C / 128) output tiles and L = N P Q
-pixels, using a partial-sum variable of S_w copies of dW when S_w > 1; a
-dense layer's weight gradient is split the same way over its rows (K = out,
-R S C = in, L = rows), its partial-sum variable holding S_w copies of dW then
-S_w copies of db.  A
-LayerNorm keeps mean and 1/std per row and 2 S floats per feature with S =
-min(ceil(rows / 32), 2048) (its rows are d floats wide); attention keeps its probabilities [B, H, T, T] and its
-backward a scratch of the same size.
+min(ceil(rows / 512), 2048) row slices; a weight gradient (convolution or
+dense layer) is split over S_w slices of its reduction, S_w being the count
+the library's kernels ask for (``ooc_wgrad_slices``), with a partial-sum
+variable of S_w copies of dW (a dense layer's then S_w copies of db) when
+S_w > 1; a LayerNorm keeps mean and 1/std per row and 2 S floats per feature
+with S = min(ceil(rows / 32), 2048) (its rows are d floats wide); attention
+keeps its probabilities [B, H, T, T] and its backward a scratch of the same
+size.
 """
 
 from __future__ import annotations
@@ -44,52 +42,6 @@ def ln_row_slices(rows):
     return min(ceil(rows / 32), 2048)
 
 
-GPU_CUS = 256   # compute units of an MI355X
-
-
-def wgrad_tile(k_out, rsc, channels):
-    """Tile of a filter gradient (the GEMM library's rule, first that applies), as
-    (rows, columns, workgroups per CU): 32 x 256 for at most 32 output channels, 64 x 192 for at
-    most 64 when that pads fewer RSC columns than 128-wide tiles, 64 x 64 for at most 64 output
-    channels and RSC <= 64; all three need output channels % 4 == 0, the first two input
-    channels % 4 == 0.  None for the general shapes."""
-    if k_out % 4:
-        return None
-    if k_out <= 32 and channels % 4 == 0:
-        return 32, 256, 2
-    pad128, pad192 = ceil(rsc / 128) * 128 - rsc, ceil(rsc / 192) * 192 - rsc
-    if k_out <= 64 and channels % 4 == 0 and pad192 < pad128:
-        return 64, 192, 2
-    if k_out <= 64 and rsc <= 64:
-        return 64, 64, 5 if channels % 4 == 0 else 4
-    return None
-
-
-def wgrad_pixel_slices(k_out, rsc, pixels, channels=None):
-    """Split-K slices of a weight-gradient GEMM (k_out x rsc outputs, reduced over ``pixels``;
-    ``channels`` is the input channel count of a filter gradient, None for a dense layer).
-
-    The GPU holds 256 CUs x (3 workgroups for the 64-wide general tile shapes, 2 for 128 x 128;
-    filter-gradient tiles as ``wgrad_tile`` says; LDS bounds the residency) at once.  A launch of tiles x s workgroups takes
-    ceil(tiles s / slots) rounds of K / s pixels each, so s minimises rounds / s: a partly
-    filled last round leaves most CUs idle behind a few.  The smallest s within 1 % of the best
-    is taken (fewer partial sums), with at most four rounds and at least 256 pixels a slice."""
-    tile = wgrad_tile(k_out, rsc, channels) if channels is not None else None
-    if tile is not None:
-        tiles, resident = ceil(rsc / tile[1]), tile[2]
-    elif k_out <= 64:
-        tiles, resident = ceil(rsc / 128), 3
-    elif rsc <= 64:
-        tiles, resident = ceil(k_out / 128), 3
-    else:
-        tiles, resident = ceil(k_out / 128) * ceil(rsc / 128), 2
-    slots = GPU_CUS * resident
-    smax = max(1, min(4 * slots // tiles, ceil(pixels / 256)))
-    cost = [ceil(tiles * s / slots) / s for s in range(1, smax + 1)]
-    best = min(cost)
-    return next(s for s, c in enumerate(cost, 1) if c <= best * 1.01)
-
-
 class Net:
     """Function sequence of one training step of ``spec``."""
 
@@ -100,6 +52,7 @@ class Net:
         self.calls = []       # (op, [(name, access)], attrs)
         self.shape = {}
         self.params = {}      # layer name -> [param names]
+        self.slices = {}      # layer name -> split-K slices of its weight gradient
         self._lower()
         self._number()
 
@@ -270,7 +223,8 @@ class Net:
             n, fin = xs
             fout = L["out_features"]
             attrs = [n, fin, fout]
-            sw = wgrad_pixel_slices(fout, fin, n)
+            sw = ooc.wgrad_slices("linear_bwd_w", attrs)
+            self.slices[name] = sw
             pairs = [(X, ooc.R), (dY, ooc.R), (self._grad_of_param(W), ooc.W),
                      (self._grad_of_param(b), ooc.W)]
             if sw > 1:
@@ -285,7 +239,8 @@ class Net:
             (W,) = self.params[name]
             a = self._conv_attrs(L, xs)
             n, _, _, c, K, R, S, _, _, P, Q = a
-            sw = wgrad_pixel_slices(K, R * S * c, n * P * Q, c)
+            sw = ooc.wgrad_slices("conv_bwd_w", a)
+            self.slices[name] = sw
             pairs = [(X, ooc.R), (dY, ooc.R), (self._grad_of_param(W), ooc.W)]
             if sw > 1:
                 pairs.append((self._decl(name + ".part", (sw * K * R * S * c,)), ooc.W))

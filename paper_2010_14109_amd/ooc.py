@@ -43,7 +43,7 @@ EXPORTS = [
     "ooc_plan_intervals", "ooc_plan_chunks", "ooc_prepare", "ooc_host_ptr", "ooc_upload",
     "ooc_download", "ooc_step", "ooc_get_stats", "ooc_fn_times", "ooc_link_probe",
     "ooc_timeline", "ooc_set_swapout_depth", "ooc_set_fixed_distance", "ooc_bestfit_extent",
-    "ooc_set_wait_order", "ooc_set_host_limit",
+    "ooc_set_wait_order", "ooc_set_host_limit", "ooc_wgrad_slices",
 ]
 
 
@@ -134,6 +134,8 @@ def load(path=LIB_PATH):
         "ooc_link_probe": ([c.c_int32, c.c_uint64, c.c_int32, c.POINTER(c.c_double),
                             c.POINTER(c.c_double), c.POINTER(c.c_double)], c.c_int32),
         "ooc_timeline": ([P, c.POINTER(ooc_span), c.c_uint64, c.POINTER(c.c_uint64)], c.c_int32),
+        "ooc_wgrad_slices": ([c.c_int32, c.POINTER(c.c_int64), c.c_int32, c.POINTER(c.c_int64)],
+                             c.c_int32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -157,6 +159,17 @@ def link_probe(device=0, nbytes=1 << 30, reps=3):
     _check(lib.ooc_link_probe(device, nbytes, reps, ctypes.byref(h), ctypes.byref(d),
                               ctypes.byref(b)), None)
     return {"h2d": h.value, "d2h": d.value, "both": b.value}
+
+
+def wgrad_slices(op, attrs):
+    """Split-K slice count of a weight-gradient function (``conv_bwd_w`` with its 11 shape
+    attributes or ``linear_bwd_w`` with M, K, N), as the library's kernels want it."""
+    lib = load()
+    a = (ctypes.c_int64 * len(attrs))(*attrs)
+    out = ctypes.c_int64()
+    _check(lib.ooc_wgrad_slices(OPS[op] if isinstance(op, str) else op, a, len(attrs),
+                                ctypes.byref(out)), None)
+    return out.value
 
 
 _NP = {"f32": np.float32, "i32": np.int32, "u8": np.uint8, "u32": np.uint32}

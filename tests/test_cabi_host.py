@@ -49,7 +49,7 @@ def specs_full():
 @pytest.mark.parametrize("keep", [False, True])
 def test_function_sequence_matches_oracle_lowering(spec, keep):
     mine = netdef.Net(spec, keep_grads=keep)
-    ref = lower(spec, keep_grads=keep)
+    ref = lower(spec, keep_grads=keep, slices=mine.slices)
     assert mine.var_bytes == [v["bytes"] for v in ref["vars"]]
     assert mine.var_kinds == [v["kind"] for v in ref["vars"]]
     assert mine.names == [v["name"] for v in ref["vars"]]
@@ -75,7 +75,7 @@ def host_ctx(net, budget, window, chunk, policy):
                          if isinstance(s, dict) else ("full" if s else "small"))
 def test_schedule_and_plan_match_oracle(spec, full):
     net = netdef.Net(spec)
-    b, k, f = as_schedule_input(lower(spec))
+    b, k, f = as_schedule_input(lower(spec, slices=net.slices))
     chunks = (2 << 20,) if full else (64, 4096)
     fracs = (1.0, 0.5, 0.25, 1 / 7.5, 0.0) if full else (1.0, 0.75, 0.5, 0.4, 0.25, 1 / 7.5, 0.2, 0.0)
     for chunk in chunks:
@@ -319,7 +319,7 @@ def test_bestfit_extent_matches_oracle(lib):
 def test_infeasible_budget_reports_error(lib):
     spec = specs_small()[0]
     net = netdef.Net(spec)
-    b, k, f = as_schedule_input(lower(spec))
+    b, k, f = as_schedule_input(lower(spec, slices=net.slices))
     ws = S.working_set_max(b, f, 1)
     ctx = ooc.Context(-1)
     net.register(ctx)
@@ -412,3 +412,75 @@ def test_host_limit_validation(lib):
         ctx.set_host_limit(ooc.UNLIMITED)           # still allowed after the schedule
     finally:
         ctx.close()
+
+
+def test_queries_report_status_and_message(lib):
+    """Each query: a NULL out-pointer (or a NULL buffer with a capacity) is OOC_E_INVALID, a
+    query before the stage it needs is OOC_E_STATE, and either way ooc_last_error names the
+    call.  A NULL context is OOC_E_INVALID with its message on ooc_last_error(NULL)."""
+    import ctypes as C
+    ctx = ooc.Context(-1)
+    a = ctx.add_var(64, ooc.INPUT)
+    t = ctx.add_var(64, ooc.TEMP)
+    ctx.add_fn("relu_fwd", [a, t], [ooc.R, ooc.W], [16])
+    ctx.set_chunk(1)
+    h = ctx.h
+    u64, i64 = C.c_uint64(), C.c_int64()
+
+    def expect(status, call, name):
+        assert call == status, name
+        msg = lib.ooc_last_error(h).decode()
+        assert msg.startswith(name), (name, msg)
+
+    n = C.byref(u64)
+    # before ooc_build_schedule
+    for name, f in (("ooc_schedule_get", lambda: lib.ooc_schedule_get(h, None, 0, n)),
+                    ("ooc_schedule_windows", lambda: lib.ooc_schedule_windows(h, None, 0, n)),
+                    ("ooc_plan_intervals", lambda: lib.ooc_plan_intervals(h, None, 0, n)),
+                    ("ooc_plan_chunks", lambda: lib.ooc_plan_chunks(h, None, 0, n)),
+                    ("ooc_bestfit_extent", lambda: lib.ooc_bestfit_extent(h, 8, n, n)),
+                    ("ooc_get_stats", lambda: lib.ooc_get_stats(h, C.byref(ooc.ooc_stats()))),
+                    ("ooc_fn_times", lambda: lib.ooc_fn_times(h, None, 0, n))):
+        expect(ooc.E_STATE, f(), name)
+    # NULL out-pointers and buffers
+    for name, f in (("ooc_schedule_get", lambda: lib.ooc_schedule_get(h, None, 0, None)),
+                    ("ooc_schedule_get", lambda: lib.ooc_schedule_get(h, None, 4, n)),
+                    ("ooc_schedule_windows", lambda: lib.ooc_schedule_windows(h, None, 0, None)),
+                    ("ooc_schedule_windows", lambda: lib.ooc_schedule_windows(h, None, 2, n)),
+                    ("ooc_incore_peak", lambda: lib.ooc_incore_peak(h, None)),
+                    ("ooc_working_set_max", lambda: lib.ooc_working_set_max(h, None)),
+                    ("ooc_plan_intervals", lambda: lib.ooc_plan_intervals(h, None, 0, None)),
+                    ("ooc_plan_intervals", lambda: lib.ooc_plan_intervals(h, None, 3, n)),
+                    ("ooc_plan_chunks", lambda: lib.ooc_plan_chunks(h, None, 0, None)),
+                    ("ooc_plan_chunks", lambda: lib.ooc_plan_chunks(h, None, 3, n)),
+                    ("ooc_bestfit_extent", lambda: lib.ooc_bestfit_extent(h, 8, None, n)),
+                    ("ooc_bestfit_extent", lambda: lib.ooc_bestfit_extent(h, 8, n, None)),
+                    ("ooc_get_stats", lambda: lib.ooc_get_stats(h, None)),
+                    ("ooc_fn_times", lambda: lib.ooc_fn_times(h, None, 0, None)),
+                    ("ooc_fn_times", lambda: lib.ooc_fn_times(h, None, 2, n)),
+                    ("ooc_timeline", lambda: lib.ooc_timeline(h, None, 0, None)),
+                    ("ooc_timeline", lambda: lib.ooc_timeline(h, None, 2, n))):
+        expect(ooc.E_INVALID, f(), name)
+    assert lib.ooc_incore_peak(h, n) == ooc.OK and u64.value == 128
+    ctx.build_schedule()
+    expect(ooc.E_INVALID, lib.ooc_bestfit_extent(h, 12, n, n), "ooc_bestfit_extent")
+    assert lib.ooc_bestfit_extent(h, 8, n, C.byref(C.c_uint64())) == ooc.OK
+    assert lib.ooc_schedule_get(h, None, 0, n) == ooc.OK and u64.value == len(ctx.schedule()[0])
+    # stages past the schedule: a host-only context cannot prepare, so no slot and no step
+    p = C.c_void_p()
+    expect(ooc.E_STATE, lib.ooc_host_ptr(h, a, C.byref(p)), "ooc_host_ptr")
+    expect(ooc.E_STATE, lib.ooc_step(h, C.c_float(0.1), C.c_float(0.0), None), "ooc_step")
+    expect(ooc.E_STATE, lib.ooc_timeline(h, None, 0, n), "no step")
+    assert lib.ooc_prepare(h) == ooc.E_UNSUPPORTED
+    assert "host-only" in lib.ooc_last_error(h).decode()
+    ctx.close()
+    # a NULL context
+    for name, f in (("ooc_incore_peak", lambda: lib.ooc_incore_peak(None, n)),
+                    ("ooc_get_stats", lambda: lib.ooc_get_stats(None, None)),
+                    ("ooc_step", lambda: lib.ooc_step(None, C.c_float(0.1), C.c_float(0.0), None))):
+        assert f() == ooc.E_INVALID
+        assert lib.ooc_last_error(None).decode() == name + ": NULL context"
+    assert lib.ooc_create(0, None) == ooc.E_INVALID
+    assert lib.ooc_last_error(None).decode() == "ooc_create: out is NULL"
+    assert lib.ooc_wgrad_slices(10, None, 0, C.byref(i64)) == ooc.E_INVALID
+    assert lib.ooc_last_error(None).decode().startswith("ooc_wgrad_slices")

@@ -133,7 +133,7 @@ def test_conv(shape):
     (_, _, Y) = run_fn("conv_fwd", [(X, ooc.R), (Wt, ooc.R), (((N, P, Q, K), "f32"), ooc.W)], a)
     assert rel_l2(Y, ops.conv_fwd(d(X), d(Wt), st, pd)) < TOL
     ref_dW = ops.conv_bwd_w(d(X), d(G), Wt.shape, st, pd)
-    for slices in sorted({1, netdef.wgrad_pixel_slices(K, k * k * C, N * P * Q, C), 3, 7}):
+    for slices in sorted({1, ooc.wgrad_slices("conv_bwd_w", a), 3, 7}):
         slices = min(slices, N * P * Q)
         args = [(X, ooc.R), (G, ooc.R), (((K, k, k, C), "f32"), ooc.W)]
         if slices > 1:

@@ -19,6 +19,7 @@ from oracle import schedule as S
 from oracle.interp import run as oracle_run
 from oracle.lower import lower, as_schedule_input
 from paper_2010_14109_amd import netdef, ooc, synth
+from tests.seq_util import lowering
 from tests.gpu_util import STAGING_BYTES, persistent_host_bytes, rel_l2, run_net
 
 pytestmark = pytest.mark.gpu
@@ -66,7 +67,7 @@ def test_step_matches_oracle_and_is_budget_independent(spec):
     check_against_oracle(spec, loss0, outs0, ref)
     assert st0["h2d_bytes"] == 0 and st0["d2h_bytes"] == 0
 
-    b, k, f = as_schedule_input(lower(spec, keep_grads=True))
+    b, k, f = as_schedule_input(lowering(spec, keep_grads=True))
     chunk = 4096
     p = S.incore_peak(b, k, f, chunk)
     ws = S.working_set_max(b, f, chunk)
@@ -191,7 +192,7 @@ def test_pageable_overflow_equals_in_core(idx, policy, wait, fixed):
     spec = tiny_specs()[idx]
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
-    b, k, f = as_schedule_input(lower(spec, keep_grads=True))
+    b, k, f = as_schedule_input(lowering(spec, keep_grads=True))
     chunk = 4096
     B = max(S.budget_for(0.25, S.incore_peak(b, k, f, chunk), chunk), S.working_set_max(b, f, chunk))
     W = B // 2 if policy == "C" else 0
@@ -265,7 +266,7 @@ def test_two_steps_keep_state_on_the_host():
     spec = tiny_specs()[2]
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
-    b, k, f = as_schedule_input(lower(spec, keep_grads=False))
+    b, k, f = as_schedule_input(lowering(spec, keep_grads=False))
     p = S.incore_peak(b, k, f, 4096)
     B = max(S.budget_for(0.3, p, 4096), S.working_set_max(b, f, 4096))
     loss2, outs2, _ = run_net(spec, x, labels, params, budget=B, chunk=4096, keep_grads=False,
@@ -286,7 +287,7 @@ def test_timeline_accounts_for_every_function_and_copy():
     spec = tiny_specs()[1]
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
-    b, k, f = as_schedule_input(lower(spec, keep_grads=False))
+    b, k, f = as_schedule_input(lowering(spec, keep_grads=False))
     p = S.incore_peak(b, k, f, 4096)
     B = max(S.budget_for(0.4, p, 4096), S.working_set_max(b, f, 4096))
     got = {}

@@ -284,6 +284,48 @@ def test_incore_limit():
         assert not any(kind == S.CANCEL for (_, _, kind, _) in out["ops"])
 
 
+def brute_incore_peak(b, k, f, chunk):
+    """P_incore from its definition, one function at a time: every INPUT, PARAM, STATE and
+    OUTPUT variable counts for the whole step (the in-core step keeps them resident, so that
+    their values can be read back after it); a TEMP counts at the functions from its first
+    to its last use; sizes are rounded up to whole chunks."""
+    uses = {}
+    for i, vs in enumerate(f):
+        for v, _ in vs:
+            uses.setdefault(v, []).append(i)
+    rounded = [-(-x // chunk) * chunk for x in b]
+    resident = sum(rounded[v] for v in range(len(b)) if k[v] != S.TEMP)
+    best = 0
+    for i in range(len(f)):
+        live = [v for v, at in uses.items() if k[v] == S.TEMP and min(at) <= i <= max(at)]
+        best = max(best, resident + sum(rounded[v] for v in live))
+    return best
+
+
+def test_incore_peak_is_the_live_set_maximum():
+    """P_incore against the brute-force live-set sum per function, on random registrations and
+    the networks at several chunk sizes; WS_max against the largest single function."""
+    rng = random.Random(12)
+    cases = [random_registration(rng, nv=rng.randint(1, 12), nf=rng.randint(1, 20))
+             for _ in range(300)]
+    cases += [as_schedule_input(lower(s)) for s in small_networks()]
+    cases += [as_schedule_input(lower(synth.workload(n))) for n in ("cnn", "resnet50_b256")]
+    for b, k, f in cases:
+        for chunk in (1, 8, 4096, 2 << 20):
+            assert S.incore_peak(b, k, f, chunk) == brute_incore_peak(b, k, f, chunk)
+            ws = max(sum(-(-b[v] // chunk) * chunk for v in {v for v, _ in vs}) for vs in f)
+            assert S.working_set_max(b, f, chunk) == ws
+    # a chain x -> t1 -> t2 -> t3: two TEMPs live at once at most (24 bytes); a TEMP kept one
+    # function past its last use would make three live at f2 (32)
+    b, k = [8, 8, 8, 8], [S.INPUT, S.TEMP, S.TEMP, S.TEMP]
+    f = [[(0, S.R), (1, S.W)], [(1, S.R), (2, S.W)], [(2, S.R), (3, S.W)], [(3, S.R)]]
+    assert S.incore_peak(b, k, f) == brute_incore_peak(b, k, f, 1) == 24
+    late = f[:2] + [[(2, S.R), (3, S.W), (1, S.R)]] + f[3:]
+    assert S.incore_peak(b, k, late) == brute_incore_peak(b, k, late, 1) == 32
+    # OUTPUT counts for the whole step, like the persistent kinds
+    assert S.incore_peak(b, [S.INPUT, S.OUTPUT, S.TEMP, S.TEMP], f) == 8 + 8 + 16
+
+
 @pytest.mark.parametrize("spec", small_networks(), ids=lambda s: s["name"])
 def test_feasibility_boundary(spec):
     b, k, f = as_schedule_input(lower(spec))
