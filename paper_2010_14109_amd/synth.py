@@ -339,3 +339,24 @@ def make_params(spec, seed=1):
         else:  # bias or beta
             params[name] = np.zeros(shape, np.float32)
     return params
+
+
+def normal_pool(n, seed, threads=16):
+    """``n`` standard-normal float32 values drawn by ``threads`` PCG64 streams spawned from
+    ``SeedSequence(seed)``, stream i filling the i-th of ``threads`` equal blocks.  The same
+    (n, seed, threads) gives the same array on any host.  Large full-size test inputs are
+    windows of one such pool."""
+    from concurrent.futures import ThreadPoolExecutor
+    out = np.empty(n, np.float32)
+    streams = np.random.SeedSequence(seed).spawn(threads)
+    step = -(-n // threads)
+
+    def fill(i):
+        block = out[i * step:(i + 1) * step]
+        if block.size:
+            np.random.Generator(np.random.PCG64(streams[i])).standard_normal(
+                size=block.size, dtype=np.float32, out=block)
+
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(fill, range(threads)))
+    return out
