@@ -186,10 +186,12 @@ def choose_chunk(net, frac, window_frac, policy="C", fixed=None, wait="oldest"):
 
 
 def run_mode(net, spec, x, labels, params, budget, window, chunk, steps, warmup, depth=None,
-             policy="C", fixed=None, wait="oldest", host_limit=None):
+             policy="C", fixed=None, wait="oldest", host_limit=None, layout="pool"):
     ctx = ooc.Context(0)
     try:
         net.register(ctx)
+        if budget != ooc.UNLIMITED:
+            ctx.set_layout(layout)
         if host_limit is not None and budget != ooc.UNLIMITED:
             ctx.set_host_limit(host_limit)
         ctx.set_policy(policy)
@@ -351,6 +353,10 @@ def main():
     ap.add_argument("--host-limit-gib", type=float, default=None,
                     help="most pinned host memory for the arena (GiB); TEMPs beyond it get "
                          "pageable homes copied through pinned staging slots")
+    ap.add_argument("--layout", default="pool", choices=("pool", "bestfit"),
+                    help="device memory of the out-of-core run: the chunk pool (Section 4), or "
+                         "one contiguous best-fit heap holding each allocation at its replayed "
+                         "offset (the allocator the pool is compared with, Fig. 3)")
     ap.add_argument("--timeline", default="",
                     help="write the last out-of-core step's kernel and copy spans (JSON) here")
     args = ap.parse_args()
@@ -390,7 +396,8 @@ def main():
     host_limit = None if args.host_limit_gib is None else int(args.host_limit_gib * (1 << 30))
     try:
         out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps,
-                       args.warmup, args.swapout_depth, policy, fixed, args.wait_order, host_limit)
+                       args.warmup, args.swapout_depth, policy, fixed, args.wait_order, host_limit,
+                       args.layout)
     except ooc.OocError as e:
         # the host could not pin the whole arena: give the TEMPs beyond a limit pageable homes
         if e.status != ooc.E_HOST_OOM or host_limit is not None:
@@ -399,7 +406,8 @@ def main():
         print(f"pinned arena refused ({e}); retrying with --host-limit-gib "
               f"{host_limit / (1 << 30):g}", file=sys.stderr, flush=True)
         out = run_mode(net, spec, x, labels, params, budget, window, chunk, args.steps,
-                       args.warmup, args.swapout_depth, policy, fixed, args.wait_order, host_limit)
+                       args.warmup, args.swapout_depth, policy, fixed, args.wait_order, host_limit,
+                       args.layout)
     if args.timeline:
         with open(args.timeline, "w") as fh:
             json.dump({"fns": net.fn_ops, "vars": net.names,
@@ -458,7 +466,7 @@ def main():
                    "scheduler": args.scheduler,
                    **({"swapin_ahead": fixed[0], "swapout_threshold": fixed[1]} if fixed else {}),
                    "policy": "cancel" if policy == "C" else "literal",
-                   "wait_order": args.wait_order,
+                   "wait_order": args.wait_order, "layout": args.layout,
                    "swapout_depth": "library default" if args.swapout_depth is None
                    else args.swapout_depth},
         "roofline": roof,
@@ -488,7 +496,8 @@ def main():
             "staged_h2d_bytes_per_step": st["staged_h2d_bytes"],
             "staged_d2h_bytes_per_step": st["staged_d2h_bytes"],
         },
-        "peak_device_bytes": {"pool": st["pool_bytes"], "max_chunks_in_use_bytes":
+        "peak_device_bytes": {"pool": st["pool_bytes"], "prepare_ms": round(st["prepare_ms"], 1),
+                              "mappings": st["n_mappings"], "max_chunks_in_use_bytes":
                               st["max_chunks_used"] * chunk, "peak_accounted": st["peak_accounted"],
                               "hipMemGetInfo_delta": st["device_bytes_delta"],
                               "runtime_overhead": st["device_bytes_delta"] - st["pool_bytes"],

@@ -104,6 +104,9 @@ enum { OOC_PRE = 0, OOC_POST = 1, OOC_END = 2 };
  *  RELU_FWD      Y = max(X, 0)        X[R] Y[W]                    n
  *  RELU_BWD      dX = dY [Y > 0]      Y[R] dY[R] dX[W]             n
  *  ADD           Y = A + B            A[R] B[R] Y[W]               n
+ *  ACC           A = A + B (in place: the sum of gradient contributions
+ *                accumulated into the running one)
+ *                                     A[RW] B[R]                   n
  *  SOFTMAX_CE    mean softmax cross-entropy over N rows; loss holds the N
  *                per-row losses then their mean (N + 1 floats), dlogits =
  *                (softmax - onehot) / N; labels int32, an out-of-range label
@@ -196,7 +199,8 @@ enum {
   OOC_OP_CONCAT_BWD = 28,
   OOC_OP_UPSAMPLE_FWD = 29,
   OOC_OP_UPSAMPLE_BWD = 30,
-  OOC_OP_COUNT = 31
+  OOC_OP_ACC = 31,
+  OOC_OP_COUNT = 32
 };
 
 /* One schedule op.  fn = N for END ops; held = budget bytes held after it
@@ -226,8 +230,9 @@ typedef struct {
   uint64_t budget;            /* as set (OOC_UNLIMITED in in-core mode) */
   uint64_t chunk;             /* m_c in use */
   uint64_t peak_accounted;    /* max chunk-rounded bytes held by the schedule */
-  uint64_t pool_chunks;       /* physical chunks created */
-  uint64_t pool_bytes;        /* pool_chunks * chunk: the device bytes the pool owns */
+  uint64_t pool_chunks;       /* physical chunks created (0 with OOC_LAYOUT_BESTFIT) */
+  uint64_t pool_bytes;        /* pool_chunks * chunk: the device bytes the pool owns (the
+                                 best-fit heap's extent with OOC_LAYOUT_BESTFIT) */
   uint64_t max_chunks_used;   /* most chunks mapped to live intervals at once */
   uint64_t device_bytes_delta;/* hipMemGetInfo used-bytes delta across prepare */
   uint64_t host_bytes;        /* pinned host arena */
@@ -314,6 +319,20 @@ ooc_status ooc_set_policy(ooc_ctx *ctx, int32_t policy);
  * answer to it.  The waits at the end of the step stay oldest first.
  * Registering stage only; OOC_E_INVALID for another value. */
 ooc_status ooc_set_wait_order(ooc_ctx *ctx, int32_t order);
+
+/* Device-memory layout.  OOC_LAYOUT_POOL (default): the chunk pool of
+ * Section 4, each residency interval in its own virtual range backed by
+ * chunks of m_c bytes.  OOC_LAYOUT_BESTFIT: the allocator the pool is
+ * compared with (Section 4, Fig. 3): one device allocation, each interval at
+ * the offset a contiguous best-fit heap gives it (requests rounded up to 256
+ * bytes, as ooc_bestfit_extent replays them).  The schedule, the copies and
+ * the results are the same; only the device bytes the layout needs differ
+ * (ooc_stats.pool_bytes: the heap's extent).  With this layout
+ * ooc_plan_intervals / ooc_plan_chunks list, instead of chunks, the heap
+ * segments each interval covers (the heap cut at every interval's first and
+ * last byte).  Registering stage only; OOC_E_INVALID for another value. */
+enum { OOC_LAYOUT_POOL = 0, OOC_LAYOUT_BESTFIT = 1 };
+ooc_status ooc_set_layout(ooc_ctx *ctx, int32_t layout);
 
 /* Most swap-outs in flight on the device-to-host stream during a step: before
  * issuing another one, the host waits for the oldest.  0 = no bound; default

@@ -98,6 +98,9 @@ def run(reg, x, labels, params, state=None, dtype=np.float64):
         elif op == "add_grad":
             A, B, Y = vs
             env[Y] = g(A) + g(B)
+        elif op == "acc_grad":
+            A, B = vs
+            env[A] = g(A) + g(B)
         elif op == "sgd":
             lr, mu = a["lr"], a["momentum"]
             step = 3 if mu else 2

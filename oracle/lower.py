@@ -7,9 +7,13 @@ uses.  One training step of a layer-sequential network becomes:
 1. the forward functions in layer order;
 2. the fused softmax cross-entropy (mean loss and the logits gradient);
 3. for every layer in reverse order: its backward functions, then one SGD
-   function for its parameters, then the additions that sum gradient
-   contributions for tensors with several consumers (in the order the
-   contributions appear).
+   function for its parameters, then the sums of the gradient contributions
+   of tensors with several consumers, in the order the contributions appear:
+   a contribution is added in place into the tensor's running gradient
+   (``acc_grad``), except while that running gradient variable is also the
+   gradient of another tensor whose layer's backward is still to come (an
+   addition passes its output gradient to both inputs); then it is added
+   into a new variable (``add_grad``).
 
 Variables are numbered by first appearance in the flattened sequence.  Each
 function lists ``(variable, access)`` pairs in this fixed order:
@@ -32,6 +36,7 @@ relu_bwd       Y R, dY R, dX W            (Y = the ReLU output)
 maxpool_bwd    idx R, dY R, dX W
 avgpool_bwd    dY R, dX W
 add_grad       g R, c R, g' W             (g' = g + c)
+acc_grad       g RW, c R                  (g = g + c)
 sgd            per parameter p in layer order: p RW, dp R [, m_p RW with momentum]
 embed_fwd      ids R, E R, pos R, Y W
 embed_bwd      ids R, dY R, dE W, dpos W
@@ -239,10 +244,21 @@ def lower(spec, keep_grads=False, slices=None):
             return
         pending.append((tensor, g))
 
+    done = set()        # tensors whose layer's backward is already in the sequence
+
+    def held_elsewhere(g, tensor):
+        """True when g is also the gradient of another tensor still waiting for its layer's
+        backward, which will read it."""
+        return any(t != tensor and t not in done and grad[t] == g for t in grad)
+
     def settle(pending):
         for tensor, g in pending:
             if tensor not in grad:
                 grad[tensor] = g
+            elif g != grad[tensor] and not held_elsewhere(grad[tensor], tensor):
+                # running gradient += contribution, in place
+                fns.append(("acc_grad", [(grad[tensor], RW), (g, R)],
+                            {"n": math.prod(shapes[tensor])}))
             else:
                 count[tensor] = count.get(tensor, 1) + 1
                 new = var(f"d:{tensor}#{count[tensor]}", shapes[tensor])
@@ -377,6 +393,7 @@ def lower(spec, keep_grads=False, slices=None):
                         {"B": Bt, "T": T, "H": H, "dh": d3 // 3 // H,
                          "causal": int(L["causal"])}))
             contribute(X, dX, pending)
+        done.add(name)
         settle(pending)
 
     # ---------------- number variables by first appearance

@@ -181,6 +181,15 @@ ooc_status ooc_set_wait_order(ooc_ctx* ctx, int32_t order) {
   return OOC_OK;
 }
 
+ooc_status ooc_set_layout(ooc_ctx* ctx, int32_t layout) {
+  REQUIRE_CTX(ctx);
+  REQUIRE_STAGE(ctx, REGISTERING, "ooc_set_layout");
+  if (layout != OOC_LAYOUT_POOL && layout != OOC_LAYOUT_BESTFIT)
+    return fail(ctx, OOC_E_INVALID, "unknown device layout");
+  ctx->layout = layout;
+  return OOC_OK;
+}
+
 ooc_status ooc_set_host_limit(ooc_ctx* ctx, uint64_t bytes) {
   REQUIRE_CTX(ctx);
   if (ctx->stage == PREPARED) return fail(ctx, OOC_E_STATE, "ooc_set_host_limit after ooc_prepare");
@@ -226,6 +235,9 @@ ooc_status ooc_build_schedule(ooc_ctx* ctx) {
   }
   ctx->sched = std::move(s);
   build_plan(ctx->vars, ctx->sched, ctx->incore, ctx->chunk, &ctx->plan);
+  const uint64_t pool_chunks_used = ctx->plan.max_chunks_used;
+  if (ctx->layout == OOC_LAYOUT_BESTFIT)
+    bestfit_layout(ctx->vars, 256, &ctx->plan, &ctx->iv_off, &ctx->heap_extent);
   ooc_stats& st = ctx->stats;
   st = ooc_stats{};
   st.budget = ctx->budget;
@@ -233,7 +245,7 @@ ooc_status ooc_build_schedule(ooc_ctx* ctx) {
   st.peak_accounted = ctx->sched.peak;
   st.sched_h2d_bytes = ctx->sched.h2d;
   st.sched_d2h_bytes = ctx->sched.d2h;
-  st.max_chunks_used = ctx->plan.max_chunks_used;
+  st.max_chunks_used = pool_chunks_used;
   st.n_intervals = ctx->plan.intervals.size();
   st.incore = ctx->incore;
   st.policy = ctx->policy;

@@ -70,6 +70,7 @@ struct ooc_ctx {
   int32_t wait_order = OOC_WAIT_OLDEST;    // see ooc_set_wait_order
   int64_t swapout_depth = 4;               // see ooc_set_swapout_depth
   uint64_t host_limit = OOC_UNLIMITED;     // see ooc_set_host_limit
+  int32_t layout = OOC_LAYOUT_POOL;        // see ooc_set_layout
   bool incore = true;
 
   ooc::Schedule sched;
@@ -80,6 +81,10 @@ struct ooc_ctx {
   void* va_base = nullptr;
   uint64_t va_bytes = 0;
   std::vector<char*> iv_ptr;              // per interval: start of its virtual range
+  // OOC_LAYOUT_BESTFIT: one allocation; each interval at its offset in it
+  std::vector<uint64_t> iv_off;
+  uint64_t heap_extent = 0;
+  void* heap = nullptr;
   std::vector<int64_t> resident;          // in-core mode: per variable, its resident interval
   char* arena = nullptr;
   uint64_t arena_bytes = 0;

@@ -30,6 +30,8 @@ hipError_t launch_fn(const Fn& fn, void* const* p, const uint64_t* bytes, float 
       return relu_bwd(F(0), F(1), F(2), a[0], s);
     case OOC_OP_ADD:
       return add(F(0), F(1), F(2), a[0], s);
+    case OOC_OP_ACC:
+      return accumulate(F(0), F(1), a[0], s);
     case OOC_OP_SOFTMAX_CE:
       return softmax_ce(F(0), static_cast<const int32_t*>(p[1]), F(2), F(3), a[0], a[1], s);
     case OOC_OP_SGD: {

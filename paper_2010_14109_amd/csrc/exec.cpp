@@ -72,6 +72,8 @@ void release_device(ooc_ctx* ctx) {
   if (ctx->ds) hipStreamDestroy(ctx->ds);
   if (ctx->ss) hipStreamDestroy(ctx->ss);
   ctx->cs = ctx->hs = ctx->ds = ctx->ss = nullptr;
+  if (ctx->heap) hipFree(ctx->heap);
+  ctx->heap = nullptr;
   if (ctx->va_base) {
     hipMemUnmap(ctx->va_base, ctx->va_bytes);
     hipMemAddressFree(ctx->va_base, ctx->va_bytes);
@@ -280,10 +282,19 @@ ooc_status prepare(ooc_ctx* ctx) {
   size_t free0 = 0, total0 = 0, free1 = 0, total1 = 0;
   HIPCK(hipMemGetInfo(&free0, &total0));
 
+  const Plan& plan = ctx->plan;
+  const int64_t NI = (int64_t)plan.intervals.size();
+  if (ctx->layout == OOC_LAYOUT_BESTFIT) {
+    // the comparison allocator: one contiguous heap, intervals at their best-fit offsets
+    HIPCK(hipMalloc(&ctx->heap, std::max<uint64_t>(ctx->heap_extent, 256)));
+    ctx->iv_ptr.assign(NI, nullptr);
+    for (int64_t J = 0; J < NI; ++J) ctx->iv_ptr[J] = (char*)ctx->heap + ctx->iv_off[J];
+    ctx->stats.n_mappings = 0;
+  }
   // Every physical chunk and every mapping of a chunk takes one entry of the
   // process's memory-map table (vm.max_map_count); beyond it the driver
   // rejects further access grants.  Refuse plans that cannot fit.
-  {
+  if (ctx->layout == OOC_LAYOUT_POOL) {
     uint64_t maps = ctx->plan.n_chunks;
     for (const Interval& iv : ctx->plan.intervals) maps += iv.chunks.size();
     const int64_t room = map_entries_left();
@@ -296,9 +307,8 @@ ooc_status prepare(ooc_ctx* ctx) {
   }
 
   // physical chunks
-  const Plan& plan = ctx->plan;
-  ctx->chunks.resize(plan.n_chunks);
-  for (uint64_t c = 0; c < plan.n_chunks; ++c) {
+  ctx->chunks.resize(ctx->layout == OOC_LAYOUT_POOL ? plan.n_chunks : 0);
+  for (uint64_t c = 0; c < ctx->chunks.size(); ++c) {
     hipError_t e = hipMemCreate(&ctx->chunks[c], ctx->chunk, &prop, 0);
     if (e != hipSuccess) {
       ctx->chunks.resize(c);
@@ -308,15 +318,14 @@ ooc_status prepare(ooc_ctx* ctx) {
     }
   }
   // one virtual range per interval, carved out of one reservation
-  const int64_t NI = (int64_t)plan.intervals.size();
   uint64_t total = 0;
   std::vector<uint64_t> off(NI);
   for (int64_t J = 0; J < NI; ++J) {
     off[J] = total;
     total += plan.intervals[J].chunks.size() * ctx->chunk;
   }
-  ctx->iv_ptr.assign(NI, nullptr);
-  if (total > 0) {
+  if (ctx->layout == OOC_LAYOUT_POOL) ctx->iv_ptr.assign(NI, nullptr);
+  if (ctx->layout == OOC_LAYOUT_POOL && total > 0) {
     HIPCK(hipMemAddressReserve(&ctx->va_base, total, ctx->chunk, nullptr, 0));
     ctx->va_bytes = total;
     uint64_t maps = 0;
@@ -609,8 +618,8 @@ ooc_status prepare(ooc_ctx* ctx) {
 
   auto t1 = std::chrono::steady_clock::now();
   ooc_stats& st = ctx->stats;
-  st.pool_chunks = plan.n_chunks;
-  st.pool_bytes = plan.n_chunks * ctx->chunk;
+  st.pool_chunks = ctx->chunks.size();
+  st.pool_bytes = ctx->layout == OOC_LAYOUT_POOL ? plan.n_chunks * ctx->chunk : ctx->heap_extent;
   st.max_chunks_used = plan.max_chunks_used;
   st.device_bytes_delta = free0 > free1 ? (uint64_t)(free0 - free1) : 0;
   st.host_bytes = hb;

@@ -921,9 +921,22 @@ hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, c
 #undef GEMM_BATCHED_CASE
 }
 
+// A 1 x 1 convolution with stride 1 and no padding is a plain product of the
+// NHWC pixel rows: its forward is X W^T, its input gradient dY W, both run on
+// the dense loaders (one add per K tile for the address, no tap arithmetic).
+bool pointwise(const ConvShape& c) {
+  return c.R == 1 && c.S == 1 && c.stride == 1 && c.pad == 0 && c.C % 4 == 0 && c.K % 4 == 0;
+}
+
 hipError_t conv_fwd(const float* X, const float* W, float* Y, const ConvShape& c, hipStream_t s) {
   const int64_t M = c.N * c.P * c.Q, N = c.K, K = c.R * c.S * c.C;
   if (!fits31(M) || !fits31(K)) return hipErrorInvalidValue;
+  if (pointwise(c) && N > 32 && aligned16(X) && aligned16(W)) {
+    // Y[NPQ][K] = X[NPQ][C] W[K][C]^T
+    auto fa = [&](auto& a) { a.p = X; a.ld = c.C; };
+    auto fb = [&](auto& b) { b.p = W; b.ld = c.C; };
+    return dispatch_dense<MatKv, MatKv, false>(fa, fb, Y, N, nullptr, M, N, K, 1, s);
+  }
   auto fa = [&](auto& a) {
     a.x = X; a.H = (int)c.H; a.W = (int)c.W; a.C = (int)c.C; a.S = (int)c.S;
     a.st = (int)c.stride; a.pad = (int)c.pad;
@@ -947,6 +960,13 @@ hipError_t conv_bwd_x(const float* W, const float* dY, float* dX, const ConvShap
                       hipStream_t s) {
   if (c.C % 4 != 0) return hipErrorInvalidValue;   // every conv with an input gradient has C % 4 == 0
   if (!fits31(c.N * c.H * c.W) || !fits31(c.R * c.S * c.K)) return hipErrorInvalidValue;
+  if (pointwise(c) && aligned16(W) && aligned16(dY)) {
+    // dX[NHW][C] = dY[NHW][K] W[K][C]
+    auto fa = [&](auto& a) { a.p = dY; a.ld = c.K; };
+    auto fb = [&](auto& b) { b.p = W; b.ld = c.C; };
+    return dispatch_dense<MatKv, MatMv, false>(fa, fb, dX, c.C, nullptr, c.N * c.H * c.W, c.C, c.K,
+                                               1, s);
+  }
   const int64_t st = c.stride;
   // one GEMM per stride class (ph, pw) of input pixels; a class no tap reaches gets zeros
   for (int64_t ph = 0; ph < st; ++ph)

@@ -60,7 +60,13 @@ struct Plan {
 // The plan's intervals served by one contiguous best-fit heap (the allocator
 // the chunk pool is compared with): highest address used and peak live bytes.
 void bestfit_extent(const std::vector<Var>& vars, const Plan& plan, uint64_t align,
-                    uint64_t* extent, uint64_t* peak_live);
+                    uint64_t* extent, uint64_t* peak_live,
+                    std::vector<uint64_t>* offsets = nullptr);
+// Lays the plan's intervals out in that heap: offsets per interval, the heap's
+// extent, and each interval's chunk list replaced by the heap segments it
+// covers (the heap cut at every interval boundary).
+void bestfit_layout(const std::vector<Var>& vars, uint64_t align, Plan* plan,
+                    std::vector<uint64_t>* offsets, uint64_t* extent);
 // Scheduler (Section 3, Fig. 2).  Returns OOC_OK, OOC_E_INFEASIBLE.  With
 // ahead >= 0 the fixed-distance rule of LMS (Section 2) replaces the byte
 // window: the window ends with f_{i+ahead} and a variable whose next use is

@@ -50,6 +50,8 @@ int64_t wgrad_slices(int64_t M, int64_t N, int64_t K, int64_t C);
 hipError_t relu_fwd(const float* x, float* y, int64_t n, hipStream_t s);
 hipError_t relu_bwd(const float* y, const float* dy, float* dx, int64_t n, hipStream_t s);
 hipError_t add(const float* a, const float* b, float* y, int64_t n, hipStream_t s);
+// a += b in place (a and b distinct)
+hipError_t accumulate(float* a, const float* b, int64_t n, hipStream_t s);
 // count parameter tensors: w[k] -= lr * (v[k] = mu v[k] + g[k]), or lr * g[k] where v[k] is null
 hipError_t sgd(int count, float* const* w, const float* const* g, float* const* v,
                const int64_t* n, float lr, float mu, hipStream_t s);

@@ -60,6 +60,25 @@ hipError_t ew(const float* a, const float* b, float* y, int64_t n, hipStream_t s
   return hipGetLastError();
 }
 
+// a += b in place: each element is read and written by the same lane, so the
+// running gradient needs no second buffer.
+__global__ void acc_kernel(float* __restrict__ a, const float* __restrict__ b, int64_t n,
+                           bool vec) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t done = 0;
+  if (vec) {
+    const int64_t n4 = n / 4;
+    for (int64_t j = i; j < n4; j += stride) {
+      const float4 x = reinterpret_cast<const float4*>(a)[j];
+      const float4 z = reinterpret_cast<const float4*>(b)[j];
+      reinterpret_cast<float4*>(a)[j] = make_float4(x.x + z.x, x.y + z.y, x.z + z.z, x.w + z.w);
+    }
+    done = n4 * 4;
+  }
+  for (int64_t j = done + i; j < n; j += stride) a[j] = a[j] + b[j];
+}
+
 // Up to kSgdSet parameter tensors of one update function in one launch: grid row y
 // updates tensor y, each element with the same arithmetic as a launch of its own.
 constexpr int kSgdSet = 8;
@@ -779,6 +798,12 @@ hipError_t relu_bwd(const float* y, const float* dy, float* dx, int64_t n, hipSt
 }
 hipError_t add(const float* a, const float* b, float* y, int64_t n, hipStream_t s) {
   return ew<2>(a, b, y, n, s);
+}
+
+hipError_t accumulate(float* a, const float* b, int64_t n, hipStream_t s) {
+  const bool vec = aligned16(a) && aligned16(b);
+  hipLaunchKernelGGL(acc_kernel, dim3(grid_for((n + 3) / 4)), dim3(TPB), 0, s, a, b, n, vec);
+  return hipGetLastError();
 }
 
 hipError_t sgd(int count, float* const* w, const float* const* g, float* const* v,

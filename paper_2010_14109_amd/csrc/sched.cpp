@@ -325,7 +325,7 @@ void build_plan(const std::vector<Var>& vars, const Schedule& s, bool incore, ui
 // the free tail if there is one.  Returns the highest address used and the
 // most bytes live at once.
 void bestfit_extent(const std::vector<Var>& vars, const Plan& plan, uint64_t align,
-                    uint64_t* extent, uint64_t* peak_live) {
+                    uint64_t* extent, uint64_t* peak_live, std::vector<uint64_t>* offsets) {
   std::map<uint64_t, uint64_t> by_off;             // hole offset -> size
   std::set<std::pair<uint64_t, uint64_t>> by_size; // (size, offset)
   uint64_t end = 0, live = 0, peak = 0;
@@ -390,6 +390,34 @@ void bestfit_extent(const std::vector<Var>& vars, const Plan& plan, uint64_t ali
   }
   *extent = end;
   *peak_live = peak;
+  if (offsets) *offsets = std::move(off);
+}
+
+// Device layout of the best-fit heap: every interval at its replayed offset.
+// The heap is cut at every interval's first and last byte into segments; an
+// interval's "chunks" become the segments it covers, so the executor's rule
+// (the first writer of memory waits for everyone who used it before) applies
+// unchanged.
+void bestfit_layout(const std::vector<Var>& vars, uint64_t align, Plan* plan,
+                    std::vector<uint64_t>* offsets, uint64_t* extent) {
+  uint64_t peak = 0;
+  bestfit_extent(vars, *plan, align, extent, &peak, offsets);
+  std::vector<uint64_t> cuts;
+  for (size_t J = 0; J < plan->intervals.size(); ++J) {
+    cuts.push_back((*offsets)[J]);
+    cuts.push_back((*offsets)[J] + round_up(vars[plan->intervals[J].var].bytes, align));
+  }
+  std::sort(cuts.begin(), cuts.end());
+  cuts.erase(std::unique(cuts.begin(), cuts.end()), cuts.end());
+  for (size_t J = 0; J < plan->intervals.size(); ++J) {
+    const uint64_t a = (*offsets)[J], b = a + round_up(vars[plan->intervals[J].var].bytes, align);
+    auto& cs = plan->intervals[J].chunks;
+    cs.clear();
+    for (size_t g = std::lower_bound(cuts.begin(), cuts.end(), a) - cuts.begin();
+         g + 1 < cuts.size() && cuts[g] < b; ++g)
+      cs.push_back((int32_t)g);
+  }
+  plan->n_chunks = cuts.empty() ? 0 : cuts.size() - 1;
 }
 
 }  // namespace ooc

@@ -49,6 +49,7 @@ const Sig kSig[OOC_OP_COUNT] = {
     {"CONCAT_BWD", -1, -1, {}},
     {"UPSAMPLE_FWD", 2, 4, {OOC_R, OOC_W}},
     {"UPSAMPLE_BWD", 2, 4, {OOC_R, OOC_W}},
+    {"ACC", 2, 1, {OOC_RW, OOC_R}},
 };
 
 const int64_t kMaxElems = int64_t(1) << 40;
@@ -119,6 +120,7 @@ std::string check_fn(const std::vector<Var>& vars, const Fn& fn) {
     case OOC_OP_RELU_FWD:
     case OOC_OP_RELU_BWD:
     case OOC_OP_ADD:
+    case OOC_OP_ACC:
       for (int j = 0; j < nv; ++j) NEED(j, a[0] * 4, "tensor");
       return "";
     case OOC_OP_SOFTMAX_CE: {

@@ -27,7 +27,7 @@ from collections import defaultdict
 
 import numpy as np
 
-from . import netdef, ooc
+from . import netdef, ooc, synth
 
 CAL_N = 268435456   # floats of the calibration ReLU: 1 GiB read, 1 GiB written
 
@@ -85,12 +85,15 @@ def run(spec, reps=20):
         ctx.set_chunk(2 << 20)
         ctx.build_schedule()
         ctx.prepare()
-        rng = np.random.default_rng(0)
+        need = sum(b // 4 for b, k, _ in vs if k in (ooc.INPUT, ooc.STATE))
+        pool = synth.normal_pool(max(need, 1), seed=0)
+        at = 0
         for (b, k, _), v in zip(vs, ids):
             if k in (ooc.INPUT, ooc.STATE):
+                w = pool[at:at + b // 4]
+                at += b // 4
                 # |N(0,1)| keeps a batch-norm inverse deviation positive
-                ctx.host_view(v, np.float32)[...] = np.abs(rng.standard_normal(b // 4)).astype(
-                    np.float32) if k == ooc.STATE else rng.standard_normal(b // 4).astype(np.float32)
+                ctx.host_view(v, np.float32)[...] = np.abs(w) if k == ooc.STATE else w
         ctx.upload()
         ctx.step(0.0, 0.0)
         t0 = time.perf_counter()

@@ -8,9 +8,12 @@ registers it through the C interface:
 * forward functions in layer order, then the fused softmax cross-entropy
   (one label per row of the logits);
 * per layer in reverse order: its backward functions, one SGD function for
-  its parameters, then the additions that sum the gradient contributions of
-  tensors consumed more than once (in the order the contributions appear);
-  an addition's own backward is the identity and needs no function.
+  its parameters, then the sums of the gradient contributions of tensors
+  consumed more than once, in the order the contributions appear: each
+  contribution is accumulated in place into the tensor's running gradient
+  (``acc``), or, while another tensor whose backward is still to come holds
+  that same gradient variable, added into a new variable (``add``); an
+  addition's own backward is the identity and needs no function.
 
 Variables are numbered by first appearance.  Variable lists, sizes and
 kinds follow the operation table of ``include/ooc.h``; the auxiliary sizes are
@@ -343,22 +346,33 @@ class Net:
                                   (dlogits, ooc.W)], [n, classes])
         grads = {logits: dlogits}
         sums = {}
+        visited = set()      # layers whose backward has been emitted
         for L in reversed(spec["layers"]):
             if L["name"] not in grads:
                 continue
             contributions = []
             self._bwd(L, grads[L["name"]], contributions)
+            visited.add(L["name"])
             for tensor, g in contributions:
                 if tensor == "x":
                     continue
-                if tensor in grads:
-                    sums[tensor] = sums.get(tensor, 1) + 1
-                    acc = self._decl(f"d:{tensor}#{sums[tensor]}", self.shape[tensor])
-                    self._call("add", [(grads[tensor], ooc.R), (g, ooc.R), (acc, ooc.W)],
-                               [prod(self.shape[tensor])])
-                    grads[tensor] = acc
-                else:
+                if tensor not in grads:
                     grads[tensor] = g
+                    continue
+                cur = grads[tensor]
+                # the running sum is accumulated in place unless another tensor whose
+                # backward is still to come holds the same gradient variable (an addition's
+                # backward hands its output gradient to both inputs)
+                shared = any(u != tensor and gv == cur and u not in visited
+                             for u, gv in grads.items())
+                n = prod(self.shape[tensor])
+                if not shared and cur != g:
+                    self._call("acc", [(cur, ooc.RW), (g, ooc.R)], [n])
+                    continue
+                sums[tensor] = sums.get(tensor, 1) + 1
+                acc = self._decl(f"d:{tensor}#{sums[tensor]}", self.shape[tensor])
+                self._call("add", [(cur, ooc.R), (g, ooc.R), (acc, ooc.W)], [n])
+                grads[tensor] = acc
 
     def _number(self):
         self.ids = {}

@@ -21,6 +21,7 @@ INPUT, PARAM, STATE, OUTPUT, TEMP = 0, 1, 2, 3, 4
 R, W, RW = 1, 2, 3
 POLICY_CANCEL, POLICY_LITERAL = 0, 1
 WAIT_OLDEST, WAIT_FURTHEST = 0, 1
+LAYOUT_POOL, LAYOUT_BESTFIT = 0, 1
 SWAPIN, ALLOC, CANCEL, WAIT_OUT, SWAPOUT, FREE = 0, 1, 2, 3, 4, 5
 PRE, POST, END = 0, 1, 2
 UNLIMITED = 2 ** 64 - 1
@@ -32,7 +33,7 @@ OPS = {
     "avgpool_fwd": 16, "avgpool_bwd": 17, "mix": 18, "embed_fwd": 19, "embed_bwd": 20,
     "layernorm_fwd": 21, "layernorm_bwd": 22, "gelu_fwd": 23, "gelu_bwd": 24,
     "attention_fwd": 25, "attention_bwd": 26, "concat_fwd": 27, "concat_bwd": 28,
-    "upsample_fwd": 29, "upsample_bwd": 30,
+    "upsample_fwd": 29, "upsample_bwd": 30, "acc": 31,
 }
 
 #: every symbol ``include/ooc.h`` declares
@@ -43,7 +44,7 @@ EXPORTS = [
     "ooc_plan_intervals", "ooc_plan_chunks", "ooc_prepare", "ooc_host_ptr", "ooc_upload",
     "ooc_download", "ooc_step", "ooc_get_stats", "ooc_fn_times", "ooc_link_probe",
     "ooc_timeline", "ooc_set_swapout_depth", "ooc_set_fixed_distance", "ooc_bestfit_extent",
-    "ooc_set_wait_order", "ooc_set_host_limit", "ooc_wgrad_slices",
+    "ooc_set_wait_order", "ooc_set_host_limit", "ooc_wgrad_slices", "ooc_set_layout",
 ]
 
 
@@ -111,6 +112,7 @@ def load(path=LIB_PATH):
         "ooc_set_fixed_distance": ([P, c.c_int64, c.c_int64], c.c_int32),
         "ooc_set_wait_order": ([P, c.c_int32], c.c_int32),
         "ooc_set_host_limit": ([P, c.c_uint64], c.c_int32),
+        "ooc_set_layout": ([P, c.c_int32], c.c_int32),
         "ooc_bestfit_extent": ([P, c.c_uint64, c.POINTER(c.c_uint64), c.POINTER(c.c_uint64)],
                                c.c_int32),
         "ooc_build_schedule": ([P], c.c_int32),
@@ -239,6 +241,11 @@ class Context:
         """``"oldest"`` / WAIT_OLDEST or ``"furthest"`` / WAIT_FURTHEST (see ooc_set_wait_order)."""
         order = {"oldest": WAIT_OLDEST, "furthest": WAIT_FURTHEST}.get(order, order)
         _check(self.lib.ooc_set_wait_order(self.h, order), self.h)
+
+    def set_layout(self, layout):
+        """``"pool"`` / LAYOUT_POOL or ``"bestfit"`` / LAYOUT_BESTFIT (see ooc_set_layout)."""
+        layout = {"pool": LAYOUT_POOL, "bestfit": LAYOUT_BESTFIT}.get(layout, layout)
+        _check(self.lib.ooc_set_layout(self.h, layout), self.h)
 
     def set_fixed_distance(self, swapin_ahead, swapout_threshold):
         _check(self.lib.ooc_set_fixed_distance(self.h, swapin_ahead, swapout_threshold), self.h)

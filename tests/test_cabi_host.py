@@ -53,7 +53,7 @@ def test_function_sequence_matches_oracle_lowering(spec, keep):
     assert mine.var_bytes == [v["bytes"] for v in ref["vars"]]
     assert mine.var_kinds == [v["kind"] for v in ref["vars"]]
     assert mine.names == [v["name"] for v in ref["vars"]]
-    opname = {"add_fwd": "add", "add_grad": "add"}
+    opname = {"add_fwd": "add", "add_grad": "add", "acc_grad": "acc"}
     assert mine.fn_ops == [opname.get(f["op"], f["op"]) for f in ref["fns"]]
     assert mine.fn_vars == [f["vars"] for f in ref["fns"]]
 
@@ -484,3 +484,54 @@ def test_queries_report_status_and_message(lib):
     assert lib.ooc_last_error(None).decode() == "ooc_create: out is NULL"
     assert lib.ooc_wgrad_slices(10, None, 0, C.byref(i64)) == ooc.E_INVALID
     assert lib.ooc_last_error(None).decode().startswith("ooc_wgrad_slices")
+
+
+def test_bestfit_layout_keeps_live_intervals_apart(lib):
+    """OOC_LAYOUT_BESTFIT: the same schedule as the chunk pool, and every two residency
+    intervals alive at the same time cover disjoint heap segments (so no two live copies share
+    device bytes); the heap's extent is the one ooc_bestfit_extent reports at 256-byte
+    alignment."""
+    rng = random.Random(31)
+    cases = []
+    for _ in range(60):
+        b, k, f = random_registration(rng, nv=rng.randint(1, 12), nf=rng.randint(1, 20))
+        ws = S.working_set_max(b, f, 8)
+        cases.append((b, k, f, rng.choice([ws, 2 * ws, 10 ** 6])))
+    for spec in specs_small():
+        net = netdef.Net(spec)
+        b, k, f = net.var_bytes, net.var_kinds, net.fn_vars
+        p = S.incore_peak(b, k, f, 4096)
+        cases.append((b, k, f, max(S.budget_for(0.25, p, 4096), S.working_set_max(b, f, 4096))))
+    for trial, (b, k, f, B) in enumerate(cases):
+        ctxs = []
+        for layout in ("pool", "bestfit"):
+            ctx = ooc.Context(-1)
+            for nb, kd in zip(b, k):
+                ctx.add_var(nb, kd)
+            for vs in f:
+                ctx.add_fn("noop", [v for v, _ in vs], [a for _, a in vs])
+            ctx.set_chunk(8 if B < 10 ** 6 or trial < 60 else 4096)
+            ctx.set_budget(B)
+            ctx.set_layout(layout)
+            ctx.build_schedule()
+            ctxs.append(ctx)
+        pool, best = ctxs
+        assert pool.schedule() == best.schedule(), trial
+        ivs = best.plan()
+        nops = len(best.schedule()[0])
+        span = [(iv["open"] if iv["open"] >= 0 else -1,
+                 iv["close"] if iv["close"] >= 0 else nops) for iv in ivs]
+        for x in range(len(ivs)):
+            for y in range(x + 1, len(ivs)):
+                if span[x][0] < span[y][1] and span[y][0] < span[x][1]:
+                    assert not set(ivs[x]["chunks"]) & set(ivs[y]["chunks"]), (trial, x, y)
+        extent, _ = pool.bestfit_extent(256)
+        assert best.stats()["max_chunks_used"] == pool.stats()["max_chunks_used"]
+        assert best.bestfit_extent(256)[0] == extent
+        for c in ctxs:
+            c.close()
+    ctx = ooc.Context(-1)
+    with pytest.raises(ooc.OocError) as e:
+        ctx.set_layout(2)
+    assert e.value.status == ooc.E_INVALID
+    ctx.close()

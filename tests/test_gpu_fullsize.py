@@ -6,8 +6,10 @@ step.  Even the oracle run in float32 differs from float64 by 3e-3 (plain CNN,
 batch 128) to 4e-2 (ResNet-50) on some gradients.  For these networks the
 bar is therefore derived from the arithmetic: for every parameter gradient,
 updated parameter and momentum buffer, the device's relative L2 error against
-float64 must be at most 4 times the float32 oracle's own error (and never
-has to be smaller than 1e-4).  The loss, a well-conditioned forward
+float64 must be at most 1.5 times the float32 oracle's own, and its largest
+element error (relative to the largest element) at most 3 times the float32
+oracle's (neither ever has to be smaller than 1e-4; see
+``gpu_util.within_fp32_error``).  The loss, a well-conditioned forward
 quantity, must match float64 within 1e-5.
 
 The out-of-core step must equal the in-core step bit for bit in the exact
@@ -21,7 +23,7 @@ import bench
 from oracle.interp import run as oracle_run
 from oracle.lower import lower
 from paper_2010_14109_amd import netdef, synth
-from tests.gpu_util import rel_l2, run_net
+from tests.gpu_util import run_net, within_fp32_error
 
 pytestmark = pytest.mark.gpu
 
@@ -34,16 +36,14 @@ def derived_check(spec, loss, outs):
     e32 = oracle_run(reg, x, labels, {k: v.astype(np.float32) for k, v in params.items()},
                      dtype=np.float32)
     assert abs(loss - e64["loss"][-1]) <= 1e-5 * abs(e64["loss"][-1])
-    worst = 0.0
+    worst = (0.0, 0.0)
     for name, val in outs.items():
         if name == "loss":
             continue
-        ref = e64[name]
-        err = rel_l2(val.reshape(ref.shape), ref)
-        base = rel_l2(e32[name], ref)
-        assert err <= max(1e-4, 4 * base), (name, err, base)
-        worst = max(worst, err / max(1e-4, base))
-    print(f"{spec['name']}: worst error / max(1e-4, fp32 oracle error) = {worst:.2f}", flush=True)
+        l2, mx = within_fp32_error(name, val, e64[name], e32[name], 1e-4)
+        worst = (max(worst[0], l2), max(worst[1], mx))
+    print(f"{spec['name']}: worst error / bound: relative L2 {worst[0]:.2f}, largest element "
+          f"{worst[1]:.2f}", flush=True)
 
 
 def bench_config(name, **over):

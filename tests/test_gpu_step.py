@@ -20,7 +20,7 @@ from oracle.interp import run as oracle_run
 from oracle.lower import lower, as_schedule_input
 from paper_2010_14109_amd import netdef, ooc, synth
 from tests.seq_util import lowering
-from tests.gpu_util import STAGING_BYTES, persistent_host_bytes, rel_l2, run_net
+from tests.gpu_util import STAGING_BYTES, persistent_host_bytes, rel_err, run_net, within_fp32_error
 
 pytestmark = pytest.mark.gpu
 TOL = 1e-4
@@ -54,7 +54,7 @@ def check_against_oracle(spec, loss, outs, ref):
             if np.linalg.norm(r) == 0:
                 assert np.abs(val).max() < 1e-6, name
             else:
-                assert rel_l2(val.reshape(r.shape), r) <= TOL, name
+                assert rel_err(val.reshape(r.shape), r) <= TOL, name
 
 
 @pytest.mark.parametrize("spec", tiny_specs(), ids=lambda s: s["name"])
@@ -133,8 +133,7 @@ def test_full_size_cnn_matches_oracle():
     for name, val in outs.items():
         if name in ref and name != "loss" and np.linalg.norm(ref[name]) > 0:
             r = ref[name]
-            bound = max(TOL, rel_l2(np.asarray(ref32[name]).reshape(r.shape), r))
-            assert rel_l2(val.reshape(r.shape), r) <= bound, name
+            within_fp32_error(name, val, r, ref32[name], TOL)
             checked += 1
     assert checked >= 60
     assert st["pool_bytes"] <= B and st["h2d_bytes"] > 0
@@ -147,15 +146,18 @@ def test_full_size_cnn_matches_oracle():
 # chunk sizes as bench.py picks them (the process memory-map table bounds the mappings); the
 # host limit in GiB where the host footprint exceeds what one process can pin
 FULL = [("resnet50_b256", {}, 4, None), ("transformer", {"batch": 24}, 8, None),
-        ("densenet", {}, 2, None), ("unet", {}, 2, None), ("resnet50_b1440", {}, 16, 56)]
+        ("densenet", {}, 2, None), ("unet", {}, 2, None), ("resnet50_b1440", {}, 16, 56),
+        ("transformer", {}, 16, 56)]
 
 
-@pytest.mark.parametrize("name,kw,chunk_mib,limit_gib", FULL, ids=[f[0] for f in FULL])
+@pytest.mark.parametrize("name,kw,chunk_mib,limit_gib", FULL,
+                         ids=[synth.workload(f[0], **f[1])["name"] for f in FULL])
 def test_full_size_out_of_core_equals_in_core(name, kw, chunk_mib, limit_gib):
     """At the full sizes and budgets the bench runs, where the oracle is too slow: one
     out-of-core step (W = B/2, policy C) leaves the loss and every updated parameter and state
     bit-identical to the in-core step, and the device pool stays within the budget.  ResNet-50
-    at batch 1440 with B = P/7.5 runs with part of its host homes pageable."""
+    at batch 1440 with B = P/7.5 and the transformer at batch 64 with B = 0.2 P run with part
+    of their host homes pageable."""
     spec = synth.workload(name, **kw)
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
@@ -412,3 +414,54 @@ def test_host_slots_are_reused_without_corruption():
                 assert ctx.stats()["host_bytes"] < temp_bytes
             finally:
                 ctx.close()
+
+
+@pytest.mark.parametrize("idx", range(len(tiny_specs())))
+def test_bestfit_layout_equals_pool(idx):
+    """The same schedule with device memory laid out by the contiguous best-fit heap instead of
+    the chunk pool (the comparison of Section 4, Fig. 3): two steps, bit-identical results; the
+    device holds the heap's extent."""
+    spec = tiny_specs()[idx]
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    b, k, f = as_schedule_input(lowering(spec, keep_grads=True))
+    chunk = 4096
+    B = max(S.budget_for(0.25, S.incore_peak(b, k, f, chunk), chunk), S.working_set_max(b, f, chunk))
+    out = {}
+    for layout in ("pool", "bestfit"):
+        print(f"{spec['name']}: {layout} layout, budget {B}", flush=True)
+        out[layout] = run_net(spec, x, labels, params, budget=B, window=B // 2, chunk=chunk,
+                              steps=2, layout=layout)
+    (lp, op, sp), (lb, ob, sb) = out["pool"], out["bestfit"]
+    assert np.float32(lp).tobytes() == np.float32(lb).tobytes()
+    for n in op:
+        assert op[n].tobytes() == ob[n].tobytes(), n
+    assert sp["pool_bytes"] <= B and sb["pool_chunks"] == 0 and sb["n_mappings"] == 0
+    assert sb["h2d_bytes"] == sp["h2d_bytes"] and sb["d2h_bytes"] == sp["d2h_bytes"]
+
+
+@pytest.mark.parametrize("frac", [0.5, 0.25])
+def test_bestfit_layout_resnet50_b256(frac):
+    """ResNet-50 at batch 256, W = B/2: the step on the best-fit heap equals the step on the
+    chunk pool bit for bit; the pool holds the budget, the heap its extent (more than the budget
+    once the schedule's allocations fragment it)."""
+    spec = synth.workload("resnet50_b256")
+    x, labels = synth.make_inputs(spec, 0)
+    params = synth.make_params(spec, 1)
+    net = netdef.Net(spec)
+    chunk = 4 << 20
+    p = S.incore_peak(net.var_bytes, net.var_kinds, net.fn_vars, chunk)
+    B = max(S.budget_for(frac, p, chunk), S.working_set_max(net.var_bytes, net.fn_vars, chunk))
+    out = {}
+    for layout in ("pool", "bestfit"):
+        print(f"resnet50 b256 at {frac} P: {layout} layout, budget {B}", flush=True)
+        out[layout] = run_net(spec, x, labels, params, budget=B, window=B // 2, chunk=chunk,
+                              keep_grads=False, layout=layout)
+    (lp, op, sp), (lb, ob, sb) = out["pool"], out["bestfit"]
+    assert np.float32(lp).tobytes() == np.float32(lb).tobytes()
+    for n in op:
+        assert op[n].tobytes() == ob[n].tobytes(), n
+    assert sp["pool_bytes"] <= B and sb["pool_bytes"] > B
+    print(f"resnet50 b256 at {frac} P: pool {sp['pool_bytes']} B, best-fit heap "
+          f"{sb['pool_bytes']} B ({sb['pool_bytes'] / B:.2f} of the budget); device bytes "
+          f"{sp['device_bytes_delta']} / {sb['device_bytes_delta']}", flush=True)
