@@ -48,7 +48,7 @@ def fn_work(op, attrs):
         return "flop", 2 * N * P * Q * K * R * S * C
     if op == "relu_fwd":
         return "byte", 8 * a[0]
-    if op in ("relu_bwd", "add"):
+    if op in ("relu_bwd", "add", "acc"):
         return "byte", 12 * a[0]
     if op == "bn_fwd":
         return "byte", 8 * a[0] * a[1]

@@ -383,7 +383,8 @@ ooc_status ooc_incore_peak(const ooc_ctx *ctx, uint64_t *bytes);
 ooc_status ooc_working_set_max(const ooc_ctx *ctx, uint64_t *bytes);
 
 /* Chunk plan (Section 4): residency intervals in opening order and the
- * concatenated chunk ids they map (lowest free chunk ids first).  Valid
+ * concatenated chunk ids they map (freed chunks reused in the order they were
+ * freed, a new chunk id only when none is free).  Valid
  * after build_schedule; host only. */
 ooc_status ooc_plan_intervals(const ooc_ctx *ctx, ooc_interval *buf, uint64_t cap, uint64_t *n);
 

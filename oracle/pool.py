@@ -9,13 +9,14 @@ order there is no external fragmentation, and the only waste is the internal
 fragmentation ``m_a - m_r < m_c`` per request (eq. 1), at most ``N_max m_c``
 in total for ``N_max`` live requests (eq. 2).
 
-The cache hands out the lowest-numbered free chunks first, which makes the
-chunk assignment of a schedule deterministic.
+The cache hands out freed chunks in the order they were freed (the least
+recently freed first), and a chunk never used before (lowest id first) only
+when no freed chunk is left.  This makes the chunk assignment of a schedule
+deterministic.
 """
 
 from __future__ import annotations
 
-import heapq
 from collections import deque
 
 SWAPIN, ALLOC, CANCEL, WAIT_OUT, SWAPOUT, FREE = 0, 1, 2, 3, 4, 5
@@ -29,16 +30,27 @@ class VAPool:
     def __init__(self, n_chunks, chunk):
         self.chunk = chunk
         self.n_chunks = n_chunks
-        self.free = list(range(n_chunks))
-        heapq.heapify(self.free)
+        self.freed = deque()      # released chunks, oldest release first
+        self.unused = 0           # chunks [unused, n_chunks) were never handed out
         self.ranges = {}          # range id -> (requested bytes, [chunk ids])
         self.next_id = 0
 
+    @property
+    def free(self):
+        """Every chunk not in use: the freed ones in queue order, then the unused ones."""
+        return list(self.freed) + list(range(self.unused, self.n_chunks))
+
     def alloc(self, m_r):
         k = -(-m_r // self.chunk)
-        if k > len(self.free):
-            raise OutOfChunks(f"need {k} chunks, {len(self.free)} free")
-        chunks = [heapq.heappop(self.free) for _ in range(k)]
+        if k > len(self.freed) + self.n_chunks - self.unused:
+            raise OutOfChunks(f"need {k} chunks, {len(self.freed) + self.n_chunks - self.unused} free")
+        chunks = []
+        for _ in range(k):
+            if self.freed:
+                chunks.append(self.freed.popleft())
+            else:
+                chunks.append(self.unused)
+                self.unused += 1
         rid = self.next_id
         self.next_id += 1
         self.ranges[rid] = (m_r, chunks)
@@ -46,8 +58,7 @@ class VAPool:
 
     def release(self, rid):
         _, chunks = self.ranges.pop(rid)
-        for c in chunks:
-            heapq.heappush(self.free, c)
+        self.freed.extend(chunks)
 
     def mapped_bytes(self):
         return sum(len(c) for _, c in self.ranges.values()) * self.chunk
@@ -90,7 +101,7 @@ def assign(ops, var_bytes, n_chunks, chunk):
             j = working.pop(u)
             intervals[j]["close"] = k
             pool.release(intervals[j]["rid"])
-        max_used = max(max_used, n_chunks - len(pool.free))
+        max_used = max(max_used, pool.unused - len(pool.freed))     # chunks in use
     for iv in intervals:
         del iv["rid"]
     return intervals, max_used

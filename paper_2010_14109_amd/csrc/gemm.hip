@@ -922,9 +922,10 @@ hipError_t gemm_batched(bool a_rowk, const float* A, int64_t lda, bool b_rowk, c
 }
 
 // A 1 x 1 convolution with stride 1 and no padding is a plain product of the
-// NHWC pixel rows: its forward is X W^T, its input gradient dY W, both run on
-// the dense loaders (one add per K tile for the address, no tap arithmetic).
-bool pointwise(const ConvShape& c) {
+// NHWC pixel rows: its forward is X W^T, its input gradient dY W and its filter
+// gradient dY^T X, all run on the dense loaders (one add per K tile for the
+// address, no tap arithmetic).
+static bool pointwise(const ConvShape& c) {
   return c.R == 1 && c.S == 1 && c.stride == 1 && c.pad == 0 && c.C % 4 == 0 && c.K % 4 == 0;
 }
 
@@ -1042,7 +1043,12 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
                                                                           M, N, K, slices, s);
       break;
     default:
-      if (c.K % 4 != 0)
+      if (pointwise(c) && aligned16(X) && aligned16(dY)) {
+        // dW[K][C] = dY^T X over the pixel rows: the dense weight gradient's loaders (the same
+        // tile shapes as the general case below, so the slice count is the same)
+        auto fx = [&](auto& b) { b.p = X; b.ld = c.C; };
+        e = dispatch_dense<MatMv, MatMv, false>(fa, fx, out, N, nullptr, M, N, K, slices, s);
+      } else if (c.K % 4 != 0)
         e = dispatch_dense<MatMs, ConvPixelPatchS, false>(fa, fb, out, N, nullptr, M, N, K, slices,
                                                           s);
       else if (c.C % 16 == 0)

@@ -83,7 +83,8 @@ void build_incore(const std::vector<Var>& vars, const std::vector<Fn>& fns, uint
 uint64_t incore_peak(const std::vector<Var>& vars, const std::vector<Fn>& fns, uint64_t chunk);
 uint64_t working_set_max(const std::vector<Var>& vars, const std::vector<Fn>& fns,
                          uint64_t chunk);
-// Chunk plan: replays the schedule through the pool (lowest free chunk first).
+// Chunk plan: replays the schedule through the pool (freed chunks reused in the order
+// they were freed; a new chunk only when none is free).
 void build_plan(const std::vector<Var>& vars, const Schedule& s, bool incore, uint64_t chunk,
                 Plan* out);
 

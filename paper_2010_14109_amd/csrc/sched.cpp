@@ -22,6 +22,7 @@
 // Budget accounting uses chunk-rounded sizes a_v = ceil(b_v / m_c) m_c
 // (eq. 1), so the chunks the pool maps never exceed the budget.
 #include <algorithm>
+#include <deque>
 #include <functional>
 #include <map>
 #include <queue>
@@ -227,19 +228,23 @@ uint64_t working_set_max(const std::vector<Var>& vars, const std::vector<Fn>& fn
   return best;
 }
 
-// Chunk cache handing out the lowest free id first.  Freed ids are always
-// below the next fresh id, so the ids in use stay below the most chunks ever
-// in use at once: the pool needs exactly that many.
+// Chunk cache handing out freed chunks in the order they were freed (least
+// recently freed first), and a chunk never used before only when none is
+// free.  A swap-in thus lands, where the budget leaves a choice, in memory
+// whose previous occupant was released longest ago, so its copy rarely waits
+// for the kernel running at the time.  Fresh ids are handed out only while the
+// queue is empty, so the ids in use stay below the most chunks ever in use at
+// once: the pool needs exactly that many.
 namespace {
 struct ChunkCache {
-  std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> freed;
+  std::deque<int32_t> freed;
   int32_t fresh = 0;
   uint64_t in_use = 0, max_in_use = 0;
   void take(uint64_t k, std::vector<int32_t>* out) {
     for (uint64_t j = 0; j < k; ++j) {
       if (!freed.empty()) {
-        out->push_back(freed.top());
-        freed.pop();
+        out->push_back(freed.front());
+        freed.pop_front();
       } else {
         out->push_back(fresh++);
       }
@@ -248,7 +253,7 @@ struct ChunkCache {
     max_in_use = std::max(max_in_use, in_use);
   }
   void give(const std::vector<int32_t>& cs) {
-    for (int32_t c : cs) freed.push(c);
+    for (int32_t c : cs) freed.push_back(c);
     in_use -= cs.size();
   }
 };
