@@ -139,8 +139,11 @@ DEFAULT_HOST_LIMIT = 56 << 30
 MAP_ENTRY_LIMIT = 40000   # chunks + mappings per plan; the process table holds ~65530
 
 
-def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None, wait="oldest"):
-    """Budget, window and (chunks, mappings) of the out-of-core and in-core plans."""
+def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None, wait="oldest",
+             budget_bytes=None):
+    """Budget, window and (chunks, mappings) of the out-of-core and in-core plans.  The budget
+    is frac * P_incore (P_incore at this chunk size), or budget_bytes when given, rounded down
+    to whole chunks and never below WS_max."""
     ctx = ooc.Context(-1)
     try:
         net.register(ctx)
@@ -148,7 +151,13 @@ def plan_for(net, frac, window_frac, chunk, policy="C", fixed=None, wait="oldest
         p_incore, ws_max = ctx.incore_peak(), ctx.working_set_max()
     finally:
         ctx.close()
-    budget = max(int(p_incore * frac) // chunk * chunk, ws_max)
+    want = int(p_incore * frac) if budget_bytes is None else budget_bytes
+    budget = want // chunk * chunk
+    if budget < ws_max:
+        if budget_bytes is not None:
+            raise ooc.OocError(ooc.E_INFEASIBLE, f"budget {budget} B is below WS_max {ws_max} B "
+                                                 f"at chunk {chunk} B")
+        budget = ws_max
     window = int(budget * window_frac)
     counts = []
     build_ms = None
@@ -333,6 +342,9 @@ def main():
     ap.add_argument("--workload", default="resnet50_b1440", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch")
     ap.add_argument("--budget-frac", type=float, default=None)
+    ap.add_argument("--budget-bytes", type=int, default=None,
+                    help="budget in bytes instead of a fraction of P_incore (the chunk-size sweep "
+                         "keeps it fixed while m_c changes)")
     ap.add_argument("--window-frac", type=float, default=0.5)
     ap.add_argument("--chunk", type=int, default=0, help="bytes; 0 = smallest that fits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -374,7 +386,7 @@ def main():
     try:
         if args.chunk:
             chunk, plan = args.chunk, plan_for(net, frac, window_frac, args.chunk, policy, fixed,
-                                               args.wait_order)
+                                               args.wait_order, args.budget_bytes)
         else:
             chunk, plan = choose_chunk(net, frac, window_frac, policy, fixed, args.wait_order)
     except ooc.OocError as e:

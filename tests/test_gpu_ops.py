@@ -151,21 +151,26 @@ def test_conv(shape):
                                            (3, 128, 3),
                                            # above 256 slices the reduction runs in two passes:
                                            # empty trailing slices, a ragged last slice group
-                                           (4096, 64, 300), (5000, 12, 513), (3000, 5, 257)])
+                                           (4096, 64, 300), (5000, 12, 513), (3000, 5, 257),
+                                           # the plain CNN's shape, slices of ragged length, 4
+                                           # and 128 channels, 1024 slices
+                                           (131072, 64, 256), (1000, 64, 2), (9999, 4, 20),
+                                           (1000, 128, 4), (524288, 64, 1024)])
 def test_batchnorm(rows, C, slices):
     X = f32(rows, C, scale=2.0) + 0.5
     g, b, G = f32(C), f32(C), f32(rows, C)
     sb = (2 + 2 * slices) * C
+    chunk = 2 << 20 if rows * C > (1 << 22) else 4096
     print(f"bn rows={rows} C={C} slices={slices}", flush=True)
     (_, _, _, Y, st) = run_fn("bn_fwd", [(X, ooc.R), (g, ooc.R), (b, ooc.R),
                                           (((rows, C), "f32"), ooc.W), (((sb,), "f32"), ooc.W)],
-                              [rows, C, slices])
+                              [rows, C, slices], chunk)
     rY, mean, invstd = ops.bn_fwd(d(X), d(g), d(b))
     assert rel_err(Y, rY) < TOL
     assert rel_err(st[:C], mean) < TOL and rel_err(st[C:2 * C], invstd) < TOL
     out = run_fn("bn_bwd", [(X, ooc.R), (g, ooc.R), (st.astype(np.float32), ooc.RW), (G, ooc.R),
                             (((rows, C), "f32"), ooc.W), (((C,), "f32"), ooc.W),
-                            (((C,), "f32"), ooc.W)], [rows, C, slices])
+                            (((C,), "f32"), ooc.W)], [rows, C, slices], chunk)
     rdX, rdg, rdb = ops.bn_bwd(d(X), d(g), d(st[:C]), d(st[C:2 * C]), d(G))
     assert rel_err(out[4], rdX) < TOL and rel_err(out[5], rdg) < TOL and rel_err(out[6], rdb) < TOL
 
