@@ -522,7 +522,8 @@ __device__ inline float comp(const float4& v, int t) {
 }
 
 // BM x BN tile; the four waves form a grid of sub-tiles made of MFMA 32 x 32
-// blocks (2 x 2 waves, or 4 x 1 / 1 x 4 for tiles 32 wide / 32 tall).
+// blocks (2 x 2 waves, or 4 x 1 for tiles 32 wide and for 256 x 64 tiles, 1 x 4 for
+// tiles 32 tall).
 // Batched problems (grid z): batch z = (zo, zi) with zi = z mod inner; operand
 // and result pointers move by zo * outer stride + zi * inner stride.  With
 // skip_upper, tiles strictly above the diagonal return without writing.
@@ -545,9 +546,9 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
                                                        int64_t N, int64_t K, int64_t k_slice,
                                                        int tiles_m, int tiles_n, Batch bt,
                                                        float* __restrict__ rowsum) {
-  // the four waves form a WM x WN grid: 4 x 1 for 32-wide tiles, 1 x 4 for
-  // 32-tall ones, else 2 x 2; each wave owns MB x NB MFMA 32 x 32 blocks
-  constexpr int WM = BN == 32 ? 4 : BM == 32 ? 1 : 2, WN = 4 / WM;
+  // the four waves form a WM x WN grid: 4 x 1 for 32-wide and 256 x 64 tiles,
+  // 1 x 4 for 32-tall ones, else 2 x 2; each wave owns MB x NB MFMA 32 x 32 blocks
+  constexpr int WM = (BN == 32 || (BM == 256 && BN == 64)) ? 4 : BM == 32 ? 1 : 2, WN = 4 / WM;
   constexpr int MB = BM / (32 * WM), NB = BN / (32 * WN);
   static_assert(MB >= 1 && NB >= 1 && MB * 32 * WM == BM && NB * 32 * WN == BN, "tile shape");
   constexpr bool kLoadsFirst = BN > 128;
@@ -705,9 +706,14 @@ hipError_t run_gemm(const LA& la, const LB& lb, float* c, OM om, int64_t slice_s
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 // Tile shape: 128 x 128, or 64 along a dimension that is at most 64 wide
-// (half of a 128-wide tile would compute zeros).
-enum Shape { S128x128, S128x64, S64x128 };
+// (half of a 128-wide tile would compute zeros).  At most 64 columns and many
+// rows (the 64-channel convolutions) take 256 x 64: each wave then owns 64 x 64
+// and one round of LDS reads feeds 16 MFMAs instead of 8 (2-3 % faster
+// measured; plain, unbatched products only, to keep the kernel count down).
+constexpr int64_t kTallRows = 65536;
+enum Shape { S128x128, S128x64, S64x128, S256x64 };
 Shape pick_shape(int64_t M, int64_t N) {
+  if (N <= 64 && M >= kTallRows) return S256x64;
   if (N <= 64 && M > 64) return S128x64;
   if (M <= 64) return S64x128;
   return S128x128;
@@ -723,6 +729,16 @@ hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const f
                     int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0, 0},
                     float* rowsum = nullptr) {
   switch (pick_shape(M, N)) {
+    case S256x64:
+      if constexpr (!BATCHED && !ROWSUM) {
+        LAT<256> a{};
+        LBT<64> b{};
+        fa(a);
+        fb(b);
+        return run_gemm<256, 64, LAT<256>, LBT<64>, OM, BIAS, false, false>(
+            a, b, c, om, slice_stride, bias, M, N, K, slices, s);
+      }
+      [[fallthrough]];
     case S128x64: {
       LAT<128> a{};
       LBT<64> b{};
@@ -848,6 +864,33 @@ hipError_t slice_sum(const float* part, float* out, int64_t n, int64_t slices, h
   hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((n + SUM_J - 1) / SUM_J)), dim3(256), 0, s,
                      part, out, n, slices);
   return hipGetLastError();
+}
+
+// The input-gradient pixels of a stride class that no filter tap reaches are
+// zeros (a 1 x 1 filter with stride 2 reaches one class of four).  Rows
+// m0 .. m0 + rows of the class, q = C / 4 float4 each; rows * q < 2^31.
+__global__ __launch_bounds__(256) void class_zero_kernel(float* __restrict__ dx, ClassOut om,
+                                                         int64_t m0, int rows, int q,
+                                                         FastDiv dq) {
+  const int n = rows * q;
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) {
+    const int r = dq.div(i);
+    *reinterpret_cast<float4*>(dx + om.row(m0 + r) + 4 * (i - r * q)) = make_float4(0, 0, 0, 0);
+  }
+}
+
+hipError_t class_zero(float* dx, const ClassOut& om, int64_t M, int64_t C, hipStream_t s) {
+  const int64_t q = C / 4;
+  const int64_t per = std::max<int64_t>(1, (int64_t(1) << 30) / q);   // rows per launch
+  for (int64_t m0 = 0; m0 < M; m0 += per) {
+    const int64_t rows = std::min(per, M - m0);
+    const int64_t blocks = std::min<int64_t>((rows * q + 255) / 256, 16384);
+    hipLaunchKernelGGL(class_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, dx, om, m0,
+                       (int)rows, (int)q, FastDiv::make(q));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace
@@ -993,7 +1036,9 @@ hipError_t conv_bwd_x(const float* W, const float* dY, float* dX, const ConvShap
       const ClassOut om{(int)c.H, (int)c.W, (int)c.C, (int)st, (int)ph, (int)pw,
                         FastDiv::make(Wc), FastDiv::make(Hc * Wc)};
       hipError_t e;
-      if (c.K % 32 == 0)
+      if (K == 0 && aligned16(dX))   // no tap: a plain fill instead of an empty product
+        e = class_zero(dX, om, M, c.C, s);
+      else if (c.K % 32 == 0)
         e = dispatch<ConvGradTapT, ConvFilterTapT, false>(fa, fb, dX, om, 0, nullptr, M, N, K, 1,
                                                           s);
       else if (c.K % 4 == 0)
@@ -1086,6 +1131,7 @@ int64_t wgrad_slices(int64_t M, int64_t N, int64_t K, int64_t C) {
     tiles = 1, resident = C % 4 == 0 ? 5 : 4;
   } else {
     switch (pick_shape(M, N)) {
+      case S256x64: tiles = (M + 255) / 256, resident = 2; break;
       case S128x64: tiles = (M + 127) / 128, resident = 3; break;
       case S64x128: tiles = (N + 127) / 128, resident = 3; break;
       default: tiles = ((M + 127) / 128) * ((N + 127) / 128), resident = 2;

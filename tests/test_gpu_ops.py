@@ -120,6 +120,12 @@ CONVS = [  # N, H, W, C, K, k, stride, pad
     (2, 10, 9, 3, 64, 3, 1, 1),
     (2, 6, 5, 64, 64, 1, 1, 0),
     (1, 6, 6, 128, 32, 3, 1, 1),
+    # at least 65536 output rows and 64 columns: 256 x 64 tiles with a ragged last tile
+    # (66825 rows), for the 3 x 3 forward and input gradient, the stride-2 classes and the
+    # pointwise (dense) path
+    (33, 45, 45, 64, 64, 3, 1, 1),
+    (33, 90, 90, 64, 64, 3, 2, 1),
+    (33, 45, 45, 64, 64, 1, 1, 0),
 ]
 
 
@@ -144,6 +150,44 @@ def test_conv(shape):
         (_, _, dX) = run_fn("conv_bwd_x", [(Wt, ooc.R), (G, ooc.R),
                                             (((N, H, Wd, C), "f32"), ooc.W)], a)
         assert rel_err(dX, ops.conv_bwd_x(d(Wt), d(G), X.shape, st, pd)) < TOL
+
+
+def test_conv_bwd_x_fills_unreached_classes():
+    """A 1 x 1 stride-2 input gradient reaches one stride class of four; the other pixels must
+    be written as zeros, not left as they were.  Out of core at the smallest budget the output
+    is mapped onto chunks that held the ones a ReLU wrote just before."""
+    N, H, Wd, C, K = 2, 10, 7, 64, 32
+    P, Q = 5, 4
+    n = N * H * Wd * C
+    Wt, G = f32(K, 1, 1, C), f32(N, P, Q, K)
+    ctx = ooc.Context(0)
+    try:
+        x1 = ctx.add_var(n * 4, ooc.INPUT)
+        t = ctx.add_var(n * 4, ooc.TEMP)
+        w = ctx.add_var(Wt.nbytes, ooc.INPUT)
+        g = ctx.add_var(G.nbytes, ooc.INPUT)
+        dx = ctx.add_var(n * 4, ooc.OUTPUT)
+        ctx.add_fn("relu_fwd", [x1, t], [ooc.R, ooc.W], [n])
+        ctx.add_fn("conv_bwd_x", [w, g, dx], [ooc.R, ooc.R, ooc.W],
+                   [N, H, Wd, C, K, 1, 1, 2, 0, P, Q])
+        ctx.set_chunk(4096)
+        ctx.set_budget(ctx.working_set_max())
+        ctx.build_schedule()
+        held = {iv["var"]: set(iv["chunks"]) for iv in ctx.plan()}
+        assert held[dx] & (held[x1] | held[t]), "the output must reuse chunks that held ones"
+        ctx.prepare()
+        ctx.host_view(x1, np.float32)[...] = 1.0
+        ctx.host_view(w, np.float32)[...] = Wt.reshape(-1)
+        ctx.host_view(g, np.float32)[...] = G.reshape(-1)
+        ctx.upload()
+        ctx.step(0.0, 0.0)
+        ctx.download()
+        got = np.array(ctx.host_view(dx, np.float32)).reshape(N, H, Wd, C)
+    finally:
+        ctx.close()
+    ref = ops.conv_bwd_x(d(Wt), d(G), (N, H, Wd, C), 2, 0)
+    assert np.all(got[:, 1::2] == 0) and np.all(got[:, :, 1::2] == 0)
+    assert rel_err(got, ref) < TOL
 
 
 # ---------------------------------------------------------------- BatchNorm
