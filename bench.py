@@ -101,6 +101,19 @@ def sgd_bytes(net, j):
     return total if mom in (0, 1) else 0
 
 
+def algorithmic_bytes(net, op):
+    """Mean compulsory bytes per launch of ``op``: every operand read once and every result
+    written once (an input gradient reads the filter and the output gradient and writes the
+    input gradient).  Split-K partial sums (``.part``) are not compulsory and are left out."""
+    tot, n = 0, 0
+    for j, o in enumerate(net.fn_ops):
+        if o == op:
+            tot += sum(net.var_bytes[v] for v, _ in net.fn_vars[j]
+                       if not net.names[v].endswith(".part"))
+            n += 1
+    return round(tot / n) if n else None
+
+
 def measured_traffic(net, op):
     """Mean HBM bytes per launch of ``op`` in this network, from the rocprofv3 FETCH_SIZE /
     WRITE_SIZE measurements recorded under profiles/ (lines ``traffic: op=... key=<attrs>
@@ -438,7 +451,9 @@ def main():
         roof = {"bound": "hbm", "achieved": round(dom["rate"], 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(dom["rate"] / PEAK_HBM_GBS, 4), "traffic": None}
     roof["traffic"] = measured_traffic(net, dom_op)
-    roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)"
+    roof["traffic_unit"] = ("bytes per launch fetched and written back by the L2 caches (rocprofv3 "
+                            "FETCH_SIZE + WRITE_SIZE, calibrated; last-level-cache hits included)")
+    roof["algorithmic_bytes"] = algorithmic_bytes(net, dom_op)
     roof["kernel"] = dom_op
     roof["launches_per_step"] = dom["launches"]
     roof["avg_launch_ms"] = round(dom["ms"] / max(1, dom["launches"]), 4)

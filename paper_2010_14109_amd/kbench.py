@@ -10,10 +10,16 @@ statistics and counters.  CASE is ``op:n1,n2,...``:
 * ``relu_fwd : n``  (reads 4 n bytes, writes 4 n bytes: the calibration kernel)
 * ``bn_fwd | bn_bwd : rows,C``  (training-mode batch normalisation over ``rows`` NHWC pixels)
 
-``python -m paper_2010_14109_amd.kbench --traffic FETCH_DIR WRITE_DIR CAL_DIR``
+``python -m paper_2010_14109_amd.kbench --traffic FETCH_DIR WRITE_DIR CAL_DIR [CALLS]``
 turns ``rocprofv3 --pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` output of a case
-(FETCH_DIR, WRITE_DIR) into HBM bytes per call, scaling each counter by what
-it reads for ``relu_fwd:268435456`` (CAL_DIR holds both counters of that run).
+(FETCH_DIR, WRITE_DIR) into bytes per call, scaling each counter by what it
+reads for ``relu_fwd:268435456`` (CAL_DIR holds both counters of that run).
+CALLS is how many calls the profiled run made (REPS + 1: one warm-up); a
+function may launch one kernel several times per call (one GEMM per stride
+class of an input gradient), so the bytes of all its dispatches are added and
+divided by CALLS.  Without CALLS every kernel counts once per call.  The
+counters see what the L2 caches fetch and write back: reads served by the
+256 MB last-level cache count too.
 """
 
 from __future__ import annotations
@@ -105,8 +111,9 @@ def run(spec, reps=20):
         ctx.close()
 
 
-def _counters(d):
-    """{kernel: {counter: mean per dispatch}} of the rocprofv3 csv files under d."""
+def _counters(d, calls=None):
+    """{kernel: {counter: value per call}} of the rocprofv3 csv files under d: the sum over
+    the kernel's dispatches / calls, or the mean per dispatch when calls is None."""
     acc = defaultdict(lambda: defaultdict(list))
     for f in glob.glob(os.path.join(d, "**", "*_counter_collection.csv"), recursive=True):
         with open(f) as fh:
@@ -114,18 +121,18 @@ def _counters(d):
                 name = r["Kernel_Name"].replace("ooc::(anonymous namespace)::", "")
                 name = name.replace("void ", "").split("(")[0]
                 acc[name][r["Counter_Name"]].append(float(r["Counter_Value"]))
-    return {k: {c: sum(x) / len(x) for c, x in v.items()} for k, v in acc.items()}
+    return {k: {c: sum(x) / (calls or len(x)) for c, x in v.items()} for k, v in acc.items()}
 
 
-def traffic(fetch_dir, write_dir, cal_dir):
-    """Calibrated HBM bytes per call: {kernel: (fetch_bytes, write_bytes)} and the scales."""
+def traffic(fetch_dir, write_dir, cal_dir, calls=None):
+    """Calibrated bytes per call: {kernel: (fetch_bytes, write_bytes)} and the scales."""
     cal = _counters(cal_dir)
     ew = [v for k, v in cal.items() if k.startswith("ew_kernel")]
     if len(ew) != 1:
         raise SystemExit(f"calibration run {cal_dir} must hold exactly one ReLU kernel")
     ref = CAL_N * 4
     fs, ws = ref / (ew[0]["FETCH_SIZE"] * 1024), ref / (ew[0]["WRITE_SIZE"] * 1024)
-    f, w = _counters(fetch_dir), _counters(write_dir)
+    f, w = _counters(fetch_dir, calls), _counters(write_dir, calls)
     out = {k: (f[k]["FETCH_SIZE"] * 1024 * fs, w.get(k, {}).get("WRITE_SIZE", 0.0) * 1024 * ws)
            for k in f}
     return out, fs, ws
@@ -133,7 +140,8 @@ def traffic(fetch_dir, write_dir, cal_dir):
 
 def main(argv):
     if argv and argv[0] == "--traffic":
-        res, fs, ws = traffic(*argv[1:4])
+        calls = int(argv[4]) if len(argv) > 4 else None
+        res, fs, ws = traffic(*argv[1:4], calls=calls)
         print(f"scales: FETCH_SIZE x {fs:.4f}, WRITE_SIZE x {ws:.4f}")
         total = 0.0
         for k, (fb, wb) in res.items():
