@@ -2,6 +2,7 @@
 (no GPU)."""
 
 import math
+import os
 import random
 
 import pytest
@@ -70,3 +71,44 @@ def test_slice_rule_rejects_bad_requests():
         with pytest.raises(ooc.OocError) as e:
             ooc.wgrad_slices(op, attrs)
         assert e.value.status == ooc.E_INVALID and "ooc_wgrad_slices" in e.value.message
+
+
+def _counter_csv(path, rows):
+    """A rocprofv3 counter-collection file: rows of (dispatch id, kernel name, counter, value)."""
+    import csv
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "p_counter_collection.csv"), "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for r in rows:
+            w.writerow(r)
+
+
+def test_traffic_adds_every_dispatch_of_a_call(tmp_path):
+    """A function that launches one kernel several times per call (the stride classes of an
+    input gradient) must count all of them: bytes per call = all dispatches / calls.  The
+    calibration ReLU moves 1 GiB each way; its counters here read half of it (scale 2)."""
+    gib_kib = (kbench.CAL_N * 4) // 1024
+    cal = tmp_path / "cal"
+    _counter_csv(str(cal / "fetch"), [(1, "void ooc::(anonymous namespace)::ew_kernel<0>(x)",
+                                       "FETCH_SIZE", gib_kib / 2)])
+    _counter_csv(str(cal / "write"), [(1, "void ooc::(anonymous namespace)::ew_kernel<0>(x)",
+                                       "WRITE_SIZE", gib_kib)])
+    calls, per_call = 3, 4
+    rows_f, rows_w = [], []
+    for d in range(calls * per_call):
+        rows_f.append((d, "void ooc::(anonymous namespace)::gemm_kernel<1>(x)", "FETCH_SIZE", 100.0))
+        rows_w.append((d, "void ooc::(anonymous namespace)::gemm_kernel<1>(x)", "WRITE_SIZE", 10.0))
+    for d in range(calls):
+        rows_f.append((100 + d, "ooc::(anonymous namespace)::class_zero_kernel(y)", "FETCH_SIZE", 0.0))
+        rows_w.append((100 + d, "ooc::(anonymous namespace)::class_zero_kernel(y)", "WRITE_SIZE", 7.0))
+    _counter_csv(str(tmp_path / "f"), rows_f)
+    _counter_csv(str(tmp_path / "w"), rows_w)
+    res, fs, ws = kbench.traffic(str(tmp_path / "f"), str(tmp_path / "w"), str(cal), calls=calls)
+    assert fs == pytest.approx(2.0) and ws == pytest.approx(1.0)
+    gemm, fill = res["gemm_kernel<1>"], res["class_zero_kernel"]
+    assert gemm == pytest.approx((per_call * 100 * 1024 * 2.0, per_call * 10 * 1024 * 1.0))
+    assert fill == pytest.approx((0.0, 7 * 1024 * 1.0))
+    # without the call count every kernel counts once per call (the mean per dispatch)
+    res1, _, _ = kbench.traffic(str(tmp_path / "f"), str(tmp_path / "w"), str(cal))
+    assert res1["gemm_kernel<1>"] == pytest.approx((100 * 1024 * 2.0, 10 * 1024 * 1.0))
