@@ -39,6 +39,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -538,6 +539,77 @@ __device__ inline void shift(L& l, int64_t d) {
   l.p += d;
 }
 
+// The wave grid of a BM x BN tile: the four waves form WM x WN, 4 x 1 for
+// 32-wide and 256 x 64 tiles, 1 x 4 for 32-tall ones, else 2 x 2; each wave
+// owns MB x NB MFMA 32 x 32 blocks.
+template <int BM, int BN>
+struct WaveGrid {
+  static constexpr int WM = (BN == 32 || (BM == 256 && BN == 64)) ? 4 : BM == 32 ? 1 : 2;
+  static constexpr int WN = 4 / WM;
+  static constexpr int MB = BM / (32 * WM), NB = BN / (32 * WN);
+  static_assert(MB >= 1 && NB >= 1 && MB * 32 * WM == BM && NB * 32 * WN == BN, "tile shape");
+};
+
+// One K tile from LDS into the accumulators: four k steps of 8 per half-wave,
+// each a round of LDS reads feeding MB x NB x 4 MFMAs.
+template <int BM, int BN, class LA, class LB, int MB, int NB>
+__device__ __forceinline__ void mma_ktile(floatx16 (&acc)[MB][NB], const float* A, const float* B,
+                                          int wm, int wn, int half, int li) {
+  using G = WaveGrid<BM, BN>;
+  static_assert(MB == G::MB && NB == G::NB, "accumulator blocks");
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int kq = half * 16 + 4 * j;
+    float4 a[G::MB], b[G::NB];
+#pragma unroll
+    for (int mb = 0; mb < G::MB; ++mb) a[mb] = read_op<LA>(A, wm * (BM / G::WM) + mb * 32 + li, kq);
+#pragma unroll
+    for (int nb = 0; nb < G::NB; ++nb) b[nb] = read_op<LB>(B, wn * (BN / G::WN) + nb * 32 + li, kq);
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int mb = 0; mb < G::MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < G::NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a[mb], s), comp(b[nb], s),
+                                                            acc[mb][nb], 0, 0, 0);
+  }
+}
+
+// The accumulators of the tile at (m0, n0) into C (plus the column's bias).
+template <int BM, int BN, class OM, bool BIAS, int MB, int NB>
+__device__ __forceinline__ void store_tile(const floatx16 (&acc)[MB][NB], float* out, const OM& om,
+                                           const float* bias, int64_t m0, int64_t n0, int64_t M,
+                                           int64_t N, int wm, int wn, int half, int li) {
+  using G = WaveGrid<BM, BN>;
+  static_assert(MB == G::MB && NB == G::NB, "accumulator blocks");
+#pragma unroll
+  for (int mb = 0; mb < G::MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < G::NB; ++nb) {
+      const int64_t col = n0 + wn * (BN / G::WN) + nb * 32 + li;
+      if (col >= N) continue;
+      const float bv = BIAS ? bias[col] : 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * (BM / G::WM) + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (row < M) out[om.row(row) + col] = acc[mb][nb][r] + bv;
+      }
+    }
+}
+
+// Issue the next tile's global loads one per two MFMAs from the start of a K
+// tile's body, so that the MFMAs cover their latency; left alone, the
+// scheduler sinks them next to the LDS stores that consume them.
+template <int NLOADS>
+__device__ __forceinline__ void interleave_loads() {
+#pragma unroll
+  for (int g = 0; g < NLOADS; ++g) {
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // one global load
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // two MFMAs
+  }
+}
+
 // ROWSUM: rowsum[slice][m] = sum over this slice's k of A[m][k]
 template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED, bool ROWSUM>
 __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __restrict__ c, OM om,
@@ -546,11 +618,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
                                                        int64_t N, int64_t K, int64_t k_slice,
                                                        int tiles_m, int tiles_n, Batch bt,
                                                        float* __restrict__ rowsum) {
-  // the four waves form a WM x WN grid: 4 x 1 for 32-wide and 256 x 64 tiles,
-  // 1 x 4 for 32-tall ones, else 2 x 2; each wave owns MB x NB MFMA 32 x 32 blocks
-  constexpr int WM = (BN == 32 || (BM == 256 && BN == 64)) ? 4 : BM == 32 ? 1 : 2, WN = 4 / WM;
-  constexpr int MB = BM / (32 * WM), NB = BN / (32 * WN);
-  static_assert(MB >= 1 && NB >= 1 && MB * 32 * WM == BM && NB * 32 * WN == BN, "tile shape");
+  constexpr int WM = WaveGrid<BM, BN>::WM, MB = WaveGrid<BM, BN>::MB, NB = WaveGrid<BM, BN>::NB;
   constexpr bool kLoadsFirst = BN > 128;
   // Workgroup (tile, slice, batch) from an XCD-aware order: the hardware hands
   // linear workgroup h to XCD h mod 8, so logical ids are laid out so that each
@@ -624,23 +692,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
     if constexpr (kLoadsFirst) __builtin_amdgcn_sched_barrier(0);
     const float* A = As[buf];
     const float* B = Bs[buf];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int kq = half * 16 + 4 * j;
-      float4 a[MB], b[NB];
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) a[mb] = read_op<LA>(A, wm * (BM / WM) + mb * 32 + li, kq);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) b[nb] = read_op<LB>(B, wn * (BN / WN) + nb * 32 + li, kq);
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a[mb], s), comp(b[nb], s),
-                                                              acc[mb][nb], 0, 0, 0);
-    }
+    mma_ktile<BM, BN, LA, LB>(acc, A, B, wm, wn, half, li);
     if constexpr (ROWSUM) {
       if (sums) {
 #pragma unroll
@@ -650,16 +702,7 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
         }
       }
     }
-    // Issue the next tile's global loads one per two MFMAs from the start of
-    // the body, so that the MFMAs cover their latency; left alone, the
-    // scheduler sinks them next to the LDS stores that consume them.
-    if constexpr (!kLoadsFirst) {
-#pragma unroll
-      for (int g = 0; g < LA::kN + LB::kN; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // one global load
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // two MFMAs
-      }
-    }
+    if constexpr (!kLoadsFirst) interleave_loads<LA::kN + LB::kN>();
     LA::store(As[buf ^ 1], ra);
     LB::store(Bs[buf ^ 1], rb);
     __syncthreads();
@@ -667,21 +710,110 @@ __global__ __launch_bounds__(THREADS) void gemm_kernel(LA la, LB lb, float* __re
   }
 
   if (sums && m0 + threadIdx.x < M) rowsum[slice * M + m0 + threadIdx.x] = rs;
-  float* out = c + slice * slice_stride;
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int64_t col = n0 + wn * (BN / WN) + nb * 32 + li;
-      if (col >= N) continue;
-      const float bv = BIAS ? bias[col] : 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * (BM / WM) + mb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (row < M) out[om.row(row) + col] = acc[mb][nb][r] + bv;
-      }
-    }
+  store_tile<BM, BN, OM, BIAS>(acc, c + slice * slice_stride, om, bias, m0, n0, M, N, wm, wn, half,
+                               li);
 }
+
+// Persistent form for short reductions of the dense loaders (one slice, no
+// batch, no row sums; chosen below): a workgroup walks the tiles L, L + G,
+// L + 2G, ... and, while it multiplies the last K tile of one output tile,
+// already loads the first K tile of its next one, so that the next tile's
+// loads and this tile's stores are in flight together.  With K of 64 or 128 a
+// tile has only two or four K tiles, and the one-tile-per-workgroup form spends
+// much of each workgroup's life in its first load and its stores.  Results are
+// those of gemm_kernel bit for bit (same K order per output).
+template <int BM, int BN, class LA, class LB, class OM, bool BIAS>
+__global__ __launch_bounds__(THREADS) void gemm_persistent(LA la, LB lb, float* __restrict__ c,
+                                                           OM om, const float* __restrict__ bias,
+                                                           int64_t M, int64_t N, int64_t K,
+                                                           int tiles_m, int tiles_n) {
+  constexpr int WM = WaveGrid<BM, BN>::WM, MB = WaveGrid<BM, BN>::MB, NB = WaveGrid<BM, BN>::NB;
+  static_assert(BN <= 128, "loads interleaved with the MFMAs, as gemm_kernel does up to 128 wide");
+  // the same XCD-aware logical order as gemm_kernel: each XCD's workgroups take
+  // one contiguous run of tiles in every round
+  const uint32_t G = gridDim.x, h = blockIdx.x;
+  const uint32_t q = G / kXcds, rem = G % kXcds, xcd = h % kXcds, local = h / kXcds;
+  const uint32_t L = xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
+  const int n_tiles = tiles_m * tiles_n;
+  int t = (int)L;
+  if (t >= n_tiles) return;   // the whole workgroup leaves together
+  __shared__ __attribute__((aligned(16))) float As[2][LA::kLds];
+  __shared__ __attribute__((aligned(16))) float Bs[2][LB::kLds];
+  const int group = 8;        // grouped tile order, as in gemm_kernel
+  const int per_group = group * tiles_n;
+  auto origin = [&](int tt, int64_t& m0, int64_t& n0) {
+    const int g = tt / per_group;
+    const int first_m = g * group;
+    const int gsize = min(tiles_m - first_m, group);
+    m0 = (int64_t)(first_m + (tt % per_group) % gsize) * BM;
+    n0 = (int64_t)((tt % per_group) / gsize) * BN;
+  };
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int half = lane >> 5;
+  const int li = lane & 31;
+  int64_t m0, n0;
+  origin(t, m0, n0);
+  la.init(m0, M);
+  lb.init(n0, N);
+  float4 ra[LA::kN], rb[LB::kN];
+  la.fetch(0, K, ra);
+  lb.fetch(0, K, rb);
+  LA::store(As[0], ra);
+  LB::store(Bs[0], rb);
+  __syncthreads();
+  int buf = 0;
+  while (true) {
+    floatx16 acc[MB][NB];
+#pragma unroll
+    for (int a = 0; a < MB; ++a)
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+    for (int64_t k0 = 0; k0 + BK < K; k0 += BK) {
+      la.fetch(k0 + BK, K, ra);
+      lb.fetch(k0 + BK, K, rb);
+      mma_ktile<BM, BN, LA, LB>(acc, As[buf], Bs[buf], wm, wn, half, li);
+      interleave_loads<LA::kN + LB::kN>();
+      LA::store(As[buf ^ 1], ra);
+      LB::store(Bs[buf ^ 1], rb);
+      __syncthreads();
+      buf ^= 1;
+    }
+    // the last K tile; the next output tile's first K tile is loaded meanwhile
+    // into the other buffer, which no wave reads until the barrier below
+    const int tn = t + (int)G;
+    const bool more = tn < n_tiles;   // uniform over the workgroup
+    int64_t m1 = 0, n1 = 0;
+    if (more) {
+      origin(tn, m1, n1);
+      la.init(m1, M);
+      lb.init(n1, N);
+      la.fetch(0, K, ra);
+      lb.fetch(0, K, rb);
+    }
+    mma_ktile<BM, BN, LA, LB>(acc, As[buf], Bs[buf], wm, wn, half, li);
+    if (more) {
+      LA::store(As[buf ^ 1], ra);
+      LB::store(Bs[buf ^ 1], rb);
+    }
+    store_tile<BM, BN, OM, BIAS>(acc, c, om, bias, m0, n0, M, N, wm, wn, half, li);
+    if (!more) break;
+    __syncthreads();
+    buf ^= 1;
+    t = tn;
+    m0 = m1;
+    n0 = n1;
+  }
+}
+
+// Loaders the persistent form is used with: the plain matrix views.
+template <class L> struct DenseView : std::false_type {};
+template <int E, bool V> struct DenseView<MatK<E, V>> : std::true_type {};
+template <int E, bool V> struct DenseView<MatM<E, V>> : std::true_type {};
+constexpr int64_t kShortK = 128;   // reductions at most this long run persistent
 
 template <int BM, int BN, class LA, class LB, class OM, bool BIAS, bool BATCHED = false,
           bool ROWSUM = false>
@@ -695,8 +827,29 @@ hipError_t run_gemm(const LA& la, const LB& lb, float* c, OM om, int64_t slice_s
     return hipErrorInvalidValue;
   int64_t k_slice = (K + slices - 1) / slices;
   k_slice = (k_slice + BK - 1) / BK * BK;
-  dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices, (unsigned)batches);
   if (ROWSUM != (rowsum != nullptr)) return hipErrorInvalidValue;
+  if constexpr (!BATCHED && !ROWSUM && DenseView<LA>::value && DenseView<LB>::value) {
+    if (slices == 1 && K <= kShortK) {
+      // one workgroup per resident slot (the occupancy query counts LDS and registers)
+      auto kern = gemm_persistent<BM, BN, LA, LB, OM, BIAS>;
+      static const int64_t slots = [&] {   // initialised once, thread-safe
+        int o = 0, n = 0, dev = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, kern, THREADS, 0) != hipSuccess ||
+            o < 1)
+          o = 1;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n < 1)
+          n = 256;
+        return (int64_t)o * n;
+      }();
+      const int64_t G = std::min<int64_t>(tiles_m * tiles_n, slots);
+      hipLaunchKernelGGL(kern, dim3((unsigned)G), dim3(THREADS), 0, s, la, lb, c, om, bias, M, N,
+                         K, (int)tiles_m, (int)tiles_n);
+      return hipGetLastError();
+    }
+  }
+  dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)slices, (unsigned)batches);
   hipLaunchKernelGGL((gemm_kernel<BM, BN, LA, LB, OM, BIAS, BATCHED, ROWSUM>), grid, dim3(THREADS), 0, s,
                      la, lb, c, om, slice_stride, bias, M, N, K, k_slice, (int)tiles_m,
                      (int)tiles_n, bt, rowsum);
