@@ -274,8 +274,14 @@ static ooc_status warm_copy_streams(ooc_ctx* ctx) {
   constexpr size_t kWarm = 8u << 20;
   void* h = nullptr;
   void* d = nullptr;
-  hipError_t e = hipHostMalloc(&h, kWarm, hipHostMallocDefault);
-  if (e == hipSuccess) e = hipMalloc(&d, kWarm);
+  // best effort: with no 8 MiB to spare on either side the steps simply pay the delay
+  if (hipHostMalloc(&h, kWarm, hipHostMallocDefault) != hipSuccess ||
+      hipMalloc(&d, kWarm) != hipSuccess) {
+    (void)hipGetLastError();
+    if (h) (void)hipHostFree(h);
+    return OOC_OK;
+  }
+  hipError_t e = hipSuccess;
   for (hipStream_t s : {ctx->hs, ctx->ds, ctx->ss}) {
     if (e == hipSuccess) e = hipMemcpyAsync(d, h, kWarm, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemcpyAsync(h, d, kWarm, hipMemcpyDeviceToHost, s);
