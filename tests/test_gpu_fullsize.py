@@ -49,7 +49,7 @@ def derived_check(spec, loss, outs):
 def bench_config(name, **over):
     spec = synth.workload(name, **over)
     net = netdef.Net(spec)
-    chunk, plan = bench.choose_chunk(net, synth.budget_fraction(name), 0.5)
+    chunk, plan = bench.choose_chunk(net, synth.budget_fraction(name), bench.window_fraction(name))
     return spec, chunk, plan
 
 
@@ -75,7 +75,7 @@ def test_resnet50_against_oracle(batch, hw):
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
     net = netdef.Net(spec, keep_grads=True)
-    chunk, plan = bench.choose_chunk(net, 1 / 7.5, 0.5)
+    chunk, plan = bench.choose_chunk(net, 1 / 7.5, bench.DEFAULT_WINDOW_FRAC)
     print(f"resnet50 b{batch} {hw}x{hw}: budget {plan['budget']} chunk {chunk}", flush=True)
     loss, outs, st = run_net(spec, x, labels, params, budget=plan["budget"],
                              window=plan["window"], chunk=chunk)

@@ -107,8 +107,9 @@ def test_full_size_mlp_matches_oracle():
 
 
 def test_full_size_cnn_matches_oracle():
-    """The plain CNN as the bench line runs it (batch 128, B = P_incore / 2, 2 MiB chunks, W = B/2,
-    policy C) against the float64 oracle, and bit-identical to the same kernels in-core.
+    """The plain CNN at the bench's batch and budget (batch 128, B = P_incore / 2, 2 MiB chunks,
+    the library's default W = B/2, policy C) against the float64 oracle, and bit-identical to
+    the same kernels in-core.
 
     At this size fp32 evaluation is not well conditioned (ReLU-mask decisions near zero flip
     between fp32 and fp64, and the batch-norm shift gradients are sums with heavy cancellation),
@@ -154,10 +155,10 @@ FULL = [("resnet50_b256", {}, 4, None), ("transformer", {"batch": 24}, 8, None),
                          ids=[synth.workload(f[0], **f[1])["name"] for f in FULL])
 def test_full_size_out_of_core_equals_in_core(name, kw, chunk_mib, limit_gib):
     """At the full sizes and budgets the bench runs, where the oracle is too slow: one
-    out-of-core step (W = B/2, policy C) leaves the loss and every updated parameter and state
-    bit-identical to the in-core step, and the device pool stays within the budget.  ResNet-50
-    at batch 1440 with B = P/7.5 and the transformer at batch 64 with B = 0.2 P run with part
-    of their host homes pageable."""
+    out-of-core step (the library's default W = B/2, policy C) leaves the loss and every updated
+    parameter and state bit-identical to the in-core step, and the device pool stays within the
+    budget. ResNet-50 at batch 1440 with B = P/7.5 and the transformer at batch 64 with B = 0.2
+    P run with part of their host homes pageable."""
     spec = synth.workload(name, **kw)
     x, labels = synth.make_inputs(spec, 0)
     params = synth.make_params(spec, 1)
