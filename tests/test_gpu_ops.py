@@ -75,23 +75,29 @@ def d(a):
 # ---------------------------------------------------------------- dense
 @pytest.mark.parametrize("M,K,N,S", [(300, 200, 130, 1), (5, 147, 10, 1), (256, 1024, 1024, 1),
                                      (1, 3, 1, 1), (3000, 200, 132, 3), (2500, 64, 1000, 2),
-                                     (4100, 36, 7, 5), (100, 40, 20, 3)])
+                                     (4100, 36, 7, 5), (100, 40, 20, 3),
+                                     # reductions of at most 128 (the persistent form) over more
+                                     # tiles than workgroups, ragged rows and columns: forward,
+                                     # input gradient, and a scalar-loader forward on 256 x 64
+                                     (70001, 100, 130, 1), (70001, 130, 100, 1),
+                                     (200001, 37, 45, 1)])
 def test_linear(M, K, N, S):
     """S > 1 cuts the rows of the weight gradient into slices (the last one of
     (100, 40, 20, 3) is empty)."""
     X, Wt, b, G = f32(M, K), f32(N, K), f32(N), f32(M, N)
     print(f"linear M={M} K={K} N={N} slices={S}", flush=True)
+    chunk = 2 << 20 if M * max(K, N) > (1 << 22) else 4096
     (_, _, _, Y) = run_fn("linear_fwd", [(X, ooc.R), (Wt, ooc.R), (b, ooc.R),
-                                          (((M, N), "f32"), ooc.W)], [M, K, N])
+                                          (((M, N), "f32"), ooc.W)], [M, K, N], chunk)
     assert rel_err(Y, ops.linear_fwd(d(X), d(Wt), d(b))) < TOL
     wargs = [(X, ooc.R), (G, ooc.R), (((N, K), "f32"), ooc.W), (((N,), "f32"), ooc.W)]
     if S > 1:
         wargs.append((((S * (N * K + N),), "f32"), ooc.W))
-    dW, db = run_fn("linear_bwd_w", wargs, [M, K, N, S])[2:4]
+    dW, db = run_fn("linear_bwd_w", wargs, [M, K, N, S], chunk)[2:4]
     rdW, rdb = ops.linear_bwd_w(d(X), d(G))
     assert rel_err(dW, rdW) < TOL and rel_err(db, rdb) < TOL
     (_, _, dX) = run_fn("linear_bwd_x", [(Wt, ooc.R), (G, ooc.R), (((M, K), "f32"), ooc.W)],
-                        [M, K, N])
+                        [M, K, N], chunk)
     assert rel_err(dX, ops.linear_bwd_x(d(Wt), d(G))) < TOL
 
 
