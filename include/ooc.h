@@ -408,7 +408,11 @@ ooc_status ooc_plan_chunks(const ooc_ctx *ctx, int32_t *buf, uint64_t cap, uint6
  * and the events.  All mapping happens here, once; a step maps nothing.
  * Each chunk and each mapping of a chunk takes one entry of the process's
  * memory-map table (vm.max_map_count, typically 65530): a plan needing more
- * than the entries left returns OOC_E_UNSUPPORTED (choose a larger chunk). */
+ * than the entries left returns OOC_E_UNSUPPORTED (choose a larger chunk).
+ * Out of core it also makes one 8 MiB copy each way on every copy stream, in
+ * a temporary device and pinned buffer freed before it returns (skipped when
+ * they cannot be allocated): the runtime sets a stream up for the DMA engines
+ * at its first large copy, which blocks the caller for several milliseconds. */
 ooc_status ooc_prepare(ooc_ctx *ctx);
 
 /* Pinned host slot of a host-backed variable (INPUT, PARAM, STATE, OUTPUT;
