@@ -85,11 +85,12 @@ def fn_work(op, attrs):
         N, H, W, C = a
         return "byte", 20 * N * H * W * C
     if op in ("attention_fwd", "attention_bwd"):
-        # q k^T and P v forward, four products of the same size backward; causal
-        # attention needs only the T (T + 1) / 2 entries on and below the diagonal
+        # q k^T and P v forward; backward, q k^T again (P is recomputed) and four products
+        # of the same size; causal attention needs only the T (T + 1) / 2 entries on and
+        # below the diagonal
         B, T, H, dh, causal = a[:5]
         pairs = T * (T + 1) // 2 if causal else T * T
-        return "flop", (2 if op == "attention_fwd" else 4) * 2 * B * H * pairs * dh
+        return "flop", (2 if op == "attention_fwd" else 5) * 2 * B * H * pairs * dh
     return "byte", 0
 
 

@@ -148,8 +148,10 @@ enum { OOC_PRE = 0, OOC_POST = 1, OOC_END = 2 };
  *                columns h dh .. (h+1) dh of each; P[b][h] = softmax(q k^T /
  *                sqrt(dh)) with keys after the query masked when causal;
  *                Y [B T][H dh] = P v                qkv[R] P[W] Y[W]    B T H dh causal
- *  ATTENTION_BWD dqkv of the above; dS is scratch of P's size
- *                                     qkv[R] P[R] dY[R] dqkv[W] dS[W]  B T H dh causal
+ *  ATTENTION_BWD dqkv of the above.  P is not kept from the forward: the
+ *                function recomputes it into its own P (bit for bit the
+ *                forward's, same kernels); dS is scratch of P's size
+ *                                     qkv[R] P[W] dY[R] dqkv[W] dS[W]  B T H dh causal
  *  CONCAT_FWD    channel concatenation of k = 1..64 row-major tensors with
  *                the same rows: Y[r] = [X_1[r] | ... | X_k[r]]
  *                                     X_1[R] .. X_k[R] Y[W]            rows c_1 .. c_k

@@ -148,9 +148,11 @@ def run(reg, x, labels, params, state=None, dtype=np.float64):
             X, Pv, Y = vs
             env[Pv], env[Y] = ops.attention_fwd(g(X), a["B"], a["T"], a["H"], bool(a["causal"]))
         elif op == "attention_bwd":
-            X, Pv, dY, dX, dS = vs
-            env[dX] = ops.attention_bwd(g(X), g(Pv), g(dY), a["B"], a["T"], a["H"])
-            env[dS] = np.zeros_like(g(Pv))
+            # the probabilities are recomputed from q and k, not kept from the forward
+            X, Pb, dY, dX, dS = vs
+            env[Pb] = ops.attention_fwd(g(X), a["B"], a["T"], a["H"], bool(a["causal"]))[0]
+            env[dX] = ops.attention_bwd(g(X), env[Pb], g(dY), a["B"], a["T"], a["H"])
+            env[dS] = np.zeros_like(env[Pb])
         else:
             raise ValueError(f"unknown function {op}")
     return env

@@ -45,7 +45,7 @@ layernorm_bwd  X R, gamma R, stats RW, dY R, dX W, dgamma W, dbeta W
 gelu_fwd       X R, Y W
 gelu_bwd       X R, dY R, dX W            (X = the GELU input)
 attention_fwd  qkv R, P W, Y W            (P = the attention probabilities [B, H, T, T])
-attention_bwd  qkv R, P R, dY R, dqkv W, dS W   (dS = scratch of P's size)
+attention_bwd  qkv R, P' W, dY R, dqkv W, dS W  (P' = P recomputed, dS = scratch)
 concat_fwd     X_1 R, ..., X_k R, Y W          (channel concatenation)
 concat_bwd     dY R, dX_1 W, ..., dX_k W
 upsample_fwd   X R, Y W                        (nearest, factor 2)
@@ -388,8 +388,9 @@ def lower(spec, keep_grads=False, slices=None):
             Bt, T = spec["input"]
             H = L["heads"]
             dX = var(f"d:{X}@{name}", xs)
+            Pb = var(name + ".Pb", (Bt, H, T, T))
             dS = var(name + ".dS", (Bt, H, T, T))
-            fns.append(("attention_bwd", [(X, R), (name + ".P", R), (dY, R), (dX, W), (dS, W)],
+            fns.append(("attention_bwd", [(X, R), (Pb, W), (dY, R), (dX, W), (dS, W)],
                         {"B": Bt, "T": T, "H": H, "dh": d3 // 3 // H,
                          "causal": int(L["causal"])}))
             contribute(X, dX, pending)

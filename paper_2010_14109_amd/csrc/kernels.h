@@ -92,7 +92,7 @@ hipError_t gelu_fwd(const float* x, float* y, int64_t n, hipStream_t s);
 hipError_t gelu_bwd(const float* x, const float* dy, float* dx, int64_t n, hipStream_t s);
 hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_t T, int64_t H,
                          int64_t dh, bool causal, hipStream_t s);
-hipError_t attention_bwd(const float* qkv, const float* P, const float* dy, float* dqkv, float* dS,
+hipError_t attention_bwd(const float* qkv, float* P, const float* dy, float* dqkv, float* dS,
                          int64_t B, int64_t T, int64_t H, int64_t dh, bool causal, hipStream_t s);
 
 hipError_t mix(void* const* ptrs, const uint64_t* words, int nvars, uint32_t seed, hipStream_t s,

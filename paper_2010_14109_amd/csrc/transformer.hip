@@ -666,25 +666,37 @@ hipError_t gelu_bwd(const float* x, const float* dy, float* dx, int64_t n, hipSt
   return gelu_launch(x, dy, dx, n, true, s);
 }
 
-hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_t T, int64_t H,
-                         int64_t dh, bool causal, hipStream_t s) {
+// P = softmax(q k^T / sqrt(dh)) per batch and head, masked when causal
+static hipError_t attention_probs(const float* qkv, float* P, int64_t B, int64_t T, int64_t H,
+                                  int64_t dh, bool causal, hipStream_t s) {
   const int64_t d = H * dh, d3 = 3 * d, TT = T * T;
   // S = q k^T into P; under the causal mask the tiles above the diagonal are left to the
   // softmax, which writes them as 0 without reading them
   BatchStrides st{H, T * d3, dh, T * d3, dh, H * TT, TT, causal ? 1 : 0};
   hipError_t e = gemm_batched(true, qkv, d3, true, qkv + d, d3, P, T, T, T, dh, B * H, st, s);
   if (e != hipSuccess) return e;
-  if ((e = softmax_rows(P, B * H * T, T, 1.f / sqrtf((float)dh), causal, s)) != hipSuccess)
-    return e;
+  return softmax_rows(P, B * H * T, T, 1.f / sqrtf((float)dh), causal, s);
+}
+
+hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_t T, int64_t H,
+                         int64_t dh, bool causal, hipStream_t s) {
+  const int64_t d = H * dh, d3 = 3 * d, TT = T * T;
+  hipError_t e = attention_probs(qkv, P, B, T, H, dh, causal, s);
+  if (e != hipSuccess) return e;
   // context = P v
   BatchStrides sv{H, H * TT, TT, T * d3, dh, T * d, dh};
   return gemm_batched(true, P, T, false, qkv + 2 * d, d3, y, d, T, dh, T, B * H, sv, s);
 }
 
-hipError_t attention_bwd(const float* qkv, const float* P, const float* dy, float* dqkv, float* dS,
+// The probabilities are recomputed here rather than kept from the forward: holding them
+// ([B, H, T, T], a quarter of the transformer's activations) across the step would make the
+// out-of-core schedule swap them out and back in, while recomputing costs one q k^T product
+// and one softmax pass.  The same kernels on the same q, k give the forward's P bit for bit.
+hipError_t attention_bwd(const float* qkv, float* P, const float* dy, float* dqkv, float* dS,
                          int64_t B, int64_t T, int64_t H, int64_t dh, bool causal, hipStream_t s) {
   const int64_t d = H * dh, d3 = 3 * d, TT = T * T;
-  hipError_t e;
+  hipError_t e = attention_probs(qkv, P, B, T, H, dh, causal, s);
+  if (e != hipSuccess) return e;
   // dv = P^T dO
   BatchStrides s1{H, H * TT, TT, T * d, dh, T * d3, dh};
   if ((e = gemm_batched(false, P, T, false, dy, d, dqkv + 2 * d, d3, T, dh, T, B * H, s1, s)) !=

@@ -44,7 +44,7 @@ const Sig kSig[OOC_OP_COUNT] = {
     {"GELU_FWD", 2, 1, {OOC_R, OOC_W}},
     {"GELU_BWD", 3, 1, {OOC_R, OOC_R, OOC_W}},
     {"ATTENTION_FWD", 3, 5, {OOC_R, OOC_W, OOC_W}},
-    {"ATTENTION_BWD", 5, 5, {OOC_R, OOC_R, OOC_R, OOC_W, OOC_W}},
+    {"ATTENTION_BWD", 5, 5, {OOC_R, OOC_W, OOC_R, OOC_W, OOC_W}},
     {"CONCAT_FWD", -1, -1, {}},
     {"CONCAT_BWD", -1, -1, {}},
     {"UPSAMPLE_FWD", 2, 4, {OOC_R, OOC_W}},

@@ -24,8 +24,9 @@ the library's kernels ask for (``ooc_wgrad_slices``), with a partial-sum
 variable of S_w copies of dW (a dense layer's then S_w copies of db) when
 S_w > 1; a LayerNorm keeps mean and 1/std per row and 2 S floats per feature
 with S = min(ceil(rows / 32), 2048) (its rows are d floats wide); attention
-keeps its probabilities [B, H, T, T] and its backward a scratch of the same
-size.
+writes its probabilities [B, H, T, T] in the forward, where they die, and its
+backward recomputes them into a variable of its own beside a scratch of the
+same size.
 """
 
 from __future__ import annotations
@@ -317,8 +318,9 @@ class Net:
             a = self._attn_attrs(L, X)
             B, T, H, dh, _ = a
             dX = self._decl(f"d:{X}@{name}", xs)
+            Pb = self._decl(name + ".Pb", (B, H, T, T))
             dS = self._decl(name + ".dS", (B, H, T, T))
-            self._call("attention_bwd", [(X, ooc.R), (name + ".P", ooc.R), (dY, ooc.R),
+            self._call("attention_bwd", [(X, ooc.R), (Pb, ooc.W), (dY, ooc.R),
                                          (dX, ooc.W), (dS, ooc.W)], a)
             out.append((X, dX))
 

@@ -540,7 +540,8 @@ def check_attention(op, a, sig, rep, rng):
     u of the score's magnitude; the row normalisation and P v sum T terms.  The backward's
     bound is 4 sqrt(T) u times the magnitude of each output, formed by the same products on
     absolute values: every stage (dP = dY v^T, the row sums of dS, dS k, dS^T q, P^T dY) sums
-    at most T terms."""
+    at most T terms; the backward recomputes P, so the forward's relative bound on P is added
+    through both factors of P in dS and through P^T dY."""
     B, T, H, dh, causal = a
     d = H * dh
     qkv = Pool.window(B * T * 3 * d, 0, 3).reshape(B * T, 3 * d)
@@ -553,6 +554,12 @@ def check_attention(op, a, sig, rep, rng):
         return np.concatenate([rows[:, p * d + h * dh:p * d + (h + 1) * dh] for p in range(3)],
                               axis=1)
 
+    def p_rel(x):
+        """Relative bound on each row of one head's P (x = its q, k, v columns)."""
+        q, k = np.abs(x[:, :dh]), np.abs(x[:, dh:2 * dh])
+        smag = (q @ k.T).max(axis=1, keepdims=True) / math.sqrt(dh)
+        return (2 * math.sqrt(dh) + 4) * U * smag + (math.sqrt(T) + 16) * U
+
     if op == "attention_fwd":
         def fill(j, v):
             as_f32(v)[...] = qkv.reshape(-1)
@@ -563,36 +570,38 @@ def check_attention(op, a, sig, rep, rng):
             for b, h in heads:
                 x = head(qkv, b, h).astype(np.float64)
                 P, Y = ops.attention_fwd(x, 1, T, 1, bool(causal))
-                q, k, v = np.abs(x[:, :dh]), np.abs(x[:, dh:2 * dh]), np.abs(x[:, 2 * dh:])
-                smag = (q @ k.T).max(axis=1, keepdims=True) / math.sqrt(dh)
-                rel = (2 * math.sqrt(dh) + 4) * U * smag + (math.sqrt(T) + 16) * U
+                rel = p_rel(x)
                 rep.close(f"P[{b},{h}]", Pg[b, h], P[0, 0], rel * P[0, 0])
                 rep.close(f"Y[{b},{h}]", Yg[b * T:(b + 1) * T, h * dh:(h + 1) * dh], Y,
-                          (rel + math.sqrt(T) * U) * (P[0, 0] @ v))
+                          (rel + math.sqrt(T) * U) * (P[0, 0] @ np.abs(x[:, 2 * dh:])))
         return
-    # backward: P is any causal row-stochastic matrix (an input of the function), dY normal
-    Pin = rng.random((B, H, T, T), dtype=np.float32)
-    if causal:
-        Pin *= np.tril(np.ones((T, T), np.float32))
-    Pin /= Pin.sum(axis=-1, keepdims=True)
+    # backward: P is recomputed from q and k into a variable of its own; dY normal
     G = Pool.window(B * T * d, 2, 3).reshape(B * T, d)
 
     def fill(j, v):
-        as_f32(v)[...] = (qkv.reshape(-1), Pin.reshape(-1), G.reshape(-1))[j]
+        as_f32(v)[...] = (qkv.reshape(-1), None, G.reshape(-1))[j]
 
     with run_case(op, a, sig, fill) as out:
+        Pg = as_f32(out[1]).reshape(B, H, T, T)
         dg = as_f32(out[3]).reshape(B * T, 3 * d)
         for b, h in heads:
             x = head(qkv, b, h).astype(np.float64)
-            p = Pin[b, h].astype(np.float64)
+            P = ops.attention_fwd(x, 1, T, 1, bool(causal))[0]
+            p, rel = P[0, 0], p_rel(x)
+            rep.close(f"P[{b},{h}]", Pg[b, h], p, rel * p)
             g = G[b * T:(b + 1) * T, h * dh:(h + 1) * dh].astype(np.float64)
-            ref = ops.attention_bwd(x, p[None, None], g, 1, T, 1)
+            ref = ops.attention_bwd(x, P, g, 1, T, 1)
             q, k, v = np.abs(x[:, :dh]), np.abs(x[:, dh:2 * dh]), np.abs(x[:, 2 * dh:])
             ga = np.abs(g)
             dP = ga @ v.T
             dS = p * (dP + (dP * p).sum(axis=1, keepdims=True)) / math.sqrt(dh)
             mag = np.concatenate([dS @ k, dS.T @ q, p.T @ ga], axis=1)
-            rep.close(f"dqkv[{b},{h}]", head(dg, b, h), ref, 4 * math.sqrt(T) * U * mag)
+            # the recomputed P's error (rel per row) enters dS through both of its factors
+            # of P and dv through P^T dY
+            carried = np.concatenate([(2 * rel * dS) @ k, (2 * rel * dS).T @ q,
+                                      (rel * p).T @ ga], axis=1)
+            rep.close(f"dqkv[{b},{h}]", head(dg, b, h), ref,
+                      4 * math.sqrt(T) * U * mag + carried)
 
 
 CHECKS = {"conv_fwd": check_conv, "conv_bwd_x": check_conv, "conv_bwd_w": check_conv,

@@ -478,8 +478,10 @@ def test_attention(B, T, H, dh, causal):
     assert rel_err(P, rP) < TOL and rel_err(Y, rY) < TOL
     if causal:   # masked scores are exact zeros, also in tiles the products skip
         assert not np.triu(P.reshape(B * H, T, T), 1).any()
-    out = run_fn("attention_bwd", [(qkv, ooc.R), (P, ooc.R), (G, ooc.R),
+    # the backward recomputes P into its own buffer with the forward's kernels: bit for bit
+    out = run_fn("attention_bwd", [(qkv, ooc.R), (((B, H, T, T), "f32"), ooc.W), (G, ooc.R),
                                    (((B * T, 3 * dmod), "f32"), ooc.W),
                                    (((B, H, T, T), "f32"), ooc.W)], [B, T, H, dh, causal])
+    assert np.array_equal(out[1], P)
     rd = ops.attention_bwd(qkv.astype(np.float64), rP, G.astype(np.float64), B, T, H)
     assert rel_err(out[3], rd) < TOL
