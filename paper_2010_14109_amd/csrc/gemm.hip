@@ -863,12 +863,18 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 // rows (the 64-channel convolutions) take 256 x 64: each wave then owns 64 x 64
 // and one round of LDS reads feeds 16 MFMAs instead of 8 (2-3 % faster
 // measured; plain, unbatched products only, to keep the kernel count down).
+// A product with fewer 128 x 128 tiles than half the CUs (a dense layer at a
+// small batch) takes 64 x 64 tiles, four times as many workgroups, each wave
+// one MFMA block (unbatched products only: a batched product has workgroups
+// enough across its batch).
 constexpr int64_t kTallRows = 65536;
-enum Shape { S128x128, S128x64, S64x128, S256x64 };
+constexpr int64_t kFewTiles = 128;
+enum Shape { S128x128, S128x64, S64x128, S256x64, S64x64 };
 Shape pick_shape(int64_t M, int64_t N) {
   if (N <= 64 && M >= kTallRows) return S256x64;
   if (N <= 64 && M > 64) return S128x64;
   if (M <= 64) return S64x128;
+  if (((M + 127) / 128) * ((N + 127) / 128) < kFewTiles) return S64x64;
   return S128x128;
 }
 
@@ -908,6 +914,16 @@ hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const f
       return run_gemm<64, 128, LAT<64>, LBT<128>, OM, BIAS, BATCHED, ROWSUM>(
           a, b, c, om, slice_stride, bias, M, N, K, slices, s, batches, bt, rowsum);
     }
+    case S64x64:
+      if constexpr (!BATCHED) {
+        LAT<64> a{};
+        LBT<64> b{};
+        fa(a);
+        fb(b);
+        return run_gemm<64, 64, LAT<64>, LBT<64>, OM, BIAS, false, ROWSUM>(
+            a, b, c, om, slice_stride, bias, M, N, K, slices, s, 1, bt, rowsum);
+      }
+      [[fallthrough]];
     default: {
       LAT<128> a{};
       LBT<128> b{};
@@ -1141,7 +1157,14 @@ hipError_t conv_fwd(const float* X, const float* W, float* Y, const ConvShape& c
     a.dS = FastDiv::make(c.S); a.dSC = FastDiv::make(c.S * c.C);
   };
   auto fb = [&](auto& b) { b.p = W; b.ld = K; };
-  if (N <= 32 && c.C % 4 == 0) {   // at most 32 output channels: 256 x 32 tiles, no empty columns
+  if (N <= 32 && c.C % 4 == 0) {
+    // at most 32 output channels: 256 x 32 tiles, no empty columns; 128 x 32 when there are
+    // fewer 256-row tiles than CUs, so that twice as many workgroups share the chip
+    if ((M + 255) / 256 < 256) {
+      if (c.C % 32 == 0)
+        return dispatch_shape<128, 32, ConvPatchT, MatKv>(fa, fb, Y, DenseOut{N}, 0, M, N, K, 1, s);
+      return dispatch_shape<128, 32, ConvPatchV, MatKv>(fa, fb, Y, DenseOut{N}, 0, M, N, K, 1, s);
+    }
     if (c.C % 32 == 0)
       return dispatch_shape<256, 32, ConvPatchT, MatKv>(fa, fb, Y, DenseOut{N}, 0, M, N, K, 1, s);
     return dispatch_shape<256, 32, ConvPatchV, MatKv>(fa, fb, Y, DenseOut{N}, 0, M, N, K, 1, s);
@@ -1267,7 +1290,7 @@ hipError_t conv_bwd_w(const float* X, const float* dY, float* dW, float* part, i
 // rows (C = input channels of a filter gradient, -1 for a dense layer).  The
 // launchers above run tiles x s workgroups; a CU holds kResident of them at
 // once (LDS bounds it: 2 for 128 x 128, 64 x 192 and 32 x 256 tiles, 3 for the
-// general 64-wide ones, 4-5 for the small 64 x 64 filter tiles), so a launch
+// general 64-wide ones, 4-5 for the 64 x 64 tiles), so a launch
 // takes ceil(tiles s / slots) rounds of K / s rows.  s minimises rounds / s
 // (a partly filled last round leaves most CUs idle behind a few), with at most
 // four rounds and at least 256 rows a slice; the smallest s within 1 % of the
@@ -1287,6 +1310,7 @@ int64_t wgrad_slices(int64_t M, int64_t N, int64_t K, int64_t C) {
       case S256x64: tiles = (M + 255) / 256, resident = 2; break;
       case S128x64: tiles = (M + 127) / 128, resident = 3; break;
       case S64x128: tiles = (N + 127) / 128, resident = 3; break;
+      case S64x64: tiles = ((M + 63) / 64) * ((N + 63) / 64), resident = 4; break;
       default: tiles = ((M + 127) / 128) * ((N + 127) / 128), resident = 2;
     }
   }

@@ -80,7 +80,10 @@ def d(a):
                                      # tiles than workgroups, ragged rows and columns: forward,
                                      # input gradient, and a scalar-loader forward on 256 x 64
                                      (70001, 100, 130, 1), (70001, 130, 100, 1),
-                                     (200001, 37, 45, 1)])
+                                     (200001, 37, 45, 1),
+                                     # few output tiles (64 x 64 tiles), reductions of at most
+                                     # 128 among them, ragged rows and columns
+                                     (640, 96, 640, 1), (333, 120, 257, 1)])
 def test_linear(M, K, N, S):
     """S > 1 cuts the rows of the weight gradient into slices (the last one of
     (100, 40, 20, 3) is empty)."""
@@ -122,10 +125,14 @@ CONVS = [  # N, H, W, C, K, k, stride, pad
     (2, 9, 9, 60, 20, 3, 1, 1),
     (1, 7, 6, 20, 64, 3, 2, 1),
     # filter gradients on 64 x 64 tiles (3 input channels, RSC 27; a 1 x 1 64 -> 64 filter) and on
-    # 32 x 256 tiles with a ragged last tile (128 -> 32 channels, RSC 1152); forward on 256 x 32
+    # 32 x 256 tiles with a ragged last tile (128 -> 32 channels, RSC 1152); forward on 128 x 32
     (2, 10, 9, 3, 64, 3, 1, 1),
     (2, 6, 5, 64, 64, 1, 1, 0),
     (1, 6, 6, 128, 32, 3, 1, 1),
+    # at most 32 output channels over at least 256 x 256 output rows: forward on 256 x 32, one
+    # filter tap per K tile and (ragged, 66560 rows) four channels per load
+    (4, 128, 128, 32, 32, 3, 1, 1),
+    (4, 128, 130, 4, 16, 3, 1, 1),
     # at least 65536 output rows and 64 columns: 256 x 64 tiles with a ragged last tile
     # (66825 rows), for the 3 x 3 forward and input gradient, the stride-2 classes and the
     # pointwise (dense) path
