@@ -863,18 +863,21 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 // rows (the 64-channel convolutions) take 256 x 64: each wave then owns 64 x 64
 // and one round of LDS reads feeds 16 MFMAs instead of 8 (2-3 % faster
 // measured; plain, unbatched products only, to keep the kernel count down).
-// A product with fewer 128 x 128 tiles than half the CUs (a dense layer at a
-// small batch) takes 64 x 64 tiles, four times as many workgroups, each wave
-// one MFMA block (unbatched products only: a batched product has workgroups
-// enough across its batch).
+// A product with fewer 128 x 128 tiles than half the CUs and a reduction of at
+// most 4096 (a dense layer at a small batch) takes 64 x 64 tiles, four times
+// as many workgroups, each wave one MFMA block.  Longer reductions keep
+// 128 x 128: those of few tiles are weight gradients, which split their rows
+// into slices instead.  Unbatched products only: a batched product has
+// workgroups enough across its batch.
 constexpr int64_t kTallRows = 65536;
 constexpr int64_t kFewTiles = 128;
+constexpr int64_t kFewTilesMaxK = 4096;
 enum Shape { S128x128, S128x64, S64x128, S256x64, S64x64 };
-Shape pick_shape(int64_t M, int64_t N) {
+Shape pick_shape(int64_t M, int64_t N, int64_t K) {
   if (N <= 64 && M >= kTallRows) return S256x64;
   if (N <= 64 && M > 64) return S128x64;
   if (M <= 64) return S64x128;
-  if (((M + 127) / 128) * ((N + 127) / 128) < kFewTiles) return S64x64;
+  if (((M + 127) / 128) * ((N + 127) / 128) < kFewTiles && K <= kFewTilesMaxK) return S64x64;
   return S128x128;
 }
 
@@ -887,7 +890,7 @@ hipError_t dispatch(FA fa, FB fb, float* c, OM om, int64_t slice_stride, const f
                     int64_t M, int64_t N, int64_t K, int64_t slices, hipStream_t s,
                     int64_t batches = 1, Batch bt = Batch{1, 0, 0, 0, 0, 0, 0, 0},
                     float* rowsum = nullptr) {
-  switch (pick_shape(M, N)) {
+  switch (pick_shape(M, N, K)) {
     case S256x64:
       if constexpr (!BATCHED && !ROWSUM) {
         LAT<256> a{};
@@ -1306,7 +1309,7 @@ int64_t wgrad_slices(int64_t M, int64_t N, int64_t K, int64_t C) {
   } else if (t == WgradTile::k64x64) {
     tiles = 1, resident = C % 4 == 0 ? 5 : 4;
   } else {
-    switch (pick_shape(M, N)) {
+    switch (pick_shape(M, N, K)) {
       case S256x64: tiles = (M + 255) / 256, resident = 2; break;
       case S128x64: tiles = (M + 127) / 128, resident = 3; break;
       case S64x128: tiles = (N + 127) / 128, resident = 3; break;
