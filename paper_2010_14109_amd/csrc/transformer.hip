@@ -689,9 +689,10 @@ hipError_t attention_fwd(const float* qkv, float* P, float* y, int64_t B, int64_
 }
 
 // The probabilities are recomputed here rather than kept from the forward: holding them
-// ([B, H, T, T], a quarter of the transformer's activations) across the step would make the
-// out-of-core schedule swap them out and back in, while recomputing costs one q k^T product
-// and one softmax pass.  The same kernels on the same q, k give the forward's P bit for bit.
+// ([B, H, T, T], the largest activation of a layer at sequence length 512) across the step
+// would make the out-of-core schedule swap them out and back in, while recomputing costs one
+// q k^T product and one softmax pass.  The same kernels on the same q, k give the forward's
+// P bit for bit.
 hipError_t attention_bwd(const float* qkv, float* P, const float* dy, float* dqkv, float* dS,
                          int64_t B, int64_t T, int64_t H, int64_t dh, bool causal, hipStream_t s) {
   const int64_t d = H * dh, d3 = 3 * d, TT = T * T;
