@@ -119,7 +119,7 @@ class Report:
     def __init__(self, case):
         self.case, self.worst = case, 0.0
 
-    def close(self, name, got, ref, bound):
+    def close(self, name, got, ref, bound, offset=0):
         ref = np.asarray(ref, np.float64)
         bound = np.broadcast_to(np.asarray(bound, np.float64), ref.shape).reshape(-1)
         got = np.asarray(got, np.float64).reshape(-1)
@@ -129,16 +129,27 @@ class Report:
         err = np.abs(got - ref)
         ratio = err / np.maximum(bound, 1e-300)
         worst = int(np.argmax(ratio))
-        assert ratio[worst] <= 1.0, (f"{self.case} {name}: element {worst} got {got[worst]!r} "
+        assert ratio[worst] <= 1.0, (f"{self.case} {name}: element {offset + worst} got {got[worst]!r} "
                                      f"ref {ref[worst]!r} bound {bound[worst]!r}")
         self.worst = max(self.worst, float(ratio[worst]))
 
-    def exact(self, name, got, ref):
-        """Equal values (a zero's sign is not compared)."""
+    def exact(self, name, got, ref, offset=0):
+        """Equal values (a zero's sign is not compared); offset = index of got[0] in the whole
+        result, for the message."""
         got, ref = np.asarray(got).reshape(-1), np.asarray(ref).reshape(-1)
         assert got.shape == ref.shape, (name, got.shape, ref.shape)
         bad = np.flatnonzero(got != ref)
-        assert bad.size == 0, f"{self.case} {name}: {bad.size} elements differ, first {bad[0]}"
+        assert bad.size == 0, (f"{self.case} {name}: {bad.size} elements differ, first "
+                               f"{offset + bad[0]}")
+
+
+# Whole-tensor comparisons run over pieces of this many elements: each piece's reference and
+# comparison stay small, so a tensor of 2^30 elements does not need several more of its size.
+PIECE = 1 << 24
+
+
+def pieces(n):
+    return ((lo, min(n, lo + PIECE)) for lo in range(0, n, PIECE))
 
 
 def sample(shape, rng, n=NSAMPLE):
@@ -294,15 +305,16 @@ def check_elementwise(op, a, sig, rep, rng):
         as_f32(v)[...] = ins[j]
 
     with run_case(op, a, sig, fill) as out:
-        got = as_f32(out[-1])
-        if op == "relu_fwd":
-            rep.exact("Y", got, np.maximum(ins[0], np.float32(0)))
-        elif op == "relu_bwd":
-            rep.exact("dX", got, np.where(ins[0] > 0, ins[1], np.float32(0)))
-        elif op == "acc":
-            rep.exact("A", as_f32(out[0]), ins[0] + ins[1])     # in place: A += B
-        else:
-            rep.exact("Y", got, ins[0] + ins[1])    # one float32 addition, correctly rounded
+        got = as_f32(out[0] if op == "acc" else out[-1])     # acc: in place, A += B
+        for lo, hi in pieces(n):
+            x, y = ins[0][lo:hi], ins[1][lo:hi]
+            if op == "relu_fwd":
+                ref = np.maximum(x, np.float32(0))
+            elif op == "relu_bwd":
+                ref = np.where(x > 0, y, np.float32(0))
+            else:
+                ref = x + y                         # one float32 addition, correctly rounded
+            rep.exact({"relu_bwd": "dX", "acc": "A"}.get(op, "Y"), got[lo:hi], ref, lo)
 
 
 def pool_taps(N, P, Q, C, k, st, pd, H, W, rng):
@@ -522,17 +534,19 @@ def check_gelu(op, a, sig, rep, rng):
         as_f32(v)[...] = X if j == 0 else G
 
     with run_case(op, a, sig, fill) as out:
-        x = X.astype(np.float64)
-        cdf = 0.5 * erfc(-x / math.sqrt(2.0))
-        xpdf = np.abs(x) * np.exp(-0.5 * x * x) / math.sqrt(2.0 * math.pi)
+        got = as_f32(out[1] if op == "gelu_fwd" else out[2])
         tiny = 2.0 ** -126
-        if op == "gelu_fwd":
-            ref = ops.gelu_fwd(x)
-            rep.close("Y", as_f32(out[1]), ref, 8 * U * np.abs(x) * (cdf + xpdf) + tiny)
-        else:
-            ref = ops.gelu_bwd(x, G.astype(np.float64))
-            rep.close("dX", as_f32(out[2]), ref,
-                      8 * U * np.abs(G) * (cdf + xpdf * (x * x + 2)) + tiny)
+        for lo, hi in pieces(n):
+            x = X[lo:hi].astype(np.float64)
+            cdf = 0.5 * erfc(-x / math.sqrt(2.0))
+            xpdf = np.abs(x) * np.exp(-0.5 * x * x) / math.sqrt(2.0 * math.pi)
+            if op == "gelu_fwd":
+                rep.close("Y", got[lo:hi], ops.gelu_fwd(x), 8 * U * np.abs(x) * (cdf + xpdf) + tiny,
+                          lo)
+            else:
+                g = G[lo:hi]
+                rep.close("dX", got[lo:hi], ops.gelu_bwd(x, g.astype(np.float64)),
+                          8 * U * np.abs(g) * (cdf + xpdf * (x * x + 2)) + tiny, lo)
 
 
 def check_attention(op, a, sig, rep, rng):
