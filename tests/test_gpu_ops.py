@@ -148,8 +148,12 @@ def test_conv(shape):
     print(f"conv {shape}", flush=True)
     P, Q = (H + 2 * pd - k) // st + 1, (Wd + 2 * pd - k) // st + 1
     a = [N, H, Wd, C, K, k, k, st, pd, P, Q]
+    # variables are virtually contiguous whatever the chunk; 2 MiB chunks keep the tensors of
+    # millions of elements to a few hundred mappings (each one a driver call) per run
+    chunk = 2 << 20 if max(N * H * Wd * C, N * P * Q * K) > (1 << 20) else 4096
     X, Wt, G = f32(N, H, Wd, C), f32(K, k, k, C), f32(N, P, Q, K)
-    (_, _, Y) = run_fn("conv_fwd", [(X, ooc.R), (Wt, ooc.R), (((N, P, Q, K), "f32"), ooc.W)], a)
+    (_, _, Y) = run_fn("conv_fwd", [(X, ooc.R), (Wt, ooc.R), (((N, P, Q, K), "f32"), ooc.W)], a,
+                       chunk)
     assert rel_err(Y, ops.conv_fwd(d(X), d(Wt), st, pd)) < TOL
     ref_dW = ops.conv_bwd_w(d(X), d(G), Wt.shape, st, pd)
     for slices in sorted({1, ooc.wgrad_slices("conv_bwd_w", a), 3, 7}):
@@ -157,11 +161,11 @@ def test_conv(shape):
         args = [(X, ooc.R), (G, ooc.R), (((K, k, k, C), "f32"), ooc.W)]
         if slices > 1:
             args.append((((slices * K * k * k * C,), "f32"), ooc.W))
-        out = run_fn("conv_bwd_w", args, a + [slices])
+        out = run_fn("conv_bwd_w", args, a + [slices], chunk)
         assert rel_err(out[2], ref_dW) < TOL, slices
     if C % 4 == 0:
         (_, _, dX) = run_fn("conv_bwd_x", [(Wt, ooc.R), (G, ooc.R),
-                                            (((N, H, Wd, C), "f32"), ooc.W)], a)
+                                            (((N, H, Wd, C), "f32"), ooc.W)], a, chunk)
         assert rel_err(dX, ops.conv_bwd_x(d(Wt), d(G), X.shape, st, pd)) < TOL
 
 
