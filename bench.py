@@ -148,7 +148,7 @@ def measured_traffic(net, op):
 
 
 # schedule-window W as a fraction of the budget.  The paper leaves W to the user and the library's
-# default is B/2; a sweep on this machine (0.1 to 0.5 of B) found B/4 best or level on every workload
+# default is B/2; a sweep on one MI355X (0.1 to 0.5 of B) found B/4 best or level on every workload
 # but the MLP: a narrower window admits swap-ins later, so fewer variables are swapped out early to
 # make room, and the host link carries fewer bytes.  The MLP's swap-ins are weights needed in both
 # passes, which want the wider window.
@@ -159,8 +159,8 @@ WINDOW_FRAC = {"mlp": 0.5}
 def window_fraction(workload):
     return WINDOW_FRAC.get(workload, DEFAULT_WINDOW_FRAC)
 
-# pinned host memory asked for when the whole arena cannot be pinned (the MI355X boxes here pin
-# at most 64 GiB per process)
+# pinned host memory asked for when the whole arena cannot be pinned (on the MI355X hosts measured
+# one process pins at most 64 GiB)
 DEFAULT_HOST_LIMIT = 56 << 30
 MAP_ENTRY_LIMIT = 40000   # chunks + mappings per plan; the process table holds ~65530
 
