@@ -16,8 +16,8 @@
 //  * whoever first writes an interval (its swap-in copy, or the first kernel
 //    using an allocated one) waits until every interval that used the same
 //    chunks before is released: its last kernel finished and its last
-//    swap-out copy completed (the device-side meaning of step (b), "wait for
-//    the swap-out right before f_i");
+//    swap-out copy completed (the device-side form of step (b) of Section 3,
+//    which completes the oldest swap-outs before f_i runs);
 //  * a swap-in waits for the last swap-out copy into the same host slot.
 // Two kinds of swap-out need no copy and are not issued: one that is later
 // cancelled (its host copy is never read: the variable is kept on the device
