@@ -16,7 +16,7 @@ import numpy as np
 import pytest
 
 from oracle import mixop, ops
-from paper_2010_14109_amd import netdef, ooc
+from paper_2010_14109_amd import ooc
 from tests.gpu_util import rel_err
 
 pytestmark = pytest.mark.gpu
