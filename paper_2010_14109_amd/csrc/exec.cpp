@@ -60,28 +60,29 @@ static const int kThreads = 8;
 
 void release_device(ooc_ctx* ctx) {
   if (ctx->device < 0) return;
-  hipSetDevice(ctx->device);
-  if (ctx->cs) hipStreamSynchronize(ctx->cs);
-  if (ctx->hs) hipStreamSynchronize(ctx->hs);
-  if (ctx->ds) hipStreamSynchronize(ctx->ds);
-  if (ctx->ss) hipStreamSynchronize(ctx->ss);
-  for (hipEvent_t e : ctx->events) hipEventDestroy(e);
+  // teardown: an error here cannot be acted on, and every resource is released regardless
+  (void)hipSetDevice(ctx->device);
+  if (ctx->cs) (void)hipStreamSynchronize(ctx->cs);
+  if (ctx->hs) (void)hipStreamSynchronize(ctx->hs);
+  if (ctx->ds) (void)hipStreamSynchronize(ctx->ds);
+  if (ctx->ss) (void)hipStreamSynchronize(ctx->ss);
+  for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
   ctx->events.clear();
-  if (ctx->cs) hipStreamDestroy(ctx->cs);
-  if (ctx->hs) hipStreamDestroy(ctx->hs);
-  if (ctx->ds) hipStreamDestroy(ctx->ds);
-  if (ctx->ss) hipStreamDestroy(ctx->ss);
+  if (ctx->cs) (void)hipStreamDestroy(ctx->cs);
+  if (ctx->hs) (void)hipStreamDestroy(ctx->hs);
+  if (ctx->ds) (void)hipStreamDestroy(ctx->ds);
+  if (ctx->ss) (void)hipStreamDestroy(ctx->ss);
   ctx->cs = ctx->hs = ctx->ds = ctx->ss = nullptr;
-  if (ctx->heap) hipFree(ctx->heap);
+  if (ctx->heap) (void)hipFree(ctx->heap);
   ctx->heap = nullptr;
   if (ctx->va_base) {
-    hipMemUnmap(ctx->va_base, ctx->va_bytes);
-    hipMemAddressFree(ctx->va_base, ctx->va_bytes);
+    (void)hipMemUnmap(ctx->va_base, ctx->va_bytes);
+    (void)hipMemAddressFree(ctx->va_base, ctx->va_bytes);
     ctx->va_base = nullptr;
   }
-  for (auto h : ctx->chunks) hipMemRelease(h);
+  for (auto h : ctx->chunks) (void)hipMemRelease(h);
   ctx->chunks.clear();
-  if (ctx->arena) hipHostFree(ctx->arena);
+  if (ctx->arena) (void)hipHostFree(ctx->arena);
   ctx->arena = nullptr;
   if (ctx->spill) munmap(ctx->spill, ctx->spill_bytes);
   ctx->spill = nullptr;
@@ -799,7 +800,8 @@ struct Stager {
   }
 
   void fill(int t) {
-    hipSetDevice(ctx->device);
+    if (const hipError_t e = hipSetDevice(ctx->device); e != hipSuccess)
+      return fail(std::string("staging: ") + hipGetErrorString(e));
     const int64_t n = (int64_t)ctx->in_copy.size();
     for (int64_t p = t; p < n; p += kThreads) {
       const Copy& c = *ctx->in_copy[p];
@@ -822,7 +824,8 @@ struct Stager {
   }
 
   void issue() {
-    hipSetDevice(ctx->device);
+    if (const hipError_t e = hipSetDevice(ctx->device); e != hipSuccess)
+      return fail(std::string("staging: ") + hipGetErrorString(e));
     const int64_t n = (int64_t)ctx->in_copy.size();
     int64_t ci = 0;
     for (int64_t p = 0; p < n; ++ci) {
@@ -848,7 +851,8 @@ struct Stager {
   }
 
   void drain(int t) {
-    hipSetDevice(ctx->device);
+    if (const hipError_t e = hipSetDevice(ctx->device); e != hipSuccess)
+      return fail(std::string("staging: ") + hipGetErrorString(e));
     const int64_t n = (int64_t)ctx->out_copy.size();
     for (int64_t q = t; q < n; q += kThreads) {
       const Copy& c = *ctx->out_copy[q];
@@ -1065,14 +1069,15 @@ ooc_status link_probe(int32_t device, uint64_t bytes, int32_t reps, double* h2d,
   };
   st = run();
   *err = ctx->err;
+  // clean-up after the probe: its result stands whatever these return
   for (auto x : e)
-    if (x) hipEventDestroy(x);
-  if (s1) hipStreamDestroy(s1);
-  if (s2) hipStreamDestroy(s2);
-  if (d1) hipFree(d1);
-  if (d2) hipFree(d2);
-  if (hp1) hipHostFree(hp1);
-  if (hp2) hipHostFree(hp2);
+    if (x) (void)hipEventDestroy(x);
+  if (s1) (void)hipStreamDestroy(s1);
+  if (s2) (void)hipStreamDestroy(s2);
+  if (d1) (void)hipFree(d1);
+  if (d2) (void)hipFree(d2);
+  if (hp1) (void)hipHostFree(hp1);
+  if (hp2) (void)hipHostFree(hp2);
   return st;
 }
 
