@@ -104,3 +104,17 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120, cwd=ROOT)
     assert r.returncode == 2
     assert "one GPU" in r.stdout
+
+
+def test_paper_figure_only_for_the_exact_table_1_setting():
+    """vs_baseline divides by the paper's 321 images/s (Table 1, Schedule + VA, batch 1440) only
+    when the run is that setting: the default workload, batch and budget, the adaptive scheduler,
+    the chunk pool and the paper's oldest-first waits."""
+    f = synth.budget_fraction("resnet50_b1440")
+    assert bench.paper_figure("resnet50_b1440", 1440, f, "adaptive", "pool", "oldest") == 321.0
+    assert bench.paper_figure("resnet50_b1440", 800, f, "adaptive", "pool", "oldest") is None
+    assert bench.paper_figure("resnet50_b1440", 1440, 0.25, "adaptive", "pool", "oldest") is None
+    assert bench.paper_figure("resnet50_b1440", 1440, f, "naive", "pool", "oldest") is None
+    assert bench.paper_figure("resnet50_b1440", 1440, f, "adaptive", "bestfit", "oldest") is None
+    assert bench.paper_figure("resnet50_b1440", 1440, f, "adaptive", "pool", "furthest") is None
+    assert bench.paper_figure("resnet50_b256", 256, 0.25, "adaptive", "pool", "oldest") is None
